@@ -1,0 +1,155 @@
+/*
+ * rla.h -- C ABI of the MI355X (gfx950) library for the Residual Linear
+ * Attention (RLA) and Residual Delta Net (RDN) sequence-mixing operators of
+ * "Enhancing linear attention with residual learning" (Sec. 3.4, "Final
+ * Formulations").
+ *
+ * Per sequence and head, with the paper's states S, R in R^{d_v x d_k}:
+ *   x_t = v_t - S_{t-1} k_t ;  r_t = Clip_[-c,c](x_t)          (Sec. 3.1, 3.3)
+ *   RDN: R_t = aR_t R_{t-1} (I - g_t k_t k_t^T) + g_t r_t k_t^T
+ *        S_t = aS_t S_{t-1} (I - b_t k_t k_t^T) + b_t v_t k_t^T
+ *   RLA: R_t = aR_t R_{t-1} + g_t r_t k_t^T ;  S_t = aS_t S_{t-1} + b_t v_t k_t^T
+ *   o_t = aS_t S_{t-1} q_t + g_t R_t q_t
+ * aS, aR are the decays of S and R (the paper ties them: pass the same
+ * array twice), b = beta the write strength of S (Sec. 3.2), g = gamma the
+ * correction factor (Sec. 3.2).  q and k are taken as given; the paper
+ * L2-normalises them (Sec. 3.3) before the operator.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Every tensor pointer is DEVICE memory owned by the caller.  The
+ *   library allocates nothing and keeps no state between calls; scratch
+ *   space is the caller's `workspace` of at least rla_workspace_size() bytes
+ *   (256-byte aligned).  Inputs are read only; outputs are fully overwritten.
+ *   Calls are asynchronous on `stream` (a hipStream_t; NULL = null stream).
+ * Layout (row-major, contiguous):
+ *   q, k                [B, T, H, d_k]      (element type: problem.dtype)
+ *   v, dO               [B, T, H, d_v]      (element type: problem.dtype)
+ *   dq, dk              [B, T, H, d_k]      (element type: problem.out_dtype)
+ *   o, dv               [B, T, H, d_v]      (element type: problem.out_dtype)
+ *   gates and their gradients  [B, T, H]    fp32
+ *   states S0, R0, S_final, R_final, dS_final, dR_final, dS0, dR0
+ *                       [N, H, d_k, d_v]    fp32, where element (i, j) is the
+ *                       paper's S[j][i] (the state is stored transposed)
+ *   With cu_seqlens (B must be 1) the T tokens are a packing of N sequences:
+ *   sequence n is tokens [cu_seqlens[n], cu_seqlens[n+1]); states reset at
+ *   every sequence start.  Without it N = B sequences of length T.
+ *   q, k, v, o, dO, dq, dk, dv must be 16-byte aligned.
+ * Gates.  Gate values, not logits: aS, aR in (0, 1], b, g in [0, 1] are
+ *   preconditions not checked on the device.  Decays below 2^-126 are
+ *   treated as 2^-126.
+ * Clip.  clip >= 0; +INFINITY disables clipping.  The clip's derivative is
+ *   taken as 1 on the closed interval [-clip, clip].
+ * Errors.  Argument, shape and workspace errors are detected on the host
+ *   before any HIP call and returned as a status; nothing is launched.
+ *   cu_seqlens is device memory and is not read by the host: on the device
+ *   sequence n spans [m_n, m_{n+1}) where m_i is the running maximum of the
+ *   offsets cu[0..i] clamped into [0, T]; for increasing offsets this is
+ *   [cu[n], cu[n+1]), and any other input yields disjoint, possibly empty,
+ *   sequences.  Tokens outside every sequence get zero outputs/gradients.
+ *   Launch failures return RLA_ERR_HIP.  No call aborts or throws.
+ * Supported shapes.  bf16: d_k, d_v in {64, 128}.  fp32: d_k = 64,
+ *   d_v in {64, 128}.  Any B, T >= 0, H >= 1.  Internally the sequence is
+ *   processed in chunks of 64 tokens; results do not depend on B or packing.
+ * Precision.  fp32 inputs: fp32 arithmetic throughout.  bf16 inputs: matrix
+ *   products on MFMA with fp32 accumulation; products of q or k with a state
+ *   use the state split into two bf16 terms (about 16 mantissa bits, fp32
+ *   range); all other product operands are fp16 (intermediates bounded by
+ *   the inputs, the clip and the gates).  States are carried in fp32.
+ *   out_dtype may be fp32 (no output rounding) or bf16 (for bf16 inputs).
+ */
+#ifndef RLA_MI355X_RLA_H
+#define RLA_MI355X_RLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RLA_OK = 0,
+  RLA_ERR_NULL_ARG = 1,    /* a required pointer is NULL */
+  RLA_ERR_SHAPE = 2,       /* a size is negative, inconsistent or unsupported */
+  RLA_ERR_DTYPE = 3,       /* unknown dtype, or dtype not supported for the shape */
+  RLA_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
+  RLA_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than required */
+  RLA_ERR_VALUE = 6,       /* bad scalar (clip < 0 or NaN) or misaligned pointer */
+  RLA_ERR_HIP = 7          /* a HIP runtime call or kernel launch failed */
+} rla_status;
+
+typedef enum { RLA_F32 = 0, RLA_BF16 = 1 } rla_dtype;
+
+/* Operation codes for rla_workspace_size. */
+typedef enum { RLA_OP_RLA_FORWARD = 0, RLA_OP_RDN_FORWARD = 1, RLA_OP_RDN_BACKWARD = 2 } rla_op;
+
+typedef struct {
+  int64_t batch;            /* B (must be 1 when cu_seqlens != NULL) */
+  int64_t seq_len;          /* T: tokens per batch row (total tokens with cu_seqlens) */
+  int64_t num_heads;        /* H */
+  int64_t head_dim_k;       /* d_k (= d_q) */
+  int64_t head_dim_v;       /* d_v */
+  int64_t num_seqs;         /* N when cu_seqlens != NULL, else ignored (N = B) */
+  const int32_t *cu_seqlens;/* device pointer to N+1 offsets, or NULL */
+  int32_t dtype;            /* rla_dtype of q, k, v, dO */
+  float clip;               /* c >= 0, or +INFINITY for no clipping */
+  int32_t out_dtype;        /* rla_dtype of o, dq, dk, dv (fp32 inputs: fp32 only) */
+} rla_problem;
+
+/* Bytes of workspace the operation needs for this problem (0 if the problem
+ * is invalid).  Pure host function. */
+size_t rla_workspace_size(const rla_problem *problem, int op);
+
+/* Human-readable name of a status code (static string). */
+const char *rla_status_string(rla_status status);
+
+/*
+ * RLA forward (paper Sec. 3.4, left box): additive base state S and additive
+ * residual state R.  S0/R0 may be NULL (zero initial states); S_final/R_final
+ * may be NULL (not written).  o is [B, T, H, d_v] in problem.out_dtype.
+ */
+rla_status rla_forward(const rla_problem *problem,
+                       const void *q, const void *k, const void *v,
+                       const float *alpha_s, const float *beta,
+                       const float *alpha_r, const float *gamma,
+                       const float *S0, const float *R0,
+                       void *o, float *S_final, float *R_final,
+                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * RDN forward (paper Sec. 3.4, right box): gated delta-rule base state S and
+ * gated delta-rule residual state R.  Arguments as for rla_forward.
+ */
+rla_status rdn_forward(const rla_problem *problem,
+                       const void *q, const void *k, const void *v,
+                       const float *alpha_s, const float *beta,
+                       const float *alpha_r, const float *gamma,
+                       const float *S0, const float *R0,
+                       void *o, float *S_final, float *R_final,
+                       void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * RDN backward: gradients of L = <dO, o> + <dS_final, S_T> + <dR_final, R_T>
+ * with respect to every input of rdn_forward, recomputing the forward from the
+ * inputs (nothing is saved between calls).  dS_final, dR_final, S0, R0 may be
+ * NULL (zeros); dS0, dR0 may be NULL (not written).  dq, dk, dv are in
+ * problem.out_dtype; gate gradients are fp32 and are with respect to the
+ * gate values (not their logarithms).
+ */
+rla_status rdn_backward(const rla_problem *problem,
+                        const void *q, const void *k, const void *v,
+                        const float *alpha_s, const float *beta,
+                        const float *alpha_r, const float *gamma,
+                        const float *S0, const float *R0,
+                        const void *dO, const float *dS_final, const float *dR_final,
+                        void *dq, void *dk, void *dv,
+                        float *dalpha_s, float *dbeta, float *dalpha_r, float *dgamma,
+                        float *dS0, float *dR0,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RLA_MI355X_RLA_H */

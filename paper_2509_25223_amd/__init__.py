@@ -1,0 +1,244 @@
+"""MI355X (gfx950) RLA / RDN sequence mixing: Python binding of librla_mi355x.so.
+
+The functions here carry the C ABI's names (include/rla.h) and only marshal
+arguments: they check torch tensors, allocate outputs and the workspace with
+torch, and pass raw device pointers plus the current HIP stream to the
+library.  Every step of the computation runs in the library's HIP kernels;
+there is no fallback, and importing fails loudly if the library is missing.
+
+Tensor conventions (all on the same CUDA/HIP device, contiguous):
+  q, k  [B, T, H, d_k]  v [B, T, H, d_v]   bf16 or fp32 (one dtype for all)
+        or [T, H, d] packed with cu_seqlens (int32 [N+1], device)
+  alpha_s, beta, alpha_r, gamma  [B, T, H] / [T, H]  fp32 gate values
+  S0, R0, states out  [N, H, d_k, d_v]  fp32, stored transposed w.r.t. the
+        paper's d_v x d_k states
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "librla_mi355x.so")
+
+RLA_OK = 0
+RLA_F32, RLA_BF16 = 0, 1
+RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD = 0, 1, 2
+
+SYMBOLS = ("rla_workspace_size", "rla_status_string", "rla_forward", "rdn_forward",
+           "rdn_backward")
+
+
+class rla_problem(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seq_len", ctypes.c_int64),
+                ("num_heads", ctypes.c_int64), ("head_dim_k", ctypes.c_int64),
+                ("head_dim_v", ctypes.c_int64), ("num_seqs", ctypes.c_int64),
+                ("cu_seqlens", ctypes.c_void_p), ("dtype", ctypes.c_int32),
+                ("clip", ctypes.c_float), ("out_dtype", ctypes.c_int32)]
+
+
+class RLAError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, status_string(status), status))
+
+
+_lib = None
+
+
+def load_library():
+    """Loads librla_mi355x.so (built by paper_2509_25223_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("librla_mi355x.so is not built; run `python -m paper_2509_25223_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, sz, pp = ctypes.c_void_p, ctypes.c_size_t, ctypes.POINTER(rla_problem)
+    lib.rla_workspace_size.argtypes = [pp, ctypes.c_int]
+    lib.rla_workspace_size.restype = sz
+    lib.rla_status_string.argtypes = [ctypes.c_int]
+    lib.rla_status_string.restype = ctypes.c_char_p
+    fwd_args = [pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp, sz, vp]
+    for name in ("rla_forward", "rdn_forward"):
+        f = getattr(lib, name)
+        f.argtypes = fwd_args
+        f.restype = ctypes.c_int
+    lib.rdn_backward.argtypes = ([pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp] * 3 +
+                                 [vp] * 4 + [vp] * 2 + [vp, sz, vp])
+    lib.rdn_backward.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().rla_status_string(int(status)).decode()
+
+
+rla_status_string = status_string
+
+
+def rla_workspace_size(problem: rla_problem, op: int) -> int:
+    return int(load_library().rla_workspace_size(ctypes.byref(problem), int(op)))
+
+
+# ---------------------------------------------------------------------------
+# torch-side marshalling
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(dt):
+    torch = _torch()
+    if dt == torch.bfloat16:
+        return RLA_BF16
+    if dt == torch.float32:
+        return RLA_F32
+    raise TypeError("dtype must be bfloat16 or float32")
+
+
+def make_problem(q, v, cu_seqlens=None, clip: float = 1.0, out_dtype=None) -> rla_problem:
+    """rla_problem for q [B,T,H,dk] / [T,H,dk] and v, with optional cu_seqlens.
+    out_dtype (dtype of o, dq, dk, dv) defaults to float32."""
+    torch = _torch()
+    if q.dtype == torch.bfloat16:
+        dtype = RLA_BF16
+    elif q.dtype == torch.float32:
+        dtype = RLA_F32
+    else:
+        raise TypeError("q, k, v must be bfloat16 or float32")
+    if q.dim() == 4:
+        B, T, H, dk = q.shape
+    elif q.dim() == 3:
+        B, (T, H, dk) = 1, q.shape
+    else:
+        raise ValueError("q must be [B, T, H, d_k] or [T, H, d_k]")
+    dv = v.shape[-1]
+    N = 0
+    if cu_seqlens is not None:
+        if B != 1:
+            raise ValueError("cu_seqlens requires B == 1")
+        if cu_seqlens.dtype != torch.int32 or not cu_seqlens.is_cuda:
+            raise TypeError("cu_seqlens must be an int32 device tensor")
+        N = cu_seqlens.numel() - 1
+    c = math.inf if clip is None else float(clip)
+    out = _dtype_code(torch.float32 if out_dtype is None else out_dtype)
+    return rla_problem(B, T, H, dk, dv, N, _ptr(cu_seqlens), dtype, c, out)
+
+
+def _check(tensors, device):
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if t.device != device:
+            raise ValueError("%s must be on %s" % (name, device))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+
+
+def _workspace(problem, op, device, workspace):
+    torch = _torch()
+    need = rla_workspace_size(problem, op)
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError("workspace too small: need %d bytes" % need)
+        return workspace, need
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=device), need
+
+
+def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_seqlens,
+             out, workspace, stream, return_states, out_dtype):
+    torch = _torch()
+    lib = load_library()
+    problem = make_problem(q, v, cu_seqlens, clip, out_dtype)
+    dev = q.device
+    _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
+                S0=S0, R0=R0), dev)
+    for t in (alpha_s, beta, alpha_r, gamma, S0, R0):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("gates and states must be float32")
+    N = problem.num_seqs if cu_seqlens is not None else problem.batch
+    odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
+    o = torch.empty(v.shape, dtype=odt, device=dev) if out is None else out
+    if o.dtype != odt or o.shape != v.shape:
+        raise ValueError("out must be %s with shape %s" % (odt, tuple(v.shape)))
+    Sf = Rf = None
+    if return_states:
+        shape = (N, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
+        Sf = torch.empty(shape, dtype=torch.float32, device=dev)
+        Rf = torch.empty(shape, dtype=torch.float32, device=dev)
+    ws, need = _workspace(problem, op, dev, workspace)
+    st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
+                            _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S0), _ptr(R0), _ptr(o),
+                            _ptr(Sf), _ptr(Rf), _ptr(ws), ws.numel(), _stream_handle(stream))
+    if st != RLA_OK:
+        raise RLAError(st, name)
+    return o, Sf, Rf
+
+
+def rla_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
+                cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
+                out_dtype=None):
+    """RLA forward (Sec. 3.4, left box).  Returns (o, S_final, R_final)."""
+    return _forward("rla_forward", RLA_OP_RLA_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
+                    clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype)
+
+
+def rdn_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
+                cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
+                out_dtype=None):
+    """RDN forward (Sec. 3.4, right box).  Returns (o, S_final, R_final)."""
+    return _forward("rdn_forward", RLA_OP_RDN_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
+                    clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype)
+
+
+def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
+                 R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
+                 stream=None, grads=None, out_dtype=None):
+    """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rdn_forward.
+    Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0."""
+    torch = _torch()
+    lib = load_library()
+    problem = make_problem(q, v, cu_seqlens, clip, out_dtype)
+    dev = q.device
+    _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
+                S0=S0, R0=R0, dO=dO, dS_final=dS_final, dR_final=dR_final), dev)
+    if dO.dtype != q.dtype:
+        raise TypeError("dO must have the dtype of q, k, v")
+    odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
+    N = problem.num_seqs if cu_seqlens is not None else problem.batch
+    if grads is None:
+        shape = (N, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
+        grads = dict(dq=torch.empty(q.shape, dtype=odt, device=dev),
+                     dk=torch.empty(k.shape, dtype=odt, device=dev),
+                     dv=torch.empty(v.shape, dtype=odt, device=dev),
+                     dalpha_s=torch.empty_like(alpha_s), dbeta=torch.empty_like(beta),
+                     dalpha_r=torch.empty_like(alpha_r), dgamma=torch.empty_like(gamma),
+                     dS0=torch.empty(shape, dtype=torch.float32, device=dev),
+                     dR0=torch.empty(shape, dtype=torch.float32, device=dev))
+    ws, need = _workspace(problem, RLA_OP_RDN_BACKWARD, dev, workspace)
+    g = grads
+    st = lib.rdn_backward(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
+                          _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S0), _ptr(R0), _ptr(dO),
+                          _ptr(dS_final), _ptr(dR_final), _ptr(g["dq"]), _ptr(g["dk"]),
+                          _ptr(g["dv"]), _ptr(g["dalpha_s"]), _ptr(g["dbeta"]),
+                          _ptr(g["dalpha_r"]), _ptr(g["dgamma"]), _ptr(g.get("dS0")),
+                          _ptr(g.get("dR0")), _ptr(ws), ws.numel(), _stream_handle(stream))
+    if st != RLA_OK:
+        raise RLAError(st, "rdn_backward")
+    return g

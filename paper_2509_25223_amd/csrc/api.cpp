@@ -1,0 +1,281 @@
+// Host side of the C ABI declared in include/rla.h: argument validation (no
+// HIP call until it passes), workspace planning and launch sequencing.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+#include "rla.h"
+
+namespace rla {
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Problem {
+  int64_t B = 0, T = 0, H = 0, DK = 0, DV = 0, N = 0, ntok = 0, max_chunks = 0;
+  bool varlen = false, bf16 = false, out_bf16 = false;
+  const int32_t* cu = nullptr;
+  float clip = -1.f;
+};
+
+struct Workspace {
+  size_t seqs = 0, chunks = 0, nchunks = 0, order = 0, gates = 0, mats = 0;
+  size_t ckS = 0, ckR = 0, mask = 0, dS = 0, dR = 0, total = 0;
+};
+
+rla_status check_problem(const rla_problem* pp, Problem& pr) {
+  if (!pp) return RLA_ERR_NULL_ARG;
+  if (pp->dtype != RLA_F32 && pp->dtype != RLA_BF16) return RLA_ERR_DTYPE;
+  if (pp->batch < 0 || pp->seq_len < 0 || pp->num_heads < 1) return RLA_ERR_SHAPE;
+  if (pp->num_heads > 65535) return RLA_ERR_SHAPE;
+  const bool dk_ok = pp->head_dim_k == 64 || pp->head_dim_k == 128;
+  const bool dv_ok = pp->head_dim_v == 64 || pp->head_dim_v == 128;
+  if (!dk_ok || !dv_ok) return RLA_ERR_SHAPE;
+  if (pp->dtype == RLA_F32 && pp->head_dim_k != 64) return RLA_ERR_DTYPE;
+  if (pp->out_dtype != RLA_F32 && pp->out_dtype != RLA_BF16) return RLA_ERR_DTYPE;
+  if (pp->dtype == RLA_F32 && pp->out_dtype != RLA_F32) return RLA_ERR_DTYPE;
+  if (isnan(pp->clip) || pp->clip < 0.f) return RLA_ERR_VALUE;
+  pr.B = pp->batch;
+  pr.T = pp->seq_len;
+  pr.H = pp->num_heads;
+  pr.DK = pp->head_dim_k;
+  pr.DV = pp->head_dim_v;
+  pr.bf16 = pp->dtype == RLA_BF16;
+  pr.out_bf16 = pp->out_dtype == RLA_BF16;
+  pr.clip = isinf(pp->clip) ? -1.f : pp->clip;
+  pr.cu = pp->cu_seqlens;
+  pr.varlen = pp->cu_seqlens != nullptr;
+  if (pr.varlen) {
+    if (pr.B != 1 || pp->num_seqs < 0 || pp->num_seqs > (int64_t)1 << 30) return RLA_ERR_SHAPE;
+    pr.N = pp->num_seqs;
+    pr.ntok = pr.T;
+    pr.max_chunks = pr.N == 0 ? 0 : (pr.T + kChunk - 1) / kChunk + pr.N;
+  } else {
+    pr.N = pr.B;
+    if (pr.T > 0 && pr.B > INT64_MAX / pr.T) return RLA_ERR_SHAPE;
+    pr.ntok = pr.B * pr.T;
+    pr.max_chunks = pr.B * ((pr.T + kChunk - 1) / kChunk);
+  }
+  if (pr.max_chunks > INT32_MAX / 2 || pr.N * pr.H > INT32_MAX / 8) return RLA_ERR_SHAPE;
+  return RLA_OK;
+}
+
+Workspace plan(const Problem& pr, int op) {
+  Workspace w;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes);
+    return at;
+  };
+  const size_t mc = (size_t)pr.max_chunks, H = (size_t)pr.H;
+  if (pr.varlen) {
+    w.seqs = take(sizeof(SeqInfo) * (size_t)pr.N);
+    w.chunks = take(sizeof(ChunkInfo) * mc);
+    w.nchunks = take(sizeof(int32_t));
+    w.order = take(sizeof(int32_t) * (size_t)pr.N);
+  }
+  w.gates = take(sizeof(float) * mc * H * kGateBlock);
+  w.mats = take((pr.bf16 ? 2 : 4) * mc * H * kNumMats * kMatElems);
+  if (op == RLA_OP_RDN_BACKWARD) {
+    const size_t st = sizeof(float) * mc * H * (size_t)pr.DK * (size_t)pr.DV;
+    w.ckS = take(st);
+    w.ckR = take(st);
+    w.mask = take((size_t)pr.ntok * H * (size_t)pr.DV);
+    w.dS = take(st);
+    w.dR = take(st);
+  }
+  w.total = off;
+  return w;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+rla_status to_status(hipError_t e) { return e == hipSuccess ? RLA_OK : RLA_ERR_HIP; }
+
+// Common set-up of OpParams from a validated problem and a workspace.
+OpParams make_params(const Problem& pr, const Workspace& w, unsigned char* ws, bool rdn) {
+  OpParams p;
+  p.H = (int32_t)pr.H;
+  p.DK = (int32_t)pr.DK;
+  p.DV = (int32_t)pr.DV;
+  p.ntok = pr.ntok;
+  p.clip = pr.clip;
+  p.rdn = rdn ? 1 : 0;
+  p.out_bf16 = pr.out_bf16 ? 1 : 0;
+  p.max_chunks = (int32_t)pr.max_chunks;
+  p.st.nseq = (int32_t)pr.N;
+  if (pr.varlen) {
+    p.st.dense_T = -1;
+    p.st.dense_nch = 0;
+    p.st.seqs = reinterpret_cast<const SeqInfo*>(ws + w.seqs);
+    p.st.chunks = reinterpret_cast<const ChunkInfo*>(ws + w.chunks);
+    p.st.nchunks = reinterpret_cast<const int32_t*>(ws + w.nchunks);
+    p.st.order = reinterpret_cast<const int32_t*>(ws + w.order);
+  } else {
+    p.st.dense_T = pr.T;
+    p.st.dense_nch = (int32_t)((pr.T + kChunk - 1) / kChunk);
+  }
+  p.gate_ws = reinterpret_cast<float*>(ws + w.gates);
+  p.mat_ws = ws + w.mats;
+  return p;
+}
+
+rla_status check_workspace(const Workspace& w, void* ws, size_t bytes) {
+  if (w.total == 0) return RLA_OK;
+  if (!ws || bytes < w.total) return RLA_ERR_WORKSPACE;
+  if (((uintptr_t)ws & (kAlign - 1)) != 0) return RLA_ERR_VALUE;
+  return RLA_OK;
+}
+
+hipError_t build_tables(const Problem& pr, const Workspace& w, unsigned char* ws,
+                        hipStream_t stream) {
+  if (!pr.varlen || pr.N == 0) return hipSuccess;
+  return launch_seq_table(pr.cu, (int32_t)pr.N, pr.ntok, (int32_t)pr.max_chunks,
+                          reinterpret_cast<SeqInfo*>(ws + w.seqs),
+                          reinterpret_cast<ChunkInfo*>(ws + w.chunks),
+                          reinterpret_cast<int32_t*>(ws + w.nchunks),
+                          reinterpret_cast<int32_t*>(ws + w.order), stream);
+}
+
+rla_status forward(bool rdn, const rla_problem* problem, const void* q, const void* k,
+                   const void* v, const float* alpha_s, const float* beta, const float* alpha_r,
+                   const float* gamma, const float* S0, const float* R0, void* o, float* S_final,
+                   float* R_final, void* workspace, size_t workspace_bytes, void* stream_) {
+  Problem pr;
+  rla_status st = check_problem(problem, pr);
+  if (st != RLA_OK) return st;
+  if (pr.ntok > 0 && (!q || !k || !v || !alpha_s || !beta || !alpha_r || !gamma || !o))
+    return RLA_ERR_NULL_ARG;
+  if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)))
+    return RLA_ERR_VALUE;
+  const Workspace w = plan(pr, rdn ? RLA_OP_RDN_FORWARD : RLA_OP_RLA_FORWARD);
+  st = check_workspace(w, workspace, workspace_bytes);
+  if (st != RLA_OK) return st;
+  if (pr.N == 0) return RLA_OK;
+
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);
+  OpParams p = make_params(pr, w, ws, rdn);
+  p.q = q; p.k = k; p.v = v;
+  p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
+  p.S0 = S0; p.R0 = R0;
+  p.o = o; p.S_fin = S_final; p.R_fin = R_final;
+
+  hipError_t e = hipSuccess;
+  if (pr.varlen && pr.ntok > 0)   // tokens outside every sequence read as zero
+    e = hipMemsetAsync(o, 0, (size_t)pr.ntok * pr.H * pr.DV * (pr.out_bf16 ? 2 : 4), stream);
+  if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
+  if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
+  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/true, /*ckpt=*/false, stream);
+  return to_status(e);
+}
+
+}  // namespace
+}  // namespace rla
+
+using namespace rla;
+
+extern "C" {
+
+size_t rla_workspace_size(const rla_problem* problem, int op) {
+  Problem pr;
+  if (check_problem(problem, pr) != RLA_OK) return 0;
+  if (op != RLA_OP_RLA_FORWARD && op != RLA_OP_RDN_FORWARD && op != RLA_OP_RDN_BACKWARD) return 0;
+  return plan(pr, op).total;
+}
+
+const char* rla_status_string(rla_status s) {
+  switch (s) {
+    case RLA_OK: return "ok";
+    case RLA_ERR_NULL_ARG: return "required pointer is NULL";
+    case RLA_ERR_SHAPE: return "unsupported or inconsistent shape";
+    case RLA_ERR_DTYPE: return "unsupported dtype for this shape";
+    case RLA_ERR_UNSUPPORTED: return "not implemented";
+    case RLA_ERR_WORKSPACE: return "workspace missing or too small";
+    case RLA_ERR_VALUE: return "bad scalar argument or misaligned pointer";
+    case RLA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+rla_status rla_forward(const rla_problem* problem, const void* q, const void* k, const void* v,
+                       const float* alpha_s, const float* beta, const float* alpha_r,
+                       const float* gamma, const float* S0, const float* R0, void* o,
+                       float* S_final, float* R_final, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  return forward(false, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, o, S_final,
+                 R_final, workspace, workspace_bytes, stream);
+}
+
+rla_status rdn_forward(const rla_problem* problem, const void* q, const void* k, const void* v,
+                       const float* alpha_s, const float* beta, const float* alpha_r,
+                       const float* gamma, const float* S0, const float* R0, void* o,
+                       float* S_final, float* R_final, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  return forward(true, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, o, S_final,
+                 R_final, workspace, workspace_bytes, stream);
+}
+
+rla_status rdn_backward(const rla_problem* problem, const void* q, const void* k, const void* v,
+                        const float* alpha_s, const float* beta, const float* alpha_r,
+                        const float* gamma, const float* S0, const float* R0, const void* dO,
+                        const float* dS_final, const float* dR_final, void* dq, void* dk,
+                        void* dv, float* dalpha_s, float* dbeta, float* dalpha_r, float* dgamma,
+                        float* dS0, float* dR0, void* workspace, size_t workspace_bytes,
+                        void* stream_) {
+  Problem pr;
+  rla_status st = check_problem(problem, pr);
+  if (st != RLA_OK) return st;
+  if (pr.ntok > 0 && (!q || !k || !v || !alpha_s || !beta || !alpha_r || !gamma || !dO ||
+                      !dq || !dk || !dv || !dalpha_s || !dbeta || !dalpha_r || !dgamma))
+    return RLA_ERR_NULL_ARG;
+  if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) ||
+                      !aligned16(dq) || !aligned16(dk) || !aligned16(dv)))
+    return RLA_ERR_VALUE;
+  const Workspace w = plan(pr, RLA_OP_RDN_BACKWARD);
+  st = check_workspace(w, workspace, workspace_bytes);
+  if (st != RLA_OK) return st;
+  if (pr.N == 0) return RLA_OK;
+
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);
+  OpParams p = make_params(pr, w, ws, true);
+  p.q = q; p.k = k; p.v = v;
+  p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
+  p.S0 = S0; p.R0 = R0;
+  p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
+  p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
+  p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
+  p.dS_ws = reinterpret_cast<float*>(ws + w.dS);
+  p.dR_ws = reinterpret_cast<float*>(ws + w.dR);
+  p.dO = dO; p.dS_fin = dS_final; p.dR_fin = dR_final;
+  p.dq = dq; p.dk = dk; p.dv = dv;
+  p.dalpha_s = dalpha_s; p.dbeta = dbeta; p.dalpha_r = dalpha_r; p.dgamma = dgamma;
+  p.dS0 = dS0; p.dR0 = dR0;
+
+  hipError_t e = hipSuccess;
+  if (pr.varlen && pr.ntok > 0) {   // tokens outside every sequence get zero gradients
+    const size_t el = pr.out_bf16 ? 2 : 4, tok = (size_t)pr.ntok * pr.H;
+    e = hipMemsetAsync(dq, 0, tok * pr.DK * el, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dk, 0, tok * pr.DK * el, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dv, 0, tok * pr.DV * el, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dalpha_s, 0, tok * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dbeta, 0, tok * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dalpha_r, 0, tok * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dgamma, 0, tok * 4, stream);
+  }
+  if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
+  if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
+  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/false, /*ckpt=*/true, stream);
+  if (e == hipSuccess) e = launch_bwd_scan(p, pr.bf16, stream);
+  if (e == hipSuccess) e = launch_bwd_grad(p, pr.bf16, stream);
+  return to_status(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,307 @@
+// Device-side building blocks shared by the gfx950 kernels: element types,
+// bf16 conversion, MFMA fragment loads from LDS, and the per-launch
+// descriptors of sequences and chunks.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rla {
+
+constexpr int kChunk = 64;      // tokens per chunk
+constexpr int kThreads = 256;   // 4 waves of 64 lanes per workgroup
+constexpr int kWaves = 4;
+
+typedef unsigned short u16;     // bf16 bit pattern
+typedef _Float16 f16;           // fp16
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef u16 u16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef u16 u16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ float bf2f(u16 x) { return __uint_as_float(((uint32_t)x) << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ u16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7f800000u) == 0x7f800000u) return (u16)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (u16)(u >> 16);
+}
+
+// Conversions between the storage type of an operand and fp32.
+template <typename T> __device__ __forceinline__ float to_f(T x);
+template <> __device__ __forceinline__ float to_f<float>(float x) { return x; }
+template <> __device__ __forceinline__ float to_f<u16>(u16 x) { return bf2f(x); }
+template <> __device__ __forceinline__ float to_f<f16>(f16 x) { return (float)x; }
+template <typename T> __device__ __forceinline__ T from_f(float x);
+template <> __device__ __forceinline__ float from_f<float>(float x) { return x; }
+template <> __device__ __forceinline__ u16 from_f<u16>(float x) { return f2bf(x); }
+template <> __device__ __forceinline__ f16 from_f<f16>(float x) { return (f16)x; }
+
+// bf16 residual of x after its bf16 rounding hi: x ~= hi + lo to ~16 bits,
+// with fp32 range.  Used for state operands (split-bf16 products).
+__device__ __forceinline__ u16 bf16_lo(float x, u16 hi) { return f2bf(x - bf2f(hi)); }
+
+// ---------------------------------------------------------------------------
+// MFMA 16x16 tiles.  One wave computes D[16 x 16] += A[16 x K] * B[K x 16].
+//   bf16 (T = u16): v_mfma_f32_16x16x32_bf16, 8 k-values per lane per step.
+//   fp32 (T = float): v_mfma_f32_16x16x4_f32, 1 k-value per lane per step.
+// A lane supplies row/column (lane & 15) and k-group (lane >> 4) of both
+// operands; the sum over k does not depend on which k a (group, slot) pair
+// stands for as long as A and B agree, so the k-order inside a step is ours.
+// The result lane holds D[4 * (lane >> 4) + r][lane & 15], r = 0..3.
+//
+// Operands live in LDS and are addressed as logical (r, k) with r the output
+// row (A) or column (B) inside the tile:
+//   KC layout: element (r, k) at base[r * ld + k]  (k contiguous, vector loads)
+//   KS layout: element (r, k) at base[k * ld + r]  (r contiguous, gathers)
+// ---------------------------------------------------------------------------
+template <typename T> struct Mfma;
+
+template <> struct Mfma<u16> {
+  static constexpr int kStep = 32;
+  typedef bf16x8 frag;
+  template <bool KC>
+  __device__ __forceinline__ static frag load(const u16* base, int ld, int k0) {
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 15, kg = (lane >> 4) * 8;
+    if constexpr (KC) {
+      const u16x8 v = *reinterpret_cast<const u16x8*>(base + r * ld + k0 + kg);
+      return __builtin_bit_cast(frag, v);
+    } else {
+      u16x8 v;
+      const u16* p = base + (k0 + kg) * ld + r;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = p[e * ld];
+      return __builtin_bit_cast(frag, v);
+    }
+  }
+  __device__ __forceinline__ static floatx4 mma(frag a, frag b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mfma<f16> {
+  static constexpr int kStep = 32;
+  typedef f16x8 frag;
+  template <bool KC>
+  __device__ __forceinline__ static frag load(const f16* base, int ld, int k0) {
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 15, kg = (lane >> 4) * 8;
+    if constexpr (KC) {
+      return *reinterpret_cast<const frag*>(base + r * ld + k0 + kg);
+    } else {
+      frag v;
+      const f16* p = base + (k0 + kg) * ld + r;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = p[e * ld];
+      return v;
+    }
+  }
+  __device__ __forceinline__ static floatx4 mma(frag a, frag b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mfma<float> {
+  static constexpr int kStep = 4;
+  typedef float frag;
+  template <bool KC>
+  __device__ __forceinline__ static frag load(const float* base, int ld, int k0) {
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 15, kg = lane >> 4;
+    if constexpr (KC) return base[r * ld + k0 + kg];
+    else return base[(k0 + kg) * ld + r];
+  }
+  __device__ __forceinline__ static floatx4 mma(frag a, frag b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
+// fp16 MFMA with a 16-deep k step (v_mfma_f32_16x16x16_f16): 4 k-values per
+// lane, for contractions over 16-wide blocks.  fp32 uses the 4-deep fp32 MFMA.
+template <typename T> struct MfmaK16;
+
+template <> struct MfmaK16<f16> {
+  static constexpr int kStep = 16;
+  typedef f16x4 frag;
+  template <bool KC>
+  __device__ __forceinline__ static frag load(const f16* base, int ld, int k0) {
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 15, kg = (lane >> 4) * 4;
+    if constexpr (KC) {
+      return *reinterpret_cast<const frag*>(base + r * ld + k0 + kg);
+    } else {
+      frag v;
+      const f16* p = base + (k0 + kg) * ld + r;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = p[e * ld];
+      return v;
+    }
+  }
+  __device__ __forceinline__ static floatx4 mma(frag a, frag b, floatx4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16f16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct MfmaK16<float> : Mfma<float> {};
+
+// acc += A(16 x K) * B(K x 16) with the MFMA traits M.
+template <class M, int K, bool AKC, bool BKC, typename T>
+__device__ __forceinline__ void mma_with(floatx4& acc, const T* A, int lda, const T* B, int ldb) {
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += M::kStep) {
+    acc = M::mma(M::template load<AKC>(A, lda, k0), M::template load<BKC>(B, ldb, k0), acc);
+  }
+}
+
+// acc += A(16 x K) * B(K x 16); A and B point at the tile's first row/column.
+template <typename T, int K, bool AKC, bool BKC>
+__device__ __forceinline__ void mma_tile(floatx4& acc, const T* A, int lda, const T* B, int ldb) {
+  typedef Mfma<T> M;
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += M::kStep) {
+    acc = M::mma(M::template load<AKC>(A, lda, k0), M::template load<BKC>(B, ldb, k0), acc);
+  }
+}
+
+// acc += A * B with the A fragments already in registers (afr[k-step]).
+template <typename T, int K, bool BKC>
+__device__ __forceinline__ void mma_rega(floatx4& acc, const typename Mfma<T>::frag* afr,
+                                        const T* B, int ldb) {
+  typedef Mfma<T> M;
+#pragma unroll
+  for (int s = 0; s < K / M::kStep; ++s)
+    acc = M::mma(afr[s], M::template load<BKC>(B, ldb, s * M::kStep), acc);
+}
+
+// A-operand fragments of a 16-row tile straight from global memory: this
+// lane's row pointer (nullptr -> zero row), row-major with k contiguous.
+template <typename T, int K>
+__device__ __forceinline__ void load_rowfrags(typename Mfma<T>::frag* afr, const T* row) {
+  typedef Mfma<T> M;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int s = 0; s < K / M::kStep; ++s) {
+    if constexpr (sizeof(T) == 2) {
+      const int k = s * M::kStep + (lane >> 4) * 8;
+      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (row) v = *reinterpret_cast<const u16x8*>(row + k);
+      afr[s] = __builtin_bit_cast(typename M::frag, v);
+    } else {
+      const int k = s * M::kStep + (lane >> 4);
+      afr[s] = row ? row[k] : 0.f;
+    }
+  }
+}
+
+__device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
+
+// Row (inside a 16-row tile) and column of accumulator element r of this lane.
+__device__ __forceinline__ int acc_row(int r) { return 4 * ((threadIdx.x & 63) >> 4) + r; }
+__device__ __forceinline__ int acc_col() { return threadIdx.x & 15; }
+
+// Stores the 4 accumulator rows of this lane, column-major into LDS as a
+// transposed tile: dst[col * ld + row]  (4 consecutive elements).
+template <typename T>
+__device__ __forceinline__ void store_acc_t(T* dst, int ld, floatx4 v) {
+  T* p = dst + acc_col() * ld + acc_row(0);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) p[r] = from_f<T>(v[r]);
+}
+
+// Stores the 4 accumulator rows of this lane into LDS row-major: dst[row * ld + col].
+template <typename T>
+__device__ __forceinline__ void store_acc(T* dst, int ld, floatx4 v) {
+  T* p = dst + acc_row(0) * ld + acc_col();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) p[r * ld] = from_f<T>(v[r]);
+}
+
+// ---------------------------------------------------------------------------
+// Sequences and chunks.  Either B dense sequences of length T (dense_T >= 0)
+// or a device table built from cu_seqlens.
+// ---------------------------------------------------------------------------
+struct SeqInfo {     // one per sequence, in the device table
+  int64_t start;
+  int32_t len;
+  int32_t chunk0;    // global index of the sequence's first chunk
+};
+
+struct ChunkInfo {   // one per chunk, in the device table
+  int64_t tok;       // first token
+  int32_t len;       // tokens in the chunk (1..64)
+  int32_t seq;
+};
+
+struct SeqTable {
+  int64_t dense_T;          // >= 0: dense layout with this T; < 0: use tables
+  int32_t nseq;             // number of sequences
+  int32_t dense_nch;        // chunks per dense sequence
+  const SeqInfo* seqs;      // [nseq]            (varlen)
+  const ChunkInfo* chunks;  // [max_chunks]      (varlen)
+  const int32_t* nchunks;   // total chunks      (varlen)
+  const int32_t* order;     // [nseq] sequences, longest first (varlen)
+};
+
+__device__ __forceinline__ SeqInfo seq_info(const SeqTable& t, int n) {
+  if (t.dense_T >= 0) return SeqInfo{(int64_t)n * t.dense_T, (int32_t)t.dense_T, n * t.dense_nch};
+  return t.seqs[n];
+}
+
+__device__ __forceinline__ int seq_order(const SeqTable& t, int i) {
+  return t.dense_T >= 0 ? i : t.order[i];
+}
+
+// Returns false if c is past the last chunk.
+__device__ __forceinline__ bool chunk_info(const SeqTable& t, int c, ChunkInfo& out) {
+  if (t.dense_T >= 0) {
+    if (t.dense_nch == 0) return false;
+    const int n = c / t.dense_nch, j = c % t.dense_nch;
+    if (n >= t.nseq) return false;
+    const int64_t tok = (int64_t)n * t.dense_T + (int64_t)j * kChunk;
+    const int64_t rem = t.dense_T - (int64_t)j * kChunk;
+    out = ChunkInfo{tok, (int32_t)(rem < kChunk ? rem : kChunk), n};
+    return true;
+  }
+  if (c >= *t.nchunks) return false;
+  out = t.chunks[c];
+  return true;
+}
+
+// Decay logarithm with the documented floor 2^-126 on the decay.
+__device__ __forceinline__ float log_decay(float a) { return __logf(fmaxf(a, 1.17549435e-38f)); }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ float wave_inclusive_scan(float x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float y = __shfl_up(x, off, 64);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+// Gate block of one (chunk, head), as written by the prep kernel:
+//   [0..63] g  : inclusive cumulative log-decay of S inside the chunk
+//   [64..]  h  : same for R
+//   [128..] beta, [192..] gamma  (0 on padding rows)
+constexpr int kGateBlock = 4 * kChunk;
+
+// Matrices of one (chunk, head), as written by the prep kernel, each 64 x 64
+// row-major (row = query token t, column = key token s):
+enum : int {
+  kMatTS = 0,   // T^S = (I + A^S)^{-1}                     (RDN only)
+  kMatMG = 1,   // e^{g_{t-1} - g_s} (k_t . k_s)       s < t
+  kMatMP = 2,   // e^{g_t - g_s}     (q_t . k_s)       s < t
+  kMatTR = 3,   // T^R = (I + A^R)^{-1}                     (RDN only)
+  kMatMR = 4,   // e^{h_t - h_s}     (q_t . k_s)       s <= t
+  kNumMats = 5
+};
+constexpr int kMatElems = kChunk * kChunk;
+
+}  // namespace rla

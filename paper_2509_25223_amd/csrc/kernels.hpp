@@ -1,0 +1,79 @@
+// Internal interface between the host API (api.cpp) and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace rla {
+
+// Everything a launch needs; passed by value to the kernels.
+struct OpParams {
+  int32_t H = 0, DK = 0, DV = 0;
+  int64_t ntok = 0;
+  float clip = -1.f;            // < 0: no clipping
+  int32_t rdn = 1;              // 1: RDN, 0: RLA
+  int32_t out_bf16 = 0;         // o, dq, dk, dv in bf16 (else fp32)
+  int32_t max_chunks = 0;       // upper bound on chunks (grid size of chunk-parallel kernels)
+  SeqTable st{};
+
+  const void* q = nullptr;
+  const void* k = nullptr;
+  const void* v = nullptr;
+  const float* alpha_s = nullptr;
+  const float* beta = nullptr;
+  const float* alpha_r = nullptr;
+  const float* gamma = nullptr;
+  const float* S0 = nullptr;
+  const float* R0 = nullptr;
+
+  void* o = nullptr;
+  float* S_fin = nullptr;
+  float* R_fin = nullptr;
+
+  // workspace regions
+  float* gate_ws = nullptr;     // [max_chunks][H][kGateBlock]
+  void* mat_ws = nullptr;       // [max_chunks][H][kNumMats][64][64]  (mm type)
+  float* ck_S = nullptr;        // [max_chunks][H][DK][DV] chunk-start S
+  float* ck_R = nullptr;        // [max_chunks][H][DK][DV] chunk-start R
+  uint8_t* ck_mask = nullptr;   // [ntok][H][DV] 1 where |x| <= clip
+  float* dS_ws = nullptr;       // [max_chunks][H][DK][DV] grad of chunk-end S
+  float* dR_ws = nullptr;       // [max_chunks][H][DK][DV] grad of chunk-end R
+
+  // backward
+  const void* dO = nullptr;
+  const float* dS_fin = nullptr;
+  const float* dR_fin = nullptr;
+  void* dq = nullptr;
+  void* dk = nullptr;
+  void* dv = nullptr;
+  float* dalpha_s = nullptr;
+  float* dbeta = nullptr;
+  float* dalpha_r = nullptr;
+  float* dgamma = nullptr;
+  float* dS0 = nullptr;
+  float* dR0 = nullptr;
+};
+
+// Builds SeqInfo / ChunkInfo / order tables from device cu_seqlens.
+hipError_t launch_seq_table(const int32_t* cu, int32_t nseq, int64_t ntok, int32_t max_chunks,
+                            SeqInfo* seqs, ChunkInfo* chunks, int32_t* nchunks, int32_t* order,
+                            hipStream_t stream);
+
+// Chunk-parallel preparation: gate cumsums, masked decayed Gram/score
+// matrices and (RDN) the two triangular inverses.
+hipError_t launch_prep(const OpParams& p, bool bf16, hipStream_t stream);
+
+// Forward state-passing scan.  write_o: produce o; ckpt: store chunk-start
+// states and clip masks for the backward.
+hipError_t launch_fwd_scan(const OpParams& p, bool bf16, bool write_o, bool ckpt,
+                           hipStream_t stream);
+
+// Reverse state-gradient scan (RDN / RLA).
+hipError_t launch_bwd_scan(const OpParams& p, bool bf16, hipStream_t stream);
+
+// Chunk-parallel gradient contractions.
+hipError_t launch_bwd_grad(const OpParams& p, bool bf16, hipStream_t stream);
+
+}  // namespace rla

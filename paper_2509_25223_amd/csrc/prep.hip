@@ -1,0 +1,239 @@
+// Chunk-parallel, state-independent work of one (chunk, head): one 256-thread
+// workgroup per pair.
+//
+// For chunk tokens t, s = 0..63 (paper Sec. 3.4 recurrences, written in the
+// chunk form; padding rows beyond the chunk's length carry k = q = 0,
+// beta = gamma = 0 and decay 1, which makes them exact no-ops):
+//   g_t = sum_{j<=t} log aS_j,  h_t = sum_{j<=t} log aR_j
+//   Gram G = K K^T and scores P = Q K^T on bf16 (or fp32) MFMA
+//   MG[t][s] = e^{g_{t-1}-g_s} G[t][s]  (s < t)   -> S_{t-1} k_t read-out
+//   MP[t][s] = e^{g_t - g_s}   P[t][s]  (s < t)   -> aS_t S_{t-1} q_t read-out
+//   MR[t][s] = e^{h_t - h_s}   P[t][s]  (s <= t)  -> R_t q_t read-out
+//   RDN only: the delta rule S_t = aS_t S_{t-1}(I - b_t k_t k_t^T) + b_t v_t k_t^T
+//   makes the chunk's corrections U solve (I + A^S) U = rhs with
+//   A^S[t][s] = b_t e^{g_t-g_s} G[t][s] (s < t); likewise A^R with (gamma, h).
+//   T^S = (I + A^S)^{-1} and T^R = (I + A^R)^{-1} are formed here in fp32 by
+//   blocked forward substitution (16 x 16 diagonal blocks, then block rows).
+// All exponents are of differences g_t - g_s <= 0 (never e^{g} e^{-g}).
+#include <type_traits>
+
+#include "kernels.hpp"
+
+namespace rla {
+
+namespace {
+
+template <typename T, int DK>
+struct PrepLayout {
+  static constexpr int kLdK = DK + (sizeof(T) == 2 ? 8 : 4);   // Kc / Qc row stride
+  static constexpr int kLdA = kChunk + 1;                       // fp32 64x64 scratch stride
+  // region 0: Kc, Qc (T) -- later reused by As, Ar, Ts, Tr (fp32)
+  static constexpr int kBytesKQ = 2 * kChunk * kLdK * (int)sizeof(T);
+  static constexpr int kBytesA = 4 * kChunk * kLdA * 4;
+  static constexpr int kBytes0 = kBytesKQ > kBytesA ? kBytesKQ : kBytesA;
+  static constexpr int kBytesW = 6 * 256 * 4;                   // block products
+  static constexpr int kBytesGates = 5 * kChunk * 4;
+  static constexpr int kBytes = kBytes0 + kBytesW + kBytesGates;
+  static_assert(kBytes <= 160 * 1024, "prep LDS");
+};
+
+// Inverse of the unit lower-triangular I + A (A strictly lower, fp32, ld = kLdA)
+// for two matrices at once: A0 -> T0, A1 -> T1.  256 threads.
+__device__ void invert_unit_lower_pair(const float* A0, const float* A1, float* T0, float* T1,
+                                       float* W) {
+  constexpr int ld = kChunk + 1;
+  const int tid = threadIdx.x;
+  // zero both inverses
+  for (int e = tid; e < kChunk * kChunk; e += kThreads) {
+    const int r = e / kChunk, c = e % kChunk;
+    T0[r * ld + c] = 0.f;
+    T1[r * ld + c] = 0.f;
+  }
+  __syncthreads();
+  // diagonal 16 x 16 blocks: thread = (matrix, block, column)
+  if (tid < 128) {
+    const int mat = tid >> 6, blk = (tid >> 4) & 3, c = tid & 15;
+    const float* A = (mat ? A1 : A0) + (16 * blk) * ld + 16 * blk;
+    float* T = (mat ? T1 : T0) + (16 * blk) * ld + 16 * blk;
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float acc = (i == c) ? 1.f : 0.f;
+#pragma unroll
+      for (int k = 0; k < i; ++k) acc -= A[i * ld + k] * x[k];
+      x[i] = (i < c) ? 0.f : acc;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) T[i * ld + c] = x[i];
+  }
+  __syncthreads();
+  // block rows bi = 1..3: T[bi][bj] = -T[bi][bi] * sum_{m=bj}^{bi-1} A[bi][m] T[m][bj]
+  for (int bi = 1; bi < 4; ++bi) {
+    const int nblk = 2 * bi;   // (matrix, bj) pairs
+    for (int e = tid; e < nblk * 256; e += kThreads) {
+      const int blk = e >> 8, mat = blk / bi, bj = blk % bi;
+      const int r = (e >> 4) & 15, c = e & 15;
+      const float* A = mat ? A1 : A0;
+      const float* T = mat ? T1 : T0;
+      float acc = 0.f;
+      for (int m = bj; m < bi; ++m) {
+        const float* arow = A + (16 * bi + r) * ld + 16 * m;
+        const float* tcol = T + (16 * m) * ld + 16 * bj + c;
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) acc += arow[kk] * tcol[kk * ld];
+      }
+      W[e] = acc;
+    }
+    __syncthreads();
+    for (int e = tid; e < nblk * 256; e += kThreads) {
+      const int blk = e >> 8, mat = blk / bi, bj = blk % bi;
+      const int r = (e >> 4) & 15, c = e & 15;
+      float* T = mat ? T1 : T0;
+      const float* trow = T + (16 * bi + r) * ld + 16 * bi;
+      const float* w = W + (blk << 8) + c;
+      float acc = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < 16; ++kk) acc += trow[kk] * w[kk * 16];
+      T[(16 * bi + r) * ld + 16 * bj + c] = -acc;
+    }
+    __syncthreads();
+  }
+}
+
+// T: input element type (bf16 bits or fp32).  The matrices are written as
+// XT: fp16 for bf16 inputs (their entries are bounded by the decays, beta,
+// gamma <= 1 and unit-scale keys; fp16 keeps 11 mantissa bits), fp32 otherwise.
+template <typename T, int DK, bool RDN>
+__global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
+  typedef PrepLayout<T, DK> L;
+  typedef typename std::conditional<sizeof(T) == 2, f16, float>::type XT;
+  extern __shared__ __align__(16) unsigned char smem[];
+  T* Kc = reinterpret_cast<T*>(smem);
+  T* Qc = Kc + kChunk * L::kLdK;
+  float* As = reinterpret_cast<float*>(smem);   // reuses region 0 after G, P
+  float* Ar = As + kChunk * L::kLdA;
+  float* Ts = Ar + kChunk * L::kLdA;
+  float* Tr = Ts + kChunk * L::kLdA;
+  float* W = reinterpret_cast<float*>(smem + L::kBytes0);
+  float* gs = W + 6 * 256;
+  float* gr = gs + kChunk;
+  float* bt = gr + kChunk;
+  float* gm = bt + kChunk;
+  float* gsp = gm + kChunk;   // g_{t-1}
+
+  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  ChunkInfo ci;
+  if (!chunk_info(p.st, c, ci)) return;
+  const int H = p.H;
+
+  // ---- load K, Q rows (zero padding beyond the chunk) ----
+  {
+    constexpr int kVec = 16 / sizeof(T);           // elements per 16-byte load
+    constexpr int kPerRow = DK / kVec;
+    const T* qg = reinterpret_cast<const T*>(p.q);
+    const T* kg = reinterpret_cast<const T*>(p.k);
+    for (int e = tid; e < kChunk * kPerRow; e += kThreads) {
+      const int t = e / kPerRow, col = (e % kPerRow) * kVec;
+      uint4 kv = make_uint4(0, 0, 0, 0), qv = make_uint4(0, 0, 0, 0);
+      if (t < ci.len) {
+        const int64_t off = ((ci.tok + t) * H + h) * (int64_t)DK + col;
+        kv = *reinterpret_cast<const uint4*>(kg + off);
+        qv = *reinterpret_cast<const uint4*>(qg + off);
+      }
+      *reinterpret_cast<uint4*>(Kc + t * L::kLdK + col) = kv;
+      *reinterpret_cast<uint4*>(Qc + t * L::kLdK + col) = qv;
+    }
+  }
+  // ---- gates: wave 0 scans log aS, wave 1 scans log aR ----
+  if (tid < 128) {
+    const int t = tid & 63;
+    const bool valid = t < ci.len;
+    const int64_t gi = (ci.tok + t) * H + h;
+    const float* a = tid < 64 ? p.alpha_s : p.alpha_r;
+    const float la = valid ? log_decay(a[gi]) : 0.f;
+    const float cum = wave_inclusive_scan(la);
+    if (tid < 64) {
+      gs[t] = cum;
+      bt[t] = valid ? p.beta[gi] : 0.f;
+      gsp[t] = cum - la;
+    } else {
+      gr[t] = cum;
+      gm[t] = valid ? p.gamma[gi] : 0.f;
+    }
+  }
+  __syncthreads();
+  float* gate_out = p.gate_ws + ((int64_t)c * H + h) * kGateBlock;
+  if (tid < 64) {
+    gate_out[tid] = gs[tid];
+    gate_out[64 + tid] = gr[tid];
+    gate_out[128 + tid] = bt[tid];
+    gate_out[192 + tid] = gm[tid];
+  }
+
+  // ---- G = K K^T and P = Q K^T: wave w owns rows 16w..16w+15 ----
+  const int w = tid >> 6;
+  floatx4 G[4], P[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    G[ct] = zero4();
+    P[ct] = zero4();
+    mma_tile<T, DK, true, true>(G[ct], Kc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
+    mma_tile<T, DK, true, true>(P[ct], Qc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
+  }
+  __syncthreads();   // Kc/Qc dead: region 0 becomes As/Ar/Ts/Tr
+
+  XT* mats = reinterpret_cast<XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    const int s = 16 * ct + acc_col();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int t = 16 * w + acc_row(r);
+      const float g = G[ct][r], pq = P[ct][r];
+      const float es = __expf(fminf(gs[t] - gs[s], 0.f));
+      const float esp = __expf(fminf(gsp[t] - gs[s], 0.f));
+      const float er = __expf(fminf(gr[t] - gr[s], 0.f));
+      const bool lower = s < t;
+      mats[kMatMG * kMatElems + t * kChunk + s] = from_f<XT>(lower ? esp * g : 0.f);
+      mats[kMatMP * kMatElems + t * kChunk + s] = from_f<XT>(lower ? es * pq : 0.f);
+      mats[kMatMR * kMatElems + t * kChunk + s] = from_f<XT>(s <= t ? er * pq : 0.f);
+      if constexpr (RDN) {
+        As[t * L::kLdA + s] = lower ? bt[t] * es * g : 0.f;
+        Ar[t * L::kLdA + s] = lower ? gm[t] * er * g : 0.f;
+      }
+    }
+  }
+  if constexpr (RDN) {
+    __syncthreads();
+    invert_unit_lower_pair(As, Ar, Ts, Tr, W);
+    for (int e = tid; e < kMatElems; e += kThreads) {
+      const int t = e / kChunk, s = e % kChunk;
+      mats[kMatTS * kMatElems + e] = from_f<XT>(Ts[t * L::kLdA + s]);
+      mats[kMatTR * kMatElems + e] = from_f<XT>(Tr[t * L::kLdA + s]);
+    }
+  }
+}
+
+template <typename T, int DK, bool RDN>
+hipError_t launch_prep_t(const OpParams& p, hipStream_t stream) {
+  typedef PrepLayout<T, DK> L;
+  auto kern = prep_kernel<T, DK, RDN>;
+  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
+  if (err != hipSuccess) return err;
+  hipLaunchKernelGGL(kern, dim3(p.max_chunks, p.H), dim3(kThreads), L::kBytes, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_prep(const OpParams& p, bool bf16, hipStream_t stream) {
+  if (p.max_chunks == 0) return hipSuccess;
+  if (bf16) {
+    if (p.DK == 128) return p.rdn ? launch_prep_t<u16, 128, true>(p, stream) : launch_prep_t<u16, 128, false>(p, stream);
+    return p.rdn ? launch_prep_t<u16, 64, true>(p, stream) : launch_prep_t<u16, 64, false>(p, stream);
+  }
+  return p.rdn ? launch_prep_t<float, 64, true>(p, stream) : launch_prep_t<float, 64, false>(p, stream);
+}
+
+}  // namespace rla

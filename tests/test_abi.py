@@ -1,0 +1,114 @@
+"""The C-ABI library: it loads, exports what include/rla.h declares, sizes its
+workspace, and rejects bad arguments on the host before any HIP call (so
+these run without a GPU; every case here fails validation)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2509_25223_amd as rla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(rla.LIB_PATH):
+        from paper_2509_25223_amd import build
+        build.build()
+    return rla.load_library()
+
+
+def declared_functions():
+    names = []
+    for hdr in sorted(os.listdir(os.path.join(ROOT, "include"))):
+        if hdr.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", hdr)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names += re.findall(r"\b(r[a-z_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(rla.SYMBOLS) <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def prob(B=2, T=100, H=3, dk=128, dv=128, dtype=rla.RLA_BF16, clip=1.0, cu=None, N=0, out=rla.RLA_F32):
+    return rla.rla_problem(B, T, H, dk, dv, N, cu, dtype, clip, out)
+
+
+def test_workspace_size(lib):
+    p = prob()
+    f = rla.rla_workspace_size(p, rla.RLA_OP_RDN_FORWARD)
+    b = rla.rla_workspace_size(p, rla.RLA_OP_RDN_BACKWARD)
+    assert 0 < f < b
+    assert rla.rla_workspace_size(p, 7) == 0
+    assert rla.rla_workspace_size(prob(dk=96), rla.RLA_OP_RDN_FORWARD) == 0
+    # more tokens never need less workspace
+    assert rla.rla_workspace_size(prob(T=1000), 1) >= f
+    # varlen plans an upper bound of chunks from T and N
+    assert rla.rla_workspace_size(prob(B=1, T=1000, cu=0x1000, N=5), 1) > 0
+
+
+FAKE = 0x7f0000000000   # 16-byte aligned, never dereferenced: validation fails first
+
+
+def call_fwd(lib, p, ptrs=None, ws=FAKE, ws_bytes=1 << 40, name="rdn_forward"):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, a=FAKE, b=FAKE, ar=FAKE, g=FAKE, S0=None, R0=None,
+                o=FAKE, Sf=None, Rf=None)
+    if ptrs:
+        args.update(ptrs)
+    f = getattr(lib, name)
+    return f(ctypes.byref(p) if p is not None else None, args["q"], args["k"], args["v"],
+             args["a"], args["b"], args["ar"], args["g"], args["S0"], args["R0"], args["o"],
+             args["Sf"], args["Rf"], ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("name", ["rla_forward", "rdn_forward"])
+def test_validation_errors(lib, name):
+    E = dict(null=1, shape=2, dtype=3, ws=5, value=6)
+    assert call_fwd(lib, None, name=name) == E["null"]
+    assert call_fwd(lib, prob(dk=96), name=name) == E["shape"]
+    assert call_fwd(lib, prob(dv=32), name=name) == E["shape"]
+    assert call_fwd(lib, prob(H=0), name=name) == E["shape"]
+    assert call_fwd(lib, prob(T=-1), name=name) == E["shape"]
+    assert call_fwd(lib, prob(dtype=5), name=name) == E["dtype"]
+    assert call_fwd(lib, prob(dtype=rla.RLA_F32, dk=128), name=name) == E["dtype"]
+    assert call_fwd(lib, prob(clip=-1.0), name=name) == E["value"]
+    assert call_fwd(lib, prob(clip=math.nan), name=name) == E["value"]
+    assert call_fwd(lib, prob(B=2, cu=FAKE, N=3), name=name) == E["shape"]
+    assert call_fwd(lib, prob(), ptrs=dict(q=None), name=name) == E["null"]
+    assert call_fwd(lib, prob(), ptrs=dict(g=None), name=name) == E["null"]
+    assert call_fwd(lib, prob(), ptrs=dict(o=None), name=name) == E["null"]
+    assert call_fwd(lib, prob(), ptrs=dict(v=FAKE + 2), name=name) == E["value"]
+    assert call_fwd(lib, prob(), ws=None, name=name) == E["ws"]
+    assert call_fwd(lib, prob(), ws_bytes=16, name=name) == E["ws"]
+    assert call_fwd(lib, prob(), ws=FAKE + 16, name=name) == E["value"]
+
+
+def test_backward_validation_errors(lib):
+    p = prob()
+    def bwd(p, **kw):
+        a = dict(q=FAKE, dO=FAKE, dq=FAKE, ws=FAKE, ws_bytes=1 << 40)
+        a.update(kw)
+        return lib.rdn_backward(ctypes.byref(p) if p is not None else None, a["q"], FAKE, FAKE,
+                                FAKE, FAKE, FAKE, FAKE, None, None, a["dO"], None, None, a["dq"],
+                                FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, a["ws"],
+                                a["ws_bytes"], None)
+    assert bwd(None) == 1
+    assert bwd(p, dO=None) == 1
+    assert bwd(p, dq=None) == 1
+    assert bwd(prob(dk=48)) == 2
+    assert bwd(p, ws_bytes=rla.rla_workspace_size(p, rla.RLA_OP_RDN_FORWARD)) == 5
+    assert bwd(p, dq=FAKE + 4) == 6
+
+
+def test_status_strings(lib):
+    for s in range(8):
+        assert rla.status_string(s)
+    assert "workspace" in rla.status_string(5)
