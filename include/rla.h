@@ -82,7 +82,12 @@ typedef enum {
 typedef enum { RLA_F32 = 0, RLA_BF16 = 1 } rla_dtype;
 
 /* Operation codes for rla_workspace_size. */
-typedef enum { RLA_OP_RLA_FORWARD = 0, RLA_OP_RDN_FORWARD = 1, RLA_OP_RDN_BACKWARD = 2 } rla_op;
+typedef enum {
+  RLA_OP_RLA_FORWARD = 0,
+  RLA_OP_RDN_FORWARD = 1,
+  RLA_OP_RDN_BACKWARD = 2,
+  RLA_OP_RLA_BACKWARD = 3
+} rla_op;
 
 typedef struct {
   int64_t batch;            /* B (must be 1 when cu_seqlens != NULL) */
@@ -100,6 +105,16 @@ typedef struct {
 /* Bytes of workspace the operation needs for this problem (0 if the problem
  * is invalid).  Pure host function. */
 size_t rla_workspace_size(const rla_problem *problem, int op);
+
+/*
+ * Profiling aid (opt-in, per calling thread): while `events` is non-NULL,
+ * each later forward/backward call on this thread records events[0] on its
+ * stream when its first kernel stage starts and events[i] after stage i,
+ * up to num_events events.  Stages: forward = {prep, scan}; backward =
+ * {prep, checkpointing forward scan, reverse scan, gradient kernel}.
+ * The events are hipEvent_t handles owned by the caller.  NULL turns it off.
+ */
+void rla_set_stage_events(void **events, int num_events);
 
 /* Human-readable name of a status code (static string). */
 const char *rla_status_string(rla_status status);
@@ -138,6 +153,20 @@ rla_status rdn_forward(const rla_problem *problem,
  * gate values (not their logarithms).
  */
 rla_status rdn_backward(const rla_problem *problem,
+                        const void *q, const void *k, const void *v,
+                        const float *alpha_s, const float *beta,
+                        const float *alpha_r, const float *gamma,
+                        const float *S0, const float *R0,
+                        const void *dO, const float *dS_final, const float *dR_final,
+                        void *dq, void *dk, void *dv,
+                        float *dalpha_s, float *dbeta, float *dalpha_r, float *dgamma,
+                        float *dS0, float *dR0,
+                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * RLA backward: as rdn_backward, for rla_forward (paper Sec. 3.4, left box).
+ */
+rla_status rla_backward(const rla_problem *problem,
                         const void *q, const void *k, const void *v,
                         const float *alpha_s, const float *beta,
                         const float *alpha_r, const float *gamma,

@@ -25,10 +25,10 @@ LIB_PATH = os.path.join(_HERE, "librla_mi355x.so")
 
 RLA_OK = 0
 RLA_F32, RLA_BF16 = 0, 1
-RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD = 0, 1, 2
+RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD, RLA_OP_RLA_BACKWARD = 0, 1, 2, 3
 
 SYMBOLS = ("rla_workspace_size", "rla_status_string", "rla_forward", "rdn_forward",
-           "rdn_backward")
+           "rla_backward", "rdn_backward", "rla_set_stage_events")
 
 
 class rla_problem(ctypes.Structure):
@@ -59,6 +59,8 @@ def load_library():
     vp, sz, pp = ctypes.c_void_p, ctypes.c_size_t, ctypes.POINTER(rla_problem)
     lib.rla_workspace_size.argtypes = [pp, ctypes.c_int]
     lib.rla_workspace_size.restype = sz
+    lib.rla_set_stage_events.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    lib.rla_set_stage_events.restype = None
     lib.rla_status_string.argtypes = [ctypes.c_int]
     lib.rla_status_string.restype = ctypes.c_char_p
     fwd_args = [pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp, sz, vp]
@@ -66,9 +68,11 @@ def load_library():
         f = getattr(lib, name)
         f.argtypes = fwd_args
         f.restype = ctypes.c_int
-    lib.rdn_backward.argtypes = ([pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp] * 3 +
-                                 [vp] * 4 + [vp] * 2 + [vp, sz, vp])
-    lib.rdn_backward.restype = ctypes.c_int
+    for name in ("rla_backward", "rdn_backward"):
+        f = getattr(lib, name)
+        f.argtypes = ([pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp] * 3 + [vp] * 4 +
+                      [vp] * 2 + [vp, sz, vp])
+        f.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -78,6 +82,22 @@ def status_string(status: int) -> str:
 
 
 rla_status_string = status_string
+
+
+def rla_set_stage_events(events) -> None:
+    """Profiling aid: record the given torch.cuda.Event objects at the start of
+    the next calls' kernel stages and after each stage (None turns it off)."""
+    global _event_handles
+    lib = load_library()
+    if events is None:
+        _event_handles = None
+        lib.rla_set_stage_events(None, 0)
+        return
+    _event_handles = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
+    lib.rla_set_stage_events(ctypes.cast(_event_handles, ctypes.c_void_p), len(events))
+
+
+_event_handles = None
 
 
 def rla_workspace_size(problem: rla_problem, op: int) -> int:
@@ -207,11 +227,9 @@ def rdn_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=No
                     clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype)
 
 
-def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
+def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
                  stream=None, grads=None, out_dtype=None):
-    """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rdn_forward.
-    Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0."""
     torch = _torch()
     lib = load_library()
     problem = make_problem(q, v, cu_seqlens, clip, out_dtype)
@@ -231,14 +249,33 @@ def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, 
                      dalpha_r=torch.empty_like(alpha_r), dgamma=torch.empty_like(gamma),
                      dS0=torch.empty(shape, dtype=torch.float32, device=dev),
                      dR0=torch.empty(shape, dtype=torch.float32, device=dev))
-    ws, need = _workspace(problem, RLA_OP_RDN_BACKWARD, dev, workspace)
+    ws, need = _workspace(problem, op, dev, workspace)
     g = grads
-    st = lib.rdn_backward(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
+    st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
                           _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S0), _ptr(R0), _ptr(dO),
                           _ptr(dS_final), _ptr(dR_final), _ptr(g["dq"]), _ptr(g["dk"]),
                           _ptr(g["dv"]), _ptr(g["dalpha_s"]), _ptr(g["dbeta"]),
                           _ptr(g["dalpha_r"]), _ptr(g["dgamma"]), _ptr(g.get("dS0")),
                           _ptr(g.get("dR0")), _ptr(ws), ws.numel(), _stream_handle(stream))
     if st != RLA_OK:
-        raise RLAError(st, "rdn_backward")
+        raise RLAError(st, name)
     return g
+
+
+def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
+                 R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
+                 stream=None, grads=None, out_dtype=None):
+    """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rdn_forward.
+    Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0."""
+    return _backward("rdn_backward", RLA_OP_RDN_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
+                     dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
+                     out_dtype)
+
+
+def rla_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
+                 R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
+                 stream=None, grads=None, out_dtype=None):
+    """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rla_forward."""
+    return _backward("rla_backward", RLA_OP_RLA_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
+                     dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
+                     out_dtype)

@@ -14,6 +14,18 @@ namespace {
 
 constexpr size_t kAlign = 256;
 
+// Opt-in stage timing (rla_set_stage_events): events recorded on the launch
+// stream at the start of a call and after each kernel stage.
+thread_local hipEvent_t* g_events = nullptr;
+thread_local int g_num_events = 0;
+thread_local int g_next_event = 0;
+
+hipError_t mark_stage(hipStream_t stream, bool first) {
+  if (first) g_next_event = 0;
+  if (!g_events || g_next_event >= g_num_events) return hipSuccess;
+  return hipEventRecord(g_events[g_next_event++], stream);
+}
+
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Problem {
@@ -82,7 +94,7 @@ Workspace plan(const Problem& pr, int op) {
   }
   w.gates = take(sizeof(float) * mc * H * kGateBlock);
   w.mats = take((pr.bf16 ? 2 : 4) * mc * H * kNumMats * kMatElems);
-  if (op == RLA_OP_RDN_BACKWARD) {
+  if (op == RLA_OP_RDN_BACKWARD || op == RLA_OP_RLA_BACKWARD) {
     const size_t st = sizeof(float) * mc * H * (size_t)pr.DK * (size_t)pr.DV;
     w.ckS = take(st);
     w.ckR = take(st);
@@ -171,8 +183,72 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
   if (pr.varlen && pr.ntok > 0)   // tokens outside every sequence read as zero
     e = hipMemsetAsync(o, 0, (size_t)pr.ntok * pr.H * pr.DV * (pr.out_bf16 ? 2 : 4), stream);
   if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
+  if (e == hipSuccess) e = mark_stage(stream, true);
   if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
   if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/true, /*ckpt=*/false, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
+  return to_status(e);
+}
+
+rla_status backward(bool rdn, const rla_problem* problem, const void* q, const void* k, const void* v,
+                        const float* alpha_s, const float* beta, const float* alpha_r,
+                        const float* gamma, const float* S0, const float* R0, const void* dO,
+                        const float* dS_final, const float* dR_final, void* dq, void* dk,
+                        void* dv, float* dalpha_s, float* dbeta, float* dalpha_r, float* dgamma,
+                        float* dS0, float* dR0, void* workspace, size_t workspace_bytes,
+                        void* stream_) {
+  Problem pr;
+  rla_status st = check_problem(problem, pr);
+  if (st != RLA_OK) return st;
+  if (pr.ntok > 0 && (!q || !k || !v || !alpha_s || !beta || !alpha_r || !gamma || !dO ||
+                      !dq || !dk || !dv || !dalpha_s || !dbeta || !dalpha_r || !dgamma))
+    return RLA_ERR_NULL_ARG;
+  if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) ||
+                      !aligned16(dq) || !aligned16(dk) || !aligned16(dv)))
+    return RLA_ERR_VALUE;
+  const Workspace w = plan(pr, rdn ? RLA_OP_RDN_BACKWARD : RLA_OP_RLA_BACKWARD);
+  st = check_workspace(w, workspace, workspace_bytes);
+  if (st != RLA_OK) return st;
+  if (pr.N == 0) return RLA_OK;
+
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);
+  OpParams p = make_params(pr, w, ws, rdn);
+  p.q = q; p.k = k; p.v = v;
+  p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
+  p.S0 = S0; p.R0 = R0;
+  p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
+  p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
+  p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
+  p.dS_ws = reinterpret_cast<float*>(ws + w.dS);
+  p.dR_ws = reinterpret_cast<float*>(ws + w.dR);
+  p.dO = dO; p.dS_fin = dS_final; p.dR_fin = dR_final;
+  p.dq = dq; p.dk = dk; p.dv = dv;
+  p.dalpha_s = dalpha_s; p.dbeta = dbeta; p.dalpha_r = dalpha_r; p.dgamma = dgamma;
+  p.dS0 = dS0; p.dR0 = dR0;
+
+  hipError_t e = hipSuccess;
+  if (pr.varlen && pr.ntok > 0) {   // tokens outside every sequence get zero gradients
+    const size_t el = pr.out_bf16 ? 2 : 4, tok = (size_t)pr.ntok * pr.H;
+    e = hipMemsetAsync(dq, 0, tok * pr.DK * el, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dk, 0, tok * pr.DK * el, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dv, 0, tok * pr.DV * el, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dalpha_s, 0, tok * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dbeta, 0, tok * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dalpha_r, 0, tok * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(dgamma, 0, tok * 4, stream);
+  }
+  if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
+  if (e == hipSuccess) e = mark_stage(stream, true);
+  if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
+  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/false, /*ckpt=*/true, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
+  if (e == hipSuccess) e = launch_bwd_scan(p, pr.bf16, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
+  if (e == hipSuccess) e = launch_bwd_grad(p, pr.bf16, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
   return to_status(e);
 }
 
@@ -186,8 +262,14 @@ extern "C" {
 size_t rla_workspace_size(const rla_problem* problem, int op) {
   Problem pr;
   if (check_problem(problem, pr) != RLA_OK) return 0;
-  if (op != RLA_OP_RLA_FORWARD && op != RLA_OP_RDN_FORWARD && op != RLA_OP_RDN_BACKWARD) return 0;
+  if (op < RLA_OP_RLA_FORWARD || op > RLA_OP_RLA_BACKWARD) return 0;
   return plan(pr, op).total;
+}
+
+void rla_set_stage_events(void** events, int num_events) {
+  g_events = reinterpret_cast<hipEvent_t*>(events);
+  g_num_events = events ? num_events : 0;
+  g_next_event = 0;
 }
 
 const char* rla_status_string(rla_status s) {
@@ -222,60 +304,28 @@ rla_status rdn_forward(const rla_problem* problem, const void* q, const void* k,
                  R_final, workspace, workspace_bytes, stream);
 }
 
+rla_status rla_backward(const rla_problem* problem, const void* q, const void* k, const void* v,
+                        const float* alpha_s, const float* beta, const float* alpha_r,
+                        const float* gamma, const float* S0, const float* R0, const void* dO,
+                        const float* dS_final, const float* dR_final, void* dq, void* dk,
+                        void* dv, float* dalpha_s, float* dbeta, float* dalpha_r, float* dgamma,
+                        float* dS0, float* dR0, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  return backward(false, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, dO, dS_final,
+                  dR_final, dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0, workspace,
+                  workspace_bytes, stream);
+}
+
 rla_status rdn_backward(const rla_problem* problem, const void* q, const void* k, const void* v,
                         const float* alpha_s, const float* beta, const float* alpha_r,
                         const float* gamma, const float* S0, const float* R0, const void* dO,
                         const float* dS_final, const float* dR_final, void* dq, void* dk,
                         void* dv, float* dalpha_s, float* dbeta, float* dalpha_r, float* dgamma,
                         float* dS0, float* dR0, void* workspace, size_t workspace_bytes,
-                        void* stream_) {
-  Problem pr;
-  rla_status st = check_problem(problem, pr);
-  if (st != RLA_OK) return st;
-  if (pr.ntok > 0 && (!q || !k || !v || !alpha_s || !beta || !alpha_r || !gamma || !dO ||
-                      !dq || !dk || !dv || !dalpha_s || !dbeta || !dalpha_r || !dgamma))
-    return RLA_ERR_NULL_ARG;
-  if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) ||
-                      !aligned16(dq) || !aligned16(dk) || !aligned16(dv)))
-    return RLA_ERR_VALUE;
-  const Workspace w = plan(pr, RLA_OP_RDN_BACKWARD);
-  st = check_workspace(w, workspace, workspace_bytes);
-  if (st != RLA_OK) return st;
-  if (pr.N == 0) return RLA_OK;
-
-  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
-  unsigned char* ws = reinterpret_cast<unsigned char*>(workspace);
-  OpParams p = make_params(pr, w, ws, true);
-  p.q = q; p.k = k; p.v = v;
-  p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
-  p.S0 = S0; p.R0 = R0;
-  p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
-  p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
-  p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
-  p.dS_ws = reinterpret_cast<float*>(ws + w.dS);
-  p.dR_ws = reinterpret_cast<float*>(ws + w.dR);
-  p.dO = dO; p.dS_fin = dS_final; p.dR_fin = dR_final;
-  p.dq = dq; p.dk = dk; p.dv = dv;
-  p.dalpha_s = dalpha_s; p.dbeta = dbeta; p.dalpha_r = dalpha_r; p.dgamma = dgamma;
-  p.dS0 = dS0; p.dR0 = dR0;
-
-  hipError_t e = hipSuccess;
-  if (pr.varlen && pr.ntok > 0) {   // tokens outside every sequence get zero gradients
-    const size_t el = pr.out_bf16 ? 2 : 4, tok = (size_t)pr.ntok * pr.H;
-    e = hipMemsetAsync(dq, 0, tok * pr.DK * el, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dk, 0, tok * pr.DK * el, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dv, 0, tok * pr.DV * el, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dalpha_s, 0, tok * 4, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dbeta, 0, tok * 4, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dalpha_r, 0, tok * 4, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dgamma, 0, tok * 4, stream);
-  }
-  if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
-  if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
-  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/false, /*ckpt=*/true, stream);
-  if (e == hipSuccess) e = launch_bwd_scan(p, pr.bf16, stream);
-  if (e == hipSuccess) e = launch_bwd_grad(p, pr.bf16, stream);
-  return to_status(e);
+                        void* stream) {
+  return backward(true, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, dO, dS_final,
+                  dR_final, dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0, workspace,
+                  workspace_bytes, stream);
 }
 
 }  // extern "C"

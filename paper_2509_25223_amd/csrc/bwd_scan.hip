@@ -1,0 +1,384 @@
+// Reverse state-gradient scan: one 256-thread workgroup per (sequence, head,
+// value block), walking the chunks from last to first with dS, dR (d_k x BV,
+// fp32) in MFMA accumulators.  It produces, for every chunk, the gradient of
+// the loss with respect to the chunk-END states (consumed by the chunk-
+// parallel gradient kernel) and, at the sequence start, dS0 and dR0.
+//
+// Adjoint of one forward chunk (see fwd_scan.hip for the forward), with
+// db = dO, dc = diag(gamma) dO and the clip mask m from the forward pass:
+//   dUR = diag(e^{h_C-h}) K dR_end + MR^T dc
+//   RDN: dYR = T^R^T dUR            RLA: dYR = dUR
+//   dX  = m * (diag(gamma) dYR)     (dr = gamma dYR, then the clip's mask)
+//   dKR = -diag(gamma e^{h}) dYR    (RDN only: UR depends on R0 through KR)
+//   dU  = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX
+//   RDN: dY = T^S^T dU              RLA: not needed (U = diag(b) V)
+//   dKS = -diag(e^{g_{t-1}}) dX - diag(b e^{g}) dY      (RLA: first term only)
+//   dS_start = e^{g_C} dS_end + Q^T diag(e^{g}) db + K^T dKS
+//   dR_start = e^{h_C} dR_end + Q^T diag(e^{h}) dc + K^T dKR
+// Every column of dS, dR only sees its own value column, so value blocks are
+// independent here as in the forward.  Operand precision as in the forward
+// scan: K x (dS, dR) uses bf16 K with the gradient state split into bf16
+// hi + lo; all other products use fp16 operands (fp32 for fp32 inputs).
+#include <type_traits>
+
+#include "kernels.hpp"
+
+namespace rla {
+
+namespace {
+
+template <typename IN, int DK, int BV, bool RDN>
+struct BwdScanLayout {
+  static constexpr bool kBF = sizeof(IN) == 2;
+  typedef typename std::conditional<kBF, f16, float>::type XT;
+  static constexpr int kPad = kBF ? 8 : 4;
+  static constexpr int kLdX = kChunk + kPad;
+  static constexpr int kLdS = DK + kPad;
+  static constexpr int kNumM = RDN ? 5 : 1;
+  static constexpr int kNumCopies = kBF ? 4 : 2;
+  static constexpr int kNumBufs = 6;
+  static constexpr int kKT = 0;
+  static constexpr int kQT = kKT + DK * kLdX * (int)sizeof(XT);
+  static constexpr int kCopies = kQT + DK * kLdX * (int)sizeof(XT);
+  static constexpr int kCopyBytes = BV * kLdS * (int)sizeof(IN);
+  static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
+  static constexpr int kBufs = kMats + kNumM * kChunk * kLdX * (int)sizeof(XT);
+  static constexpr int kBufBytes = BV * kLdX * (int)sizeof(XT);
+  static constexpr int kMask = kBufs + kNumBufs * kBufBytes;
+  static constexpr int kGates = kMask + kChunk * BV;
+  static constexpr int kBytes = kGates + 10 * kChunk * 4;
+  static_assert(kBytes <= 160 * 1024, "backward scan LDS");
+};
+
+// per-token block slots ([BV][64], value-major); aliases follow lifetimes:
+// db is last read in P4 and dKS first written in P5 (RLA: db last read in P1,
+// dKS written in P3); dc is last read in P2 and dX first written in P3; dUR
+// is last read in P3 and dU first written in P4.
+enum { bDB_DKS = 0, bDC_DX = 1, bQDB = 2, bQDC = 3, bDUR_DU = 4, bDKR = 5 };
+
+template <typename IN>
+__device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int ld, floatx4 v) {
+  const int off = acc_col() * ld + acc_row(0);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if constexpr (sizeof(IN) == 2) {
+      const u16 h = f2bf(v[r]);
+      hi[off + r] = h;
+      lo[off + r] = bf16_lo(v[r], h);
+    } else {
+      hi[off + r] = v[r];
+    }
+  }
+}
+
+template <typename IN, int DK, int BV, bool RDN>
+__global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
+  typedef BwdScanLayout<IN, DK, BV, RDN> L;
+  typedef typename L::XT XT;
+  typedef Mfma<IN> MI;
+  constexpr bool BF = L::kBF;
+  constexpr int JT = BV / 16;
+  constexpr int IT = DK / 64;
+  constexpr int KS_STEPS = DK / MI::kStep;
+  extern __shared__ __align__(16) unsigned char smem[];
+  XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
+  XT* QT = reinterpret_cast<XT*>(smem + L::kQT);
+  IN* dShi = reinterpret_cast<IN*>(smem + L::kCopies);
+  IN* dRhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
+  IN* dSlo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);   // bf16 only
+  IN* dRlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);   // bf16 only
+  XT* mats = reinterpret_cast<XT*>(smem + L::kMats);
+  auto buf = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBufs + b * L::kBufBytes); };
+  uint8_t* mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
+  float* gbt = reinterpret_cast<float*>(smem + L::kGates);
+  float* ggm = gbt + kChunk;
+  float* egs = ggm + kChunk;
+  float* egsp = egs + kChunk;
+  float* egr = egsp + kChunk;
+  float* dls = egr + kChunk;
+  float* dlr = dls + kChunk;
+  float* edge = dlr + kChunk;
+  // matrix slots: RDN {TS, MG, MP, TR, MR}; RLA {MR}
+  XT* mTS = mats;
+  XT* mMG = mats + 1 * kChunk * L::kLdX;
+  XT* mMP = mats + 2 * kChunk * L::kLdX;
+  XT* mTR = mats + 3 * kChunk * L::kLdX;
+  XT* mMR = mats + (RDN ? 4 : 0) * kChunk * L::kLdX;
+
+  const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int nvb = DV / BV;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int pair = (slot / nvb) * 8 + xcd, vb = slot % nvb;
+  if (pair >= p.st.nseq * H) return;
+  const int n = seq_order(p.st, pair / H), h = pair % H;
+  const SeqInfo si = seq_info(p.st, n);
+  const int nch = (si.len + kChunk - 1) / kChunk;
+  const int j0 = vb * BV;
+  const int64_t state_off = ((int64_t)n * H + h) * DK * DV;
+
+  floatx4 dS[IT][JT], dR[IT][JT];
+#pragma unroll
+  for (int it = 0; it < IT; ++it)
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+        dS[it][jt][r] = p.dS_fin ? p.dS_fin[state_off + (int64_t)i * DV + j] : 0.f;
+        dR[it][jt][r] = p.dR_fin ? p.dR_fin[state_off + (int64_t)i * DV + j] : 0.f;
+      }
+  auto write_copies = [&]() {
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        const int o = (jt * 16) * L::kLdS + w * (DK / 4) + it * 16;
+        store_state_copy<IN>(dShi + o, dSlo + o, L::kLdS, dS[it][jt]);
+        store_state_copy<IN>(dRhi + o, dRlo + o, L::kLdS, dR[it][jt]);
+      }
+  };
+  write_copies();
+
+  const IN* qg = reinterpret_cast<const IN*>(p.q);
+  const IN* kg = reinterpret_cast<const IN*>(p.k);
+  const IN* dog = reinterpret_cast<const IN*>(p.dO);
+  const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
+
+  for (int c = nch - 1; c >= 0; --c) {
+    const int gc = si.chunk0 + c;
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = min(kChunk, si.len - c * kChunk);
+
+    {   // gradient w.r.t. this chunk's end states
+      const int64_t off = ((int64_t)gc * H + h) * DK * DV;
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+            p.dS_ws[off + (int64_t)i * DV + j] = dS[it][jt][r];
+            p.dR_ws[off + (int64_t)i * DV + j] = dR[it][jt][r];
+          }
+    }
+
+    // ---- stage the chunk ----
+    typename MI::frag Kf[KS_STEPS];
+    {
+      typename MI::frag Qf[KS_STEPS];
+      const int t = 16 * w + (lane & 15);
+      const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
+      load_rowfrags<IN, DK>(Kf, t < len ? kg + roff : nullptr);
+      load_rowfrags<IN, DK>(Qf, t < len ? qg + roff : nullptr);
+#pragma unroll
+      for (int s = 0; s < KS_STEPS; ++s) {
+        if constexpr (BF) {
+          const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s]);
+          const u16x8 qv = __builtin_bit_cast(u16x8, Qf[s]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int i = s * 32 + (lane >> 4) * 8 + e;
+            KT[i * L::kLdX + t] = from_f<XT>(bf2f(kv[e]));
+            QT[i * L::kLdX + t] = from_f<XT>(bf2f(qv[e]));
+          }
+        } else {
+          const int i = s * 4 + (lane >> 4);
+          KT[i * L::kLdX + t] = Kf[s];
+          QT[i * L::kLdX + t] = Qf[s];
+        }
+      }
+      XT* dbT = buf(bDB_DKS);
+      for (int e = tid; e < kChunk * BV; e += kThreads) {
+        const int tt = e / BV, j = e % BV;
+        const int64_t gi = ((tok + tt) * H + h) * (int64_t)DV + j0 + j;
+        dbT[j * L::kLdX + tt] = from_f<XT>(tt < len ? to_f<IN>(dog[gi]) : 0.f);
+        mask[tt * BV + j] = tt < len ? p.ck_mask[gi] : 0;
+      }
+      constexpr int kVecM = 16 / sizeof(XT);
+      constexpr int kMatVecs = kMatElems / kVecM;
+      const XT* mg = matg + ((int64_t)gc * H + h) * kNumMats * kMatElems;
+      constexpr int kSrc[5] = {kMatTS, kMatMG, kMatMP, kMatTR, kMatMR};
+#pragma unroll
+      for (int m = 0; m < L::kNumM; ++m) {
+        const int src = RDN ? kSrc[m] : kMatMR;
+        for (int e = tid; e < kMatVecs; e += kThreads) {
+          const int tt = e / (kChunk / kVecM), ss = (e % (kChunk / kVecM)) * kVecM;
+          *reinterpret_cast<uint4*>(mats + (m * kChunk + tt) * L::kLdX + ss) =
+              *reinterpret_cast<const uint4*>(mg + src * kMatElems + tt * kChunk + ss);
+        }
+      }
+      if (tid < kChunk) {
+        const float* gb = p.gate_ws + ((int64_t)gc * H + h) * kGateBlock;
+        const int tt = tid;
+        const float gs = gb[tt], gsl = gb[kChunk - 1], gsp = tt > 0 ? gb[tt - 1] : 0.f;
+        const float gr = gb[64 + tt], grl = gb[64 + kChunk - 1];
+        gbt[tt] = gb[128 + tt];
+        ggm[tt] = gb[192 + tt];
+        egs[tt] = __expf(gs);
+        egsp[tt] = __expf(gsp);
+        egr[tt] = __expf(gr);
+        dls[tt] = __expf(gsl - gs);
+        dlr[tt] = __expf(grl - gr);
+        if (tt == 0) {
+          edge[0] = __expf(gsl);
+          edge[1] = __expf(grl);
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- P1: K dS_end, K dR_end (split state); scaled copies of dO ----
+    floatx4 KdS[JT], KdR[JT];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      KdS[jt] = zero4();
+      KdR[jt] = zero4();
+      const int o = jt * 16 * L::kLdS;
+      if constexpr (RDN) mma_rega<IN, DK, true>(KdS[jt], Kf, dShi + o, L::kLdS);
+      mma_rega<IN, DK, true>(KdR[jt], Kf, dRhi + o, L::kLdS);
+      if constexpr (BF) {
+        if constexpr (RDN) mma_rega<IN, DK, true>(KdS[jt], Kf, dSlo + o, L::kLdS);
+        mma_rega<IN, DK, true>(KdR[jt], Kf, dRlo + o, L::kLdS);
+      }
+      floatx4 dc, qdb, qdc;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 16 * w + acc_row(r), j = jt * 16 + acc_col();
+        const float o = to_f<XT>(buf(bDB_DKS)[j * L::kLdX + t]);
+        dc[r] = ggm[t] * o;
+        qdb[r] = egs[t] * o;
+        qdc[r] = egr[t] * dc[r];
+      }
+      store_acc_t<XT>(buf(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dc);
+      store_acc_t<XT>(buf(bQDB) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdb);
+      store_acc_t<XT>(buf(bQDC) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdc);
+    }
+    __syncthreads();
+
+    // ---- P2: dUR = diag(e^{h_C-h}) K dR_end + MR^T dc ----
+    floatx4 dUR[JT];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      floatx4 a = zero4();
+      mma_tile<XT, kChunk, false, true>(a, mMR + 16 * w, L::kLdX, buf(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) dUR[jt][r] = dlr[16 * w + acc_row(r)] * KdR[jt][r] + a[r];
+      if constexpr (RDN) store_acc_t<XT>(buf(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dUR[jt]);
+    }
+    __syncthreads();
+
+    // ---- P3: dYR, dX, dKR (RLA: dKS) ----
+    floatx4 dX[JT];
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      floatx4 dYR = dUR[jt];
+      if constexpr (RDN) {
+        dYR = zero4();
+        mma_tile<XT, kChunk, false, true>(dYR, mTR + 16 * w, L::kLdX, buf(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+      }
+      floatx4 dkr, dks;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 16 * w + acc_row(r), j = jt * 16 + acc_col();
+        dX[jt][r] = mask[t * BV + j] ? ggm[t] * dYR[r] : 0.f;
+        dkr[r] = -ggm[t] * egr[t] * dYR[r];
+        dks[r] = -egsp[t] * dX[jt][r];
+      }
+      if constexpr (RDN) {
+        store_acc_t<XT>(buf(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
+        store_acc_t<XT>(buf(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dkr);
+      } else {
+        store_acc_t<XT>(buf(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
+      }
+    }
+    __syncthreads();
+
+    if constexpr (RDN) {
+      // ---- P4: dU = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX ----
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        floatx4 a = zero4(), b = zero4(), du;
+        mma_tile<XT, kChunk, false, true>(a, mMP + 16 * w, L::kLdX, buf(bDB_DKS) + jt * 16 * L::kLdX, L::kLdX);
+        mma_tile<XT, kChunk, false, true>(b, mMG + 16 * w, L::kLdX, buf(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
+        store_acc_t<XT>(buf(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+      }
+      __syncthreads();
+      // ---- P5: dY = T^S^T dU, dKS ----
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        floatx4 dY = zero4(), dks;
+        mma_tile<XT, kChunk, false, true>(dY, mTS + 16 * w, L::kLdX, buf(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * w + acc_row(r);
+          dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[r];
+        }
+        store_acc_t<XT>(buf(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
+      }
+      __syncthreads();
+    }
+
+    // ---- P6: state gradients at the chunk start ----
+    const float eS = edge[0], eR = edge[1];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int i0 = w * (DK / 4) + it * 16;
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        dS[it][jt] *= eS;
+        dR[it][jt] *= eR;
+        const int bo = jt * 16 * L::kLdX;
+        mma_tile<XT, kChunk, true, true>(dS[it][jt], QT + i0 * L::kLdX, L::kLdX, buf(bQDB) + bo, L::kLdX);
+        mma_tile<XT, kChunk, true, true>(dS[it][jt], KT + i0 * L::kLdX, L::kLdX, buf(bDB_DKS) + bo, L::kLdX);
+        mma_tile<XT, kChunk, true, true>(dR[it][jt], QT + i0 * L::kLdX, L::kLdX, buf(bQDC) + bo, L::kLdX);
+        if constexpr (RDN)
+          mma_tile<XT, kChunk, true, true>(dR[it][jt], KT + i0 * L::kLdX, L::kLdX, buf(bDKR) + bo, L::kLdX);
+      }
+    }
+    __syncthreads();
+    write_copies();
+  }
+
+  if (p.dS0 || p.dR0) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+          if (p.dS0) p.dS0[state_off + (int64_t)i * DV + j] = dS[it][jt][r];
+          if (p.dR0) p.dR0[state_off + (int64_t)i * DV + j] = dR[it][jt][r];
+        }
+  }
+}
+
+template <typename IN, int DK, int BV, bool RDN>
+hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
+  typedef BwdScanLayout<IN, DK, BV, RDN> L;
+  auto kern = bwd_scan_kernel<IN, DK, BV, RDN>;
+  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
+  if (err != hipSuccess) return err;
+  const int nvb = p.DV / BV;
+  const int npairs = p.st.nseq * p.H;
+  const int grid = ((npairs + 7) / 8) * 8 * nvb;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), L::kBytes, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_bwd_scan(const OpParams& p, bool bf16, hipStream_t stream) {
+  if (bf16) {
+    if (p.DK == 128) return p.rdn ? launch_bwd_scan_t<u16, 128, 32, true>(p, stream) : launch_bwd_scan_t<u16, 128, 32, false>(p, stream);
+    return p.rdn ? launch_bwd_scan_t<u16, 64, 32, true>(p, stream) : launch_bwd_scan_t<u16, 64, 32, false>(p, stream);
+  }
+  return p.rdn ? launch_bwd_scan_t<float, 64, 16, true>(p, stream) : launch_bwd_scan_t<float, 64, 16, false>(p, stream);
+}
+
+}  // namespace rla

@@ -77,3 +77,57 @@ def select(inp, seqs, heads):
     lens = [cu[n + 1] - cu[n] for n in seqs]
     out["cu_seqlens"] = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
     return out
+
+
+def gpu_backward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dS_final=None,
+                 dR_final=None, dense_B=None, out_dtype=None):
+    """Runs rla_backward / rdn_backward on packed inputs; returns numpy grads."""
+    import torch
+    td = torch_dtype(dtype)
+    q, k, v, dO = (dev(inp[n], td, device) for n in ("q", "k", "v", "dO"))
+    gates = [dev(inp[n], torch.float32, device) for n in ("alpha_s", "beta", "alpha_r", "gamma")]
+    opt = lambda a: None if a is None else dev(a, torch.float32, device)
+    cu = None
+    if dense_B:
+        B = dense_B
+        T = q.shape[0] // B
+        q, k, v, dO = (x.view(B, T, *x.shape[1:]) for x in (q, k, v, dO))
+        gates = [g.view(B, T, -1) for g in gates]
+    else:
+        cu = torch.from_numpy(np.asarray(inp["cu_seqlens"], dtype=np.int32)).to(device)
+    fn = rla.rdn_backward if variant == "rdn" else rla.rla_backward
+    g = fn(q, k, v, *gates, dO, clip=clip, S0=opt(S0), R0=opt(R0), dS_final=opt(dS_final),
+           dR_final=opt(dR_final), cu_seqlens=cu, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    out = {}
+    for key, t in g.items():
+        a = host(t)
+        if key in ("dq", "dk", "dv"):
+            a = a.reshape(-1, *a.shape[-2:])
+        elif key not in ("dS0", "dR0"):
+            a = a.reshape(-1, a.shape[-1])
+        out[key] = a
+    return out
+
+
+def oracle_backward(variant, inp, clip=1.0, S0=None, R0=None, dS_final=None, dR_final=None):
+    return oracle.backward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
+                           inp["alpha_r"], inp["gamma"], inp["dO"], clip=clip, S0=S0, R0=R0,
+                           dS_final=dS_final, dR_final=dR_final, cu_seqlens=inp["cu_seqlens"])
+
+
+def nudge(variant, inp, dtype, clip=1.0, S0=None, R0=None, margin=None):
+    """Moves v (on its dtype's grid) so no pre-clip residual is within `margin`
+    of the clip kink; masks taken in two precisions then agree."""
+    if margin is None:
+        margin = 1e-2 if dtype == "bf16" else 1e-4
+    v, moved = oracle.nudge_margin(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"],
+                                   inp["beta"], inp["alpha_r"], inp["gamma"], clip=clip, S0=S0,
+                                   R0=R0, cu_seqlens=inp["cu_seqlens"], margin=margin,
+                                   grid="bf16" if dtype == "bf16" else "f32")
+    out = dict(inp)
+    out["v"] = v.astype(np.float32)
+    return out, moved
+
+
+GRAD_KEYS = ("dq", "dk", "dv", "dalpha_s", "dbeta", "dalpha_r", "dgamma", "dS0", "dR0")

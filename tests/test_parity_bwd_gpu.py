@@ -1,0 +1,91 @@
+"""GPU backward parity: rdn_backward / rla_backward through the C ABI against
+the oracle's hand-derived adjoint (itself pinned to finite differences), on
+identical seeded inputs, for all nine gradient tensors.
+
+Clip masks are a step function of the residual; the inputs are moved (on the
+input dtype's grid) so no residual lies within 1e-2 (bf16) / 1e-4 (fp32) of
+the kink, so both sides take the same mask."""
+import math
+
+import numpy as np
+import pytest
+
+import datagen
+from tests.gpu_util import (GRAD_KEYS, TOL, gpu_backward, nudge, oracle_backward, rel_err,
+                            select)
+
+pytestmark = pytest.mark.gpu
+
+
+def check(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dSf=None, dRf=None,
+          dense_B=None, label=""):
+    inp, moved = nudge(variant, inp, dtype, clip=clip, S0=S0, R0=R0)
+    g = gpu_backward(variant, inp, dtype, device, clip=clip, S0=S0, R0=R0, dS_final=dSf,
+                     dR_final=dRf, dense_B=dense_B)
+    ref = oracle_backward(variant, inp, clip=clip, S0=S0, R0=R0, dS_final=dSf, dR_final=dRf)
+    errs = {key: rel_err(g[key], ref[key]) for key in GRAD_KEYS}
+    print("[%s %s %s moved=%d] %s" % (variant, dtype, label, moved,
+                                      " ".join("%s=%.1e" % kv for kv in errs.items())))
+    for key, e in errs.items():
+        assert e <= TOL[dtype], (key, e)
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128), ("bf16", 64)])
+def test_dense_ragged(device, variant, dtype, d):
+    wl = datagen.small(variant + "_fwdbwd", dtype, [150, 150], H=2, d=d, varlen=False)
+    inp = datagen.make_inputs(wl, seed=201)
+    check(variant, inp, dtype, device, dense_B=2, label="B2 T150 d%d" % d)
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_states_in_and_out(device, variant, dtype, d):
+    """Non-zero S0, R0 and upstream gradients on the final states."""
+    wl = datagen.small(variant + "_fwdbwd", dtype, [100], H=2, d=d, varlen=False)
+    inp = datagen.make_inputs(wl, seed=202)
+    S0, R0 = datagen.random_states(9, 1, 2, d, d)
+    dSf, dRf = datagen.random_states(10, 1, 2, d, d, scale=1.0)
+    check(variant, inp, dtype, device, S0=S0, R0=R0, dSf=dSf, dRf=dRf, dense_B=1, label="states")
+    check(variant, inp, dtype, device, clip=math.inf, S0=S0, R0=R0, dense_B=1, label="noclip")
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_varlen_edges(device, variant, dtype, d):
+    lens = [1, 63, 0, 64, 65, 130]
+    wl = datagen.small(variant + "_fwdbwd", dtype, lens, H=2, d=d)
+    inp = datagen.make_inputs(wl, seed=203)
+    S0, R0 = datagen.random_states(11, len(lens), 2, d, d)
+    check(variant, inp, dtype, device, S0=S0, R0=R0, label="varlen")
+
+
+@pytest.mark.slow
+def test_full_training_workload_sampled(device):
+    """The fwd+bwd workload at full size (B=4, T=4096, H=16, d=128, bf16),
+    checked on sampled (sequence, head) pairs: the sampled pairs' v is moved
+    off the clip kink by the oracle, the GPU runs the whole problem."""
+    wl = datagen.WORKLOADS[5]
+    inp = datagen.make_inputs(wl, seed=5)
+    cu = inp["cu_seqlens"]
+    samples = [(0, 3), (3, 15)]
+    for n, h in samples:
+        sub = select(inp, [n], [h])
+        sub, _ = nudge("rdn", sub, "bf16")
+        inp["v"][cu[n]:cu[n + 1], h] = sub["v"][:, 0]
+    g = gpu_backward("rdn", inp, "bf16", device, dense_B=wl.B)
+    for n, h in samples:
+        sub = select(inp, [n], [h])
+        ref = oracle_backward("rdn", sub)
+        sl = slice(cu[n], cu[n + 1])
+        errs = {}
+        for key in GRAD_KEYS:
+            if key in ("dS0", "dR0"):
+                errs[key] = rel_err(g[key][n, h], ref[key][0, 0])
+            elif key in ("dq", "dk", "dv"):
+                errs[key] = rel_err(g[key][sl, h], ref[key][:, 0])
+            else:
+                errs[key] = rel_err(g[key][sl, h], ref[key][:, 0])
+        print("[cfg5 seq%d head%d] %s" % (n, h, " ".join("%s=%.1e" % kv for kv in errs.items())))
+        for key, e in errs.items():
+            assert e <= TOL["bf16"], (n, h, key, e)
