@@ -87,16 +87,22 @@ def dense(name, op, dtype, B, T, H, d, decay_mu=2.0, clip=1.0) -> Workload:
     return Workload(name, op, dtype, H, d, d, (T,) * B, False, decay_mu, clip)
 
 
-#: The five workloads: the small fp32 case, the three forward workloads and the
-#: training-step workload whose fwd+bwd throughput is the headline metric.
-WORKLOADS: Dict[int, Workload] = {
-    1: dense("rdn_fwd_f32_B1_H2_T256_d64", "rdn_fwd", "f32", 1, 256, 2, 64),
-    2: dense("rla_fwd_bf16_B4_H16_T2048_d128", "rla_fwd", "bf16", 4, 2048, 16, 128, decay_mu=3.0),
-    3: dense("rdn_fwd_bf16_B8_H16_T4096_d128", "rdn_fwd", "bf16", 8, 4096, 16, 128),
-    4: Workload("rdn_fwd_varlen_bf16_262144tok_H16_d128", "rdn_fwd", "bf16", 16, 128, 128,
-                varlen_lengths(4, 262144, 512, 32768), True),
-    5: dense("rdn_fwdbwd_bf16_B4_H16_T4096_d128", "rdn_fwdbwd", "bf16", 4, 4096, 16, 128),
-}
+#: The workloads: a small fp32 case, three forward workloads at language-model
+#: shapes (dense RLA, dense RDN, packed variable-length RDN) and the
+#: forward+backward training-step workload.
+_ALL = [
+    dense("rdn_fwd_f32_B1_H2_T256_d64", "rdn_fwd", "f32", 1, 256, 2, 64),
+    dense("rla_fwd_bf16_B4_H16_T2048_d128", "rla_fwd", "bf16", 4, 2048, 16, 128, decay_mu=3.0),
+    dense("rdn_fwd_bf16_B8_H16_T4096_d128", "rdn_fwd", "bf16", 8, 4096, 16, 128),
+    Workload("rdn_fwd_varlen_bf16_262144tok_H16_d128", "rdn_fwd", "bf16", 16, 128, 128,
+             varlen_lengths(4, 262144, 512, 32768), True),
+    dense("rdn_fwdbwd_bf16_B4_H16_T4096_d128", "rdn_fwdbwd", "bf16", 4, 4096, 16, 128),
+]
+WORKLOADS: Dict[str, Workload] = {wl.name: wl for wl in _ALL}
+#: seed of each workload's inputs
+SEEDS: Dict[str, int] = {wl.name: i + 1 for i, wl in enumerate(_ALL)}
+#: the training-step workload (forward + backward) used by the benchmark
+TRAINING = "rdn_fwdbwd_bf16_B4_H16_T4096_d128"
 
 
 def round_to_bf16(x: np.ndarray) -> np.ndarray:

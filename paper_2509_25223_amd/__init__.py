@@ -93,6 +93,11 @@ def rla_set_stage_events(events) -> None:
         _event_handles = None
         lib.rla_set_stage_events(None, 0)
         return
+    for e in events:
+        if not e.cuda_event:   # torch creates its event on the first record
+            e.record()
+    if not all(e.cuda_event for e in events):
+        raise RuntimeError("could not create the HIP events")
     _event_handles = (ctypes.c_void_p * len(events))(*[e.cuda_event for e in events])
     lib.rla_set_stage_events(ctypes.cast(_event_handles, ctypes.c_void_p), len(events))
 

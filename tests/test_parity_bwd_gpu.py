@@ -65,8 +65,8 @@ def test_full_training_workload_sampled(device):
     """The fwd+bwd workload at full size (B=4, T=4096, H=16, d=128, bf16),
     checked on sampled (sequence, head) pairs: the sampled pairs' v is moved
     off the clip kink by the oracle, the GPU runs the whole problem."""
-    wl = datagen.WORKLOADS[5]
-    inp = datagen.make_inputs(wl, seed=5)
+    wl = datagen.WORKLOADS[datagen.TRAINING]
+    inp = datagen.make_inputs(wl, seed=datagen.SEEDS[datagen.TRAINING])
     cu = inp["cu_seqlens"]
     samples = [(0, 3), (3, 15)]
     for n, h in samples:
@@ -86,6 +86,6 @@ def test_full_training_workload_sampled(device):
                 errs[key] = rel_err(g[key][sl, h], ref[key][:, 0])
             else:
                 errs[key] = rel_err(g[key][sl, h], ref[key][:, 0])
-        print("[cfg5 seq%d head%d] %s" % (n, h, " ".join("%s=%.1e" % kv for kv in errs.items())))
+        print("[%s seq%d head%d] %s" % (wl.name, n, h, " ".join("%s=%.1e" % kv for kv in errs.items())))
         for key, e in errs.items():
             assert e <= TOL["bf16"], (n, h, key, e)

@@ -92,17 +92,20 @@ def test_empty_problem(device):
 
 # --- full-size workloads, sampled (sequence, head) pairs ---------------------
 
-FULL = {2: [(0, 0), (3, 15)], 3: [(0, 5), (7, 15)], 4: [(0, 0), (None, 9)]}
+FULL = {"rdn_fwd_f32_B1_H2_T256_d64": [(0, 0), (0, 1)],
+        "rla_fwd_bf16_B4_H16_T2048_d128": [(0, 0), (3, 15)],
+        "rdn_fwd_bf16_B8_H16_T4096_d128": [(0, 5), (7, 15)],
+        "rdn_fwd_varlen_bf16_262144tok_H16_d128": [(0, 0), (None, 9)]}
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
-def test_full_workload_sampled(device, cfg):
-    wl = datagen.WORKLOADS[cfg]
-    inp = datagen.make_inputs(wl, seed=cfg, grads=False)
+@pytest.mark.parametrize("name", sorted(FULL))
+def test_full_workload_sampled(device, name):
+    wl = datagen.WORKLOADS[name]
+    inp = datagen.make_inputs(wl, seed=datagen.SEEDS[name], grads=False)
     dense_B = None if wl.varlen else wl.B
     o, Sf, Rf = gpu_forward(wl.variant, inp, wl.dtype, device, clip=wl.clip, dense_B=dense_B)
-    samples = FULL.get(cfg, [(0, h) for h in range(wl.H)])
+    samples = FULL[name]
     cu = inp["cu_seqlens"]
     for n, h in samples:
         if n is None:
@@ -112,6 +115,6 @@ def test_full_workload_sampled(device, cfg):
         sl = slice(cu[n], cu[n + 1])
         errs = dict(o=rel_err(o[sl, h:h + 1], ro), S=rel_err(Sf[n, h], rS[0, 0]),
                     R=rel_err(Rf[n, h], rR[0, 0]))
-        print("[cfg%d seq%d head%d] %s" % (cfg, n, h, " ".join("%s=%.2e" % kv for kv in errs.items())))
+        print("[%s seq%d head%d] %s" % (name, n, h, " ".join("%s=%.2e" % kv for kv in errs.items())))
         for key, e in errs.items():
-            assert e <= TOL[wl.dtype], (cfg, n, h, key, e)
+            assert e <= TOL[wl.dtype], (name, n, h, key, e)
