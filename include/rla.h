@@ -100,7 +100,21 @@ typedef struct {
   int32_t dtype;            /* rla_dtype of q, k, v, dO */
   float clip;               /* c >= 0, or +INFINITY for no clipping */
   int32_t out_dtype;        /* rla_dtype of o, dq, dk, dv (fp32 inputs: fp32 only) */
+  uint32_t flags;           /* RLA_FLAG_* bits, 0 by default */
 } rla_problem;
+
+/*
+ * Save-for-backward (training).  With RLA_FLAG_SAVE_FOR_BACKWARD a forward
+ * call needs a workspace of rla_workspace_size(problem, <backward op>) bytes
+ * and leaves in it what the matching backward recomputes otherwise (the chunk
+ * tables and matrices, the chunk-start states and the clip masks).  With
+ * RLA_FLAG_USE_SAVED a backward call skips that recomputation and reads the
+ * workspace instead: the caller guarantees that the last forward written to
+ * that workspace had the same problem and inputs and the save flag (this
+ * cannot be checked).  Without the flags every call is self-contained.
+ */
+#define RLA_FLAG_SAVE_FOR_BACKWARD 1u
+#define RLA_FLAG_USE_SAVED 2u
 
 /* Bytes of workspace the operation needs for this problem (0 if the problem
  * is invalid).  Pure host function. */

@@ -24,6 +24,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "librla_mi355x.so")
 
 RLA_OK = 0
+RLA_FLAG_SAVE_FOR_BACKWARD, RLA_FLAG_USE_SAVED = 1, 2
 RLA_F32, RLA_BF16 = 0, 1
 RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD, RLA_OP_RLA_BACKWARD = 0, 1, 2, 3
 
@@ -36,7 +37,8 @@ class rla_problem(ctypes.Structure):
                 ("num_heads", ctypes.c_int64), ("head_dim_k", ctypes.c_int64),
                 ("head_dim_v", ctypes.c_int64), ("num_seqs", ctypes.c_int64),
                 ("cu_seqlens", ctypes.c_void_p), ("dtype", ctypes.c_int32),
-                ("clip", ctypes.c_float), ("out_dtype", ctypes.c_int32)]
+                ("clip", ctypes.c_float), ("out_dtype", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
 
 
 class RLAError(RuntimeError):
@@ -137,7 +139,8 @@ def _dtype_code(dt):
     raise TypeError("dtype must be bfloat16 or float32")
 
 
-def make_problem(q, v, cu_seqlens=None, clip: float = 1.0, out_dtype=None) -> rla_problem:
+def make_problem(q, v, cu_seqlens=None, clip: float = 1.0, out_dtype=None,
+                 flags: int = 0) -> rla_problem:
     """rla_problem for q [B,T,H,dk] / [T,H,dk] and v, with optional cu_seqlens.
     out_dtype (dtype of o, dq, dk, dv) defaults to float32."""
     torch = _torch()
@@ -163,7 +166,7 @@ def make_problem(q, v, cu_seqlens=None, clip: float = 1.0, out_dtype=None) -> rl
         N = cu_seqlens.numel() - 1
     c = math.inf if clip is None else float(clip)
     out = _dtype_code(torch.float32 if out_dtype is None else out_dtype)
-    return rla_problem(B, T, H, dk, dv, N, _ptr(cu_seqlens), dtype, c, out)
+    return rla_problem(B, T, H, dk, dv, N, _ptr(cu_seqlens), dtype, c, out, flags)
 
 
 def _check(tensors, device):
@@ -187,10 +190,13 @@ def _workspace(problem, op, device, workspace):
 
 
 def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_seqlens,
-             out, workspace, stream, return_states, out_dtype):
+             out, workspace, stream, return_states, out_dtype, save_for_backward):
     torch = _torch()
     lib = load_library()
-    problem = make_problem(q, v, cu_seqlens, clip, out_dtype)
+    problem = make_problem(q, v, cu_seqlens, clip, out_dtype,
+                           RLA_FLAG_SAVE_FOR_BACKWARD if save_for_backward else 0)
+    if save_for_backward:
+        op = RLA_OP_RDN_BACKWARD if op == RLA_OP_RDN_FORWARD else RLA_OP_RLA_BACKWARD
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S0=S0, R0=R0), dev)
@@ -218,26 +224,35 @@ def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_
 
 def rla_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
                 cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
-                out_dtype=None):
-    """RLA forward (Sec. 3.4, left box).  Returns (o, S_final, R_final)."""
+                out_dtype=None, save_for_backward=False):
+    """RLA forward (Sec. 3.4, left box).  Returns (o, S_final, R_final).
+    With save_for_backward the (backward-sized) workspace keeps what the
+    matching backward call with use_saved=True reads instead of recomputing."""
     return _forward("rla_forward", RLA_OP_RLA_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
-                    clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype)
+                    clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
+                    save_for_backward)
 
 
 def rdn_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
                 cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
-                out_dtype=None):
-    """RDN forward (Sec. 3.4, right box).  Returns (o, S_final, R_final)."""
+                out_dtype=None, save_for_backward=False):
+    """RDN forward (Sec. 3.4, right box).  Returns (o, S_final, R_final).
+    With save_for_backward the (backward-sized) workspace keeps what the
+    matching backward call with use_saved=True reads instead of recomputing."""
     return _forward("rdn_forward", RLA_OP_RDN_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
-                    clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype)
+                    clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
+                    save_for_backward)
 
 
 def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None):
+                 stream=None, grads=None, out_dtype=None, use_saved=False):
     torch = _torch()
     lib = load_library()
-    problem = make_problem(q, v, cu_seqlens, clip, out_dtype)
+    if use_saved and workspace is None:
+        raise ValueError("use_saved needs the workspace of the saving forward call")
+    problem = make_problem(q, v, cu_seqlens, clip, out_dtype,
+                           RLA_FLAG_USE_SAVED if use_saved else 0)
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S0=S0, R0=R0, dO=dO, dS_final=dS_final, dR_final=dR_final), dev)
@@ -269,18 +284,19 @@ def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float 
 
 def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None):
+                 stream=None, grads=None, out_dtype=None, use_saved=False):
     """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rdn_forward.
-    Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0."""
+    Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0.
+    use_saved: read what rdn_forward(save_for_backward=True) left in `workspace`."""
     return _backward("rdn_backward", RLA_OP_RDN_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
-                     out_dtype)
+                     out_dtype, use_saved)
 
 
 def rla_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None):
+                 stream=None, grads=None, out_dtype=None, use_saved=False):
     """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rla_forward."""
     return _backward("rla_backward", RLA_OP_RLA_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
-                     out_dtype)
+                     out_dtype, use_saved)

@@ -30,7 +30,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Problem {
   int64_t B = 0, T = 0, H = 0, DK = 0, DV = 0, N = 0, ntok = 0, max_chunks = 0;
-  bool varlen = false, bf16 = false, out_bf16 = false;
+  bool varlen = false, bf16 = false, out_bf16 = false, save = false, use_saved = false;
   const int32_t* cu = nullptr;
   float clip = -1.f;
 };
@@ -52,6 +52,9 @@ rla_status check_problem(const rla_problem* pp, Problem& pr) {
   if (pp->out_dtype != RLA_F32 && pp->out_dtype != RLA_BF16) return RLA_ERR_DTYPE;
   if (pp->dtype == RLA_F32 && pp->out_dtype != RLA_F32) return RLA_ERR_DTYPE;
   if (isnan(pp->clip) || pp->clip < 0.f) return RLA_ERR_VALUE;
+  if (pp->flags & ~(RLA_FLAG_SAVE_FOR_BACKWARD | RLA_FLAG_USE_SAVED)) return RLA_ERR_VALUE;
+  pr.save = (pp->flags & RLA_FLAG_SAVE_FOR_BACKWARD) != 0;
+  pr.use_saved = (pp->flags & RLA_FLAG_USE_SAVED) != 0;
   pr.B = pp->batch;
   pr.T = pp->seq_len;
   pr.H = pp->num_heads;
@@ -166,7 +169,9 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
     return RLA_ERR_NULL_ARG;
   if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)))
     return RLA_ERR_VALUE;
-  const Workspace w = plan(pr, rdn ? RLA_OP_RDN_FORWARD : RLA_OP_RLA_FORWARD);
+  const int op = pr.save ? (rdn ? RLA_OP_RDN_BACKWARD : RLA_OP_RLA_BACKWARD)
+                         : (rdn ? RLA_OP_RDN_FORWARD : RLA_OP_RLA_FORWARD);
+  const Workspace w = plan(pr, op);
   st = check_workspace(w, workspace, workspace_bytes);
   if (st != RLA_OK) return st;
   if (pr.N == 0) return RLA_OK;
@@ -178,6 +183,11 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
   p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
   p.S0 = S0; p.R0 = R0;
   p.o = o; p.S_fin = S_final; p.R_fin = R_final;
+  if (pr.save) {
+    p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
+    p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
+    p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
+  }
 
   hipError_t e = hipSuccess;
   if (pr.varlen && pr.ntok > 0)   // tokens outside every sequence read as zero
@@ -186,7 +196,7 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
   if (e == hipSuccess) e = mark_stage(stream, true);
   if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
-  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/true, /*ckpt=*/false, stream);
+  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/true, /*ckpt=*/pr.save, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
   return to_status(e);
 }
@@ -239,12 +249,14 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
     if (e == hipSuccess) e = hipMemsetAsync(dalpha_r, 0, tok * 4, stream);
     if (e == hipSuccess) e = hipMemsetAsync(dgamma, 0, tok * 4, stream);
   }
-  if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
+  if (e == hipSuccess && !pr.use_saved) e = build_tables(pr, w, ws, stream);
   if (e == hipSuccess) e = mark_stage(stream, true);
-  if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
-  if (e == hipSuccess) e = mark_stage(stream, false);
-  if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/false, /*ckpt=*/true, stream);
-  if (e == hipSuccess) e = mark_stage(stream, false);
+  if (!pr.use_saved) {
+    if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
+    if (e == hipSuccess) e = mark_stage(stream, false);
+    if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/false, /*ckpt=*/true, stream);
+    if (e == hipSuccess) e = mark_stage(stream, false);
+  }
   if (e == hipSuccess) e = launch_bwd_scan(p, pr.bf16, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
   if (e == hipSuccess) e = launch_bwd_grad(p, pr.bf16, stream);

@@ -34,7 +34,10 @@ struct BwdScanLayout {
   static constexpr int kPad = kBF ? 8 : 4;
   static constexpr int kLdX = kChunk + kPad;
   static constexpr int kLdS = DK + kPad;
-  static constexpr int kNumM = RDN ? 5 : 1;
+  // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs T^S and
+  // MR (first and last released) are double-buffered
+  static constexpr bool kDB = kBF;
+  static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 2 : 1);
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kNumBufs = 6;
   static constexpr int kKT = 0;
@@ -42,12 +45,25 @@ struct BwdScanLayout {
   static constexpr int kCopies = kQT + DK * kLdX * (int)sizeof(XT);
   static constexpr int kCopyBytes = BV * kLdS * (int)sizeof(IN);
   static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
-  static constexpr int kBufs = kMats + kNumM * kChunk * kLdX * (int)sizeof(XT);
+  static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
   static constexpr int kBufBytes = BV * kLdX * (int)sizeof(XT);
   static constexpr int kMask = kBufs + kNumBufs * kBufBytes;
-  static constexpr int kGates = kMask + kChunk * BV;
+  static constexpr int kMaskBytes = kChunk * BV;
+  static constexpr int kGraw = kMask + kMaskBytes;
+  static constexpr int kGates = kGraw + kGateBlock * 4;
   static constexpr int kBytes = kGates + 10 * kChunk * 4;
+  static_assert(kMaskBytes % 1024 == 0, "mask block moved in whole DMA instructions");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
+  // RDN: TS[2] MG MP TR MR[2]; RLA: MR[2]
+  __device__ static constexpr int slot(int mat, int buf) {
+    if (!RDN) return kDB ? buf : 0;
+    if (mat == kMatTS) return kDB ? buf : 0;
+    const int b = kDB ? 2 : 1;
+    if (mat == kMatMG) return b;
+    if (mat == kMatMP) return b + 1;
+    if (mat == kMatTR) return b + 2;
+    return kDB ? b + 3 + buf : b + 3;   // MR
+  }
 };
 
 // per-token block slots ([BV][64], value-major); aliases follow lifetimes:
@@ -59,15 +75,18 @@ enum { bDB_DKS = 0, bDC_DX = 1, bQDB = 2, bQDC = 3, bDUR_DU = 4, bDKR = 5 };
 template <typename IN>
 __device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int ld, floatx4 v) {
   const int off = acc_col() * ld + acc_row(0);
+  if constexpr (sizeof(IN) == 2) {   // 8-byte stores of 4 consecutive rows
+    u16x4 h4, l4;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    if constexpr (sizeof(IN) == 2) {
-      const u16 h = f2bf(v[r]);
-      hi[off + r] = h;
-      lo[off + r] = bf16_lo(v[r], h);
-    } else {
-      hi[off + r] = v[r];
+    for (int r = 0; r < 4; ++r) {
+      h4[r] = f2bf(v[r]);
+      l4[r] = bf16_lo(v[r], h4[r]);
     }
+    *reinterpret_cast<u16x4*>(hi + off) = h4;
+    *reinterpret_cast<u16x4*>(lo + off) = l4;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) hi[off + r] = v[r];
   }
 }
 
@@ -87,9 +106,12 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   IN* dRhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
   IN* dSlo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);   // bf16 only
   IN* dRlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);   // bf16 only
-  XT* mats = reinterpret_cast<XT*>(smem + L::kMats);
-  auto buf = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBufs + b * L::kBufBytes); };
+  auto mat = [&](int m, int buf) {
+    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
+  };
+  auto blk = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBufs + b * L::kBufBytes); };
   uint8_t* mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
+  float* graw = reinterpret_cast<float*>(smem + L::kGraw);
   float* gbt = reinterpret_cast<float*>(smem + L::kGates);
   float* ggm = gbt + kChunk;
   float* egs = ggm + kChunk;
@@ -98,12 +120,6 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   float* dls = egr + kChunk;
   float* dlr = dls + kChunk;
   float* edge = dlr + kChunk;
-  // matrix slots: RDN {TS, MG, MP, TR, MR}; RLA {MR}
-  XT* mTS = mats;
-  XT* mMG = mats + 1 * kChunk * L::kLdX;
-  XT* mMP = mats + 2 * kChunk * L::kLdX;
-  XT* mTR = mats + 3 * kChunk * L::kLdX;
-  XT* mMR = mats + (RDN ? 4 : 0) * kChunk * L::kLdX;
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int nvb = DV / BV;
@@ -144,10 +160,101 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   const IN* dog = reinterpret_cast<const IN*>(p.dO);
   const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
 
+  // ---- staging of the next (earlier) chunk while this one computes ----
+  //   K, Q, dO: register prefetch after P1 (transposed / converted at commit)
+  //   gates, T^S, MR: LDS-DMA after P1 (T^S, MR double-buffered)
+  //   T^R, mask: after P3;  MG, MP: after P4 (their last uses)
+  // bf16 inputs; fp32 inputs single-buffer every matrix and move them all
+  // after the chunk's last barrier.
+  constexpr int kOPerThread = kChunk * BV / kThreads;
+  typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];
+  IN on[kOPerThread];
+  auto chunk_len = [&](int c) { return min(kChunk, si.len - c * kChunk); };
+  auto mat_src = [&](int c, int m) {
+    return matg + ((int64_t)(si.chunk0 + c) * H + h) * kNumMats * kMatElems + m * kMatElems;
+  };
+  auto issue_regs = [&](int c) {
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    const int t = 16 * w + (lane & 15);
+    const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
+    load_rowfrags<IN, DK>(Kn, t < len ? kg + roff : nullptr);
+    load_rowfrags<IN, DK>(Qn, t < len ? qg + roff : nullptr);
+#pragma unroll
+    for (int u = 0; u < kOPerThread; ++u) {
+      const int e = tid + u * kThreads, tt = e / BV, j = e % BV;
+      on[u] = tt < len ? dog[((tok + tt) * H + h) * (int64_t)DV + j0 + j] : from_f<IN>(0.f);
+    }
+  };
+  auto issue_gates = [&](int c) {
+    if (w == 0)
+      dma_linear_wave(p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock, graw,
+                      kGateBlock * 4);
+  };
+  auto issue_mask = [&](int c) {   // rows of BV bytes; padding rows read row 0 (masked by 0 grads)
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    constexpr int kPerRow = BV / 16;
+#pragma unroll
+    for (int m = 0; m < L::kMaskBytes / 1024; ++m) {
+      if (w == m) {
+        const int P = m * 64 + lane, t = P / kPerRow, cc = P % kPerRow;
+        const int ts = t < len ? t : 0;
+        const uint8_t* src = p.ck_mask + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * 16;
+        dma16(src, mask + m * 1024);
+      }
+    }
+  };
+  auto issue_early = [&](int c) {   // after P1
+    issue_gates(c);
+    if constexpr (L::kDB) {
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, c & 1));
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
+    }
+  };
+  auto issue_mid = [&](int c) {     // after P3
+    if constexpr (L::kDB) {
+      issue_mask(c);
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+    }
+  };
+  auto issue_late = [&](int c) {    // after P4
+    if constexpr (L::kDB && RDN) {
+      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
+      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
+    }
+  };
+  auto issue_all_single = [&](int c) {   // fp32: everything after the last barrier
+    if constexpr (!L::kDB) {
+      issue_mask(c);
+      if constexpr (RDN) {
+        dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
+        dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
+        dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
+        dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+      }
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0));
+    }
+  };
+  if (nch > 0) {
+    const int c = nch - 1;
+    issue_regs(c);
+    issue_gates(c);
+    issue_mask(c);
+    if constexpr (RDN) {
+      dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, c & 1));
+      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
+      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
+      dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+    }
+    dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
+    wait_vmem();
+  }
+  barrier_lds();
+
   for (int c = nch - 1; c >= 0; --c) {
     const int gc = si.chunk0 + c;
-    const int64_t tok = si.start + (int64_t)c * kChunk;
-    const int len = min(kChunk, si.len - c * kChunk);
+    const int buf = c & 1;
 
     {   // gradient w.r.t. this chunk's end states
       const int64_t off = ((int64_t)gc * H + h) * DK * DV;
@@ -163,58 +270,40 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
           }
     }
 
-    // ---- stage the chunk ----
+    // ---- commit: K fragments, K^T and Q^T (XT), dO^T, gate vectors ----
     typename MI::frag Kf[KS_STEPS];
     {
-      typename MI::frag Qf[KS_STEPS];
       const int t = 16 * w + (lane & 15);
-      const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
-      load_rowfrags<IN, DK>(Kf, t < len ? kg + roff : nullptr);
-      load_rowfrags<IN, DK>(Qf, t < len ? qg + roff : nullptr);
 #pragma unroll
-      for (int s = 0; s < KS_STEPS; ++s) {
+      for (int s2 = 0; s2 < KS_STEPS; ++s2) {
+        Kf[s2] = Kn[s2];
         if constexpr (BF) {
-          const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s]);
-          const u16x8 qv = __builtin_bit_cast(u16x8, Qf[s]);
+          const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
+          const u16x8 qv = __builtin_bit_cast(u16x8, Qn[s2]);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const int i = s * 32 + (lane >> 4) * 8 + e;
+            const int i = s2 * 32 + (lane >> 4) * 8 + e;
             KT[i * L::kLdX + t] = from_f<XT>(bf2f(kv[e]));
             QT[i * L::kLdX + t] = from_f<XT>(bf2f(qv[e]));
           }
         } else {
-          const int i = s * 4 + (lane >> 4);
-          KT[i * L::kLdX + t] = Kf[s];
-          QT[i * L::kLdX + t] = Qf[s];
+          const int i = s2 * 4 + (lane >> 4);
+          KT[i * L::kLdX + t] = Kn[s2];
+          QT[i * L::kLdX + t] = Qn[s2];
         }
       }
-      XT* dbT = buf(bDB_DKS);
-      for (int e = tid; e < kChunk * BV; e += kThreads) {
-        const int tt = e / BV, j = e % BV;
-        const int64_t gi = ((tok + tt) * H + h) * (int64_t)DV + j0 + j;
-        dbT[j * L::kLdX + tt] = from_f<XT>(tt < len ? to_f<IN>(dog[gi]) : 0.f);
-        mask[tt * BV + j] = tt < len ? p.ck_mask[gi] : 0;
-      }
-      constexpr int kVecM = 16 / sizeof(XT);
-      constexpr int kMatVecs = kMatElems / kVecM;
-      const XT* mg = matg + ((int64_t)gc * H + h) * kNumMats * kMatElems;
-      constexpr int kSrc[5] = {kMatTS, kMatMG, kMatMP, kMatTR, kMatMR};
+      XT* dbT = blk(bDB_DKS);
 #pragma unroll
-      for (int m = 0; m < L::kNumM; ++m) {
-        const int src = RDN ? kSrc[m] : kMatMR;
-        for (int e = tid; e < kMatVecs; e += kThreads) {
-          const int tt = e / (kChunk / kVecM), ss = (e % (kChunk / kVecM)) * kVecM;
-          *reinterpret_cast<uint4*>(mats + (m * kChunk + tt) * L::kLdX + ss) =
-              *reinterpret_cast<const uint4*>(mg + src * kMatElems + tt * kChunk + ss);
-        }
+      for (int u = 0; u < kOPerThread; ++u) {
+        const int e = tid + u * kThreads, tt = e / BV, j = e % BV;
+        dbT[j * L::kLdX + tt] = from_f<XT>(to_f<IN>(on[u]));
       }
       if (tid < kChunk) {
-        const float* gb = p.gate_ws + ((int64_t)gc * H + h) * kGateBlock;
         const int tt = tid;
-        const float gs = gb[tt], gsl = gb[kChunk - 1], gsp = tt > 0 ? gb[tt - 1] : 0.f;
-        const float gr = gb[64 + tt], grl = gb[64 + kChunk - 1];
-        gbt[tt] = gb[128 + tt];
-        ggm[tt] = gb[192 + tt];
+        const float gs = graw[tt], gsp = tt > 0 ? graw[tt - 1] : 0.f, gsl = graw[kChunk - 1];
+        const float gr = graw[64 + tt], grl = graw[64 + kChunk - 1];
+        gbt[tt] = graw[128 + tt];
+        ggm[tt] = graw[192 + tt];
         egs[tt] = __expf(gs);
         egsp[tt] = __expf(gsp);
         egr[tt] = __expf(gr);
@@ -226,7 +315,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         }
       }
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- P1: K dS_end, K dR_end (split state); scaled copies of dO ----
     floatx4 KdS[JT], KdR[JT];
@@ -245,28 +334,32 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r), j = jt * 16 + acc_col();
-        const float o = to_f<XT>(buf(bDB_DKS)[j * L::kLdX + t]);
-        dc[r] = ggm[t] * o;
-        qdb[r] = egs[t] * o;
+        const float o2 = to_f<XT>(blk(bDB_DKS)[j * L::kLdX + t]);
+        dc[r] = ggm[t] * o2;
+        qdb[r] = egs[t] * o2;
         qdc[r] = egr[t] * dc[r];
       }
-      store_acc_t<XT>(buf(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dc);
-      store_acc_t<XT>(buf(bQDB) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdb);
-      store_acc_t<XT>(buf(bQDC) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdc);
+      store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dc);
+      store_acc_t<XT>(blk(bQDB) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdb);
+      store_acc_t<XT>(blk(bQDC) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdc);
     }
-    __syncthreads();
+    barrier_lds();
+    if (c > 0) {
+      issue_regs(c - 1);
+      issue_early(c - 1);
+    }
 
     // ---- P2: dUR = diag(e^{h_C-h}) K dR_end + MR^T dc ----
     floatx4 dUR[JT];
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       floatx4 a = zero4();
-      mma_tile<XT, kChunk, false, true>(a, mMR + 16 * w, L::kLdX, buf(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+      mma_swz_cols<XT>(a, mat(kMatMR, buf), 16 * w, blk(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
 #pragma unroll
       for (int r = 0; r < 4; ++r) dUR[jt][r] = dlr[16 * w + acc_row(r)] * KdR[jt][r] + a[r];
-      if constexpr (RDN) store_acc_t<XT>(buf(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dUR[jt]);
+      if constexpr (RDN) store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dUR[jt]);
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- P3: dYR, dX, dKR (RLA: dKS) ----
     floatx4 dX[JT];
@@ -275,7 +368,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       floatx4 dYR = dUR[jt];
       if constexpr (RDN) {
         dYR = zero4();
-        mma_tile<XT, kChunk, false, true>(dYR, mTR + 16 * w, L::kLdX, buf(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_cols<XT>(dYR, mat(kMatTR, 0), 16 * w, blk(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
       }
       floatx4 dkr, dks;
 #pragma unroll
@@ -286,39 +379,41 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         dks[r] = -egsp[t] * dX[jt][r];
       }
       if constexpr (RDN) {
-        store_acc_t<XT>(buf(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
-        store_acc_t<XT>(buf(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dkr);
+        store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
+        store_acc_t<XT>(blk(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dkr);
       } else {
-        store_acc_t<XT>(buf(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
+        store_acc_t<XT>(blk(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
       }
     }
-    __syncthreads();
+    barrier_lds();
+    if (c > 0) issue_mid(c - 1);
 
     if constexpr (RDN) {
       // ---- P4: dU = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX ----
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 a = zero4(), b = zero4(), du;
-        mma_tile<XT, kChunk, false, true>(a, mMP + 16 * w, L::kLdX, buf(bDB_DKS) + jt * 16 * L::kLdX, L::kLdX);
-        mma_tile<XT, kChunk, false, true>(b, mMG + 16 * w, L::kLdX, buf(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_cols<XT>(a, mat(kMatMP, 0), 16 * w, blk(bDB_DKS) + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_cols<XT>(b, mat(kMatMG, 0), 16 * w, blk(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
-        store_acc_t<XT>(buf(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
       }
-      __syncthreads();
+      barrier_lds();
+      if (c > 0) issue_late(c - 1);
       // ---- P5: dY = T^S^T dU, dKS ----
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 dY = zero4(), dks;
-        mma_tile<XT, kChunk, false, true>(dY, mTS + 16 * w, L::kLdX, buf(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_cols<XT>(dY, mat(kMatTS, buf), 16 * w, blk(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
           dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[r];
         }
-        store_acc_t<XT>(buf(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
+        store_acc_t<XT>(blk(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
       }
-      __syncthreads();
+      barrier_lds();
     }
 
     // ---- P6: state gradients at the chunk start ----
@@ -331,14 +426,19 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         dS[it][jt] *= eS;
         dR[it][jt] *= eR;
         const int bo = jt * 16 * L::kLdX;
-        mma_tile<XT, kChunk, true, true>(dS[it][jt], QT + i0 * L::kLdX, L::kLdX, buf(bQDB) + bo, L::kLdX);
-        mma_tile<XT, kChunk, true, true>(dS[it][jt], KT + i0 * L::kLdX, L::kLdX, buf(bDB_DKS) + bo, L::kLdX);
-        mma_tile<XT, kChunk, true, true>(dR[it][jt], QT + i0 * L::kLdX, L::kLdX, buf(bQDC) + bo, L::kLdX);
+        mma_tile<XT, kChunk, true, true>(dS[it][jt], QT + i0 * L::kLdX, L::kLdX, blk(bQDB) + bo, L::kLdX);
+        mma_tile<XT, kChunk, true, true>(dS[it][jt], KT + i0 * L::kLdX, L::kLdX, blk(bDB_DKS) + bo, L::kLdX);
+        mma_tile<XT, kChunk, true, true>(dR[it][jt], QT + i0 * L::kLdX, L::kLdX, blk(bQDC) + bo, L::kLdX);
         if constexpr (RDN)
-          mma_tile<XT, kChunk, true, true>(dR[it][jt], KT + i0 * L::kLdX, L::kLdX, buf(bDKR) + bo, L::kLdX);
+          mma_tile<XT, kChunk, true, true>(dR[it][jt], KT + i0 * L::kLdX, L::kLdX, blk(bDKR) + bo, L::kLdX);
       }
     }
-    __syncthreads();
+    barrier_lds();
+    if constexpr (!L::kDB) {
+      if (c > 0) issue_all_single(c - 1);
+    }
+    wait_vmem();
+    barrier_lds();
     write_copies();
   }
 

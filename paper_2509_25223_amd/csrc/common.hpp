@@ -23,13 +23,8 @@ typedef u16 u16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ float bf2f(u16 x) { return __uint_as_float(((uint32_t)x) << 16); }
 
-// fp32 -> bf16, round to nearest even (NaN stays NaN).
-__device__ __forceinline__ u16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7f800000u) == 0x7f800000u) return (u16)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (u16)(u >> 16);
-}
+// fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ u16 f2bf(float f) { return __builtin_bit_cast(u16, (__bf16)f); }
 
 // Conversions between the storage type of an operand and fp32.
 template <typename T> __device__ __forceinline__ float to_f(T x);
@@ -200,6 +195,123 @@ __device__ __forceinline__ void load_rowfrags(typename Mfma<T>::frag* afr, const
 
 __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
 
+// ---------------------------------------------------------------------------
+// 64 x 64 matrices staged in LDS by LDS-DMA (global_load_lds_dwordx4): the
+// hardware writes lane i's 16 bytes at base + 16 i, so a tile is stored
+// unpadded, and the 16-byte chunks of row r are XOR-swizzled with r so that
+// 16 rows read at the same column hit distinct banks.
+//   logical (row r, chunk c) -> physical byte r * kRowB + ((c ^ (r & (kCpr-1))) << 4)
+// ---------------------------------------------------------------------------
+template <typename T> struct Swz {
+  static constexpr int kRowB = kChunk * (int)sizeof(T);   // bytes per row
+  static constexpr int kCpr = kRowB / 16;                 // 16-byte chunks per row
+  static constexpr int kBytes = kChunk * kRowB;
+  static constexpr int kDmaPerWave = kBytes / 1024 / kWaves;   // 1 KiB per instruction
+  __device__ __forceinline__ static int off(int r, int col) {   // byte offset of element
+    const int c = (col * (int)sizeof(T)) >> 4, inside = (col * (int)sizeof(T)) & 15;
+    return r * kRowB + ((c ^ (r & (kCpr - 1))) << 4) + inside;
+  }
+};
+
+// One LDS-DMA instruction: lane i copies 16 bytes from `src` (its own global
+// address) to `lds` + 16 i.  (Pointers go through char* so that the builtin
+// type-checks in the host pass too.)
+__device__ __forceinline__ void dma16(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds(reinterpret_cast<const char*>(src),
+                                   reinterpret_cast<char*>(lds), 16, 0, 0);
+}
+
+// DMA of one row-major 64 x 64 matrix (global) into a swizzled LDS tile; every
+// wave issues kDmaPerWave instructions.  Completion: s_waitcnt vmcnt + barrier.
+template <typename T>
+__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds) {
+  typedef Swz<T> S;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int m = 0; m < S::kDmaPerWave; ++m) {
+    const int blk = w * S::kDmaPerWave + m;
+    const int P = blk * 64 + lane;                 // physical chunk index
+    const int r = P / S::kCpr, pc = P % S::kCpr;
+    const int c = pc ^ (r & (S::kCpr - 1));        // logical chunk stored there
+    const char* src = reinterpret_cast<const char*>(gsrc) + r * S::kRowB + c * 16;
+    dma16(src, reinterpret_cast<char*>(lds) + blk * 1024);
+  }
+}
+
+// DMA of `bytes` contiguous bytes (a multiple of 1 KiB) by wave `wave` only.
+__device__ __forceinline__ void dma_linear_wave(const void* gsrc, void* lds, int bytes) {
+  const int lane = threadIdx.x & 63;
+  for (int b = 0; b < bytes; b += 1024)
+    dma16(reinterpret_cast<const char*>(gsrc) + b + lane * 16, reinterpret_cast<char*>(lds) + b);
+}
+
+// Waits for this wave's outstanding vector memory operations (loads, stores
+// and LDS-DMA): s_waitcnt vmcnt(0).  A barrier afterwards makes every wave's
+// DMA data visible.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Workgroup barrier for LDS data: waits for this wave's LDS operations
+// (lgkmcnt(0)) and meets the other waves, but leaves global loads, stores and
+// LDS-DMA in flight (__syncthreads' release fence would drain them).  LDS-DMA
+// data is published by wait_vmem() before such a barrier.
+__device__ __forceinline__ void barrier_lds() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// A-operand fragment of a swizzled matrix: rows r0..r0+15 ("KC": row-major use).
+template <typename T>
+__device__ __forceinline__ typename Mfma<T>::frag swz_load_rows(const T* base, int r0, int k0) {
+  typedef Mfma<T> M;
+  const int lane = threadIdx.x & 63;
+  const int r = r0 + (lane & 15);
+  const char* b = reinterpret_cast<const char*>(base);
+  if constexpr (sizeof(T) == 2) {
+    return *reinterpret_cast<const typename M::frag*>(b + Swz<T>::off(r, k0 + (lane >> 4) * 8));
+  } else {
+    return *reinterpret_cast<const float*>(b + Swz<T>::off(r, k0 + (lane >> 4)));
+  }
+}
+
+// A-operand fragment of the TRANSPOSE of a swizzled matrix: A(t, s) = M[s][t]
+// for t = t0..t0+15 (gathers).
+template <typename T>
+__device__ __forceinline__ typename Mfma<T>::frag swz_load_cols(const T* base, int t0, int k0) {
+  typedef Mfma<T> M;
+  const int lane = threadIdx.x & 63;
+  const int t = t0 + (lane & 15);
+  const char* b = reinterpret_cast<const char*>(base);
+  if constexpr (sizeof(T) == 2) {
+    typename M::frag v;
+    const int s0 = k0 + (lane >> 4) * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = *reinterpret_cast<const T*>(b + Swz<T>::off(s0 + e, t));
+    return v;
+  } else {
+    return *reinterpret_cast<const float*>(b + Swz<T>::off(k0 + (lane >> 4), t));
+  }
+}
+
+// acc += M[r0.., :] * B   (M swizzled 64 x 64, B given as [n][k] rows with ld)
+template <typename T>
+__device__ __forceinline__ void mma_swz_rows(floatx4& acc, const T* M, int r0, const T* B, int ldb) {
+  typedef Mfma<T> F;
+#pragma unroll
+  for (int k0 = 0; k0 < kChunk; k0 += F::kStep)
+    acc = F::mma(swz_load_rows<T>(M, r0, k0), F::template load<true>(B, ldb, k0), acc);
+}
+
+// acc += M^T[t0.., :] * B
+template <typename T>
+__device__ __forceinline__ void mma_swz_cols(floatx4& acc, const T* M, int t0, const T* B, int ldb) {
+  typedef Mfma<T> F;
+#pragma unroll
+  for (int k0 = 0; k0 < kChunk; k0 += F::kStep)
+    acc = F::mma(swz_load_cols<T>(M, t0, k0), F::template load<true>(B, ldb, k0), acc);
+}
+
 // Row (inside a 16-row tile) and column of accumulator element r of this lane.
 __device__ __forceinline__ int acc_row(int r) { return 4 * ((threadIdx.x & 63) >> 4) + r; }
 __device__ __forceinline__ int acc_col() { return threadIdx.x & 15; }
@@ -209,8 +321,16 @@ __device__ __forceinline__ int acc_col() { return threadIdx.x & 15; }
 template <typename T>
 __device__ __forceinline__ void store_acc_t(T* dst, int ld, floatx4 v) {
   T* p = dst + acc_col() * ld + acc_row(0);
+  if constexpr (sizeof(T) == 2) {   // one 8-byte store (p is 8-byte aligned)
+    typedef T T4 __attribute__((ext_vector_type(4)));
+    T4 w;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) p[r] = from_f<T>(v[r]);
+    for (int r = 0; r < 4; ++r) w[r] = from_f<T>(v[r]);
+    *reinterpret_cast<T4*>(p) = w;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) p[r] = from_f<T>(v[r]);
+  }
 }
 
 // Stores the 4 accumulator rows of this lane into LDS row-major: dst[row * ld + col].

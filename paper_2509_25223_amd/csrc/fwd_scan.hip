@@ -37,20 +37,39 @@ struct FwdLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
   typedef typename std::conditional<kBF, f16, float>::type XT;
   static constexpr int kPad = kBF ? 8 : 4;
-  static constexpr int kLdX = kChunk + kPad;    // K^T rows, matrices, per-token blocks
+  static constexpr int kLdX = kChunk + kPad;    // K^T rows, per-token blocks
   static constexpr int kLdS = DK + kPad;        // state copies [BV][DK]
-  static constexpr int kNumM = RDN ? 5 : 3;
+  // matrix slots (swizzled 64 x 64 tiles filled by LDS-DMA); with bf16 inputs
+  // T^R and MR are double-buffered so the next chunk's copies land early
+  static constexpr bool kDB = kBF;
+  static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 4 : 3);
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kKT = 0;
   static constexpr int kCopies = kKT + DK * kLdX * (int)sizeof(XT);
   static constexpr int kCopyBytes = BV * kLdS * (int)sizeof(IN);
   static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
-  static constexpr int kBufs = kMats + kNumM * kChunk * kLdX * (int)sizeof(XT);
+  static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
   static constexpr int kBufBytes = BV * kLdX * (int)sizeof(XT);
   static constexpr int kVc = kBufs + 5 * kBufBytes;
-  static constexpr int kGates = kVc + kChunk * BV * (int)sizeof(IN);
+  static constexpr int kVBytes = kChunk * BV * (int)sizeof(IN);
+  static constexpr int kGraw = kVc + kVBytes;
+  static constexpr int kGates = kGraw + kGateBlock * 4;
   static constexpr int kBytes = kGates + 10 * kChunk * 4;
+  static_assert(kVBytes == 4 * 1024, "V block = one DMA instruction per wave");
   static_assert(kBytes <= 160 * 1024, "forward scan LDS");
+  // slot of each matrix (RDN: TS MG MP TR[2] MR[2]; RLA: MG MP MR[2])
+  __device__ static constexpr int slot(int mat, int buf) {
+    if (RDN) {
+      if (mat == kMatTS) return 0;
+      if (mat == kMatMG) return 1;
+      if (mat == kMatMP) return 2;
+      if (mat == kMatTR) return kDB ? 3 + buf : 3;
+      return kDB ? 5 + buf : 4;   // MR
+    }
+    if (mat == kMatMG) return 0;
+    if (mat == kMatMP) return 1;
+    return kDB ? 2 + buf : 2;     // MR
+  }
 };
 
 // Writes this lane's 4 accumulator rows of a state tile into the transposed
@@ -58,15 +77,18 @@ struct FwdLayout {
 template <typename IN>
 __device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int ld, floatx4 v) {
   const int off = acc_col() * ld + acc_row(0);
+  if constexpr (sizeof(IN) == 2) {   // 8-byte stores of 4 consecutive rows
+    u16x4 h4, l4;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    if constexpr (sizeof(IN) == 2) {
-      const u16 h = f2bf(v[r]);
-      hi[off + r] = h;
-      lo[off + r] = bf16_lo(v[r], h);
-    } else {
-      hi[off + r] = v[r];
+    for (int r = 0; r < 4; ++r) {
+      h4[r] = f2bf(v[r]);
+      l4[r] = bf16_lo(v[r], h4[r]);
     }
+    *reinterpret_cast<u16x4*>(hi + off) = h4;
+    *reinterpret_cast<u16x4*>(lo + off) = l4;
+  } else {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) hi[off + r] = v[r];
   }
 }
 
@@ -85,13 +107,16 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   IN* Rhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
   IN* Slo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);   // bf16 only
   IN* Rlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);   // bf16 only
-  XT* mats = reinterpret_cast<XT*>(smem + L::kMats);
+  auto mat = [&](int m, int buf) {
+    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
+  };
   XT* Yt = reinterpret_cast<XT*>(smem + L::kBufs);               // Y, later YR
   XT* Ut = reinterpret_cast<XT*>(smem + L::kBufs + 1 * L::kBufBytes);
   XT* URt = reinterpret_cast<XT*>(smem + L::kBufs + 2 * L::kBufBytes);
   XT* DUt = reinterpret_cast<XT*>(smem + L::kBufs + 3 * L::kBufBytes);
   XT* DURt = reinterpret_cast<XT*>(smem + L::kBufs + 4 * L::kBufBytes);
   IN* Vc = reinterpret_cast<IN*>(smem + L::kVc);
+  float* graw = reinterpret_cast<float*>(smem + L::kGraw);   // prep's gate block
   float* gbt = reinterpret_cast<float*>(smem + L::kGates);   // beta
   float* ggm = gbt + kChunk;        // gamma
   float* egs = ggm + kChunk;        // e^{g_t}
@@ -100,13 +125,6 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   float* dls = egr + kChunk;        // e^{g_C - g_t}
   float* dlr = dls + kChunk;        // e^{h_C - h_t}
   float* edge = dlr + kChunk;       // [0] = e^{g_C}, [1] = e^{h_C}
-
-  // matrix slots in LDS: RDN {TS, MG, MP, TR, MR}, RLA {MG, MP, MR}
-  XT* mTS = mats;
-  XT* mMG = mats + (RDN ? 1 : 0) * kChunk * L::kLdX;
-  XT* mMP = mats + (RDN ? 2 : 1) * kChunk * L::kLdX;
-  XT* mTR = mats + 3 * kChunk * L::kLdX;
-  XT* mMR = mats + (RDN ? 4 : 2) * kChunk * L::kLdX;
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   // XCD-aware block mapping: the value blocks of one (sequence, head) pair get
@@ -152,10 +170,68 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   OT* og = reinterpret_cast<OT*>(p.o);
   const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
 
+  // ---- staging of chunk c+1 while chunk c computes ----
+  //   K, Q fragments: register prefetch (issued after P1, when chunk c's are dead)
+  //   V block, gate block, T^R, MR: LDS-DMA after P1 (V, gates dead; T^R/MR
+  //     double-buffered); T^S, MG, MP: LDS-DMA after P3 (their last use)
+  // Completion: every wave waits for its vector memory operations and the
+  // whole workgroup passes a barrier at the end of chunk c.
+  typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];
+  auto chunk_len = [&](int c) { return min(kChunk, si.len - c * kChunk); };
+  auto mat_src = [&](int c, int m) {
+    return matg + ((int64_t)(si.chunk0 + c) * H + h) * kNumMats * kMatElems + m * kMatElems;
+  };
+  auto issue_regs = [&](int c) {
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int t = 16 * w + (lane & 15);
+    const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
+    const bool ok = t < chunk_len(c);
+    load_rowfrags<IN, DK>(Kn, ok ? kg + roff : nullptr);
+    load_rowfrags<IN, DK>(Qn, ok ? qg + roff : nullptr);
+  };
+  auto issue_early = [&](int c) {   // V, gates, T^R, MR
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    {   // V block: wave w moves rows 16w..16w+15 (64 bytes each)
+      constexpr int kChunksPerRow = BV * (int)sizeof(IN) / 16;
+      const int P = w * 64 + lane, t = P / kChunksPerRow, cc = P % kChunksPerRow;
+      const int ts = t < len ? t : len - 1;   // padding rows: any valid row (multiplied by 0)
+      const IN* src = vg + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * (16 / (int)sizeof(IN));
+      dma16(src, reinterpret_cast<char*>(Vc) + w * 1024);
+    }
+    if (w == 0)
+      dma_linear_wave(p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock, graw,
+                      kGateBlock * 4);
+    if constexpr (L::kDB) {
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, c & 1));
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
+    }
+  };
+  auto issue_late = [&](int c) {    // T^S, MG, MP
+    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
+    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
+    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
+  };
+  auto issue_tail = [&](int c) {    // T^R, MR when single-buffered
+    if constexpr (!L::kDB) {
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0));
+    }
+  };
+  if (nch > 0) {
+    issue_regs(0);
+    issue_early(0);
+    issue_late(0);
+    issue_tail(0);
+    wait_vmem();
+  }
+  barrier_lds();
+
   for (int c = 0; c < nch; ++c) {
     const int gc = si.chunk0 + c;
     const int64_t tok = si.start + (int64_t)c * kChunk;
-    const int len = min(kChunk, si.len - c * kChunk);
+    const int len = chunk_len(c);
+    const int buf = c & 1;
 
     if constexpr (CKPT) {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV;
@@ -171,53 +247,30 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
           }
     }
 
-    // ---- stage the chunk: K, Q fragments of this wave's rows into registers,
-    //      K^T (XT) into LDS, V block, matrices, gates ----
+    // ---- commit: K, Q fragments from the prefetch registers, K^T (XT) and
+    //      the gate-derived vectors into LDS ----
     typename MI::frag Kf[KS_STEPS], Qf[KS_STEPS];
     {
       const int t = 16 * w + (lane & 15);
-      const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
-      load_rowfrags<IN, DK>(Kf, t < len ? kg + roff : nullptr);
-      load_rowfrags<IN, DK>(Qf, t < len ? qg + roff : nullptr);
 #pragma unroll
-      for (int s = 0; s < KS_STEPS; ++s) {
+      for (int s2 = 0; s2 < KS_STEPS; ++s2) {
+        Kf[s2] = Kn[s2];
+        Qf[s2] = Qn[s2];
         if constexpr (BF) {
-          const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s]);
+          const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s2]);
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            KT[(s * 32 + (lane >> 4) * 8 + e) * L::kLdX + t] = from_f<XT>(bf2f(kv[e]));
+            KT[(s2 * 32 + (lane >> 4) * 8 + e) * L::kLdX + t] = from_f<XT>(bf2f(kv[e]));
         } else {
-          KT[(s * 4 + (lane >> 4)) * L::kLdX + t] = Kf[s];
-        }
-      }
-      constexpr int kVecV = 16 / sizeof(IN), kVPerRow = BV / kVecV;
-      for (int e = tid; e < kChunk * kVPerRow; e += kThreads) {
-        const int tt = e / kVPerRow, jj = (e % kVPerRow) * kVecV;
-        uint4 vv = make_uint4(0, 0, 0, 0);
-        if (tt < len) vv = *reinterpret_cast<const uint4*>(vg + ((tok + tt) * H + h) * (int64_t)DV + j0 + jj);
-        *reinterpret_cast<uint4*>(Vc + tt * BV + jj) = vv;
-      }
-      constexpr int kVecM = 16 / sizeof(XT);
-      constexpr int kMatVecs = kMatElems / kVecM;
-      const XT* mg = matg + ((int64_t)gc * H + h) * kNumMats * kMatElems;
-      constexpr int kSrc[5] = {kMatTS, kMatMG, kMatMP, kMatTR, kMatMR};
-      constexpr int kSrcRla[3] = {kMatMG, kMatMP, kMatMR};
-#pragma unroll
-      for (int m = 0; m < L::kNumM; ++m) {
-        const int src = RDN ? kSrc[m] : kSrcRla[m];
-        for (int e = tid; e < kMatVecs; e += kThreads) {
-          const int tt = e / (kChunk / kVecM), ss = (e % (kChunk / kVecM)) * kVecM;
-          *reinterpret_cast<uint4*>(mats + (m * kChunk + tt) * L::kLdX + ss) =
-              *reinterpret_cast<const uint4*>(mg + src * kMatElems + tt * kChunk + ss);
+          KT[(s2 * 4 + (lane >> 4)) * L::kLdX + t] = Kf[s2];
         }
       }
       if (tid < kChunk) {
-        const float* gb = p.gate_ws + ((int64_t)gc * H + h) * kGateBlock;
         const int tt = tid;
-        const float gs = gb[tt], gsl = gb[kChunk - 1], gsp = tt > 0 ? gb[tt - 1] : 0.f;
-        const float gr = gb[64 + tt], grl = gb[64 + kChunk - 1];
-        gbt[tt] = gb[128 + tt];
-        ggm[tt] = gb[192 + tt];
+        const float gs = graw[tt], gsp = tt > 0 ? graw[tt - 1] : 0.f, gsl = graw[kChunk - 1];
+        const float gr = graw[64 + tt], grl = graw[64 + kChunk - 1];
+        gbt[tt] = graw[128 + tt];
+        ggm[tt] = graw[192 + tt];
         egs[tt] = __expf(gs);
         egsp[tt] = __expf(gsp);
         egr[tt] = __expf(gr);
@@ -229,9 +282,9 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         }
       }
     }
-    __syncthreads();
+    barrier_lds();
 
-    // ---- KS, QS, KR, QR for rows 16w..16w+15 ----
+    // ---- P1: KS, QS, KR, QR for rows 16w..16w+15 ----
     floatx4 KS[JT], QS[JT], KR[JT], QR[JT];
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
@@ -256,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r);
         vloc[jt][r] = to_f<IN>(Vc[t * BV + jt * 16 + acc_col()]);
-        y[r] = RDN ? gbt[t] * (vloc[jt][r] - egs[t] * KS[jt][r]) : gbt[t] * vloc[jt][r];
+        y[r] = RDN ? gbt[t] * __builtin_fmaf(-egs[t], KS[jt][r], vloc[jt][r]) : gbt[t] * vloc[jt][r];
       }
       if constexpr (RDN) {
         store_acc_t<XT>(Yt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
@@ -268,42 +321,47 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
       }
     }
-    __syncthreads();
+    barrier_lds();
+    if (c + 1 < nch) {
+      issue_regs(c + 1);
+      issue_early(c + 1);
+    }
 
-    if constexpr (RDN) {   // U = T^S Y
+    if constexpr (RDN) {   // ---- P2: U = T^S Y ----
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 u = zero4();
-        mma_tile<XT, kChunk, true, true>(u, mTS + 16 * w * L::kLdX, L::kLdX, Yt + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_rows<XT>(u, mat(kMatTS, 0), 16 * w, Yt + jt * 16 * L::kLdX, L::kLdX);
         floatx4 du;
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * u[r];
         store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
         store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
       }
-      __syncthreads();
+      barrier_lds();
     }
 
-    // ---- residual, clip, base read-out ----
+    // ---- P3: residual, clip, base read-out ----
+    // (explicit fmas: every instantiation, saving or not, rounds alike)
     floatx4 base[JT];
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       floatx4 mgu = zero4(), mpu = zero4();
-      mma_tile<XT, kChunk, true, true>(mgu, mMG + 16 * w * L::kLdX, L::kLdX, Ut + jt * 16 * L::kLdX, L::kLdX);
-      mma_tile<XT, kChunk, true, true>(mpu, mMP + 16 * w * L::kLdX, L::kLdX, Ut + jt * 16 * L::kLdX, L::kLdX);
+      mma_swz_rows<XT>(mgu, mat(kMatMG, 0), 16 * w, Ut + jt * 16 * L::kLdX, L::kLdX);
+      mma_swz_rows<XT>(mpu, mat(kMatMP, 0), 16 * w, Ut + jt * 16 * L::kLdX, L::kLdX);
       floatx4 y;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r);
-        const float x = vloc[jt][r] - egsp[t] * KS[jt][r] - mgu[r];
+        const float x = __builtin_fmaf(-egsp[t], KS[jt][r], vloc[jt][r]) - mgu[r];
         const float rr = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
         if constexpr (CKPT) {
           if (t < len)
             p.ck_mask[((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col()] =
                 (clip < 0.f || fabsf(x) <= clip) ? 1 : 0;
         }
-        base[jt][r] = egs[t] * QS[jt][r] + mpu[r];
-        y[r] = RDN ? ggm[t] * (rr - egr[t] * KR[jt][r]) : ggm[t] * rr;
+        base[jt][r] = __builtin_fmaf(egs[t], QS[jt][r], mpu[r]);
+        y[r] = RDN ? ggm[t] * __builtin_fmaf(-egr[t], KR[jt][r], rr) : ggm[t] * rr;
       }
       if constexpr (RDN) {
         store_acc_t<XT>(Yt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
@@ -315,35 +373,35 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
       }
     }
-    __syncthreads();
+    if constexpr (!L::kDB) wait_vmem();   // single-buffered T^R / MR of this chunk
+    barrier_lds();
+    if (c + 1 < nch) issue_late(c + 1);
 
-    if constexpr (RDN) {   // UR = T^R YR
+    if constexpr (RDN) {   // ---- P4: UR = T^R YR ----
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 u = zero4();
-        mma_tile<XT, kChunk, true, true>(u, mTR + 16 * w * L::kLdX, L::kLdX, Yt + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_rows<XT>(u, mat(kMatTR, buf), 16 * w, Yt + jt * 16 * L::kLdX, L::kLdX);
         floatx4 du;
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * u[r];
         store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
         store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
       }
-      __syncthreads();
+      barrier_lds();
     }
 
-    // ---- correction read-out and output ----
+    // ---- P5: correction read-out, output (stored after the barrier) ----
+    float outv[JT][4];
     if constexpr (WRITE_O) {
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 mru = zero4();
-        mma_tile<XT, kChunk, true, true>(mru, mMR + 16 * w * L::kLdX, L::kLdX, URt + jt * 16 * L::kLdX, L::kLdX);
+        mma_swz_rows<XT>(mru, mat(kMatMR, buf), 16 * w, URt + jt * 16 * L::kLdX, L::kLdX);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
-          const float cc = egr[t] * QR[jt][r] + mru[r];
-          if (t < len)
-            og[((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col()] =
-                from_f<OT>(base[jt][r] + ggm[t] * cc);
+          outv[jt][r] = __builtin_fmaf(ggm[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
         }
       }
     }
@@ -361,7 +419,20 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         mma_tile<XT, kChunk, true, true>(Racc[it][jt], Ai, L::kLdX, DURt + jt * 16 * L::kLdX, L::kLdX);
       }
     }
-    __syncthreads();   // all reads of the state copies, K^T and the blocks are done
+    // the next chunk's DMA data must have landed before anyone reads it
+    wait_vmem();
+    barrier_lds();
+    if (c + 1 < nch) issue_tail(c + 1);   // single-buffered T^R / MR: waited at P3
+    if constexpr (WRITE_O) {
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * w + acc_row(r);
+          if (t < len)
+            og[((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col()] = from_f<OT>(outv[jt][r]);
+        }
+    }
     write_state_copies();
   }
 

@@ -39,7 +39,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def prob(B=2, T=100, H=3, dk=128, dv=128, dtype=rla.RLA_BF16, clip=1.0, cu=None, N=0, out=rla.RLA_F32):
-    return rla.rla_problem(B, T, H, dk, dv, N, cu, dtype, clip, out)
+    return rla.rla_problem(B, T, H, dk, dv, N, cu, dtype, clip, out, 0)
 
 
 def test_workspace_size(lib):

@@ -89,3 +89,39 @@ def test_full_training_workload_sampled(device):
         print("[%s seq%d head%d] %s" % (wl.name, n, h, " ".join("%s=%.1e" % kv for kv in errs.items())))
         for key, e in errs.items():
             assert e <= TOL["bf16"], (n, h, key, e)
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("varlen", [False, True])
+def test_saved_forward_path_is_identical(device, variant, varlen):
+    """forward(save_for_backward) + backward(use_saved) gives bit-identical
+    outputs and gradients to the self-contained calls (same kernels, same
+    arithmetic; the backward only skips recomputing what the forward left)."""
+    import torch
+    import paper_2509_25223_amd as rla
+    from tests.gpu_util import dev
+    lens = [70, 0, 130] if varlen else [150, 150]
+    wl = datagen.small(variant + "_fwdbwd", "bf16", lens, H=2, d=128, varlen=varlen)
+    inp = datagen.make_inputs(wl, seed=204)
+    q, k, v, dO = (dev(inp[n], torch.bfloat16, device) for n in ("q", "k", "v", "dO"))
+    g = [dev(inp[n], torch.float32, device) for n in ("alpha_s", "beta", "alpha_r", "gamma")]
+    cu = None
+    if varlen:
+        cu = torch.from_numpy(inp["cu_seqlens"].astype(np.int32)).to(device)
+    else:
+        q, k, v, dO = (x.view(2, 150, *x.shape[1:]) for x in (q, k, v, dO))
+        g = [x.view(2, 150, -1) for x in g]
+    fwd = rla.rdn_forward if variant == "rdn" else rla.rla_forward
+    bwd = rla.rdn_backward if variant == "rdn" else rla.rla_backward
+    o1, S1, R1 = fwd(q, k, v, *g, cu_seqlens=cu)
+    ref = bwd(q, k, v, *g, dO, cu_seqlens=cu)
+    prob = rla.make_problem(q, v, cu)
+    ws = torch.empty(rla.rla_workspace_size(prob, rla.RLA_OP_RDN_BACKWARD if variant == "rdn"
+                                            else rla.RLA_OP_RLA_BACKWARD),
+                     dtype=torch.uint8, device=device)
+    o2, S2, R2 = fwd(q, k, v, *g, cu_seqlens=cu, workspace=ws, save_for_backward=True)
+    got = bwd(q, k, v, *g, dO, cu_seqlens=cu, workspace=ws, use_saved=True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(S1, S2) and torch.equal(R1, R2)
+    for key in GRAD_KEYS:
+        assert torch.equal(ref[key], got[key]), key
