@@ -143,28 +143,85 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   const XT* mg = reinterpret_cast<const XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
   const int64_t soff = ((int64_t)c * H + h) * DK * DV;
 
-  // ---- chunk-constant staging: K, Q (XT, row-major), matrices, gates ----
-  for (int e = tid; e < kChunk * DK; e += kThreads) {
-    const int t = e / DK, i = e % DK;
-    float kv = 0.f, qv = 0.f;
-    if (t < len) {
-      const int64_t off = ((tok + t) * H + h) * (int64_t)DK + i;
-      kv = to_f<IN>(kg[off]);
-      qv = to_f<IN>(qg[off]);
+  // ---- per value block inputs, prefetched into registers one block ahead:
+  //      V and dO rows (16-byte vectors), the clip mask rows, the four state
+  //      blocks (fp32, 4 columns per vector) ----
+  constexpr int kVR = kBVG * (int)sizeof(IN) / 16;            // vectors per V / dO row
+  constexpr int kVPT = 2 * kChunk * kVR / kThreads;           // V + dO vectors per thread
+  constexpr int kSPT = DK * (kBVG / 4) / kThreads;            // float4 per thread per state
+  static_assert(kVPT >= 1 && kSPT >= 1, "block prefetch shape");
+  uint4 pv[kVPT];
+  uint4 pm;
+  float4 ps[4][kSPT];
+  auto prefetch = [&](int j0) {
+#pragma unroll
+    for (int u = 0; u < kVPT; ++u) {
+      const int e = tid + u * kThreads, which = e / (kChunk * kVR), r = e % (kChunk * kVR);
+      const int t = r / kVR, cv = r % kVR;
+      const IN* src = (which ? dog : vg) + ((tok + t) * H + h) * (int64_t)DV + j0 +
+                      cv * (16 / (int)sizeof(IN));
+      pv[u] = t < len ? *reinterpret_cast<const uint4*>(src) : uint4{0, 0, 0, 0};
     }
-    KX[t * L::kLdK + i] = from_f<XT>(kv);
-    QX[t * L::kLdK + i] = from_f<XT>(qv);
+    pm = uint4{0, 0, 0, 0};
+    if (tid < len)
+      pm = *reinterpret_cast<const uint4*>(p.ck_mask + ((tok + tid) * H + h) * (int64_t)DV + j0);
+    const float* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
+#pragma unroll
+    for (int u = 0; u < kSPT; ++u) {
+      const int e = tid + u * kThreads, i = e / (kBVG / 4), qd = e % (kBVG / 4);
+      const int64_t gi = soff + (int64_t)i * DV + j0 + 4 * qd;
+#pragma unroll
+      for (int m = 0; m < 4; ++m) ps[m][u] = *reinterpret_cast<const float4*>(srcs[m] + gi);
+    }
+  };
+  prefetch(0);
+
+  // ---- chunk-constant staging: K, Q (XT, row-major), matrices, gates ----
+  {
+    constexpr int kE = 16 / (int)sizeof(IN);                  // elements per vector
+    constexpr int kKV = kChunk * DK / kE / kThreads;          // vectors per thread per matrix
+    uint4 kv[kKV], qv[kKV];
+#pragma unroll
+    for (int u = 0; u < kKV; ++u) {
+      const int e = tid + u * kThreads, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
+      const int64_t off = ((tok + t) * H + h) * (int64_t)DK + i;
+      kv[u] = t < len ? *reinterpret_cast<const uint4*>(kg + off) : uint4{0, 0, 0, 0};
+      qv[u] = t < len ? *reinterpret_cast<const uint4*>(qg + off) : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int u = 0; u < kKV; ++u) {
+      const int e = tid + u * kThreads, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
+      if constexpr (L::kBF) {   // bf16 -> fp16, 8 at a time
+        const u16x8 a = __builtin_bit_cast(u16x8, kv[u]), b = __builtin_bit_cast(u16x8, qv[u]);
+        f16x8 ka, qa;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) { ka[x] = (f16)bf2f(a[x]); qa[x] = (f16)bf2f(b[x]); }
+        *reinterpret_cast<f16x8*>(KX + t * L::kLdK + i) = ka;
+        *reinterpret_cast<f16x8*>(QX + t * L::kLdK + i) = qa;
+      } else {
+        *reinterpret_cast<uint4*>(KX + t * L::kLdK + i) = kv[u];
+        *reinterpret_cast<uint4*>(QX + t * L::kLdK + i) = qv[u];
+      }
+    }
   }
   const XT *mTS, *mMG, *mMP, *mTR, *mMR;
   int ldm;
   if constexpr (L::kMatsInLds) {
     XT* mats = reinterpret_cast<XT*>(smem + L::kMats);
     constexpr int kVecM = 16 / sizeof(XT);
-    for (int e = tid; e < 5 * kMatElems / kVecM; e += kThreads) {
+    constexpr int kMV = 5 * kMatElems / kVecM / kThreads;   // vectors per thread
+    uint4 mv[kMV];
+#pragma unroll
+    for (int u = 0; u < kMV; ++u) {
+      const int e = tid + u * kThreads;
+      mv[u] = *reinterpret_cast<const uint4*>(mg + e * kVecM);
+    }
+#pragma unroll
+    for (int u = 0; u < kMV; ++u) {
+      const int e = tid + u * kThreads;
       const int m = e / (kMatElems / kVecM), r = e % (kMatElems / kVecM);
       const int t = r / (kChunk / kVecM), s = (r % (kChunk / kVecM)) * kVecM;
-      *reinterpret_cast<uint4*>(mats + (m * kChunk + t) * L::kLdX + s) =
-          *reinterpret_cast<const uint4*>(mg + m * kMatElems + t * kChunk + s);
+      *reinterpret_cast<uint4*>(mats + (m * kChunk + t) * L::kLdX + s) = mv[u];
     }
     ldm = L::kLdX;
     mTS = mats + kMatTS * kChunk * L::kLdX;
@@ -213,61 +270,76 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   float rgsp[4] = {0, 0, 0, 0}, rgr[4] = {0, 0, 0, 0};
   float gsC = 0.f, grC = 0.f;   // gradients w.r.t. g_C, h_C (partial, this thread)
   const int trow0 = 16 * w;
+  barrier_lds();   // staged K, Q, matrices and gates
 
   for (int j0 = 0; j0 < DV; j0 += kBVG) {
-    // ---- load this block: V, dO, mask, and the four state blocks (scaled) ----
-    for (int e = tid; e < kChunk * kBVG; e += kThreads) {
-      const int t = e / kBVG, j = e % kBVG;
-      const int64_t gi = ((tok + t) * H + h) * (int64_t)DV + j0 + j;
-      const bool ok = t < len;
-      VB[t * kBVG + j] = ok ? vg[gi] : from_f<IN>(0.f);
-      blk(kDBT)[j * L::kLdX + t] = from_f<XT>(ok ? to_f<IN>(dog[gi]) : 0.f);
-      mask[t * kBVG + j] = ok ? p.ck_mask[gi] : 0;
+    // ---- this block's inputs from the prefetch registers into LDS; the
+    //      state blocks scaled to fp16 ----
+#pragma unroll
+    for (int u = 0; u < kVPT; ++u) {
+      const int e = tid + u * kThreads, which = e / (kChunk * kVR), r = e % (kChunk * kVR);
+      const int t = r / kVR, cv = r % kVR, j = cv * (16 / (int)sizeof(IN));
+      if (which == 0) {
+        *reinterpret_cast<uint4*>(VB + t * kBVG + j) = pv[u];
+      } else {
+        const IN* x = reinterpret_cast<const IN*>(&pv[u]);
+#pragma unroll
+        for (int y = 0; y < 16 / (int)sizeof(IN); ++y)
+          blk(kDBT)[(j + y) * L::kLdX + t] = from_f<XT>(to_f<IN>(x[y]));
+      }
     }
-    constexpr int kPerThread = DK * kBVG / kThreads;   // 8 (DK=128) or 4 (DK=64)
-    float sv[4][kPerThread];
+    if (tid < kChunk) *reinterpret_cast<uint4*>(mask + tid * kBVG) = pm;
     float mx[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int u = 0; u < kPerThread; ++u) {
-      const int e = tid + u * kThreads, i = e / kBVG, j = e % kBVG;
-      const int64_t gi = soff + (int64_t)i * DV + j0 + j;
-      sv[0][u] = p.ck_S[gi];
-      sv[1][u] = p.ck_R[gi];
-      sv[2][u] = p.dS_ws[gi];
-      sv[3][u] = p.dR_ws[gi];
+    for (int u = 0; u < kSPT; ++u) {
 #pragma unroll
-      for (int m = 0; m < 4; ++m) mx[m] = fmaxf(mx[m], fabsf(sv[m][u]));
+      for (int m = 0; m < 4; ++m)
+        mx[m] = fmaxf(mx[m], fmaxf(fmaxf(fabsf(ps[m][u].x), fabsf(ps[m][u].y)),
+                                   fmaxf(fabsf(ps[m][u].z), fabsf(ps[m][u].w))));
+      // states at the chunk start times their end gradients (for g_C, h_C)
+      gsC += edge[0] * (ps[0][u].x * ps[2][u].x + ps[0][u].y * ps[2][u].y +
+                        ps[0][u].z * ps[2][u].z + ps[0][u].w * ps[2][u].w);
+      grC += edge[1] * (ps[1][u].x * ps[3][u].x + ps[1][u].y * ps[3][u].y +
+                        ps[1][u].z * ps[3][u].z + ps[1][u].w * ps[3][u].w);
     }
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       const float wm = wave_max(mx[m]);
       if (lane == 0) red[w * 4 + m] = wm;
     }
-    __syncthreads();
+    barrier_lds();
     float scl[4];   // power-of-two scale: value = scl * stored
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
       const float bmax = fmaxf(fmaxf(red[m], red[4 + m]), fmaxf(red[8 + m], red[12 + m]));
-      float s = 1.f;
+      float sc = 1.f;
       if constexpr (L::kBF) {
         if (bmax > 16384.f) {
           int ex;
           frexpf(bmax / 16384.f, &ex);
-          s = ldexpf(1.f, ex);
+          sc = ldexpf(1.f, ex);
         }
       }
-      scl[m] = s;
+      scl[m] = sc;
     }
     {
       XT* dst[4] = {S0N, R0N, dS1N, dR1N};
 #pragma unroll
-      for (int u = 0; u < kPerThread; ++u) {
-        const int e = tid + u * kThreads, i = e / kBVG, j = e % kBVG;
+      for (int u = 0; u < kSPT; ++u) {
+        const int e = tid + u * kThreads, i = e / (kBVG / 4), qd = e % (kBVG / 4);
 #pragma unroll
-        for (int m = 0; m < 4; ++m) dst[m][i * L::kLdV + j] = from_f<XT>(sv[m][u] / scl[m]);
+        for (int m = 0; m < 4; ++m) {
+          const float inv = 1.f / scl[m];
+          XT* d = dst[m] + i * L::kLdV + 4 * qd;
+          d[0] = from_f<XT>(ps[m][u].x * inv);
+          d[1] = from_f<XT>(ps[m][u].y * inv);
+          d[2] = from_f<XT>(ps[m][u].z * inv);
+          d[3] = from_f<XT>(ps[m][u].w * inv);
+        }
       }
     }
-    __syncthreads();
+    barrier_lds();
+    if (j0 + kBVG < DV) prefetch(j0 + kBVG);
 
     // ---- A: state products, elementwise Y / dO copies ----
     floatx4 KS, QS, KR, QR, KdS, KdR;
@@ -310,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       store_acc_t<XT>(blk(kEDBT) + trow0, L::kLdX, edb);
       store_acc_t<XT>(blk(kEDCT) + trow0, L::kLdX, edc);
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- B: U = T^S Y (RDN) ----
     floatx4 U;
@@ -322,7 +394,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) du[r] = dls[trow0 + acc_row(r)] * U[r];
       store_acc_t<XT>(blk(kUT) + trow0, L::kLdX, U);
       store_acc_t<XT>(blk(kDUT) + trow0, L::kLdX, du);
-      __syncthreads();
+      barrier_lds();
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) U[r] = gbt[trow0 + acc_row(r)] * vv[r];
@@ -351,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
         store_acc_t<XT>(blk(kDURT) + trow0, L::kLdX, du);
       }
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- D: UR = T^R YR (RDN) ----
     floatx4 UR;
@@ -363,7 +435,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) du[r] = dlr[trow0 + acc_row(r)] * UR[r];
       store_acc_t<XT>(blk(kURT) + trow0, L::kLdX, UR);
       store_acc_t<XT>(blk(kDURT) + trow0, L::kLdX, du);
-      __syncthreads();
+      barrier_lds();
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) UR[r] = ggm[trow0 + acc_row(r)] * rr[r];
@@ -381,7 +453,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     }
     if constexpr (RDN) {
       store_acc_t<XT>(blk(kDURt) + trow0, L::kLdX, dUR);
-      __syncthreads();
+      barrier_lds();
     }
 
     // ---- F: dYR, dX, dKR ----
@@ -406,7 +478,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     store_acc_t<XT>(blk(kDXT) + trow0, L::kLdX, dX);
     store_acc_t<XT>(blk(kDKRT) + trow0, L::kLdX, dKR);
     store_acc_t<XT>(blk(kDYRT) + trow0, L::kLdX, dYR);
-    __syncthreads();
+    barrier_lds();
 
     // ---- G: dU = e^{g_C-g} K dS1 + MP^T dO - MG^T dX ----
     floatx4 dU = zero4();
@@ -419,7 +491,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     }
     if constexpr (RDN) {
       store_acc_t<XT>(blk(kDUt) + trow0, L::kLdX, dU);
-      __syncthreads();
+      barrier_lds();
     }
 
     // ---- H: dY, dKS, dV, row sums of the S path ----
@@ -446,7 +518,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       if constexpr (RDN) store_acc_t<XT>(blk(kDYT) + trow0, L::kLdX, dY);
       store_acc_t<XT>(blk(kDKST) + trow0, L::kLdX, dKS);
     }
-    __syncthreads();
+    barrier_lds();
 
     // ---- I: contractions over this value block ----
 #pragma unroll
@@ -472,13 +544,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
         mma_with<M16, kBVG, false, false>(W5[st], blk(kDYRT) + trow0, L::kLdX, blk(kURT) + 16 * st, L::kLdX);
       }
     }
-    // states at the chunk start times their end gradients (for g_C, h_C)
-#pragma unroll
-    for (int u = 0; u < kPerThread; ++u) {
-      gsC += edge[0] * sv[0][u] * sv[2][u];
-      grC += edge[1] * sv[1][u] * sv[3][u];
-    }
-    __syncthreads();
+    barrier_lds();
   }
 
   // ---- row sums of the value loop ----
@@ -506,7 +572,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   float* ZS = reinterpret_cast<float*>(smem + L::kZ);
   float* ZP = ZS + kChunk * L::kLdZ;
   float* ZR = ZP + kChunk * L::kLdZ;
-  __syncthreads();   // matrices / states / blocks are dead beyond this point
+  barrier_lds();   // matrices / states / blocks are dead beyond this point
   {
     float pb[4] = {0, 0, 0, 0}, pg[4] = {0, 0, 0, 0};
 #pragma unroll
@@ -544,7 +610,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       }
     }
   }
-  __syncthreads();
+  barrier_lds();
 
   // ---- E2: gate gradients (wave 0) ----
   if (tid < kChunk) {
