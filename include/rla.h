@@ -49,7 +49,9 @@
  *   sequences.  Tokens outside every sequence get zero outputs/gradients.
  *   Launch failures return RLA_ERR_HIP.  No call aborts or throws.
  * Supported shapes.  bf16: d_k, d_v in {64, 128}.  fp32: d_k = 64,
- *   d_v in {64, 128}.  Any B, T >= 0, H >= 1.  Internally the sequence is
+ *   d_v in {64, 128} for the forward; the backward (and a forward with
+ *   RLA_FLAG_SAVE_FOR_BACKWARD) in fp32 needs d_v = 64 and returns
+ *   RLA_ERR_UNSUPPORTED otherwise.  Any B, T >= 0, H >= 1.  Internally the sequence is
  *   processed in chunks of 64 tokens; results do not depend on B or packing.
  * Precision.  fp32 inputs: fp32 arithmetic throughout.  bf16 inputs: matrix
  *   products on MFMA with fp32 accumulation; products of q or k with a state

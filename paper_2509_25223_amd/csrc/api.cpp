@@ -37,7 +37,7 @@ struct Problem {
 
 struct Workspace {
   size_t seqs = 0, chunks = 0, nchunks = 0, order = 0, gates = 0, mats = 0;
-  size_t ckS = 0, ckR = 0, mask = 0, dS = 0, dR = 0, total = 0;
+  size_t ckS = 0, ckR = 0, mask = 0, dS = 0, dR = 0, fblk = 0, bblk = 0, total = 0;
 };
 
 rla_status check_problem(const rla_problem* pp, Problem& pr) {
@@ -104,6 +104,9 @@ Workspace plan(const Problem& pr, int op) {
     w.mask = take((size_t)pr.ntok * H * (size_t)pr.DV);
     w.dS = take(st);
     w.dR = take(st);
+    const size_t bl = (pr.bf16 ? 2 : 4) * mc * H * kNumBlk * kChunk * (size_t)pr.DV;
+    w.fblk = take(bl);
+    w.bblk = take(bl);
   }
   w.total = off;
   return w;
@@ -169,6 +172,7 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
     return RLA_ERR_NULL_ARG;
   if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)))
     return RLA_ERR_VALUE;
+  if (pr.save && !pr.bf16 && pr.DV != 64) return RLA_ERR_UNSUPPORTED;
   const int op = pr.save ? (rdn ? RLA_OP_RDN_BACKWARD : RLA_OP_RLA_BACKWARD)
                          : (rdn ? RLA_OP_RDN_FORWARD : RLA_OP_RLA_FORWARD);
   const Workspace w = plan(pr, op);
@@ -187,6 +191,7 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
     p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
     p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
     p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
+    p.fwd_blk = ws + w.fblk;
   }
 
   hipError_t e = hipSuccess;
@@ -217,6 +222,7 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dO) ||
                       !aligned16(dq) || !aligned16(dk) || !aligned16(dv)))
     return RLA_ERR_VALUE;
+  if (!pr.bf16 && pr.DV != 64) return RLA_ERR_UNSUPPORTED;
   const Workspace w = plan(pr, rdn ? RLA_OP_RDN_BACKWARD : RLA_OP_RLA_BACKWARD);
   st = check_workspace(w, workspace, workspace_bytes);
   if (st != RLA_OK) return st;
@@ -233,6 +239,8 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
   p.dS_ws = reinterpret_cast<float*>(ws + w.dS);
   p.dR_ws = reinterpret_cast<float*>(ws + w.dR);
+  p.fwd_blk = ws + w.fblk;
+  p.bwd_blk = ws + w.bblk;
   p.dO = dO; p.dS_fin = dS_final; p.dR_fin = dR_final;
   p.dq = dq; p.dk = dk; p.dv = dv;
   p.dalpha_s = dalpha_s; p.dbeta = dbeta; p.dalpha_r = dalpha_r; p.dgamma = dgamma;

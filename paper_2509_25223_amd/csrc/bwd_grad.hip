@@ -1,27 +1,38 @@
 // Chunk-parallel gradient contractions: one 256-thread workgroup per (chunk,
-// head).  Inputs per chunk: its start states S0, R0 (from the checkpointing
-// forward scan), the gradients dS1, dR1 of its end states (from the reverse
-// scan), the clip mask, and the prep kernel's gates and matrices.  The
-// workgroup re-derives the chunk's forward intermediates (U, X, r, UR, c) and
-// backward intermediates (dUR, dYR, dX, dU, dY, dKS, dKR) one block of 16
-// value columns at a time, and accumulates over the blocks:
-//   dQ += diag(e^g) dO S0^T + diag(e^h gamma) dO R0^T
-//   dK += diag(e^{g_C-g}) U dS1^T + diag(e^{h_C-h}) UR dR1^T + dKS S0^T + dKR R0^T
-//   W1 = dO U^T, W2 = diag(gamma) dO UR^T, W3 = dX U^T, W4 = dY U^T, W5 = dYR UR^T
-//   dV = dX + diag(b) dY   (RLA: dX + diag(b) dU)
-// and the row sums that the gates' gradients need.  Then, from W1..W5, the
-// Gram G = K K^T, the scores P = Q K^T and the decays,
-//   dP = E^S (.) W1 (.) L- + E^R (.) W2 (.) L
-//   dG = [ -E' (.) W3 - diag(b) E^S (.) W4 - diag(gamma) E^R (.) W5 ] (.) L-
-//   dQ += dP K,  dK += dP^T Q + (dG + dG^T) K
-// where the E's are the decay matrices of prep.hip and dA^S = -W4, dA^R = -W5
-// are the gradients of the triangular systems (A = I + ... inverted by T:
-// dA = -T^T dU (T Y)^T = -dY U^T).  Gate gradients: d log a over a chunk is
-// the suffix sum of the gradients of the cumulative sums g_t, h_t.
+// head).  The forward scan saved, per chunk, the start states S0, R0 and the
+// blocks U, UR and r (clipped residual); the reverse scan saved the end-state
+// gradients dS1, dR1 and the blocks dX, dY, dYR (RLA: dU, dUR in the dY, dYR
+// places) and already wrote dv.  What is left are contractions over the value
+// dimension plus chunk-local products; nothing of the scans is recomputed.
 //
-// Precision (bf16 inputs): all products on fp16 MFMA with fp32 accumulation.
-// The state blocks are scaled by a power of two per (chunk, head, block) so
-// their fp16 copies cannot overflow; the scale is undone on the products.
+// With E^S, E', E^R the decay matrices of prep.hip and the row scalings e^g,
+// e^{g_{t-1}}, e^h, dls = e^{g_C-g}, dlr = e^{h_C-h}:
+//   F1 = dO S0^T, F2 = dO R0^T, FK1 = dX S0^T, FK2 = dY S0^T, FK3 = dYR R0^T,
+//   FK4 = U dS1^T, FK5 = UR dR1^T                      (RLA: no FK2, FK3)
+//   dQ = e^g F1 + gamma e^h F2 + dP K
+//   dK = -e^{g_{t-1}} FK1 - b e^g FK2 - gamma e^h FK3 + dls FK4 + dlr FK5
+//        + dP^T Q + (dG + dG^T) K
+//   W1 = dO U^T, W2 = dO UR^T, W3 = dX U^T, W4 = dY U^T, W5 = dYR UR^T
+//   dP = E^S (.) W1 (.) L- + diag(gamma) E^R (.) W2 (.) L
+//   dG = [-E' (.) W3 - diag(b) E^S (.) W4 - diag(gamma) E^R (.) W5] (.) L-
+// (dA^S = -W4 and dA^R = -W5 are the gradients of the triangular systems.)
+// The gate gradients need per-token sums over the value dimension of
+// products of a backward and a forward quantity.  Those that involve a state
+// are row-dots of Q or K with the F matrices above, e.g.
+// sum_j dO_tj (Q S0)_tj = sum_i Q_ti F1_ti, so they come out of the same
+// contractions; sum_j dY_tj V_tj and sum_j dYR_tj r_tj (RLA: dU V, dUR r) are
+// taken elementwise.  d log a over a chunk is the suffix sum of the gradients
+// of the cumulative sums g_t, h_t.
+//
+// Work split: wave w owns the d_k tiles w (and w + 4) for the F contractions,
+// dQ and dK, over all 64 tokens; the 10 lower 16 x 16 tiles of the chunk's
+// token x token matrices are dealt round-robin for W, G = K K^T, P = Q K^T,
+// dP and dG.  State rows stream from HBM (fp32) straight into MFMA B
+// fragments; the token blocks are moved into LDS by LDS-DMA.
+//
+// Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation; a state
+// row is scaled by a power of two before its fp16 conversion when its
+// magnitude needs it, and the scale is undone on the product column.
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -30,91 +41,150 @@ namespace rla {
 
 namespace {
 
-constexpr int kBVG = 16;   // value columns per block
+// A [rows][COLS] tile in LDS with the 16-byte chunks of row r XOR-swizzled by
+// r, so that 16 rows read at one column hit distinct banks.
+template <typename T, int COLS>
+struct Tile {
+  static constexpr int kRowB = COLS * (int)sizeof(T);
+  static constexpr int kCpr = kRowB / 16;
+  static_assert((kCpr & (kCpr - 1)) == 0, "power-of-two chunks per row");
+  __device__ __forceinline__ static int off(int r, int col) {   // byte offset
+    const int b = col * (int)sizeof(T);
+    return r * kRowB + (((b >> 4) ^ (r & (kCpr - 1))) << 4) + (b & 15);
+  }
+  // MFMA fragment of rows r0 .. r0+15 at k = k0 (k contiguous in a row)
+  template <typename M>
+  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0) {
+    constexpr int kPL = M::kStep / 4;   // k-values per lane
+    const int lane = threadIdx.x & 63;
+    const char* b = reinterpret_cast<const char*>(base);
+    return *reinterpret_cast<const typename M::frag*>(
+        b + off(r0 + (lane & 15), k0 + kPL * (lane >> 4)));
+  }
+  __device__ __forceinline__ static T at(const void* base, int r, int col) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + off(r, col));
+  }
+  // LDS-DMA of 64 contiguous rows (global, unswizzled) into the swizzled tile;
+  // every wave issues an equal share.  Completion: wait_vmem + barrier.
+  __device__ __forceinline__ static void dma64(const T* gsrc, void* lds) {
+    constexpr int kInst = kChunk * kRowB / 1024;
+    static_assert(kInst % kWaves == 0, "equal DMA share per wave");
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int m = 0; m < kInst / kWaves; ++m) {
+      const int blk = w * (kInst / kWaves) + m;
+      const int P = blk * 64 + lane;   // physical 16-byte chunk
+      const int r = P / kCpr, c = (P % kCpr) ^ (r & (kCpr - 1));
+      dma16(reinterpret_cast<const char*>(gsrc) + r * kRowB + c * 16,
+            reinterpret_cast<char*>(lds) + blk * 1024);
+    }
+  }
+};
 
-template <typename IN, int DK, bool RDN>
+// token blocks in LDS
+enum { bDO = 0, bU, bUR, bDX, bDY, bDYR, kNumTokBlk };
+// per-token sums (LDS, fp32, one set per wave): direct gate terms of
+// g_t, g_{t-1}, h_t, beta, gamma; row / column sums of the Z matrices
+enum { sGS = 0, sGSP, sGR, sB, sGM, sZRS, sZCS, sZRP, sZCP, sZRR, sZCR, kNumSums };
+
+template <typename IN, int DK, int DV>
 struct GradLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
   typedef typename std::conditional<kBF, f16, float>::type XT;
-  static constexpr int kPad = kBF ? 8 : 4;
-  static constexpr int kLdK = DK + kPad;     // KX, QX rows
-  static constexpr int kLdX = kChunk + kPad; // matrices, per-token blocks [16][64], dP, dG
-  static constexpr int kLdV = kBVG + kPad;   // state blocks [DK][16]
-  static constexpr int kLdZ = kChunk + 1;    // fp32 Z matrices
-  static constexpr bool kMatsInLds = kBF;
-  static constexpr int kNumBlocks = 16;
-  static constexpr int kKX = 0;
-  static constexpr int kQX = kKX + kChunk * kLdK * (int)sizeof(XT);
-  static constexpr int kMats = kQX + kChunk * kLdK * (int)sizeof(XT);
-  static constexpr int kMatBytes = kMatsInLds ? 5 * kChunk * kLdX * (int)sizeof(XT) : 0;
-  static constexpr int kStates = kMats + kMatBytes;
-  static constexpr int kStateBytes = DK * kLdV * (int)sizeof(XT);
-  static constexpr int kBlocks = kStates + 4 * kStateBytes;
-  static constexpr int kBlockBytes = kBVG * kLdX * (int)sizeof(XT);
-  // after the value loop: Z matrices over states + blocks; dP, dG over the
-  // matrices (bf16) or after the Z matrices (fp32)
-  static constexpr int kZ = kStates;
-  static constexpr int kZBytes = 3 * kChunk * kLdZ * 4;
-  static constexpr int kDPG = kMatsInLds ? kMats : kZ + kZBytes;
-  static constexpr int kDPGBytes = 2 * kChunk * kLdX * (int)sizeof(XT);
-  static constexpr int kLoopEnd = kBlocks + kNumBlocks * kBlockBytes;
-  static constexpr int kEndUse = kMatsInLds ? kZ + kZBytes : kDPG + kDPGBytes;
-  static constexpr int kEndOfBlocks = kLoopEnd > kEndUse ? kLoopEnd : kEndUse;
-  static_assert(!kMatsInLds || kDPGBytes <= kMatBytes, "dP region");
-  static constexpr int kVB = kEndOfBlocks;
-  static constexpr int kMask = kVB + kChunk * kBVG * (int)sizeof(IN);
-  static constexpr int kGates = kMask + kChunk * kBVG;
-  static constexpr int kNumGateArrays = 12;
-  static constexpr int kRows = kGates + kNumGateArrays * kChunk * 4;
-  static constexpr int kNumRows = 8;
-  static constexpr int kRed = kRows + kNumRows * kChunk * 4;
-  static constexpr int kBytes = kRed + 64 * 4;
+  typedef Tile<XT, DK> TK;    // K, Q rows
+  typedef Tile<XT, DV> TV;    // token blocks
+  static constexpr int kLdP = kChunk + (kBF ? 8 : 4);   // padded rows of dP, dP^T, dG+dG^T, K^T, Q^T
+  static constexpr int kK = 0;
+  static constexpr int kQ = kK + kChunk * TK::kRowB;
+  static constexpr int kBlk = kQ + kChunk * TK::kRowB;
+  static constexpr int kBlkBytes = kChunk * TV::kRowB;
+  // after the W / G / P products the token blocks are dead; their region then
+  // holds dP, dP^T, dG + dG^T ([64][kLdP]) and K^T, Q^T ([DK][kLdP])
+  static constexpr int kDP = kBlk;
+  static constexpr int kDPT = kDP + kChunk * kLdP * (int)sizeof(XT);
+  static constexpr int kDG = kDPT + kChunk * kLdP * (int)sizeof(XT);
+  static constexpr int kKT = kDG + kChunk * kLdP * (int)sizeof(XT);
+  static constexpr int kQT = kKT + DK * kLdP * (int)sizeof(XT);
+  static constexpr int kOvlEnd = kQT + DK * kLdP * (int)sizeof(XT);
+  static constexpr int kBlkEnd = kBlk + kNumTokBlk * kBlkBytes;
+  static constexpr int kGates = kBlkEnd > kOvlEnd ? kBlkEnd : kOvlEnd;
+  static constexpr int kNumGateArrays = 11;
+  static constexpr int kSums = kGates + kNumGateArrays * kChunk * 4;
+  static constexpr int kRed = kSums + kWaves * kNumSums * kChunk * 4;   // per-wave sums
+  static constexpr int kBytes = kRed + 16 * 4;
   static_assert(kBytes <= 160 * 1024, "gradient kernel LDS");
 };
 
-// per-token block slots, each [16][64] value-major
-enum {
-  kYT = 0,  // Y, later YR
-  kUT, kDUT, kURT, kDURT, kDBT, kDCT, kEDBT, kEDCT, kDURt, kDXT, kDKRT, kDYRT, kDUt, kDYT, kDKST
-};
-// row accumulator slots
-enum { rBeta = 0, rGamma, rGS, rGSP, rGR, rZS, rZP, rZR };
+// DPP lane exchange inside a row of 16 lanes
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                                0xF, 0xF, false));
+}
 
-__device__ __forceinline__ float sum16(float x) {   // over the 16 lanes sharing a lane>>4
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) x += __shfl_xor(x, off, 64);
+// Sum over aligned groups of N lanes (N = 2, 4, 8, 16) inside a 16-lane row;
+// every lane of a group gets the group's sum.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  x += dpp<0xB1>(x);                        // quad_perm [1,0,3,2]
+  if constexpr (N >= 4) x += dpp<0x4E>(x);  // quad_perm [2,3,0,1]
+  if constexpr (N >= 8) x += dpp<0x141>(x); // row_half_mirror
+  if constexpr (N >= 16) x += dpp<0x140>(x); // row_mirror
   return x;
 }
 
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) x += __shfl_xor(x, off, 64);
+  x = group_sum<16>(x);
+  x += __shfl_xor(x, 16, 64);
+  x += __shfl_xor(x, 32, 64);
   return x;
 }
 
-__device__ __forceinline__ float wave_max(float x) {
+// Per-wave per-token sums in LDS, updated branch-free: all lanes that hold
+// the same sum write the same value to the same address.
+// Row sums of a tile quantity (lane: rows 4*(lane>>4)+r) into dst[t0 + row].
+__device__ __forceinline__ void acc_rows(float* dst, int t0, const float (&v)[4]) {
 #pragma unroll
-  for (int off = 1; off < 64; off <<= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
-  return x;
+  for (int r = 0; r < 4; ++r) {
+    const float s = group_sum<16>(v[r]);
+    float* a = dst + t0 + acc_row(r);
+    *a = *a + s;
+  }
 }
 
-template <typename IN, int DK, bool RDN, typename OT>
+// Column sums of a tile quantity (lane: column lane & 15) into dst[s0 + column].
+__device__ __forceinline__ void acc_cols(float* dst, int s0, const float (&v)[4]) {
+  float s = v[0] + v[1] + v[2] + v[3];
+  s += __shfl_xor(s, 16, 64);
+  s += __shfl_xor(s, 32, 64);
+  float* a = dst + s0 + (threadIdx.x & 15);
+  *a = *a + s;
+}
+
+template <typename IN, int DK, int DV, bool RDN, typename OT>
 __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
-  typedef GradLayout<IN, DK, RDN> L;
+  typedef GradLayout<IN, DK, DV> L;
   typedef typename L::XT XT;
-  typedef Mfma<XT> M;       // 32-deep (fp16) / 4-deep (fp32) steps
-  typedef MfmaK16<XT> M16;  // 16-deep steps for contractions over a value block
-  constexpr int IT = DK / 16;
+  typedef typename L::TK TK;
+  typedef typename L::TV TV;
+  typedef Mfma<XT> M;
+  typedef typename M::frag Frag;
+  constexpr bool BF = L::kBF;
+  constexpr int KSV = DV / M::kStep;   // k-steps over the value dimension
+  constexpr int KSK = DK / M::kStep;   // k-steps over d_k
+  constexpr int KSC = kChunk / M::kStep;
+  constexpr int kIT = DK / 64;         // d_k tiles per wave
+  static_assert(sizeof(IN) == sizeof(XT), "bf16 inputs pair with fp16 operands, fp32 with fp32");
+  constexpr int kE = 16 / (int)sizeof(IN);   // elements per 16-byte vector
   extern __shared__ __align__(16) unsigned char smem[];
-  XT* KX = reinterpret_cast<XT*>(smem + L::kKX);
-  XT* QX = reinterpret_cast<XT*>(smem + L::kQX);
-  XT* S0N = reinterpret_cast<XT*>(smem + L::kStates);
-  XT* R0N = reinterpret_cast<XT*>(smem + L::kStates + 1 * L::kStateBytes);
-  XT* dS1N = reinterpret_cast<XT*>(smem + L::kStates + 2 * L::kStateBytes);
-  XT* dR1N = reinterpret_cast<XT*>(smem + L::kStates + 3 * L::kStateBytes);
-  auto blk = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBlocks + b * L::kBlockBytes); };
-  IN* VB = reinterpret_cast<IN*>(smem + L::kVB);
-  uint8_t* mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
+  unsigned char* Kl = smem + L::kK;
+  unsigned char* Ql = smem + L::kQ;
+  auto tokblk = [&](int b) { return smem + L::kBlk + b * L::kBlkBytes; };
+  XT* dPm = reinterpret_cast<XT*>(smem + L::kDP);
+  XT* dPTm = reinterpret_cast<XT*>(smem + L::kDPT);
+  XT* dGm = reinterpret_cast<XT*>(smem + L::kDG);
+  XT* KTm = reinterpret_cast<XT*>(smem + L::kKT);
+  XT* QTm = reinterpret_cast<XT*>(smem + L::kQT);
   float* gbt = reinterpret_cast<float*>(smem + L::kGates);
   float* ggm = gbt + kChunk;
   float* egs = ggm + kChunk;
@@ -126,61 +196,53 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   float* gspv = gsv + kChunk;   // g_{t-1}
   float* grv = gspv + kChunk;   // h_t
   float* edge = grv + kChunk;   // e^{g_C}, e^{h_C}
-  float* rows = reinterpret_cast<float*>(smem + L::kRows);
+  float* sums = reinterpret_cast<float*>(smem + L::kSums);   // [wave][kNumSums][64]
   float* red = reinterpret_cast<float*>(smem + L::kRed);
 
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  float* wsum = sums + w * kNumSums * kChunk;   // this wave's sums
+  auto sum_row = [&](int q) { return wsum + q * kChunk; };
+  auto total = [&](int q, int t) {               // over the waves
+    float x = 0.f;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) x += sums[(v * kNumSums + q) * kChunk + t];
+    return x;
+  };
   ChunkInfo ci;
   if (!chunk_info(p.st, c, ci)) return;
-  const int H = p.H, DV = p.DV, len = ci.len;
+  const int H = p.H, len = ci.len;
   const int64_t tok = ci.tok;
-  const float clip = p.clip;
 
   const IN* qg = reinterpret_cast<const IN*>(p.q);
   const IN* kg = reinterpret_cast<const IN*>(p.k);
   const IN* vg = reinterpret_cast<const IN*>(p.v);
   const IN* dog = reinterpret_cast<const IN*>(p.dO);
-  const XT* mg = reinterpret_cast<const XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
+  const XT* fb = reinterpret_cast<const XT*>(p.fwd_blk);
+  const XT* bb = reinterpret_cast<const XT*>(p.bwd_blk);
   const int64_t soff = ((int64_t)c * H + h) * DK * DV;
 
-  // ---- per value block inputs, prefetched into registers one block ahead:
-  //      V and dO rows (16-byte vectors), the clip mask rows, the four state
-  //      blocks (fp32, 4 columns per vector) ----
-  constexpr int kVR = kBVG * (int)sizeof(IN) / 16;            // vectors per V / dO row
-  constexpr int kVPT = 2 * kChunk * kVR / kThreads;           // V + dO vectors per thread
-  constexpr int kSPT = DK * (kBVG / 4) / kThreads;            // float4 per thread per state
-  static_assert(kVPT >= 1 && kSPT >= 1, "block prefetch shape");
-  uint4 pv[kVPT];
-  uint4 pm;
-  float4 ps[4][kSPT];
-  auto prefetch = [&](int j0) {
-#pragma unroll
-    for (int u = 0; u < kVPT; ++u) {
-      const int e = tid + u * kThreads, which = e / (kChunk * kVR), r = e % (kChunk * kVR);
-      const int t = r / kVR, cv = r % kVR;
-      const IN* src = (which ? dog : vg) + ((tok + t) * H + h) * (int64_t)DV + j0 +
-                      cv * (16 / (int)sizeof(IN));
-      pv[u] = t < len ? *reinterpret_cast<const uint4*>(src) : uint4{0, 0, 0, 0};
-    }
-    pm = uint4{0, 0, 0, 0};
-    if (tid < len)
-      pm = *reinterpret_cast<const uint4*>(p.ck_mask + ((tok + tid) * H + h) * (int64_t)DV + j0);
-    const float* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
-#pragma unroll
-    for (int u = 0; u < kSPT; ++u) {
-      const int e = tid + u * kThreads, i = e / (kBVG / 4), qd = e % (kBVG / 4);
-      const int64_t gi = soff + (int64_t)i * DV + j0 + 4 * qd;
-#pragma unroll
-      for (int m = 0; m < 4; ++m) ps[m][u] = *reinterpret_cast<const float4*>(srcs[m] + gi);
-    }
-  };
-  prefetch(0);
+  // ---------------- phase 0: staging ----------------
+  TV::dma64(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
+  TV::dma64(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
+  TV::dma64(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
+  TV::dma64(bb + blk_off(c, h, H, 1, DV), tokblk(bDY));
+  TV::dma64(bb + blk_off(c, h, H, 2, DV), tokblk(bDYR));
 
-  // ---- chunk-constant staging: K, Q (XT, row-major), matrices, gates ----
+  // V and r rows for the elementwise sums (consumed after the staging barrier)
+  constexpr int kVV = kChunk * DV / kE / kThreads;
+  uint4 vrow[kVV], rrow[kVV];
+#pragma unroll
+  for (int u = 0; u < kVV; ++u) {
+    const int e = tid + u * kThreads, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
+    vrow[u] = t < len ? *reinterpret_cast<const uint4*>(vg + ((tok + t) * H + h) * (int64_t)DV + j)
+                      : uint4{0, 0, 0, 0};
+    rrow[u] = *reinterpret_cast<const uint4*>(fb + blk_off(c, h, H, 2, DV) + t * DV + j);
+  }
+  // K, Q, dO rows: converted to the operand type, stored swizzled
   {
-    constexpr int kE = 16 / (int)sizeof(IN);                  // elements per vector
-    constexpr int kKV = kChunk * DK / kE / kThreads;          // vectors per thread per matrix
-    uint4 kv[kKV], qv[kKV];
+    constexpr int kKV = kChunk * DK / kE / kThreads;
+    constexpr int kOV = kChunk * DV / kE / kThreads;
+    uint4 kv[kKV], qv[kKV], ov[kOV];
 #pragma unroll
     for (int u = 0; u < kKV; ++u) {
       const int e = tid + u * kThreads, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
@@ -189,53 +251,33 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       qv[u] = t < len ? *reinterpret_cast<const uint4*>(qg + off) : uint4{0, 0, 0, 0};
     }
 #pragma unroll
+    for (int u = 0; u < kOV; ++u) {
+      const int e = tid + u * kThreads, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
+      ov[u] = t < len ? *reinterpret_cast<const uint4*>(dog + ((tok + t) * H + h) * (int64_t)DV + j)
+                      : uint4{0, 0, 0, 0};
+    }
+    auto conv = [&](uint4 x) -> uint4 {
+      if constexpr (BF) {
+        const u16x8 a = __builtin_bit_cast(u16x8, x);
+        f16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = (f16)bf2f(a[e]);
+        return __builtin_bit_cast(uint4, o);
+      } else {
+        return x;
+      }
+    };
+#pragma unroll
     for (int u = 0; u < kKV; ++u) {
       const int e = tid + u * kThreads, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
-      if constexpr (L::kBF) {   // bf16 -> fp16, 8 at a time
-        const u16x8 a = __builtin_bit_cast(u16x8, kv[u]), b = __builtin_bit_cast(u16x8, qv[u]);
-        f16x8 ka, qa;
-#pragma unroll
-        for (int x = 0; x < 8; ++x) { ka[x] = (f16)bf2f(a[x]); qa[x] = (f16)bf2f(b[x]); }
-        *reinterpret_cast<f16x8*>(KX + t * L::kLdK + i) = ka;
-        *reinterpret_cast<f16x8*>(QX + t * L::kLdK + i) = qa;
-      } else {
-        *reinterpret_cast<uint4*>(KX + t * L::kLdK + i) = kv[u];
-        *reinterpret_cast<uint4*>(QX + t * L::kLdK + i) = qv[u];
-      }
-    }
-  }
-  const XT *mTS, *mMG, *mMP, *mTR, *mMR;
-  int ldm;
-  if constexpr (L::kMatsInLds) {
-    XT* mats = reinterpret_cast<XT*>(smem + L::kMats);
-    constexpr int kVecM = 16 / sizeof(XT);
-    constexpr int kMV = 5 * kMatElems / kVecM / kThreads;   // vectors per thread
-    uint4 mv[kMV];
-#pragma unroll
-    for (int u = 0; u < kMV; ++u) {
-      const int e = tid + u * kThreads;
-      mv[u] = *reinterpret_cast<const uint4*>(mg + e * kVecM);
+      *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(kv[u]);
+      *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(qv[u]);
     }
 #pragma unroll
-    for (int u = 0; u < kMV; ++u) {
-      const int e = tid + u * kThreads;
-      const int m = e / (kMatElems / kVecM), r = e % (kMatElems / kVecM);
-      const int t = r / (kChunk / kVecM), s = (r % (kChunk / kVecM)) * kVecM;
-      *reinterpret_cast<uint4*>(mats + (m * kChunk + t) * L::kLdX + s) = mv[u];
+    for (int u = 0; u < kOV; ++u) {
+      const int e = tid + u * kThreads, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
+      *reinterpret_cast<uint4*>(tokblk(bDO) + TV::off(t, j)) = conv(ov[u]);
     }
-    ldm = L::kLdX;
-    mTS = mats + kMatTS * kChunk * L::kLdX;
-    mMG = mats + kMatMG * kChunk * L::kLdX;
-    mMP = mats + kMatMP * kChunk * L::kLdX;
-    mTR = mats + kMatTR * kChunk * L::kLdX;
-    mMR = mats + kMatMR * kChunk * L::kLdX;
-  } else {
-    ldm = kChunk;
-    mTS = mg + kMatTS * kMatElems;
-    mMG = mg + kMatMG * kMatElems;
-    mMP = mg + kMatMP * kMatElems;
-    mTR = mg + kMatTR * kMatElems;
-    mMR = mg + kMatMR * kMatElems;
   }
   if (tid < kChunk) {
     const float* gb = p.gate_ws + ((int64_t)c * H + h) * kGateBlock;
@@ -257,381 +299,347 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       edge[1] = __expf(grl);
     }
   }
+  for (int e = tid; e < kWaves * kNumSums * kChunk; e += kThreads) sums[e] = 0.f;
+  wait_vmem();
+  barrier_lds();
 
-  // accumulators: dQ, dK rows of this wave; W1..W5 rows of this wave
-  floatx4 dQ[IT], dK[IT], W1[4], W2[4], W3[4], W4[4], W5[4];
+  // elementwise sums: dY . V (RLA: dU . V) for beta, dYR . r (RLA: dUR . r) for gamma
+  {
+    constexpr int kPerRow = DV / kE;   // threads sharing a row
 #pragma unroll
-  for (int it = 0; it < IT; ++it) { dQ[it] = zero4(); dK[it] = zero4(); }
+    for (int u = 0; u < kVV; ++u) {
+      const int e = tid + u * kThreads, t = e / kPerRow, j = (e % kPerRow) * kE;
+      const uint4 dy = *reinterpret_cast<const uint4*>(tokblk(bDY) + TV::off(t, j));
+      const uint4 dyr = *reinterpret_cast<const uint4*>(tokblk(bDYR) + TV::off(t, j));
+      const XT* a = reinterpret_cast<const XT*>(&dy);
+      const XT* b = reinterpret_cast<const XT*>(&dyr);
+      const IN* x = reinterpret_cast<const IN*>(&vrow[u]);
+      const XT* y = reinterpret_cast<const XT*>(&rrow[u]);
+      float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-  for (int st = 0; st < 4; ++st) {
-    W1[st] = zero4(); W2[st] = zero4(); W3[st] = zero4(); W4[st] = zero4(); W5[st] = zero4();
-  }
-  float rb[4] = {0, 0, 0, 0}, rgm[4] = {0, 0, 0, 0}, rgs[4] = {0, 0, 0, 0};
-  float rgsp[4] = {0, 0, 0, 0}, rgr[4] = {0, 0, 0, 0};
-  float gsC = 0.f, grC = 0.f;   // gradients w.r.t. g_C, h_C (partial, this thread)
-  const int trow0 = 16 * w;
-  barrier_lds();   // staged K, Q, matrices and gates
-
-  for (int j0 = 0; j0 < DV; j0 += kBVG) {
-    // ---- this block's inputs from the prefetch registers into LDS; the
-    //      state blocks scaled to fp16 ----
-#pragma unroll
-    for (int u = 0; u < kVPT; ++u) {
-      const int e = tid + u * kThreads, which = e / (kChunk * kVR), r = e % (kChunk * kVR);
-      const int t = r / kVR, cv = r % kVR, j = cv * (16 / (int)sizeof(IN));
-      if (which == 0) {
-        *reinterpret_cast<uint4*>(VB + t * kBVG + j) = pv[u];
-      } else {
-        const IN* x = reinterpret_cast<const IN*>(&pv[u]);
-#pragma unroll
-        for (int y = 0; y < 16 / (int)sizeof(IN); ++y)
-          blk(kDBT)[(j + y) * L::kLdX + t] = from_f<XT>(to_f<IN>(x[y]));
+      for (int k = 0; k < kE; ++k) {
+        s1 += to_f<XT>(a[k]) * to_f<IN>(x[k]);
+        s2 += to_f<XT>(b[k]) * to_f<XT>(y[k]);
       }
+      s1 = group_sum<kPerRow>(s1);
+      s2 = group_sum<kPerRow>(s2);
+      sum_row(sB)[t] += s1;
+      sum_row(sGM)[t] += s2;
     }
-    if (tid < kChunk) *reinterpret_cast<uint4*>(mask + tid * kBVG) = pm;
-    float mx[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int u = 0; u < kSPT; ++u) {
-#pragma unroll
-      for (int m = 0; m < 4; ++m)
-        mx[m] = fmaxf(mx[m], fmaxf(fmaxf(fabsf(ps[m][u].x), fabsf(ps[m][u].y)),
-                                   fmaxf(fabsf(ps[m][u].z), fabsf(ps[m][u].w))));
-      // states at the chunk start times their end gradients (for g_C, h_C)
-      gsC += edge[0] * (ps[0][u].x * ps[2][u].x + ps[0][u].y * ps[2][u].y +
-                        ps[0][u].z * ps[2][u].z + ps[0][u].w * ps[2][u].w);
-      grC += edge[1] * (ps[1][u].x * ps[3][u].x + ps[1][u].y * ps[3][u].y +
-                        ps[1][u].z * ps[3][u].z + ps[1][u].w * ps[3][u].w);
-    }
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const float wm = wave_max(mx[m]);
-      if (lane == 0) red[w * 4 + m] = wm;
-    }
-    barrier_lds();
-    float scl[4];   // power-of-two scale: value = scl * stored
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      const float bmax = fmaxf(fmaxf(red[m], red[4 + m]), fmaxf(red[8 + m], red[12 + m]));
-      float sc = 1.f;
-      if constexpr (L::kBF) {
-        if (bmax > 16384.f) {
-          int ex;
-          frexpf(bmax / 16384.f, &ex);
-          sc = ldexpf(1.f, ex);
-        }
-      }
-      scl[m] = sc;
-    }
-    {
-      XT* dst[4] = {S0N, R0N, dS1N, dR1N};
-#pragma unroll
-      for (int u = 0; u < kSPT; ++u) {
-        const int e = tid + u * kThreads, i = e / (kBVG / 4), qd = e % (kBVG / 4);
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const float inv = 1.f / scl[m];
-          XT* d = dst[m] + i * L::kLdV + 4 * qd;
-          d[0] = from_f<XT>(ps[m][u].x * inv);
-          d[1] = from_f<XT>(ps[m][u].y * inv);
-          d[2] = from_f<XT>(ps[m][u].z * inv);
-          d[3] = from_f<XT>(ps[m][u].w * inv);
-        }
-      }
-    }
-    barrier_lds();
-    if (j0 + kBVG < DV) prefetch(j0 + kBVG);
-
-    // ---- A: state products, elementwise Y / dO copies ----
-    floatx4 KS, QS, KR, QR, KdS, KdR;
-    {
-      KS = zero4(); QS = zero4(); KR = zero4(); QR = zero4(); KdS = zero4(); KdR = zero4();
-      const XT* Kw = KX + trow0 * L::kLdK;
-      const XT* Qw = QX + trow0 * L::kLdK;
-      mma_with<M, DK, true, false>(KS, Kw, L::kLdK, S0N, L::kLdV);
-      mma_with<M, DK, true, false>(QS, Qw, L::kLdK, S0N, L::kLdV);
-      mma_with<M, DK, true, false>(KR, Kw, L::kLdK, R0N, L::kLdV);
-      mma_with<M, DK, true, false>(QR, Qw, L::kLdK, R0N, L::kLdV);
-      mma_with<M, DK, true, false>(KdS, Kw, L::kLdK, dS1N, L::kLdV);
-      mma_with<M, DK, true, false>(KdR, Kw, L::kLdK, dR1N, L::kLdV);
-      KS *= scl[0]; QS *= scl[0]; KR *= scl[1]; QR *= scl[1]; KdS *= scl[2]; KdR *= scl[3];
-    }
-    float vv[4], dob[4], yarg[4];
-    {
-      floatx4 y, dc, edb, edc;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = trow0 + acc_row(r), j = acc_col();
-        vv[r] = to_f<IN>(VB[t * kBVG + j]);
-        dob[r] = to_f<XT>(blk(kDBT)[j * L::kLdX + t]);
-        yarg[r] = RDN ? vv[r] - egs[t] * KS[r] : vv[r];
-        y[r] = gbt[t] * yarg[r];
-        dc[r] = ggm[t] * dob[r];
-        edb[r] = egs[t] * dob[r];
-        edc[r] = egr[t] * dc[r];
-      }
-      if constexpr (RDN) {
-        store_acc_t<XT>(blk(kYT) + trow0, L::kLdX, y);
-      } else {
-        floatx4 du;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) du[r] = dls[trow0 + acc_row(r)] * y[r];
-        store_acc_t<XT>(blk(kUT) + trow0, L::kLdX, y);
-        store_acc_t<XT>(blk(kDUT) + trow0, L::kLdX, du);
-      }
-      store_acc_t<XT>(blk(kDCT) + trow0, L::kLdX, dc);
-      store_acc_t<XT>(blk(kEDBT) + trow0, L::kLdX, edb);
-      store_acc_t<XT>(blk(kEDCT) + trow0, L::kLdX, edc);
-    }
-    barrier_lds();
-
-    // ---- B: U = T^S Y (RDN) ----
-    floatx4 U;
-    if constexpr (RDN) {
-      U = zero4();
-      mma_with<M, kChunk, true, true>(U, mTS + trow0 * ldm, ldm, blk(kYT), L::kLdX);
-      floatx4 du;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) du[r] = dls[trow0 + acc_row(r)] * U[r];
-      store_acc_t<XT>(blk(kUT) + trow0, L::kLdX, U);
-      store_acc_t<XT>(blk(kDUT) + trow0, L::kLdX, du);
-      barrier_lds();
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) U[r] = gbt[trow0 + acc_row(r)] * vv[r];
-    }
-
-    // ---- C: residual and the R path's right-hand side ----
-    float rr[4], yrarg[4];
-    {
-      floatx4 mgu = zero4(), y;
-      mma_with<M, kChunk, true, true>(mgu, mMG + trow0 * ldm, ldm, blk(kUT), L::kLdX);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = trow0 + acc_row(r);
-        const float x = vv[r] - egsp[t] * KS[r] - mgu[r];
-        rr[r] = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
-        yrarg[r] = RDN ? rr[r] - egr[t] * KR[r] : rr[r];
-        y[r] = ggm[t] * yrarg[r];
-      }
-      if constexpr (RDN) {
-        store_acc_t<XT>(blk(kYT) + trow0, L::kLdX, y);
-      } else {
-        floatx4 du;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) du[r] = dlr[trow0 + acc_row(r)] * y[r];
-        store_acc_t<XT>(blk(kURT) + trow0, L::kLdX, y);
-        store_acc_t<XT>(blk(kDURT) + trow0, L::kLdX, du);
-      }
-    }
-    barrier_lds();
-
-    // ---- D: UR = T^R YR (RDN) ----
-    floatx4 UR;
-    if constexpr (RDN) {
-      UR = zero4();
-      mma_with<M, kChunk, true, true>(UR, mTR + trow0 * ldm, ldm, blk(kYT), L::kLdX);
-      floatx4 du;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) du[r] = dlr[trow0 + acc_row(r)] * UR[r];
-      store_acc_t<XT>(blk(kURT) + trow0, L::kLdX, UR);
-      store_acc_t<XT>(blk(kDURT) + trow0, L::kLdX, du);
-      barrier_lds();
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) UR[r] = ggm[trow0 + acc_row(r)] * rr[r];
-    }
-
-    // ---- E: correction read-out c, and dUR = e^{h_C-h} K dR1 + MR^T dc ----
-    floatx4 cc = zero4(), dUR = zero4();
-    mma_with<M, kChunk, true, true>(cc, mMR + trow0 * ldm, ldm, blk(kURT), L::kLdX);
-    mma_with<M, kChunk, false, true>(dUR, mMR + trow0, ldm, blk(kDCT), L::kLdX);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = trow0 + acc_row(r);
-      cc[r] += egr[t] * QR[r];
-      dUR[r] += dlr[t] * KdR[r];
-    }
-    if constexpr (RDN) {
-      store_acc_t<XT>(blk(kDURt) + trow0, L::kLdX, dUR);
-      barrier_lds();
-    }
-
-    // ---- F: dYR, dX, dKR ----
-    floatx4 dYR = dUR, dX, dKR;
-    if constexpr (RDN) {
-      dYR = zero4();
-      mma_with<M, kChunk, false, true>(dYR, mTR + trow0, ldm, blk(kDURt), L::kLdX);
-    }
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = trow0 + acc_row(r), j = acc_col();
-      dX[r] = mask[t * kBVG + j] ? ggm[t] * dYR[r] : 0.f;
-      dKR[r] = RDN ? -ggm[t] * egr[t] * dYR[r] : 0.f;
-      // gamma: o = b + gamma c, and (RDN) YR = gamma (r - e^h KR) / (RLA) UR = gamma r
-      rgm[r] += dob[r] * cc[r] + dYR[r] * yrarg[r];
-      // h_t through e^{h_t} in c and (RDN) in YR; h_t, h_C through the R update
-      const float kdu = KdR[r] * UR[r] * dlr[t];
-      rgr[r] += ggm[t] * dob[r] * egr[t] * QR[r] - kdu;
-      if constexpr (RDN) rgr[r] += -ggm[t] * egr[t] * dYR[r] * KR[r];
-      grC += kdu;
-    }
-    store_acc_t<XT>(blk(kDXT) + trow0, L::kLdX, dX);
-    store_acc_t<XT>(blk(kDKRT) + trow0, L::kLdX, dKR);
-    store_acc_t<XT>(blk(kDYRT) + trow0, L::kLdX, dYR);
-    barrier_lds();
-
-    // ---- G: dU = e^{g_C-g} K dS1 + MP^T dO - MG^T dX ----
-    floatx4 dU = zero4();
-    {
-      floatx4 b = zero4();
-      mma_with<M, kChunk, false, true>(dU, mMP + trow0, ldm, blk(kDBT), L::kLdX);
-      mma_with<M, kChunk, false, true>(b, mMG + trow0, ldm, blk(kDXT), L::kLdX);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) dU[r] += dls[trow0 + acc_row(r)] * KdS[r] - b[r];
-    }
-    if constexpr (RDN) {
-      store_acc_t<XT>(blk(kDUt) + trow0, L::kLdX, dU);
-      barrier_lds();
-    }
-
-    // ---- H: dY, dKS, dV, row sums of the S path ----
-    {
-      floatx4 dY = dU, dKS;
-      if constexpr (RDN) {
-        dY = zero4();
-        mma_with<M, kChunk, false, true>(dY, mTS + trow0, ldm, blk(kDUt), L::kLdX);
-      }
-      OT* dvg = reinterpret_cast<OT*>(p.dv);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = trow0 + acc_row(r);
-        dKS[r] = -egsp[t] * dX[r] - (RDN ? gbt[t] * egs[t] * dY[r] : 0.f);
-        if (t < len)
-          dvg[((tok + t) * H + h) * (int64_t)DV + j0 + acc_col()] = from_f<OT>(dX[r] + gbt[t] * dY[r]);
-        rb[r] += dY[r] * yarg[r];
-        const float kdu = KdS[r] * U[r] * dls[t];
-        rgs[r] += egs[t] * dob[r] * QS[r] - kdu;
-        if constexpr (RDN) rgs[r] += -gbt[t] * egs[t] * dY[r] * KS[r];
-        rgsp[r] += -egsp[t] * dX[r] * KS[r];
-        gsC += kdu;
-      }
-      if constexpr (RDN) store_acc_t<XT>(blk(kDYT) + trow0, L::kLdX, dY);
-      store_acc_t<XT>(blk(kDKST) + trow0, L::kLdX, dKS);
-    }
-    barrier_lds();
-
-    // ---- I: contractions over this value block ----
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int io = it * 16 * L::kLdV;
-      floatx4 t0 = zero4(), t1 = zero4(), t2 = zero4(), t3 = zero4(), t4 = zero4(), t5 = zero4();
-      mma_with<M16, kBVG, false, true>(t0, blk(kEDBT) + trow0, L::kLdX, S0N + io, L::kLdV);
-      mma_with<M16, kBVG, false, true>(t1, blk(kEDCT) + trow0, L::kLdX, R0N + io, L::kLdV);
-      mma_with<M16, kBVG, false, true>(t2, blk(kDUT) + trow0, L::kLdX, dS1N + io, L::kLdV);
-      mma_with<M16, kBVG, false, true>(t3, blk(kDURT) + trow0, L::kLdX, dR1N + io, L::kLdV);
-      mma_with<M16, kBVG, false, true>(t4, blk(kDKST) + trow0, L::kLdX, S0N + io, L::kLdV);
-      if constexpr (RDN) mma_with<M16, kBVG, false, true>(t5, blk(kDKRT) + trow0, L::kLdX, R0N + io, L::kLdV);
-      dQ[it] += scl[0] * t0 + scl[1] * t1;
-      dK[it] += scl[2] * t2 + scl[3] * t3 + scl[0] * t4 + scl[1] * t5;
-    }
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      mma_with<M16, kBVG, false, false>(W1[st], blk(kDBT) + trow0, L::kLdX, blk(kUT) + 16 * st, L::kLdX);
-      mma_with<M16, kBVG, false, false>(W2[st], blk(kDCT) + trow0, L::kLdX, blk(kURT) + 16 * st, L::kLdX);
-      mma_with<M16, kBVG, false, false>(W3[st], blk(kDXT) + trow0, L::kLdX, blk(kUT) + 16 * st, L::kLdX);
-      if constexpr (RDN) {
-        mma_with<M16, kBVG, false, false>(W4[st], blk(kDYT) + trow0, L::kLdX, blk(kUT) + 16 * st, L::kLdX);
-        mma_with<M16, kBVG, false, false>(W5[st], blk(kDYRT) + trow0, L::kLdX, blk(kURT) + 16 * st, L::kLdX);
-      }
-    }
-    barrier_lds();
   }
 
-  // ---- row sums of the value loop ----
+  // ---------------- phase 1: contractions over the value dimension ----------------
+  floatx4 dQ[kIT][4], dK[kIT][4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float a = sum16(rb[r]), b = sum16(rgm[r]), s1 = sum16(rgs[r]), s2 = sum16(rgsp[r]),
-                s3 = sum16(rgr[r]);
-    if ((lane & 15) == 0) {
-      const int t = trow0 + acc_row(r);
-      rows[rBeta * kChunk + t] = a;
-      rows[rGamma * kChunk + t] = b;
-      rows[rGS * kChunk + t] = s1;
-      rows[rGSP * kChunk + t] = s2;
-      rows[rGR * kChunk + t] = s3;
+  for (int m = 0; m < kIT; ++m)
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) { dQ[m][tt] = zero4(); dK[m][tt] = zero4(); }
+  float gsC = 0.f, grC = 0.f;
+
+  // a state's rows i0 .. i0+15 as raw fp32 values in B-fragment order
+  constexpr int kRaw = BF ? 2 * KSV : KSV;
+  typedef typename std::conditional<BF, float4, float>::type RawT;
+  const float* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
+  auto load_raw = [&](RawT (&raw)[kRaw], int st, int i0) {
+    const float* rowp = srcs[st] + soff + (int64_t)(i0 + (lane & 15)) * DV;
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks) {
+      if constexpr (BF) {
+        const int j = ks * M::kStep + 8 * (lane >> 4);
+        raw[2 * ks] = *reinterpret_cast<const float4*>(rowp + j);
+        raw[2 * ks + 1] = *reinterpret_cast<const float4*>(rowp + j + 4);
+      } else {
+        raw[ks] = rowp[ks * M::kStep + (lane >> 4)];
+      }
+    }
+  };
+  // operand fragments; returns the power-of-two scale of this lane's row
+  auto convert = [&](const RawT (&raw)[kRaw], Frag (&fr)[KSV]) -> float {
+    if constexpr (BF) {
+      float mx = 0.f;
+#pragma unroll
+      for (int x = 0; x < kRaw; ++x)
+        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(raw[x].x), fabsf(raw[x].y)),
+                             fmaxf(fabsf(raw[x].z), fabsf(raw[x].w))));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float scl = 1.f;
+      if (mx > 16384.f) {
+        int ex;
+        frexpf(mx / 16384.f, &ex);
+        scl = ldexpf(1.f, ex);
+      }
+      const float inv = 1.f / scl;
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) {
+        const float4 a = raw[2 * ks], b = raw[2 * ks + 1];
+        fr[ks] = f16x8{(f16)(a.x * inv), (f16)(a.y * inv), (f16)(a.z * inv), (f16)(a.w * inv),
+                       (f16)(b.x * inv), (f16)(b.y * inv), (f16)(b.z * inv), (f16)(b.w * inv)};
+      }
+      return scl;
+    } else {
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) fr[ks] = raw[ks];
+      return 1.f;
+    }
+  };
+  // sum over this lane's elements of (scaled fragment) x (raw values)
+  auto frag_dot = [&](const Frag (&fr)[KSV], float scl, const RawT (&raw)[kRaw]) {
+    float s = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks) {
+      if constexpr (BF) {
+        const float4 a = raw[2 * ks], b = raw[2 * ks + 1];
+        s += (float)fr[ks][0] * a.x + (float)fr[ks][1] * a.y + (float)fr[ks][2] * a.z +
+             (float)fr[ks][3] * a.w + (float)fr[ks][4] * b.x + (float)fr[ks][5] * b.y +
+             (float)fr[ks][6] * b.z + (float)fr[ks][7] * b.w;
+      } else {
+        s += fr[ks] * raw[ks];
+      }
+    }
+    return s * scl;
+  };
+  // [16 tokens x 16 state rows] tile: token block rows 16 tt times the state
+  // rows of the fragments, contracted over the value dimension
+  auto contract = [&](int b, int tt, const Frag (&fr)[KSV], float scl) {
+    floatx4 acc = zero4();
+#pragma unroll
+    for (int ks = 0; ks < KSV; ++ks)
+      acc = M::mma(TV::template frag<M>(tokblk(b), 16 * tt, ks * M::kStep), fr[ks], acc);
+    return acc * scl;
+  };
+
+  // per d_k tile: S0 with dS1, then R0 with dR1; the next pair's rows are
+  // loaded while the current pair's products run
+  RawT rawA[kRaw], rawB[kRaw];
+  load_raw(rawA, 0, 16 * w);
+  load_raw(rawB, 2, 16 * w);
+#pragma unroll
+  for (int m = 0; m < kIT; ++m) {
+    // the token-block fragments are reloaded per d_k tile: keeping them
+    // across tiles would need ~400 registers
+    asm volatile("" ::: "memory");
+    const int i0 = 16 * (w + 4 * m);
+    const int icol = i0 + (lane & 15);   // this lane's output column
+    // K, Q at this lane's output positions of token tile tt
+    auto kq_of = [&](int tt, float (&kq)[4], float (&qq)[4]) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        kq[r] = to_f<XT>(TK::at(Kl, 16 * tt + acc_row(r), icol));
+        qq[r] = to_f<XT>(TK::at(Ql, 16 * tt + acc_row(r), icol));
+      }
+    };
+    Frag f0[KSV], f1[KSV];
+    // ---- S0 (rawA) and dS1 (rawB) ----
+    {
+      const float sS = convert(rawA, f0);
+      gsC += edge[0] * frag_dot(f0, sS, rawB);   // e^{g_C} <S0, dS1>
+      const float sD = convert(rawB, f1);
+      load_raw(rawA, 1, i0);
+      load_raw(rawB, 3, i0);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        asm volatile("" ::: "memory");   // bounds how far fragment loads are hoisted
+        // F1 = dO S0^T, FK1 = dX S0^T, FK2 = dY S0^T, FK4 = U dS1^T
+        const floatx4 F1 = contract(bDO, tt, f0, sS);
+        const floatx4 FK1 = contract(bDX, tt, f0, sS);
+        floatx4 FK2 = zero4();
+        if constexpr (RDN) FK2 = contract(bDY, tt, f0, sS);
+        const floatx4 FK4 = contract(bU, tt, f1, sD);
+        float kq[4], qq[4], ags[4], agsp[4], ab[4];
+        kq_of(tt, kq, qq);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * tt + acc_row(r);
+          const float c1 = egs[t] * F1[r], c2 = -egsp[t] * FK1[r], c6 = dls[t] * FK4[r];
+          dQ[m][tt][r] += c1;
+          dK[m][tt][r] += c2 + c6;
+          ags[r] = qq[r] * c1 - kq[r] * c6;
+          agsp[r] = kq[r] * c2;
+          gsC += kq[r] * c6;
+          ab[r] = 0.f;
+          if constexpr (RDN) {
+            const float e2 = -egs[t] * FK2[r];
+            dK[m][tt][r] += gbt[t] * e2;
+            ags[r] += kq[r] * gbt[t] * e2;
+            ab[r] = kq[r] * e2;
+          }
+        }
+        acc_rows(sum_row(sGS), 16 * tt, ags);
+        acc_rows(sum_row(sGSP), 16 * tt, agsp);
+        if constexpr (RDN) acc_rows(sum_row(sB), 16 * tt, ab);
+      }
+    }
+    // ---- R0 (rawA) and dR1 (rawB) ----
+    {
+      const float sR = convert(rawA, f0);
+      grC += edge[1] * frag_dot(f0, sR, rawB);   // e^{h_C} <R0, dR1>
+      const float sE = convert(rawB, f1);
+      if (m + 1 < kIT) {
+        load_raw(rawA, 0, i0 + 64);
+        load_raw(rawB, 2, i0 + 64);
+      }
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        asm volatile("" ::: "memory");
+        // F2 = dO R0^T, FK3 = dYR R0^T, FK5 = UR dR1^T
+        const floatx4 F2 = contract(bDO, tt, f0, sR);
+        floatx4 FK3 = zero4();
+        if constexpr (RDN) FK3 = contract(bDYR, tt, f0, sR);
+        const floatx4 FK5 = contract(bUR, tt, f1, sE);
+        float kq[4], qq[4], agr[4], agm[4];
+        kq_of(tt, kq, qq);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * tt + acc_row(r);
+          const float e4 = egr[t] * F2[r], c4 = ggm[t] * e4, c7 = dlr[t] * FK5[r];
+          dQ[m][tt][r] += c4;
+          dK[m][tt][r] += c7;
+          agr[r] = qq[r] * c4 - kq[r] * c7;
+          agm[r] = qq[r] * e4;
+          grC += kq[r] * c7;
+          if constexpr (RDN) {
+            const float e5 = -egr[t] * FK3[r], c5 = ggm[t] * e5;
+            dK[m][tt][r] += c5;
+            agr[r] += kq[r] * c5;
+            agm[r] += kq[r] * e5;
+          }
+        }
+        acc_rows(sum_row(sGR), 16 * tt, agr);
+        acc_rows(sum_row(sGM), 16 * tt, agm);
+      }
     }
   }
   {
     const float a = wave_sum(gsC), b = wave_sum(grC);
-    if (lane == 0) { red[16 + w] = a; red[20 + w] = b; }
+    if (lane == 0) { red[w] = a; red[4 + w] = b; }
   }
 
-  // ---- E1: Gram / scores, decay matrices, dP, dG and the Z matrices ----
-  XT* dPm = reinterpret_cast<XT*>(smem + L::kDPG);
-  XT* dGm = dPm + kChunk * L::kLdX;
-  float* ZS = reinterpret_cast<float*>(smem + L::kZ);
-  float* ZP = ZS + kChunk * L::kLdZ;
-  float* ZR = ZP + kChunk * L::kLdZ;
-  barrier_lds();   // matrices / states / blocks are dead beyond this point
-  {
-    float pb[4] = {0, 0, 0, 0}, pg[4] = {0, 0, 0, 0};
+  // ---------------- phase 2: W, G, P on the lower token tiles ----------------
+  constexpr int kMyTiles = 3;   // at most 3 of the 10 lower tiles per wave
+  floatx4 tW1[kMyTiles], tW2[kMyTiles], tW3[kMyTiles], tW4[kMyTiles], tW5[kMyTiles];
+  floatx4 tG[kMyTiles], tP[kMyTiles];
+  auto tile_of = [](int idx, int& tt, int& st) {   // lower tiles, row by row
+    tt = idx >= 6 ? 3 : idx >= 3 ? 2 : idx >= 1 ? 1 : 0;
+    st = idx - (tt * (tt + 1)) / 2;
+  };
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      floatx4 G = zero4(), P = zero4();
-      mma_with<M, DK, true, true>(G, KX + trow0 * L::kLdK, L::kLdK, KX + 16 * st * L::kLdK, L::kLdK);
-      mma_with<M, DK, true, true>(P, QX + trow0 * L::kLdK, L::kLdK, KX + 16 * st * L::kLdK, L::kLdK);
-      floatx4 dp, dg;
+  for (int x = 0; x < kMyTiles; ++x) {
+    asm volatile("" ::: "memory");
+    const int idx = w + 4 * x;
+    tW1[x] = zero4(); tW2[x] = zero4(); tW3[x] = zero4(); tW4[x] = zero4(); tW5[x] = zero4();
+    tG[x] = zero4(); tP[x] = zero4();
+    if (idx < 10) {
+      int tt, st;
+      tile_of(idx, tt, st);
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) {
+        const int k0 = ks * M::kStep;
+        const Frag fo = TV::template frag<M>(tokblk(bDO), 16 * tt, k0);
+        const Frag fx = TV::template frag<M>(tokblk(bDX), 16 * tt, k0);
+        const Frag fu = TV::template frag<M>(tokblk(bU), 16 * st, k0);
+        const Frag fur = TV::template frag<M>(tokblk(bUR), 16 * st, k0);
+        tW1[x] = M::mma(fo, fu, tW1[x]);
+        tW2[x] = M::mma(fo, fur, tW2[x]);
+        tW3[x] = M::mma(fx, fu, tW3[x]);
+        if constexpr (RDN) {
+          tW4[x] = M::mma(TV::template frag<M>(tokblk(bDY), 16 * tt, k0), fu, tW4[x]);
+          tW5[x] = M::mma(TV::template frag<M>(tokblk(bDYR), 16 * tt, k0), fur, tW5[x]);
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) {
+        const int k0 = ks * M::kStep;
+        const Frag fk = TK::template frag<M>(Kl, 16 * st, k0);
+        tG[x] = M::mma(TK::template frag<M>(Kl, 16 * tt, k0), fk, tG[x]);
+        tP[x] = M::mma(TK::template frag<M>(Ql, 16 * tt, k0), fk, tP[x]);
+      }
+    }
+  }
+  barrier_lds();   // token blocks dead: their region becomes dP, dP^T, dG + dG^T, K^T, Q^T
+
+  // ---- dP, dG and the sums over the decay-matrix products ----
+  constexpr int ldp = L::kLdP;
+#pragma unroll
+  for (int x = 0; x < kMyTiles; ++x) {
+    const int idx = w + 4 * x;
+    if (idx < 10) {
+      int tt, st;
+      tile_of(idx, tt, st);
+      float zs[4], zp[4], zr[4], zb[4], zg[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int t = trow0 + acc_row(r), s = 16 * st + acc_col();
+        const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
         const bool lower = s < t, diag = s <= t;
         const float es = __expf(fminf(gsv[t] - gsv[s], 0.f));
         const float ep = __expf(fminf(gspv[t] - gsv[s], 0.f));
         const float er = __expf(fminf(grv[t] - grv[s], 0.f));
-        const float dAs = RDN ? -W4[st][r] : 0.f, dAr = RDN ? -W5[st][r] : 0.f;
-        dp[r] = (lower ? es * W1[st][r] : 0.f) + (diag ? er * W2[st][r] : 0.f);
-        dg[r] = lower ? (-ep * W3[st][r] + gbt[t] * es * dAs + ggm[t] * er * dAr) : 0.f;
-        ZS[t * L::kLdZ + s] = lower ? es * (P[r] * W1[st][r] + gbt[t] * G[r] * dAs) : 0.f;
-        ZP[t * L::kLdZ + s] = lower ? -ep * G[r] * W3[st][r] : 0.f;
-        ZR[t * L::kLdZ + s] = (diag ? er * P[r] * W2[st][r] : 0.f) + (lower ? ggm[t] * er * G[r] * dAr : 0.f);
-        pb[r] += lower ? dAs * es * G[r] : 0.f;
-        pg[r] += lower ? dAr * er * G[r] : 0.f;
+        const float W1 = tW1[x][r], W2 = tW2[x][r], W3 = tW3[x][r];
+        const float G = tG[x][r], P = tP[x][r];
+        const float dAs = RDN ? -tW4[x][r] : 0.f, dAr = RDN ? -tW5[x][r] : 0.f;
+        const float gw2 = ggm[t] * W2;
+        const float dp = (lower ? es * W1 : 0.f) + (diag ? er * gw2 : 0.f);
+        const float dg = lower ? (-ep * W3 + gbt[t] * es * dAs + ggm[t] * er * dAr) : 0.f;
+        zs[r] = lower ? es * (P * W1 + gbt[t] * G * dAs) : 0.f;
+        zp[r] = lower ? -ep * G * W3 : 0.f;
+        zr[r] = (diag ? er * P * gw2 : 0.f) + (lower ? ggm[t] * er * G * dAr : 0.f);
+        zb[r] = lower ? dAs * es * G : 0.f;
+        zg[r] = (lower ? dAr * er * G : 0.f) + (diag ? er * P * W2 : 0.f);
+        dPm[t * ldp + s] = from_f<XT>(dp);
+        dPTm[s * ldp + t] = from_f<XT>(dp);
+        if (lower) {   // dG + dG^T: the two halves have disjoint supports
+          dGm[t * ldp + s] = from_f<XT>(dg);
+          dGm[s * ldp + t] = from_f<XT>(dg);
+        } else if (s == t) {
+          dGm[t * ldp + t] = from_f<XT>(0.f);
+        }
       }
-      store_acc<XT>(dPm + trow0 * L::kLdX + 16 * st, L::kLdX, dp);
-      store_acc<XT>(dGm + trow0 * L::kLdX + 16 * st, L::kLdX, dg);
+      acc_rows(sum_row(sZRS), 16 * tt, zs);
+      acc_rows(sum_row(sZRP), 16 * tt, zp);
+      acc_rows(sum_row(sZRR), 16 * tt, zr);
+      acc_rows(sum_row(sB), 16 * tt, zb);
+      acc_rows(sum_row(sGM), 16 * tt, zg);
+      acc_cols(sum_row(sZCS), 16 * st, zs);
+      acc_cols(sum_row(sZCP), 16 * st, zp);
+      acc_cols(sum_row(sZCR), 16 * st, zr);
     }
+  }
+  // dP above the diagonal and dP^T below it are zero: the 6 upper tiles
+  for (int x = w; x < 6; x += kWaves) {
+    const int tt = x < 3 ? 0 : x < 5 ? 1 : 2;
+    const int st = tt + 1 + x - (tt == 0 ? 0 : tt == 1 ? 3 : 5);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float a = sum16(pb[r]), b = sum16(pg[r]);
-      if ((lane & 15) == 0) {
-        const int t = trow0 + acc_row(r);
-        rows[rBeta * kChunk + t] += a;
-        rows[rGamma * kChunk + t] += b;
-      }
+      const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
+      dPm[t * ldp + s] = from_f<XT>(0.f);
+      dPTm[s * ldp + t] = from_f<XT>(0.f);
+    }
+  }
+  // K^T, Q^T for the final products
+  for (int e = tid; e < kChunk * DK / kE; e += kThreads) {
+    const int s = e / (DK / kE), i = (e % (DK / kE)) * kE;
+    const uint4 kv = *reinterpret_cast<const uint4*>(Kl + TK::off(s, i));
+    const uint4 qv = *reinterpret_cast<const uint4*>(Ql + TK::off(s, i));
+    const XT* a = reinterpret_cast<const XT*>(&kv);
+    const XT* b = reinterpret_cast<const XT*>(&qv);
+#pragma unroll
+    for (int k = 0; k < kE; ++k) {
+      KTm[(i + k) * ldp + s] = a[k];
+      QTm[(i + k) * ldp + s] = b[k];
     }
   }
   barrier_lds();
 
-  // ---- E2: gate gradients (wave 0) ----
+  // ---------------- phase 3: gate gradients; dQ += dP K, dK += dP^T Q + (dG + dG^T) K ----------------
   if (tid < kChunk) {
     const int t = tid;
-    float rzs = 0.f, czs = 0.f, rzp = 0.f, czp = 0.f, rzr = 0.f, czr = 0.f, rzp1 = 0.f;
-    for (int s = 0; s < kChunk; ++s) {
-      rzs += ZS[t * L::kLdZ + s];
-      czs += ZS[s * L::kLdZ + t];
-      rzp += ZP[t * L::kLdZ + s];
-      czp += ZP[s * L::kLdZ + t];
-      rzr += ZR[t * L::kLdZ + s];
-      czr += ZR[s * L::kLdZ + t];
-      if (t + 1 < kChunk) rzp1 += ZP[(t + 1) * L::kLdZ + s];
-    }
-    const float gsC_all = red[16] + red[17] + red[18] + red[19];
-    const float grC_all = red[20] + red[21] + red[22] + red[23];
-    float dgs = rows[rGS * kChunk + t] + rzs - czs - czp +
-                (t + 1 < kChunk ? rows[rGSP * kChunk + t + 1] + rzp1 : 0.f) +
-                (t == kChunk - 1 ? gsC_all : 0.f);
-    float dgr = rows[rGR * kChunk + t] + rzr - czr + (t == kChunk - 1 ? grC_all : 0.f);
-    (void)rzp;
+    const float gsC_all = red[0] + red[1] + red[2] + red[3];
+    const float grC_all = red[4] + red[5] + red[6] + red[7];
+    const float dgs = total(sGS, t) + total(sZRS, t) - total(sZCS, t) - total(sZCP, t) +
+                      (t + 1 < kChunk ? total(sGSP, t + 1) + total(sZRP, t + 1) : 0.f) +
+                      (t == kChunk - 1 ? gsC_all : 0.f);
+    const float dgr = total(sGR, t) + total(sZRR, t) - total(sZCR, t) +
+                      (t == kChunk - 1 ? grC_all : 0.f);
     // suffix sums over the chunk: d log a_j = sum_{t >= j} d g_t
     float ss = dgs, sr = dgr;
 #pragma unroll
@@ -644,40 +652,47 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       const float as = p.alpha_s[gi], ar = p.alpha_r[gi];
       p.dalpha_s[gi] = as >= 1.17549435e-38f ? ss / as : 0.f;
       p.dalpha_r[gi] = ar >= 1.17549435e-38f ? sr / ar : 0.f;
-      p.dbeta[gi] = rows[rBeta * kChunk + t];
-      p.dgamma[gi] = rows[rGamma * kChunk + t];
+      p.dbeta[gi] = total(sB, t);
+      p.dgamma[gi] = total(sGM, t);
     }
   }
-
-  // ---- E2: dQ += dP K, dK += dP^T Q + dG K + dG^T K ----
 #pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const XT* Ki = KX + 16 * it;
-    const XT* Qi = QX + 16 * it;
-    mma_with<M, kChunk, true, false>(dQ[it], dPm + trow0 * L::kLdX, L::kLdX, Ki, L::kLdK);
-    mma_with<M, kChunk, false, false>(dK[it], dPm + trow0, L::kLdX, Qi, L::kLdK);
-    mma_with<M, kChunk, true, false>(dK[it], dGm + trow0 * L::kLdX, L::kLdX, Ki, L::kLdK);
-    mma_with<M, kChunk, false, false>(dK[it], dGm + trow0, L::kLdX, Ki, L::kLdK);
+  for (int m = 0; m < kIT; ++m) {
+    const int i0 = 16 * (w + 4 * m);
+#pragma unroll
+    for (int ks = 0; ks < KSC; ++ks) {
+      const int k0 = ks * M::kStep;
+      const Frag fk = M::template load<true>(KTm + i0 * ldp, ldp, k0);
+      const Frag fq = M::template load<true>(QTm + i0 * ldp, ldp, k0);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        dQ[m][tt] = M::mma(M::template load<true>(dPm + 16 * tt * ldp, ldp, k0), fk, dQ[m][tt]);
+        dK[m][tt] = M::mma(M::template load<true>(dPTm + 16 * tt * ldp, ldp, k0), fq, dK[m][tt]);
+        dK[m][tt] = M::mma(M::template load<true>(dGm + 16 * tt * ldp, ldp, k0), fk, dK[m][tt]);
+      }
+    }
   }
   OT* dqg = reinterpret_cast<OT*>(p.dq);
   OT* dkg = reinterpret_cast<OT*>(p.dk);
 #pragma unroll
-  for (int it = 0; it < IT; ++it)
+  for (int m = 0; m < kIT; ++m)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int t = trow0 + acc_row(r);
-      if (t < len) {
-        const int64_t gi = ((tok + t) * H + h) * (int64_t)DK + 16 * it + acc_col();
-        dqg[gi] = from_f<OT>(dQ[it][r]);
-        dkg[gi] = from_f<OT>(dK[it][r]);
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 16 * tt + acc_row(r);
+        if (t < len) {
+          const int64_t gi = ((tok + t) * H + h) * (int64_t)DK + 16 * (w + 4 * m) + acc_col();
+          dqg[gi] = from_f<OT>(dQ[m][tt][r]);
+          dkg[gi] = from_f<OT>(dK[m][tt][r]);
+        }
       }
-    }
 }
 
-template <typename IN, int DK, bool RDN, typename OT>
+template <typename IN, int DK, int DV, bool RDN, typename OT>
 hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
-  typedef GradLayout<IN, DK, RDN> L;
-  auto kern = bwd_grad_kernel<IN, DK, RDN, OT>;
+  typedef GradLayout<IN, DK, DV> L;
+  auto kern = bwd_grad_kernel<IN, DK, DV, RDN, OT>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;
@@ -688,7 +703,9 @@ hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
 
 template <typename IN, int DK, typename OT>
 hipError_t launch_grad_dk(const OpParams& p, hipStream_t s) {
-  return p.rdn ? launch_grad_t<IN, DK, true, OT>(p, s) : launch_grad_t<IN, DK, false, OT>(p, s);
+  if (p.DV == 128)
+    return p.rdn ? launch_grad_t<IN, DK, 128, true, OT>(p, s) : launch_grad_t<IN, DK, 128, false, OT>(p, s);
+  return p.rdn ? launch_grad_t<IN, DK, 64, true, OT>(p, s) : launch_grad_t<IN, DK, 64, false, OT>(p, s);
 }
 
 }  // namespace
@@ -699,7 +716,9 @@ hipError_t launch_bwd_grad(const OpParams& p, bool bf16, hipStream_t stream) {
       return p.DK == 128 ? launch_grad_dk<u16, 128, u16>(p, stream) : launch_grad_dk<u16, 64, u16>(p, stream);
     return p.DK == 128 ? launch_grad_dk<u16, 128, float>(p, stream) : launch_grad_dk<u16, 64, float>(p, stream);
   }
-  return launch_grad_dk<float, 64, float>(p, stream);
+  // fp32: d_k = d_v = 64 (checked by the host API)
+  return p.rdn ? launch_grad_t<float, 64, 64, true, float>(p, stream)
+               : launch_grad_t<float, 64, 64, false, float>(p, stream);
 }
 
 }  // namespace rla

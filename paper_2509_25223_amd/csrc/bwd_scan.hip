@@ -15,6 +15,8 @@
 //   dKS = -diag(e^{g_{t-1}}) dX - diag(b e^{g}) dY      (RLA: first term only)
 //   dS_start = e^{g_C} dS_end + Q^T diag(e^{g}) db + K^T dKS
 //   dR_start = e^{h_C} dR_end + Q^T diag(e^{h}) dc + K^T dKR
+// Also written per chunk: dv = dX + diag(b) dY (RLA: dX + diag(b) dU), and
+// the blocks dX, dY (RLA: dU), dYR (RLA: dUR) for the gradient kernel.
 // Every column of dS, dR only sees its own value column, so value blocks are
 // independent here as in the forward.  Operand precision as in the forward
 // scan: K x (dS, dR) uses bf16 K with the gradient state split into bf16
@@ -37,7 +39,7 @@ struct BwdScanLayout {
   // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs T^S and
   // MR (first and last released) are double-buffered
   static constexpr bool kDB = kBF;
-  static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 2 : 1);
+  static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 4 : 3);
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kNumBufs = 6;
   static constexpr int kKT = 0;
@@ -54,9 +56,13 @@ struct BwdScanLayout {
   static constexpr int kBytes = kGates + 10 * kChunk * 4;
   static_assert(kMaskBytes % 1024 == 0, "mask block moved in whole DMA instructions");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
-  // RDN: TS[2] MG MP TR MR[2]; RLA: MR[2]
+  // RDN: TS[2] MG MP TR MR[2]; RLA: MG MP MR[2]
   __device__ static constexpr int slot(int mat, int buf) {
-    if (!RDN) return kDB ? buf : 0;
+    if (!RDN) {
+      if (mat == kMatMG) return 0;
+      if (mat == kMatMP) return 1;
+      return kDB ? 2 + buf : 2;   // MR
+    }
     if (mat == kMatTS) return kDB ? buf : 0;
     const int b = kDB ? 2 : 1;
     if (mat == kMatMG) return b;
@@ -67,9 +73,9 @@ struct BwdScanLayout {
 };
 
 // per-token block slots ([BV][64], value-major); aliases follow lifetimes:
-// db is last read in P4 and dKS first written in P5 (RLA: db last read in P1,
-// dKS written in P3); dc is last read in P2 and dX first written in P3; dUR
-// is last read in P3 and dU first written in P4.
+// db is last read in P4 and dKS first written in P5; dc is last read in P2
+// and dX first written in P3; dUR is last read in P3 and dU first written in
+// P4.  RLA keeps dKS in the dKR slot (dKR = 0 there).
 enum { bDB_DKS = 0, bDC_DX = 1, bQDB = 2, bQDC = 3, bDUR_DU = 4, bDKR = 5 };
 
 template <typename IN>
@@ -159,6 +165,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   const IN* kg = reinterpret_cast<const IN*>(p.k);
   const IN* dog = reinterpret_cast<const IN*>(p.dO);
   const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
+  XT* bblk = reinterpret_cast<XT*>(p.bwd_blk);
 
   // ---- staging of the next (earlier) chunk while this one computes ----
   //   K, Q, dO: register prefetch after P1 (transposed / converted at commit)
@@ -219,7 +226,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     }
   };
   auto issue_late = [&](int c) {    // after P4
-    if constexpr (L::kDB && RDN) {
+    if constexpr (L::kDB) {
       dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
       dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
     }
@@ -229,10 +236,10 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       issue_mask(c);
       if constexpr (RDN) {
         dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
-        dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
-        dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
         dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
       }
+      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
+      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
       dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0));
     }
   };
@@ -243,10 +250,10 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     issue_mask(c);
     if constexpr (RDN) {
       dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, c & 1));
-      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
-      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
       dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
     }
+    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
+    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
     dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
     wait_vmem();
   }
@@ -255,6 +262,21 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   for (int c = nch - 1; c >= 0; --c) {
     const int gc = si.chunk0 + c;
     const int buf = c & 1;
+    const int len = chunk_len(c);
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    // dv = dX + diag(b) dV_tail, rows of this chunk only
+    auto store_dv = [&](int jt, const floatx4& dx, const floatx4& tail) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 16 * w + acc_row(r);
+        if (t < len) {
+          const int64_t o = ((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col();
+          const float val = __builtin_fmaf(gbt[t], tail[r], dx[r]);
+          if (p.out_bf16) reinterpret_cast<u16*>(p.dv)[o] = f2bf(val);
+          else reinterpret_cast<float*>(p.dv)[o] = val;
+        }
+      }
+    };
 
     {   // gradient w.r.t. this chunk's end states
       const int64_t off = ((int64_t)gc * H + h) * DK * DV;
@@ -324,10 +346,10 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       KdS[jt] = zero4();
       KdR[jt] = zero4();
       const int o = jt * 16 * L::kLdS;
-      if constexpr (RDN) mma_rega<IN, DK, true>(KdS[jt], Kf, dShi + o, L::kLdS);
+      mma_rega<IN, DK, true>(KdS[jt], Kf, dShi + o, L::kLdS);
       mma_rega<IN, DK, true>(KdR[jt], Kf, dRhi + o, L::kLdS);
       if constexpr (BF) {
-        if constexpr (RDN) mma_rega<IN, DK, true>(KdS[jt], Kf, dSlo + o, L::kLdS);
+        mma_rega<IN, DK, true>(KdS[jt], Kf, dSlo + o, L::kLdS);
         mma_rega<IN, DK, true>(KdR[jt], Kf, dRlo + o, L::kLdS);
       }
       floatx4 dc, qdb, qdc;
@@ -378,29 +400,32 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         dkr[r] = -ggm[t] * egr[t] * dYR[r];
         dks[r] = -egsp[t] * dX[jt][r];
       }
-      if constexpr (RDN) {
-        store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
-        store_acc_t<XT>(blk(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dkr);
-      } else {
-        store_acc_t<XT>(blk(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
-      }
+      store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
+      store_acc_t<XT>(blk(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, RDN ? dkr : dks);
+      store_rows_masked<XT>(bblk + blk_off(gc, h, H, 0, DV) + j0 + jt * 16, DV, 16 * w, len, dX[jt]);
+      store_rows_masked<XT>(bblk + blk_off(gc, h, H, 2, DV) + j0 + jt * 16, DV, 16 * w, len, dYR);
     }
     barrier_lds();
     if (c > 0) issue_mid(c - 1);
 
-    if constexpr (RDN) {
-      // ---- P4: dU = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX ----
+    // ---- P4: dU = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX ----
 #pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-        floatx4 a = zero4(), b = zero4(), du;
-        mma_swz_cols<XT>(a, mat(kMatMP, 0), 16 * w, blk(bDB_DKS) + jt * 16 * L::kLdX, L::kLdX);
-        mma_swz_cols<XT>(b, mat(kMatMG, 0), 16 * w, blk(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+    for (int jt = 0; jt < JT; ++jt) {
+      floatx4 a = zero4(), b = zero4(), du;
+      mma_swz_cols<XT>(a, mat(kMatMP, 0), 16 * w, blk(bDB_DKS) + jt * 16 * L::kLdX, L::kLdX);
+      mma_swz_cols<XT>(b, mat(kMatMG, 0), 16 * w, blk(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
+      for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
+      if constexpr (RDN) {
         store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+      } else {   // RLA: U = diag(b) V, so dV gets b dU
+        store_rows_masked<XT>(bblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, du);
+        store_dv(jt, dX[jt], du);
       }
-      barrier_lds();
-      if (c > 0) issue_late(c - 1);
+    }
+    barrier_lds();
+    if (c > 0) issue_late(c - 1);
+    if constexpr (RDN) {
       // ---- P5: dY = T^S^T dU, dKS ----
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
@@ -412,6 +437,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
           dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[r];
         }
         store_acc_t<XT>(blk(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
+        store_rows_masked<XT>(bblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, dY);
+        store_dv(jt, dX[jt], dY);
       }
       barrier_lds();
     }
@@ -427,7 +454,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         dR[it][jt] *= eR;
         const int bo = jt * 16 * L::kLdX;
         mma_tile<XT, kChunk, true, true>(dS[it][jt], QT + i0 * L::kLdX, L::kLdX, blk(bQDB) + bo, L::kLdX);
-        mma_tile<XT, kChunk, true, true>(dS[it][jt], KT + i0 * L::kLdX, L::kLdX, blk(bDB_DKS) + bo, L::kLdX);
+        mma_tile<XT, kChunk, true, true>(dS[it][jt], KT + i0 * L::kLdX, L::kLdX,
+                                         blk(RDN ? bDB_DKS : bDKR) + bo, L::kLdX);
         mma_tile<XT, kChunk, true, true>(dR[it][jt], QT + i0 * L::kLdX, L::kLdX, blk(bQDC) + bo, L::kLdX);
         if constexpr (RDN)
           mma_tile<XT, kChunk, true, true>(dR[it][jt], KT + i0 * L::kLdX, L::kLdX, blk(bDKR) + bo, L::kLdX);

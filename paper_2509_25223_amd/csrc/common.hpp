@@ -195,6 +195,7 @@ __device__ __forceinline__ void load_rowfrags(typename Mfma<T>::frag* afr, const
 
 __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
 
+
 // ---------------------------------------------------------------------------
 // 64 x 64 matrices staged in LDS by LDS-DMA (global_load_lds_dwordx4): the
 // hardware writes lane i's 16 bytes at base + 16 i, so a tile is stored
@@ -315,6 +316,18 @@ __device__ __forceinline__ void mma_swz_cols(floatx4& acc, const T* M, int t0, c
 // Row (inside a 16-row tile) and column of accumulator element r of this lane.
 __device__ __forceinline__ int acc_row(int r) { return 4 * ((threadIdx.x & 63) >> 4) + r; }
 __device__ __forceinline__ int acc_col() { return threadIdx.x & 15; }
+
+// Stores this lane's 4 accumulator rows of a [token][column] tile into a
+// token-major array (row stride ld): rows t0 + acc_row(r), column acc_col();
+// rows at or past `len` are written as 0.
+template <typename T>
+__device__ __forceinline__ void store_rows_masked(T* base, int ld, int t0, int len, floatx4 v) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int t = t0 + acc_row(r);
+    base[(int64_t)t * ld + acc_col()] = from_f<T>(t < len ? v[r] : 0.f);
+  }
+}
 
 // Stores the 4 accumulator rows of this lane, column-major into LDS as a
 // transposed tile: dst[col * ld + row]  (4 consecutive elements).

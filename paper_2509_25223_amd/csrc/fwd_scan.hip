@@ -22,8 +22,8 @@
 //     mantissa, fp32 range): two MFMAs per step.
 //   everything else: fp16 operands (intermediates bounded by the data, clip
 //     and gates), fp32 accumulation.
-// With `CKPT` the chunk-start states and the clip mask |x| <= c are stored
-// for the backward pass.
+// With `CKPT` the chunk-start states, the clip mask |x| <= c and the blocks
+// U, UR and r (token-major, mm type) are stored for the backward pass.
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -169,6 +169,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   const IN* vg = reinterpret_cast<const IN*>(p.v);
   OT* og = reinterpret_cast<OT*>(p.o);
   const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
+  XT* fblk = reinterpret_cast<XT*>(p.fwd_blk);   // CKPT: U, UR, r blocks
 
   // ---- staging of chunk c+1 while chunk c computes ----
   //   K, Q fragments: register prefetch (issued after P1, when chunk c's are dead)
@@ -319,6 +320,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * y[r];
         store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
         store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        if constexpr (CKPT)
+          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 0, DV) + j0 + jt * 16, DV, 16 * w, len, y);
       }
     }
     barrier_lds();
@@ -337,6 +340,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * u[r];
         store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
         store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        if constexpr (CKPT)
+          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 0, DV) + j0 + jt * 16, DV, 16 * w, len, u);
       }
       barrier_lds();
     }
@@ -349,12 +354,13 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
       floatx4 mgu = zero4(), mpu = zero4();
       mma_swz_rows<XT>(mgu, mat(kMatMG, 0), 16 * w, Ut + jt * 16 * L::kLdX, L::kLdX);
       mma_swz_rows<XT>(mpu, mat(kMatMP, 0), 16 * w, Ut + jt * 16 * L::kLdX, L::kLdX);
-      floatx4 y;
+      floatx4 y, rv;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r);
         const float x = __builtin_fmaf(-egsp[t], KS[jt][r], vloc[jt][r]) - mgu[r];
         const float rr = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
+        rv[r] = rr;
         if constexpr (CKPT) {
           if (t < len)
             p.ck_mask[((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col()] =
@@ -371,7 +377,11 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * y[r];
         store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
         store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        if constexpr (CKPT)
+          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, y);
       }
+      if constexpr (CKPT)
+        store_rows_masked<XT>(fblk + blk_off(gc, h, H, 2, DV) + j0 + jt * 16, DV, 16 * w, len, rv);
     }
     if constexpr (!L::kDB) wait_vmem();   // single-buffered T^R / MR of this chunk
     barrier_lds();
@@ -387,6 +397,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * u[r];
         store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
         store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        if constexpr (CKPT)
+          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, u);
       }
       barrier_lds();
     }

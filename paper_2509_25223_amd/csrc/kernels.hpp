@@ -8,6 +8,13 @@
 
 namespace rla {
 
+constexpr int kNumBlk = 3;   // per-token blocks per (chunk, head) in fwd_blk / bwd_blk
+
+// Element offset of block b of (global chunk gc, head h) in fwd_blk / bwd_blk.
+__host__ __device__ inline int64_t blk_off(int64_t gc, int h, int H, int b, int DV) {
+  return ((gc * H + h) * kNumBlk + b) * (int64_t)kChunk * DV;
+}
+
 // Everything a launch needs; passed by value to the kernels.
 struct OpParams {
   int32_t H = 0, DK = 0, DV = 0;
@@ -40,6 +47,10 @@ struct OpParams {
   uint8_t* ck_mask = nullptr;   // [ntok][H][DV] 1 where |x| <= clip
   float* dS_ws = nullptr;       // [max_chunks][H][DK][DV] grad of chunk-end S
   float* dR_ws = nullptr;       // [max_chunks][H][DK][DV] grad of chunk-end R
+  // per-token blocks saved for the gradient kernel, [max_chunks][H][3][64][DV]
+  // (mm type, token-major, rows past the end of a sequence are zero):
+  void* fwd_blk = nullptr;      // U, UR, r (clipped residual) from the forward scan
+  void* bwd_blk = nullptr;      // dX, dY (RLA: dU), dYR (RLA: dUR) from the reverse scan
 
   // backward
   const void* dO = nullptr;
@@ -66,11 +77,12 @@ hipError_t launch_seq_table(const int32_t* cu, int32_t nseq, int64_t ntok, int32
 hipError_t launch_prep(const OpParams& p, bool bf16, hipStream_t stream);
 
 // Forward state-passing scan.  write_o: produce o; ckpt: store chunk-start
-// states and clip masks for the backward.
+// states, clip masks and the U, UR, r blocks for the backward.
 hipError_t launch_fwd_scan(const OpParams& p, bool bf16, bool write_o, bool ckpt,
                            hipStream_t stream);
 
-// Reverse state-gradient scan (RDN / RLA).
+// Reverse state-gradient scan (RDN / RLA); also writes dv and the dX, dY,
+// dYR blocks.
 hipError_t launch_bwd_scan(const OpParams& p, bool bf16, hipStream_t stream);
 
 // Chunk-parallel gradient contractions.
