@@ -5,16 +5,19 @@ One step = rdn_forward + rdn_backward (the whole hot path) on the workload
 B=4, T=4096, H=16, d_k=d_v=128, bf16 inputs, fp32 accumulation and fp32
 outputs (o, dq, dk, dv), gates fp32, clip 1, zero initial states, dO ~ N(0,1).
 Inputs are seeded synthetic data (datagen) resident in HBM before timing.
-As in training, the forward saves its chunk states and clip masks in the
-workspace and the backward reads them instead of recomputing the forward.
+As in training, the forward saves what the backward needs (chunk states,
+clip masks, the U, UR, r blocks) in the workspace and the backward reads it
+instead of recomputing the forward.
 
-Prints ONE JSON line with the throughput (tokens/s, whole job), the roofline
-of the dominant kernel (algorithmic MFMA flops per launch / its launch time,
-measured with HIP events recorded on the launch stream around each kernel
-stage), and the fp64 CPU oracle timed on a bounded sample of the same
+Prints ONE JSON line with the throughput (tokens/s, whole job), per-stage
+launch times (HIP events recorded on the launch stream around each kernel
+stage) with their algorithmic TFLOP/s and GB/s, the roofline of the dominant
+kernel (its binding resource: algorithmic bytes or flops per launch over its
+launch time), and the fp64 CPU oracle timed on a bounded sample of the same
 workload on this host.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+                    [--copy-calibration-mib M]
 """
 from __future__ import annotations
 
@@ -33,21 +36,60 @@ PEAK_MFMA_TFLOPS = 2500.0   # MI355X dense fp16/bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
-def stage_flops_per_chunk_head(stage: str, d: int, C: int = CHUNK, rdn: bool = True) -> float:
-    """Algorithmic matrix-product flops of one (chunk, head) for each kernel
-    stage of the RDN fwd+bwd path (d = d_k = d_v).  Each product is counted
-    once as 2*m*n*k, whatever precision splitting the kernel uses."""
-    cd2, c2d = 2.0 * C * d * d, 2.0 * C * C * d
-    if stage == "prep":           # G = K K^T, P = Q K^T
-        return 2 * c2d
+# HBM bytes per launch of each kernel on this workload, from rocprofv3
+# FETCH_SIZE / WRITE_SIZE runs scaled by a 1 GiB device copy's counts (the
+# numbers and commands are in profiles/), keyed by a hash of the kernel's
+# sources: a kernel changed since its counters were taken reports null.
+MEASURED_TRAFFIC = {
+    "bwd_grad": ("563cc1bd7280f056", ("bwd_grad.hip", "common.hpp", "kernels.hpp"), 1883479626, 424625152),
+    "bwd_scan": ("6c3058f8dc931fe6", ("bwd_scan.hip", "common.hpp", "kernels.hpp"), 407247528, 880806502),
+    "fwd_scan": ("7dbbe0ab6b90d766", ("fwd_scan.hip", "common.hpp", "kernels.hpp"), 373586733, 905978675),
+    "prep": ("04b8f825e0b2d63a", ("prep.hip", "common.hpp", "kernels.hpp"), 150075069, 172199117),
+}
+
+
+def measured_traffic(stage: str):
+    """Counter-derived HBM bytes per launch, or None if the kernel changed."""
+    import hashlib
+    if stage not in MEASURED_TRAFFIC:
+        return None
+    digest, files, read, written = MEASURED_TRAFFIC[stage]
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, "paper_2509_25223_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return read + written if h.hexdigest()[:16] == digest else None
+
+
+def stage_model(stage: str, d: int, C: int = CHUNK) -> tuple:
+    """Algorithmic (flops, HBM bytes) of one (chunk, head) for each kernel
+    stage of the RDN fwd+bwd path with bf16 inputs, fp32 outputs, d_k = d_v = d.
+
+    Flops: each matrix product counted once as 2*m*n*k (no split-precision
+    repeats); products restricted to a triangle count only its C(C+1)/2 rows
+    x columns.  Bytes: every tensor the stage must read or write once
+    (inputs bf16, prep's matrices and the saved token blocks fp16, states and
+    outputs fp32)."""
+    cd2, c2d, tri = 2.0 * C * d * d, 2.0 * C * C * d, float(C * (C + 1)) * d
+    tok_bf16, tok_h, tok_f32 = C * d * 2, C * d * 2, C * d * 4
+    state = d * d * 4
+    mats = 5 * C * C * 2
+    gates_in, gate_blk = 4 * C * 4, 256 * 4
+    if stage == "prep":           # G = K K^T, P = Q K^T, two triangular inverses
+        return 2 * c2d + 2 * (C ** 3) / 3.0, 2 * tok_bf16 + gates_in + mats + gate_blk
     if stage == "fwd_scan":       # KS QS KR QR, T^S Y MG U MP U T^R YR MR UR, S/R updates
-        return 6 * cd2 + 5 * c2d
-    if stage == "fwd_scan_ckpt":  # KS KR, T^S Y MG U T^R YR, S/R updates
-        return 4 * cd2 + 3 * c2d
+        flops = 6 * cd2 + 5 * c2d
+        # K Q V, matrices, gates; o, chunk-start S R, clip mask, U UR r
+        return flops, 3 * tok_bf16 + mats + gate_blk + tok_f32 + 2 * state + C * d + 3 * tok_h
     if stage == "bwd_scan":       # K dS K dR, 5 transposed C x C products, dS/dR updates (4)
-        return 6 * cd2 + 5 * c2d
-    if stage == "bwd_grad":       # recompute 4+4, bwd 2+5, dQ/dK 6, W1..W5, G P, 4 final
-        return 12 * cd2 + 14 * c2d + 6 * c2d
+        flops = 6 * cd2 + 5 * c2d
+        # K Q dO, matrices, gates, mask; dS dR at chunk ends, dX dY dYR, dv
+        return flops, 3 * tok_bf16 + mats + gate_blk + C * d + 2 * state + 3 * tok_h + tok_f32
+    if stage == "bwd_grad":       # 7 state products, W1..W5 G P (lower), dP K dP^T Q (dG+dG^T) K
+        flops = 7 * cd2 + 7 * tri + 3 * c2d
+        # K Q V dO, S0 R0 dS1 dR1, U UR r dX dY dYR, gates; dq dk, gate grads
+        return flops, (4 * tok_bf16 + 4 * state + 6 * tok_h + gate_blk + 2 * C * 4
+                       + 2 * tok_f32 + 4 * C * 4)
     raise KeyError(stage)
 
 
@@ -58,6 +100,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run one device-to-device copy of this many MiB (a kernel of "
+                         "known traffic, for scaling hardware byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the operator shards by (sequence, head) with no "
@@ -100,6 +145,14 @@ def main() -> int:
         fwd()
         bwd()
 
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src_ = torch.ones(n, dtype=torch.float32, device=dev)
+        dst_ = torch.empty_like(src_)
+        dst_.copy_(src_)
+        torch.cuda.synchronize()
+        del src_, dst_
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -138,34 +191,45 @@ def main() -> int:
         for i, name in enumerate(names):
             stage_ms[tag + name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
     units = B * ((T + CHUNK - 1) // CHUNK) * H   # (chunk, head) pairs per launch
+    stages = {}
+    for key, ms in stage_ms.items():
+        fl, by = stage_model(key.split(".", 1)[1], d)
+        tf = fl * units / (ms * 1e-3) / 1e12
+        gb = by * units / (ms * 1e-3) / 1e9
+        stages[key] = {"ms": round(ms, 4), "tflops": round(tf, 2), "gbs": round(gb, 1),
+                       "mfma_frac": round(tf / PEAK_MFMA_TFLOPS, 4),
+                       "hbm_frac": round(gb / PEAK_HBM_GBS, 4),
+                       "traffic": measured_traffic(key.split(".", 1)[1])}
     dom = max(stage_ms, key=stage_ms.get)
-    dom_flops = stage_flops_per_chunk_head(dom.split(".", 1)[1], d) * units
-    achieved = dom_flops / (stage_ms[dom] * 1e-3) / 1e12
+    ds = stages[dom]
     kernel_names = {"prep": "prep_kernel", "fwd_scan": "fwd_scan_kernel (saving)",
-                    "fwd_scan_ckpt": "fwd_scan_kernel (checkpointing)",
                     "bwd_scan": "bwd_scan_kernel", "bwd_grad": "bwd_grad_kernel"}
-    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_MFMA_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_MFMA_TFLOPS, 4), "traffic": None,
-                "kernel": kernel_names[dom.split(".", 1)[1]], "stage": dom,
-                "flops_per_launch": dom_flops, "launch_ms": round(stage_ms[dom], 4)}
+    fl, by = stage_model(dom.split(".", 1)[1], d)
+    if ds["hbm_frac"] >= ds["mfma_frac"]:
+        roofline = {"bound": "hbm", "achieved": ds["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": ds["hbm_frac"], "traffic": ds["traffic"],
+                    "bytes_per_launch": by * units}
+    else:
+        roofline = {"bound": "mfma", "achieved": ds["tflops"], "peak": PEAK_MFMA_TFLOPS,
+                    "unit": "TFLOP/s", "frac": ds["mfma_frac"], "traffic": ds["traffic"],
+                    "flops_per_launch": fl * units}
+    roofline.update({"kernel": kernel_names[dom.split(".", 1)[1]], "stage": dom,
+                     "launch_ms": ds["ms"], "units_per_launch": units})
 
-    # ---- CPU baseline: the fp64 oracle on a bounded sample of the workload ----
+    # ---- CPU baseline: the fp64 oracle on the same workload ----
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        sample_T = T
-        sub = {n: inp[n][:sample_T] for n in ("q", "k", "v", "alpha_s", "beta", "alpha_r",
-                                               "gamma", "dO")}
+        names = ("q", "k", "v", "alpha_s", "beta", "alpha_r", "gamma", "dO")
+        cu = wl.cu_seqlens()
         c0 = time.perf_counter()
-        oracle.forward("rdn", sub["q"], sub["k"], sub["v"], sub["alpha_s"], sub["beta"],
-                       sub["alpha_r"], sub["gamma"], clip=wl.clip)
-        oracle.backward("rdn", sub["q"], sub["k"], sub["v"], sub["alpha_s"], sub["beta"],
-                        sub["alpha_r"], sub["gamma"], sub["dO"], clip=wl.clip)
+        oracle.forward("rdn", *[inp[n] for n in names[:7]], clip=wl.clip, cu_seqlens=cu)
+        oracle.backward("rdn", *[inp[n] for n in names], clip=wl.clip, cu_seqlens=cu)
         c1 = time.perf_counter()
-        cpu = {"value": round(sample_T / (c1 - c0), 2), "unit": "tokens/s",
+        cpu = {"value": round(B * T / (c1 - c0), 2), "unit": "tokens/s",
                "cores": oracle.threads(), "kind": "oracle",
-               "sample": "sequence 0 (%d tokens, all %d heads), fwd+bwd, fp64 (%.1f s wall)"
-                         % (sample_T, H, c1 - c0)}
+               "sample": "the whole workload (%d sequences x %d tokens, %d heads), forward then "
+                         "backward, fp64 token recurrence (%.1f s wall)" % (B, T, H, c1 - c0)}
 
     line = {
         "metric": "RDN fwd+bwd tokens/sec on 1 MI355X (H=16,d=128,T=4096)",
@@ -183,7 +247,7 @@ def main() -> int:
         "config": {"workload": wl.name, "B": B, "T": T, "H": H, "d_k": d, "d_v": d,
                    "chunk": CHUNK, "clip": wl.clip, "outputs": "fp32",
                    "parallelism": "single GPU"},
-        "stage_ms": {k_: round(v_, 4) for k_, v_ in stage_ms.items()},
+        "stages": stages,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

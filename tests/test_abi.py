@@ -106,6 +106,17 @@ def test_backward_validation_errors(lib):
     assert bwd(prob(dk=48)) == 2
     assert bwd(p, ws_bytes=rla.rla_workspace_size(p, rla.RLA_OP_RDN_FORWARD)) == 5
     assert bwd(p, dq=FAKE + 4) == 6
+    # fp32 backward needs d_v = 64 (the gradient kernel's fp32 token blocks fill LDS)
+    assert bwd(prob(dtype=rla.RLA_F32, dk=64, dv=128)) == 4
+    assert bwd(prob(dtype=rla.RLA_F32, dk=64, dv=64), ws=None) == 5
+
+
+def test_saving_forward_shares_the_backward_limits(lib):
+    p = prob(dtype=rla.RLA_F32, dk=64, dv=128)
+    p.flags = rla.RLA_FLAG_SAVE_FOR_BACKWARD
+    assert call_fwd(lib, p) == 4
+    p.flags = 0
+    assert call_fwd(lib, p, ws=None) == 5   # plain forward: reaches the workspace check
 
 
 def test_status_strings(lib):
