@@ -24,10 +24,10 @@
 // taken elementwise.  d log a over a chunk is the suffix sum of the gradients
 // of the cumulative sums g_t, h_t.
 //
-// Work split: wave w owns the d_k tiles w (and w + 4) for the F contractions,
-// dQ and dK, over all 64 tokens; the 10 lower 16 x 16 tiles of the chunk's
-// token x token matrices are dealt round-robin for W, G = K K^T, P = Q K^T,
-// dP and dG.  State rows stream from HBM (fp32) straight into MFMA B
+// Work split: d_k / 16 waves; wave w owns d_k tile w (16 state rows) for the
+// F contractions, dQ and dK, over all 64 tokens; the 10 lower 16 x 16 tiles
+// of the chunk's token x token matrices are dealt round-robin for W,
+// G = K K^T, P = Q K^T, dP and dG.  State rows stream from HBM (fp32) straight into MFMA B
 // fragments; the token blocks are moved into LDS by LDS-DMA.
 //
 // Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation; a state
@@ -65,14 +65,15 @@ struct Tile {
     return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + off(r, col));
   }
   // LDS-DMA of 64 contiguous rows (global, unswizzled) into the swizzled tile;
-  // every wave issues an equal share.  Completion: wait_vmem + barrier.
+  // each of the NW waves issues an equal share.  Completion: wait_vmem + barrier.
+  template <int NW>
   __device__ __forceinline__ static void dma64(const T* gsrc, void* lds) {
     constexpr int kInst = kChunk * kRowB / 1024;
-    static_assert(kInst % kWaves == 0, "equal DMA share per wave");
+    static_assert(kInst % NW == 0, "equal DMA share per wave");
     const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
-    for (int m = 0; m < kInst / kWaves; ++m) {
-      const int blk = w * (kInst / kWaves) + m;
+    for (int m = 0; m < kInst / NW; ++m) {
+      const int blk = w * (kInst / NW) + m;
       const int P = blk * 64 + lane;   // physical 16-byte chunk
       const int r = P / kCpr, c = (P % kCpr) ^ (r & (kCpr - 1));
       dma16(reinterpret_cast<const char*>(gsrc) + r * kRowB + c * 16,
@@ -90,6 +91,8 @@ enum { sGS = 0, sGSP, sGR, sB, sGM, sZRS, sZCS, sZRP, sZCP, sZRR, sZCR, kNumSums
 template <typename IN, int DK, int DV>
 struct GradLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
+  static constexpr int kNW = DK / 16;        // one wave per 16-row d_k tile
+  static constexpr int kNT = 64 * kNW;       // threads per workgroup
   typedef typename std::conditional<kBF, f16, float>::type XT;
   typedef Tile<XT, DK> TK;    // K, Q rows
   typedef Tile<XT, DV> TV;    // token blocks
@@ -110,7 +113,7 @@ struct GradLayout {
   static constexpr int kGates = kBlkEnd > kOvlEnd ? kBlkEnd : kOvlEnd;
   static constexpr int kNumGateArrays = 11;
   static constexpr int kSums = kGates + kNumGateArrays * kChunk * 4;
-  static constexpr int kRed = kSums + kWaves * kNumSums * kChunk * 4;   // per-wave sums
+  static constexpr int kRed = kSums + kNW * kNumSums * kChunk * 4;   // per-wave sums
   static constexpr int kBytes = kRed + 16 * 4;
   static_assert(kBytes <= 160 * 1024, "gradient kernel LDS");
 };
@@ -162,8 +165,9 @@ __device__ __forceinline__ void acc_cols(float* dst, int s0, const float (&v)[4]
 }
 
 template <typename IN, int DK, int DV, bool RDN, typename OT>
-__global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
+__global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   typedef GradLayout<IN, DK, DV> L;
+  constexpr int NW = L::kNW, NT = L::kNT;
   typedef typename L::XT XT;
   typedef typename L::TK TK;
   typedef typename L::TV TV;
@@ -173,7 +177,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   constexpr int KSV = DV / M::kStep;   // k-steps over the value dimension
   constexpr int KSK = DK / M::kStep;   // k-steps over d_k
   constexpr int KSC = kChunk / M::kStep;
-  constexpr int kIT = DK / 64;         // d_k tiles per wave
+  constexpr int kIT = DK / 16 / NW;    // d_k tiles per wave
   static_assert(sizeof(IN) == sizeof(XT), "bf16 inputs pair with fp16 operands, fp32 with fp32");
   constexpr int kE = 16 / (int)sizeof(IN);   // elements per 16-byte vector
   extern __shared__ __align__(16) unsigned char smem[];
@@ -205,7 +209,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   auto total = [&](int q, int t) {               // over the waves
     float x = 0.f;
 #pragma unroll
-    for (int v = 0; v < kWaves; ++v) x += sums[(v * kNumSums + q) * kChunk + t];
+    for (int v = 0; v < NW; ++v) x += sums[(v * kNumSums + q) * kChunk + t];
     return x;
   };
   ChunkInfo ci;
@@ -222,37 +226,37 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   const int64_t soff = ((int64_t)c * H + h) * DK * DV;
 
   // ---------------- phase 0: staging ----------------
-  TV::dma64(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
-  TV::dma64(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
-  TV::dma64(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
-  TV::dma64(bb + blk_off(c, h, H, 1, DV), tokblk(bDY));
-  TV::dma64(bb + blk_off(c, h, H, 2, DV), tokblk(bDYR));
+  TV::template dma64<NW>(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
+  TV::template dma64<NW>(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
+  TV::template dma64<NW>(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
+  TV::template dma64<NW>(bb + blk_off(c, h, H, 1, DV), tokblk(bDY));
+  TV::template dma64<NW>(bb + blk_off(c, h, H, 2, DV), tokblk(bDYR));
 
   // V and r rows for the elementwise sums (consumed after the staging barrier)
-  constexpr int kVV = kChunk * DV / kE / kThreads;
+  constexpr int kVV = kChunk * DV / kE / NT;
   uint4 vrow[kVV], rrow[kVV];
 #pragma unroll
   for (int u = 0; u < kVV; ++u) {
-    const int e = tid + u * kThreads, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
+    const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
     vrow[u] = t < len ? *reinterpret_cast<const uint4*>(vg + ((tok + t) * H + h) * (int64_t)DV + j)
                       : uint4{0, 0, 0, 0};
     rrow[u] = *reinterpret_cast<const uint4*>(fb + blk_off(c, h, H, 2, DV) + t * DV + j);
   }
   // K, Q, dO rows: converted to the operand type, stored swizzled
   {
-    constexpr int kKV = kChunk * DK / kE / kThreads;
-    constexpr int kOV = kChunk * DV / kE / kThreads;
+    constexpr int kKV = kChunk * DK / kE / NT;
+    constexpr int kOV = kChunk * DV / kE / NT;
     uint4 kv[kKV], qv[kKV], ov[kOV];
 #pragma unroll
     for (int u = 0; u < kKV; ++u) {
-      const int e = tid + u * kThreads, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
+      const int e = tid + u * NT, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
       const int64_t off = ((tok + t) * H + h) * (int64_t)DK + i;
       kv[u] = t < len ? *reinterpret_cast<const uint4*>(kg + off) : uint4{0, 0, 0, 0};
       qv[u] = t < len ? *reinterpret_cast<const uint4*>(qg + off) : uint4{0, 0, 0, 0};
     }
 #pragma unroll
     for (int u = 0; u < kOV; ++u) {
-      const int e = tid + u * kThreads, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
+      const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
       ov[u] = t < len ? *reinterpret_cast<const uint4*>(dog + ((tok + t) * H + h) * (int64_t)DV + j)
                       : uint4{0, 0, 0, 0};
     }
@@ -269,13 +273,13 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     };
 #pragma unroll
     for (int u = 0; u < kKV; ++u) {
-      const int e = tid + u * kThreads, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
+      const int e = tid + u * NT, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
       *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(kv[u]);
       *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(qv[u]);
     }
 #pragma unroll
     for (int u = 0; u < kOV; ++u) {
-      const int e = tid + u * kThreads, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
+      const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
       *reinterpret_cast<uint4*>(tokblk(bDO) + TV::off(t, j)) = conv(ov[u]);
     }
   }
@@ -299,7 +303,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       edge[1] = __expf(grl);
     }
   }
-  for (int e = tid; e < kWaves * kNumSums * kChunk; e += kThreads) sums[e] = 0.f;
+  for (int e = tid; e < NW * kNumSums * kChunk; e += NT) sums[e] = 0.f;
   wait_vmem();
   barrier_lds();
 
@@ -308,7 +312,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     constexpr int kPerRow = DV / kE;   // threads sharing a row
 #pragma unroll
     for (int u = 0; u < kVV; ++u) {
-      const int e = tid + u * kThreads, t = e / kPerRow, j = (e % kPerRow) * kE;
+      const int e = tid + u * NT, t = e / kPerRow, j = (e % kPerRow) * kE;
       const uint4 dy = *reinterpret_cast<const uint4*>(tokblk(bDY) + TV::off(t, j));
       const uint4 dyr = *reinterpret_cast<const uint4*>(tokblk(bDYR) + TV::off(t, j));
       const XT* a = reinterpret_cast<const XT*>(&dy);
@@ -419,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     // the token-block fragments are reloaded per d_k tile: keeping them
     // across tiles would need ~400 registers
     asm volatile("" ::: "memory");
-    const int i0 = 16 * (w + 4 * m);
+    const int i0 = 16 * (w + NW * m);
     const int icol = i0 + (lane & 15);   // this lane's output column
     // K, Q at this lane's output positions of token tile tt
     auto kq_of = [&](int tt, float (&kq)[4], float (&qq)[4]) {
@@ -476,8 +480,8 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       grC += edge[1] * frag_dot(f0, sR, rawB);   // e^{h_C} <R0, dR1>
       const float sE = convert(rawB, f1);
       if (m + 1 < kIT) {
-        load_raw(rawA, 0, i0 + 64);
-        load_raw(rawB, 2, i0 + 64);
+        load_raw(rawA, 0, i0 + 16 * NW);
+        load_raw(rawB, 2, i0 + 16 * NW);
       }
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
@@ -512,11 +516,11 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   }
   {
     const float a = wave_sum(gsC), b = wave_sum(grC);
-    if (lane == 0) { red[w] = a; red[4 + w] = b; }
+    if (lane == 0) { red[w] = a; red[NW + w] = b; }
   }
 
   // ---------------- phase 2: W, G, P on the lower token tiles ----------------
-  constexpr int kMyTiles = 3;   // at most 3 of the 10 lower tiles per wave
+  constexpr int kMyTiles = (10 + NW - 1) / NW;   // share of the 10 lower tiles per wave
   floatx4 tW1[kMyTiles], tW2[kMyTiles], tW3[kMyTiles], tW4[kMyTiles], tW5[kMyTiles];
   floatx4 tG[kMyTiles], tP[kMyTiles];
   auto tile_of = [](int idx, int& tt, int& st) {   // lower tiles, row by row
@@ -526,7 +530,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
   for (int x = 0; x < kMyTiles; ++x) {
     asm volatile("" ::: "memory");
-    const int idx = w + 4 * x;
+    const int idx = w + NW * x;
     tW1[x] = zero4(); tW2[x] = zero4(); tW3[x] = zero4(); tW4[x] = zero4(); tW5[x] = zero4();
     tG[x] = zero4(); tP[x] = zero4();
     if (idx < 10) {
@@ -562,7 +566,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   constexpr int ldp = L::kLdP;
 #pragma unroll
   for (int x = 0; x < kMyTiles; ++x) {
-    const int idx = w + 4 * x;
+    const int idx = w + NW * x;
     if (idx < 10) {
       int tt, st;
       tile_of(idx, tt, st);
@@ -605,7 +609,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     }
   }
   // dP above the diagonal and dP^T below it are zero: the 6 upper tiles
-  for (int x = w; x < 6; x += kWaves) {
+  for (int x = w; x < 6; x += NW) {
     const int tt = x < 3 ? 0 : x < 5 ? 1 : 2;
     const int st = tt + 1 + x - (tt == 0 ? 0 : tt == 1 ? 3 : 5);
 #pragma unroll
@@ -616,7 +620,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
     }
   }
   // K^T, Q^T for the final products
-  for (int e = tid; e < kChunk * DK / kE; e += kThreads) {
+  for (int e = tid; e < kChunk * DK / kE; e += NT) {
     const int s = e / (DK / kE), i = (e % (DK / kE)) * kE;
     const uint4 kv = *reinterpret_cast<const uint4*>(Kl + TK::off(s, i));
     const uint4 qv = *reinterpret_cast<const uint4*>(Ql + TK::off(s, i));
@@ -633,8 +637,9 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   // ---------------- phase 3: gate gradients; dQ += dP K, dK += dP^T Q + (dG + dG^T) K ----------------
   if (tid < kChunk) {
     const int t = tid;
-    const float gsC_all = red[0] + red[1] + red[2] + red[3];
-    const float grC_all = red[4] + red[5] + red[6] + red[7];
+    float gsC_all = 0.f, grC_all = 0.f;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) { gsC_all += red[v]; grC_all += red[NW + v]; }
     const float dgs = total(sGS, t) + total(sZRS, t) - total(sZCS, t) - total(sZCP, t) +
                       (t + 1 < kChunk ? total(sGSP, t + 1) + total(sZRP, t + 1) : 0.f) +
                       (t == kChunk - 1 ? gsC_all : 0.f);
@@ -658,7 +663,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
   }
 #pragma unroll
   for (int m = 0; m < kIT; ++m) {
-    const int i0 = 16 * (w + 4 * m);
+    const int i0 = 16 * (w + NW * m);
 #pragma unroll
     for (int ks = 0; ks < KSC; ++ks) {
       const int k0 = ks * M::kStep;
@@ -682,7 +687,7 @@ __global__ __launch_bounds__(kThreads) void bwd_grad_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * tt + acc_row(r);
         if (t < len) {
-          const int64_t gi = ((tok + t) * H + h) * (int64_t)DK + 16 * (w + 4 * m) + acc_col();
+          const int64_t gi = ((tok + t) * H + h) * (int64_t)DK + 16 * (w + NW * m) + acc_col();
           dqg[gi] = from_f<OT>(dQ[m][tt][r]);
           dkg[gi] = from_f<OT>(dK[m][tt][r]);
         }
@@ -697,7 +702,7 @@ hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;
   if (p.max_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(kern, dim3(p.max_chunks, p.H), dim3(kThreads), L::kBytes, stream, p);
+  hipLaunchKernelGGL(kern, dim3(p.max_chunks, p.H), dim3(L::kNT), L::kBytes, stream, p);
   return hipGetLastError();
 }
 
