@@ -38,6 +38,7 @@ struct Problem {
 struct Workspace {
   size_t seqs = 0, chunks = 0, nchunks = 0, order = 0, gates = 0, mats = 0;
   size_t ckS = 0, ckR = 0, mask = 0, dS = 0, dR = 0, fblk = 0, bblk = 0, total = 0;
+  size_t ckS_sc = 0, ckR_sc = 0, dS_sc = 0, dR_sc = 0;
 };
 
 rla_status check_problem(const rla_problem* pp, Problem& pr) {
@@ -98,12 +99,20 @@ Workspace plan(const Problem& pr, int op) {
   w.gates = take(sizeof(float) * mc * H * kGateBlock);
   w.mats = take((pr.bf16 ? 2 : 4) * mc * H * kNumMats * kMatElems);
   if (op == RLA_OP_RDN_BACKWARD || op == RLA_OP_RLA_BACKWARD) {
-    const size_t st = sizeof(float) * mc * H * (size_t)pr.DK * (size_t)pr.DV;
+    // states: fp16 with per-(row, 32 columns) scales for bf16 inputs, fp32 otherwise
+    const size_t st = (pr.bf16 ? 2 : 4) * mc * H * (size_t)pr.DK * (size_t)pr.DV;
+    const size_t sc = pr.bf16 ? sizeof(float) * mc * H * (size_t)pr.DK * (size_t)(pr.DV / 32) : 0;
     w.ckS = take(st);
     w.ckR = take(st);
     w.mask = take((size_t)pr.ntok * H * (size_t)pr.DV);
     w.dS = take(st);
     w.dR = take(st);
+    if (sc) {
+      w.ckS_sc = take(sc);
+      w.ckR_sc = take(sc);
+      w.dS_sc = take(sc);
+      w.dR_sc = take(sc);
+    }
     const size_t bl = (pr.bf16 ? 2 : 4) * mc * H * kNumBlk * kChunk * (size_t)pr.DV;
     w.fblk = take(bl);
     w.bblk = take(bl);
@@ -142,6 +151,23 @@ OpParams make_params(const Problem& pr, const Workspace& w, unsigned char* ws, b
   p.gate_ws = reinterpret_cast<float*>(ws + w.gates);
   p.mat_ws = ws + w.mats;
   return p;
+}
+
+// Workspace regions written by a saving forward and read by the backward.
+void set_saved(const Problem& pr, const Workspace& w, unsigned char* ws, OpParams& p) {
+  p.ck_S = ws + w.ckS;
+  p.ck_R = ws + w.ckR;
+  p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
+  p.dS_ws = ws + w.dS;
+  p.dR_ws = ws + w.dR;
+  if (pr.bf16) {
+    p.ck_S_sc = reinterpret_cast<float*>(ws + w.ckS_sc);
+    p.ck_R_sc = reinterpret_cast<float*>(ws + w.ckR_sc);
+    p.dS_sc = reinterpret_cast<float*>(ws + w.dS_sc);
+    p.dR_sc = reinterpret_cast<float*>(ws + w.dR_sc);
+  }
+  p.fwd_blk = ws + w.fblk;
+  p.bwd_blk = ws + w.bblk;
 }
 
 rla_status check_workspace(const Workspace& w, void* ws, size_t bytes) {
@@ -187,12 +213,7 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
   p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
   p.S0 = S0; p.R0 = R0;
   p.o = o; p.S_fin = S_final; p.R_fin = R_final;
-  if (pr.save) {
-    p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
-    p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
-    p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
-    p.fwd_blk = ws + w.fblk;
-  }
+  if (pr.save) set_saved(pr, w, ws, p);
 
   hipError_t e = hipSuccess;
   if (pr.varlen && pr.ntok > 0)   // tokens outside every sequence read as zero
@@ -234,13 +255,7 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   p.q = q; p.k = k; p.v = v;
   p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
   p.S0 = S0; p.R0 = R0;
-  p.ck_S = reinterpret_cast<float*>(ws + w.ckS);
-  p.ck_R = reinterpret_cast<float*>(ws + w.ckR);
-  p.ck_mask = reinterpret_cast<uint8_t*>(ws + w.mask);
-  p.dS_ws = reinterpret_cast<float*>(ws + w.dS);
-  p.dR_ws = reinterpret_cast<float*>(ws + w.dR);
-  p.fwd_blk = ws + w.fblk;
-  p.bwd_blk = ws + w.bblk;
+  set_saved(pr, w, ws, p);
   p.dO = dO; p.dS_fin = dS_final; p.dR_fin = dR_final;
   p.dq = dq; p.dk = dk; p.dv = dv;
   p.dalpha_s = dalpha_s; p.dbeta = dbeta; p.dalpha_r = dalpha_r; p.dgamma = dgamma;

@@ -30,9 +30,9 @@
 // G = K K^T, P = Q K^T, dP and dG.  State rows stream from HBM (fp32) straight into MFMA B
 // fragments; the token blocks are moved into LDS by LDS-DMA.
 //
-// Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation; a state
-// row is scaled by a power of two before its fp16 conversion when its
-// magnitude needs it, and the scale is undone on the product column.
+// Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation.  The
+// scans store the states in fp16 scaled by a power of two per (row, 32
+// columns); a contraction applies each k-step's scale to the accumulator.
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -117,24 +117,6 @@ struct GradLayout {
   static constexpr int kBytes = kRed + 16 * 4;
   static_assert(kBytes <= 160 * 1024, "gradient kernel LDS");
 };
-
-// DPP lane exchange inside a row of 16 lanes
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
-                                                                0xF, 0xF, false));
-}
-
-// Sum over aligned groups of N lanes (N = 2, 4, 8, 16) inside a 16-lane row;
-// every lane of a group gets the group's sum.
-template <int N>
-__device__ __forceinline__ float group_sum(float x) {
-  x += dpp<0xB1>(x);                        // quad_perm [1,0,3,2]
-  if constexpr (N >= 4) x += dpp<0x4E>(x);  // quad_perm [2,3,0,1]
-  if constexpr (N >= 8) x += dpp<0x141>(x); // row_half_mirror
-  if constexpr (N >= 16) x += dpp<0x140>(x); // row_mirror
-  return x;
-}
 
 __device__ __forceinline__ float wave_sum(float x) {
   x = group_sum<16>(x);
@@ -340,84 +322,68 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     for (int tt = 0; tt < 4; ++tt) { dQ[m][tt] = zero4(); dK[m][tt] = zero4(); }
   float gsC = 0.f, grC = 0.f;
 
-  // a state's rows i0 .. i0+15 as raw fp32 values in B-fragment order
-  constexpr int kRaw = BF ? 2 * KSV : KSV;
-  typedef typename std::conditional<BF, float4, float>::type RawT;
-  const float* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
-  auto load_raw = [&](RawT (&raw)[kRaw], int st, int i0) {
-    const float* rowp = srcs[st] + soff + (int64_t)(i0 + (lane & 15)) * DV;
-#pragma unroll
-    for (int ks = 0; ks < KSV; ++ks) {
-      if constexpr (BF) {
-        const int j = ks * M::kStep + 8 * (lane >> 4);
-        raw[2 * ks] = *reinterpret_cast<const float4*>(rowp + j);
-        raw[2 * ks + 1] = *reinterpret_cast<const float4*>(rowp + j + 4);
-      } else {
-        raw[ks] = rowp[ks * M::kStep + (lane >> 4)];
-      }
-    }
+  // A state's rows i0 .. i0+15 as MFMA B fragments (row = lane & 15), with
+  // the power-of-two scale of each (row, 32-column k-step) for fp16 states.
+  struct StateRows {
+    Frag fr[KSV];
+    float sc[KSV];
   };
-  // operand fragments; returns the power-of-two scale of this lane's row
-  auto convert = [&](const RawT (&raw)[kRaw], Frag (&fr)[KSV]) -> float {
+  const void* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
+  const float* scs[4] = {p.ck_S_sc, p.ck_R_sc, p.dS_sc, p.dR_sc};
+  const int64_t sco = ((int64_t)c * H + h) * DK * (DV / 32);
+  auto load_rows = [&](StateRows& x, int st, int i0) {
+    const int i = i0 + (lane & 15);
     if constexpr (BF) {
-      float mx = 0.f;
-#pragma unroll
-      for (int x = 0; x < kRaw; ++x)
-        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(raw[x].x), fabsf(raw[x].y)),
-                             fmaxf(fabsf(raw[x].z), fabsf(raw[x].w))));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      float scl = 1.f;
-      if (mx > 16384.f) {
-        int ex;
-        frexpf(mx / 16384.f, &ex);
-        scl = ldexpf(1.f, ex);
-      }
-      const float inv = 1.f / scl;
+      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * DV;
+      const float* scp = scs[st] + sco + (int64_t)i * (DV / 32);
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks) {
-        const float4 a = raw[2 * ks], b = raw[2 * ks + 1];
-        fr[ks] = f16x8{(f16)(a.x * inv), (f16)(a.y * inv), (f16)(a.z * inv), (f16)(a.w * inv),
-                       (f16)(b.x * inv), (f16)(b.y * inv), (f16)(b.z * inv), (f16)(b.w * inv)};
+        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + ks * M::kStep + 8 * (lane >> 4));
+        x.sc[ks] = scp[ks];
       }
-      return scl;
     } else {
+      const float* rowp = reinterpret_cast<const float*>(srcs[st]) + soff + (int64_t)i * DV;
 #pragma unroll
-      for (int ks = 0; ks < KSV; ++ks) fr[ks] = raw[ks];
-      return 1.f;
+      for (int ks = 0; ks < KSV; ++ks) {
+        x.fr[ks] = rowp[ks * M::kStep + (lane >> 4)];
+        x.sc[ks] = 1.f;
+      }
     }
   };
-  // sum over this lane's elements of (scaled fragment) x (raw values)
-  auto frag_dot = [&](const Frag (&fr)[KSV], float scl, const RawT (&raw)[kRaw]) {
+  // sum over this lane's elements of a (.) b
+  auto frag_dot = [&](const StateRows& a, const StateRows& b) {
     float s = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KSV; ++ks) {
+      float d = 0.f;
       if constexpr (BF) {
-        const float4 a = raw[2 * ks], b = raw[2 * ks + 1];
-        s += (float)fr[ks][0] * a.x + (float)fr[ks][1] * a.y + (float)fr[ks][2] * a.z +
-             (float)fr[ks][3] * a.w + (float)fr[ks][4] * b.x + (float)fr[ks][5] * b.y +
-             (float)fr[ks][6] * b.z + (float)fr[ks][7] * b.w;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d += (float)a.fr[ks][e] * (float)b.fr[ks][e];
       } else {
-        s += fr[ks] * raw[ks];
+        d = a.fr[ks] * b.fr[ks];
       }
+      s += d * (a.sc[ks] * b.sc[ks]);
     }
-    return s * scl;
+    return s;
   };
   // [16 tokens x 16 state rows] tile: token block rows 16 tt times the state
-  // rows of the fragments, contracted over the value dimension
-  auto contract = [&](int b, int tt, const Frag (&fr)[KSV], float scl) {
+  // rows, contracted over the value dimension; each k-step's scale is applied
+  // by rescaling the accumulator (powers of two: exact)
+  auto contract = [&](int b, int tt, const StateRows& x) {
     floatx4 acc = zero4();
 #pragma unroll
-    for (int ks = 0; ks < KSV; ++ks)
-      acc = M::mma(TV::template frag<M>(tokblk(b), 16 * tt, ks * M::kStep), fr[ks], acc);
-    return acc * scl;
+    for (int ks = 0; ks < KSV; ++ks) {
+      if (ks > 0) acc *= x.sc[ks - 1] * (1.f / x.sc[ks]);
+      acc = M::mma(TV::template frag<M>(tokblk(b), 16 * tt, ks * M::kStep), x.fr[ks], acc);
+    }
+    return acc * x.sc[KSV - 1];
   };
 
   // per d_k tile: S0 with dS1, then R0 with dR1; the next pair's rows are
   // loaded while the current pair's products run
-  RawT rawA[kRaw], rawB[kRaw];
-  load_raw(rawA, 0, 16 * w);
-  load_raw(rawB, 2, 16 * w);
+  StateRows rowA, rowB;
+  load_rows(rowA, 0, 16 * w);
+  load_rows(rowB, 2, 16 * w);
 #pragma unroll
   for (int m = 0; m < kIT; ++m) {
     // the token-block fragments are reloaded per d_k tile: keeping them
@@ -433,23 +399,21 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
         qq[r] = to_f<XT>(TK::at(Ql, 16 * tt + acc_row(r), icol));
       }
     };
-    Frag f0[KSV], f1[KSV];
-    // ---- S0 (rawA) and dS1 (rawB) ----
+    // ---- S0 (rowA) and dS1 (rowB) ----
     {
-      const float sS = convert(rawA, f0);
-      gsC += edge[0] * frag_dot(f0, sS, rawB);   // e^{g_C} <S0, dS1>
-      const float sD = convert(rawB, f1);
-      load_raw(rawA, 1, i0);
-      load_raw(rawB, 3, i0);
+      const StateRows s0 = rowA, d1 = rowB;
+      gsC += edge[0] * frag_dot(s0, d1);   // e^{g_C} <S0, dS1>
+      load_rows(rowA, 1, i0);
+      load_rows(rowB, 3, i0);
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
         asm volatile("" ::: "memory");   // bounds how far fragment loads are hoisted
         // F1 = dO S0^T, FK1 = dX S0^T, FK2 = dY S0^T, FK4 = U dS1^T
-        const floatx4 F1 = contract(bDO, tt, f0, sS);
-        const floatx4 FK1 = contract(bDX, tt, f0, sS);
+        const floatx4 F1 = contract(bDO, tt, s0);
+        const floatx4 FK1 = contract(bDX, tt, s0);
         floatx4 FK2 = zero4();
-        if constexpr (RDN) FK2 = contract(bDY, tt, f0, sS);
-        const floatx4 FK4 = contract(bU, tt, f1, sD);
+        if constexpr (RDN) FK2 = contract(bDY, tt, s0);
+        const floatx4 FK4 = contract(bU, tt, d1);
         float kq[4], qq[4], ags[4], agsp[4], ab[4];
         kq_of(tt, kq, qq);
 #pragma unroll
@@ -474,23 +438,22 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
         if constexpr (RDN) acc_rows(sum_row(sB), 16 * tt, ab);
       }
     }
-    // ---- R0 (rawA) and dR1 (rawB) ----
+    // ---- R0 (rowA) and dR1 (rowB) ----
     {
-      const float sR = convert(rawA, f0);
-      grC += edge[1] * frag_dot(f0, sR, rawB);   // e^{h_C} <R0, dR1>
-      const float sE = convert(rawB, f1);
+      const StateRows r0 = rowA, e1 = rowB;
+      grC += edge[1] * frag_dot(r0, e1);   // e^{h_C} <R0, dR1>
       if (m + 1 < kIT) {
-        load_raw(rawA, 0, i0 + 16 * NW);
-        load_raw(rawB, 2, i0 + 16 * NW);
+        load_rows(rowA, 0, i0 + 16 * NW);
+        load_rows(rowB, 2, i0 + 16 * NW);
       }
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
         asm volatile("" ::: "memory");
         // F2 = dO R0^T, FK3 = dYR R0^T, FK5 = UR dR1^T
-        const floatx4 F2 = contract(bDO, tt, f0, sR);
+        const floatx4 F2 = contract(bDO, tt, r0);
         floatx4 FK3 = zero4();
-        if constexpr (RDN) FK3 = contract(bDYR, tt, f0, sR);
-        const floatx4 FK5 = contract(bUR, tt, f1, sE);
+        if constexpr (RDN) FK3 = contract(bDYR, tt, r0);
+        const floatx4 FK5 = contract(bUR, tt, e1);
         float kq[4], qq[4], agr[4], agm[4];
         kq_of(tt, kq, qq);
 #pragma unroll

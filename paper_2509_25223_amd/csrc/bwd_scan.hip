@@ -36,10 +36,10 @@ struct BwdScanLayout {
   static constexpr int kPad = kBF ? 8 : 4;
   static constexpr int kLdX = kChunk + kPad;
   static constexpr int kLdS = DK + kPad;
-  // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs T^S and
-  // MR (first and last released) are double-buffered
+  // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs MR
+  // (first used) is double-buffered
   static constexpr bool kDB = kBF;
-  static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 4 : 3);
+  static constexpr int kNumSlots = RDN ? (kDB ? 6 : 5) : (kDB ? 4 : 3);
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kNumBufs = 6;
   static constexpr int kKT = 0;
@@ -53,22 +53,22 @@ struct BwdScanLayout {
   static constexpr int kMaskBytes = kChunk * BV;
   static constexpr int kGraw = kMask + kMaskBytes;
   static constexpr int kGates = kGraw + kGateBlock * 4;
-  static constexpr int kBytes = kGates + 10 * kChunk * 4;
+  static constexpr int kYst = kGates + 10 * kChunk * 4;   // dYR staging [BV][kLdX]
+  static constexpr int kBytes = kYst + kBufBytes;
   static_assert(kMaskBytes % 1024 == 0, "mask block moved in whole DMA instructions");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
-  // RDN: TS[2] MG MP TR MR[2]; RLA: MG MP MR[2]
+  // RDN: TS MG MP TR MR[2]; RLA: MG MP MR[2]
   __device__ static constexpr int slot(int mat, int buf) {
     if (!RDN) {
       if (mat == kMatMG) return 0;
       if (mat == kMatMP) return 1;
       return kDB ? 2 + buf : 2;   // MR
     }
-    if (mat == kMatTS) return kDB ? buf : 0;
-    const int b = kDB ? 2 : 1;
-    if (mat == kMatMG) return b;
-    if (mat == kMatMP) return b + 1;
-    if (mat == kMatTR) return b + 2;
-    return kDB ? b + 3 + buf : b + 3;   // MR
+    if (mat == kMatTS) return 0;
+    if (mat == kMatMG) return 1;
+    if (mat == kMatMP) return 2;
+    if (mat == kMatTR) return 3;
+    return kDB ? 4 + buf : 4;   // MR
   }
 };
 
@@ -126,6 +126,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   float* dls = egr + kChunk;
   float* dlr = dls + kChunk;
   float* edge = dlr + kChunk;
+  XT* Yst = reinterpret_cast<XT*>(smem + L::kYst);   // dYR of this chunk
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int nvb = DV / BV;
@@ -169,8 +170,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 
   // ---- staging of the next (earlier) chunk while this one computes ----
   //   K, Q, dO: register prefetch after P1 (transposed / converted at commit)
-  //   gates, T^S, MR: LDS-DMA after P1 (T^S, MR double-buffered)
-  //   T^R, mask: after P3;  MG, MP: after P4 (their last uses)
+  //   gates, MR: LDS-DMA after P1 (MR double-buffered)
+  //   T^R, mask: after P3;  MG, MP: after P4;  T^S: after P5 (their last uses)
   // bf16 inputs; fp32 inputs single-buffer every matrix and move them all
   // after the chunk's last barrier.
   constexpr int kOPerThread = kChunk * BV / kThreads;
@@ -214,10 +215,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   };
   auto issue_early = [&](int c) {   // after P1
     issue_gates(c);
-    if constexpr (L::kDB) {
-      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, c & 1));
-      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
-    }
+    if constexpr (L::kDB) dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
   };
   auto issue_mid = [&](int c) {     // after P3
     if constexpr (L::kDB) {
@@ -230,6 +228,9 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
       dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
     }
+  };
+  auto issue_after5 = [&](int c) {  // after P5 (RDN)
+    if constexpr (L::kDB && RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
   };
   auto issue_all_single = [&](int c) {   // fp32: everything after the last barrier
     if constexpr (!L::kDB) {
@@ -249,7 +250,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     issue_gates(c);
     issue_mask(c);
     if constexpr (RDN) {
-      dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, c & 1));
+      dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
       dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
     }
     dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
@@ -277,20 +278,6 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         }
       }
     };
-
-    {   // gradient w.r.t. this chunk's end states
-      const int64_t off = ((int64_t)gc * H + h) * DK * DV;
-#pragma unroll
-      for (int it = 0; it < IT; ++it)
-#pragma unroll
-        for (int jt = 0; jt < JT; ++jt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
-            p.dS_ws[off + (int64_t)i * DV + j] = dS[it][jt][r];
-            p.dR_ws[off + (int64_t)i * DV + j] = dR[it][jt][r];
-          }
-    }
 
     // ---- commit: K fragments, K^T and Q^T (XT), dO^T, gate vectors ----
     typename MI::frag Kf[KS_STEPS];
@@ -365,6 +352,50 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       store_acc_t<XT>(blk(bQDB) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdb);
       store_acc_t<XT>(blk(bQDC) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdc);
     }
+    // gradient w.r.t. this chunk's end states for the gradient kernel, read
+    // back from the state copies (rows i of [BV][DK]) and written row-major in
+    // 16-byte vectors; bf16 inputs: fp16 scaled per (row, 32 columns)
+    {
+      const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
+      constexpr int kVE = BF ? 8 : 4;            // elements per vector
+      constexpr int kVPR = BV / kVE;             // vectors per state row
+      constexpr int kItems = DK * kVPR / kThreads;
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const IN* hi = sidx == 0 ? dShi : dRhi;
+        const IN* lo = sidx == 0 ? dSlo : dRlo;
+#pragma unroll
+        for (int u = 0; u < kItems; ++u) {
+          const int e = tid + u * kThreads, i = e / kVPR, v = e % kVPR;
+          float x[kVE];
+#pragma unroll
+          for (int k = 0; k < kVE; ++k) {
+            const int o2 = (v * kVE + k) * L::kLdS + i;
+            x[k] = to_f<IN>(hi[o2]);
+            if constexpr (BF) x[k] += to_f<IN>(lo[o2]);
+          }
+          if constexpr (BF) {
+            static_assert(kVPR == 4, "one 32-column scale block = 4 lanes");
+            float mx = 0.f;
+#pragma unroll
+            for (int k = 0; k < kVE; ++k) mx = fmaxf(mx, fabsf(x[k]));
+            const float sc = pow2_scale(group_max<4>(mx)), inv = 1.f / sc;
+            f16x8 hv;
+#pragma unroll
+            for (int k = 0; k < kVE; ++k) hv[k] = (f16)(x[k] * inv);
+            f16* dst = reinterpret_cast<f16*>(sidx == 0 ? p.dS_ws : p.dR_ws);
+            *reinterpret_cast<f16x8*>(dst + off + (int64_t)i * DV + v * kVE) = hv;
+            float* scd = sidx == 0 ? p.dS_sc : p.dR_sc;
+            scd[((int64_t)gc * H + h) * DK * (DV / 32) + (int64_t)i * (DV / 32) + j0 / 32] = sc;
+          } else {
+            float* dst = reinterpret_cast<float*>(sidx == 0 ? p.dS_ws : p.dR_ws);
+            *reinterpret_cast<float4*>(dst + off + (int64_t)i * DV + v * kVE) =
+                float4{x[0], x[1], x[2], x[3]};
+          }
+        }
+      }
+    }
+
     barrier_lds();
     if (c > 0) {
       issue_regs(c - 1);
@@ -402,8 +433,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       }
       store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
       store_acc_t<XT>(blk(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, RDN ? dkr : dks);
-      store_rows_masked<XT>(bblk + blk_off(gc, h, H, 0, DV) + j0 + jt * 16, DV, 16 * w, len, dX[jt]);
-      store_rows_masked<XT>(bblk + blk_off(gc, h, H, 2, DV) + j0 + jt * 16, DV, 16 * w, len, dYR);
+      store_acc_t<XT>(Yst + jt * 16 * L::kLdX + 16 * w, L::kLdX, dYR);
     }
     barrier_lds();
     if (c > 0) issue_mid(c - 1);
@@ -418,8 +448,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
       if constexpr (RDN) {
         store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-      } else {   // RLA: U = diag(b) V, so dV gets b dU
-        store_rows_masked<XT>(bblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, du);
+      } else {   // RLA: U = diag(b) V, so dV gets b dU; dU is kept for the block store
+        store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
         store_dv(jt, dX[jt], du);
       }
     }
@@ -427,20 +457,26 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     if (c > 0) issue_late(c - 1);
     if constexpr (RDN) {
       // ---- P5: dY = T^S^T dU, dKS ----
+      floatx4 dY[JT];
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
-        floatx4 dY = zero4(), dks;
-        mma_swz_cols<XT>(dY, mat(kMatTS, buf), 16 * w, blk(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+        floatx4 dks;
+        dY[jt] = zero4();
+        mma_swz_cols<XT>(dY[jt], mat(kMatTS, 0), 16 * w, blk(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
-          dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[r];
+          dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[jt][r];
         }
         store_acc_t<XT>(blk(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
-        store_rows_masked<XT>(bblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, dY);
-        store_dv(jt, dX[jt], dY);
+        store_dv(jt, dX[jt], dY[jt]);
       }
       barrier_lds();
+      if (c > 0) issue_after5(c - 1);
+      // dU is dead: its slot keeps dY for the block store (P6 does not read it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+        store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dY[jt]);
     }
 
     // ---- P6: state gradients at the chunk start ----
@@ -467,6 +503,23 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     }
     wait_vmem();
     barrier_lds();
+    {   // this chunk's dX, dY, dYR (value-major in LDS) as token-major rows in
+        // 16-byte stores; rows past the end are zero.  The buffers are next
+        // written after the coming chunk's first barrier.
+      constexpr int kVE = 16 / (int)sizeof(XT);
+      constexpr int kVPR = BV / kVE;
+      static_assert(kChunk * kVPR == kThreads, "one block vector per thread");
+      const int t = tid / kVPR, v = tid % kVPR;
+#pragma unroll
+      for (int b = 0; b < 3; ++b) {
+        const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
+        XT vals[kVE];
+#pragma unroll
+        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? srcb[(v * kVE + k) * L::kLdX + t] : from_f<XT>(0.f);
+        *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + v * kVE) =
+            *reinterpret_cast<const uint4*>(vals);
+      }
+    }
     write_copies();
   }
 

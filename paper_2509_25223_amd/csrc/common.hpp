@@ -317,16 +317,43 @@ __device__ __forceinline__ void mma_swz_cols(floatx4& acc, const T* M, int t0, c
 __device__ __forceinline__ int acc_row(int r) { return 4 * ((threadIdx.x & 63) >> 4) + r; }
 __device__ __forceinline__ int acc_col() { return threadIdx.x & 15; }
 
-// Stores this lane's 4 accumulator rows of a [token][column] tile into a
-// token-major array (row stride ld): rows t0 + acc_row(r), column acc_col();
-// rows at or past `len` are written as 0.
-template <typename T>
-__device__ __forceinline__ void store_rows_masked(T* base, int ld, int t0, int len, floatx4 v) {
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int t = t0 + acc_row(r);
-    base[(int64_t)t * ld + acc_col()] = from_f<T>(t < len ? v[r] : 0.f);
-  }
+// DPP lane exchange inside a row of 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                                0xF, 0xF, false));
+}
+
+// Sum / max over aligned groups of N lanes (N = 2, 4, 8, 16) inside a 16-lane
+// row; every lane of a group gets the result.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  x += dpp<0xB1>(x);                         // quad_perm [1,0,3,2]
+  if constexpr (N >= 4) x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  if constexpr (N >= 8) x += dpp<0x141>(x);  // row_half_mirror
+  if constexpr (N >= 16) x += dpp<0x140>(x); // row_mirror
+  return x;
+}
+template <int N>
+__device__ __forceinline__ float group_max(float x) {
+  x = fmaxf(x, dpp<0xB1>(x));
+  if constexpr (N >= 4) x = fmaxf(x, dpp<0x4E>(x));
+  if constexpr (N >= 8) x = fmaxf(x, dpp<0x141>(x));
+  if constexpr (N >= 16) x = fmaxf(x, dpp<0x140>(x));
+  return x;
+}
+
+// Power-of-two scale s for a block of values with largest magnitude mx:
+// mx / s lies in [2^13, 2^14), so the block stored as fp16 (x / s) keeps
+// fp16's full relative precision for its largest entries and cannot overflow.
+// Blocks of zeros (or non-finite maxima) get s = 1.
+__device__ __forceinline__ float pow2_scale(float mx) {
+  if (!(mx > 0.f) || !(mx < __builtin_inff())) return 1.f;
+  int e;
+  frexpf(mx, &e);   // mx in [2^(e-1), 2^e)
+  e = e - 14;
+  e = e < -126 ? -126 : e > 127 ? 127 : e;
+  return ldexpf(1.f, e);
 }
 
 // Stores the 4 accumulator rows of this lane, column-major into LDS as a

@@ -54,7 +54,14 @@ struct FwdLayout {
   static constexpr int kVBytes = kChunk * BV * (int)sizeof(IN);
   static constexpr int kGraw = kVc + kVBytes;
   static constexpr int kGates = kGraw + kGateBlock * 4;
-  static constexpr int kBytes = kGates + 10 * kChunk * 4;
+  // output staging, so that o, the clip mask and r leave in 16-byte stores:
+  // r value-major [BV][kLdX] (XT), mask token-major [64][BV] bytes, o
+  // token-major [64][BV + 4] fp32
+  static constexpr int kRst = kGates + 10 * kChunk * 4;
+  static constexpr int kMst = kRst + kBufBytes;
+  static constexpr int kLdO = BV + 4;
+  static constexpr int kOst = kMst + kChunk * BV;
+  static constexpr int kBytes = kOst + kChunk * kLdO * 4;
   static_assert(kVBytes == 4 * 1024, "V block = one DMA instruction per wave");
   static_assert(kBytes <= 160 * 1024, "forward scan LDS");
   // slot of each matrix (RDN: TS MG MP TR[2] MR[2]; RLA: MG MP MR[2])
@@ -125,6 +132,9 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   float* dls = egr + kChunk;        // e^{g_C - g_t}
   float* dlr = dls + kChunk;        // e^{h_C - h_t}
   float* edge = dlr + kChunk;       // [0] = e^{g_C}, [1] = e^{h_C}
+  XT* Rst = reinterpret_cast<XT*>(smem + L::kRst);            // r (saving mode)
+  uint8_t* Mst = reinterpret_cast<uint8_t*>(smem + L::kMst);  // clip mask (saving mode)
+  float* Ost = reinterpret_cast<float*>(smem + L::kOst);      // o
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   // XCD-aware block mapping: the value blocks of one (sequence, head) pair get
@@ -234,20 +244,6 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     const int len = chunk_len(c);
     const int buf = c & 1;
 
-    if constexpr (CKPT) {
-      const int64_t off = ((int64_t)gc * H + h) * DK * DV;
-#pragma unroll
-      for (int it = 0; it < IT; ++it)
-#pragma unroll
-        for (int jt = 0; jt < JT; ++jt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
-            p.ck_S[off + (int64_t)i * DV + j] = Sacc[it][jt][r];
-            p.ck_R[off + (int64_t)i * DV + j] = Racc[it][jt][r];
-          }
-    }
-
     // ---- commit: K, Q fragments from the prefetch registers, K^T (XT) and
     //      the gate-derived vectors into LDS ----
     typename MI::frag Kf[KS_STEPS], Qf[KS_STEPS];
@@ -302,6 +298,49 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         mma_rega<IN, DK, true>(QR[jt], Qf, Rlo + o, L::kLdS);
       }
     }
+    // chunk-start states for the gradient kernel, read back from the state
+    // copies (rows i of [BV][DK]) and written row-major in 16-byte vectors;
+    // bf16 inputs: fp16 scaled by a power of two per (row, 32 columns)
+    if constexpr (CKPT) {
+      const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
+      constexpr int kVE = BF ? 8 : 4;            // elements per vector
+      constexpr int kVPR = BV / kVE;             // vectors per state row
+      constexpr int kItems = DK * kVPR / kThreads;
+#pragma unroll
+      for (int sidx = 0; sidx < 2; ++sidx) {
+        const IN* hi = sidx == 0 ? Shi : Rhi;
+        const IN* lo = sidx == 0 ? Slo : Rlo;
+#pragma unroll
+        for (int u = 0; u < kItems; ++u) {
+          const int e = tid + u * kThreads, i = e / kVPR, v = e % kVPR;
+          float x[kVE];
+#pragma unroll
+          for (int k = 0; k < kVE; ++k) {
+            const int o2 = (v * kVE + k) * L::kLdS + i;
+            x[k] = to_f<IN>(hi[o2]);
+            if constexpr (BF) x[k] += to_f<IN>(lo[o2]);
+          }
+          if constexpr (BF) {
+            static_assert(kVPR == 4, "one 32-column scale block = 4 lanes");
+            float mx = 0.f;
+#pragma unroll
+            for (int k = 0; k < kVE; ++k) mx = fmaxf(mx, fabsf(x[k]));
+            const float sc = pow2_scale(group_max<4>(mx)), inv = 1.f / sc;
+            f16x8 hv;
+#pragma unroll
+            for (int k = 0; k < kVE; ++k) hv[k] = (f16)(x[k] * inv);
+            f16* dst = reinterpret_cast<f16*>(sidx == 0 ? p.ck_S : p.ck_R);
+            *reinterpret_cast<f16x8*>(dst + off + (int64_t)i * DV + v * kVE) = hv;
+            float* scd = sidx == 0 ? p.ck_S_sc : p.ck_R_sc;
+            scd[((int64_t)gc * H + h) * DK * (DV / 32) + (int64_t)i * (DV / 32) + j0 / 32] = sc;
+          } else {
+            float* dst = reinterpret_cast<float*>(sidx == 0 ? p.ck_S : p.ck_R);
+            *reinterpret_cast<float4*>(dst + off + (int64_t)i * DV + v * kVE) =
+                float4{x[0], x[1], x[2], x[3]};
+          }
+        }
+      }
+    }
     float vloc[JT][4];
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
@@ -320,8 +359,6 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * y[r];
         store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
         store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-        if constexpr (CKPT)
-          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 0, DV) + j0 + jt * 16, DV, 16 * w, len, y);
       }
     }
     barrier_lds();
@@ -340,8 +377,6 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * u[r];
         store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
         store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-        if constexpr (CKPT)
-          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 0, DV) + j0 + jt * 16, DV, 16 * w, len, u);
       }
       barrier_lds();
     }
@@ -361,11 +396,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         const float x = __builtin_fmaf(-egsp[t], KS[jt][r], vloc[jt][r]) - mgu[r];
         const float rr = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
         rv[r] = rr;
-        if constexpr (CKPT) {
-          if (t < len)
-            p.ck_mask[((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col()] =
-                (clip < 0.f || fabsf(x) <= clip) ? 1 : 0;
-        }
+        if constexpr (CKPT) Mst[t * BV + jt * 16 + acc_col()] = (clip < 0.f || fabsf(x) <= clip) ? 1 : 0;
         base[jt][r] = __builtin_fmaf(egs[t], QS[jt][r], mpu[r]);
         y[r] = RDN ? ggm[t] * __builtin_fmaf(-egr[t], KR[jt][r], rr) : ggm[t] * rr;
       }
@@ -377,11 +408,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * y[r];
         store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
         store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-        if constexpr (CKPT)
-          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, y);
       }
-      if constexpr (CKPT)
-        store_rows_masked<XT>(fblk + blk_off(gc, h, H, 2, DV) + j0 + jt * 16, DV, 16 * w, len, rv);
+      if constexpr (CKPT) store_acc_t<XT>(Rst + jt * 16 * L::kLdX + 16 * w, L::kLdX, rv);
     }
     if constexpr (!L::kDB) wait_vmem();   // single-buffered T^R / MR of this chunk
     barrier_lds();
@@ -397,14 +425,11 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * u[r];
         store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
         store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-        if constexpr (CKPT)
-          store_rows_masked<XT>(fblk + blk_off(gc, h, H, 1, DV) + j0 + jt * 16, DV, 16 * w, len, u);
       }
       barrier_lds();
     }
 
-    // ---- P5: correction read-out, output (stored after the barrier) ----
-    float outv[JT][4];
+    // ---- P5: correction read-out; o staged, stored after the end barrier ----
     if constexpr (WRITE_O) {
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
@@ -413,7 +438,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
-          outv[jt][r] = __builtin_fmaf(ggm[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
+          Ost[t * L::kLdO + jt * 16 + acc_col()] =
+              __builtin_fmaf(ggm[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
         }
       }
     }
@@ -435,15 +461,51 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     wait_vmem();
     barrier_lds();
     if (c + 1 < nch) issue_tail(c + 1);   // single-buffered T^R / MR: waited at P3
+    // ---- this chunk's staged outputs, in 16-byte stores (the buffers are
+    //      next written after the coming chunk's first barrier) ----
     if constexpr (WRITE_O) {
+      constexpr int kVE = 16 / (int)sizeof(OT);
+      constexpr int kVPR = BV / kVE;
+      static_assert((kChunk * kVPR) % kThreads == 0, "whole o vectors per thread");
 #pragma unroll
-      for (int jt = 0; jt < JT; ++jt)
+      for (int u = 0; u < kChunk * kVPR / kThreads; ++u) {
+        const int e = tid + u * kThreads, t = e / kVPR, v = e % kVPR;
+        if (t < len) {
+          OT* dst = og + ((tok + t) * H + h) * (int64_t)DV + j0 + v * kVE;
+          const float* src = Ost + t * L::kLdO + v * kVE;
+          if constexpr (sizeof(OT) == 4) {
+            *reinterpret_cast<float4*>(dst) = *reinterpret_cast<const float4*>(src);
+          } else {
+            u16x8 ov;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int t = 16 * w + acc_row(r);
-          if (t < len)
-            og[((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col()] = from_f<OT>(outv[jt][r]);
+            for (int k = 0; k < 8; ++k) ov[k] = f2bf(src[k]);
+            *reinterpret_cast<u16x8*>(dst) = ov;
+          }
         }
+      }
+    }
+    if constexpr (CKPT) {
+      {   // clip mask rows
+        constexpr int kVPR = BV / 16;
+        const int t = tid / kVPR, v = tid % kVPR;
+        if (tid < kChunk * kVPR && t < len)
+          *reinterpret_cast<uint4*>(p.ck_mask + ((tok + t) * H + h) * (int64_t)DV + j0 + v * 16) =
+              *reinterpret_cast<const uint4*>(Mst + t * BV + v * 16);
+      }
+      // U, UR, r rows (value-major in LDS): rows past the end are zero
+      constexpr int kVE = 16 / (int)sizeof(XT);
+      constexpr int kVPR = BV / kVE;
+      static_assert(kChunk * kVPR == kThreads, "one block vector per thread");
+      const int t = tid / kVPR, v = tid % kVPR;
+#pragma unroll
+      for (int b = 0; b < 3; ++b) {
+        const XT* srcb = b == 0 ? Ut : b == 1 ? URt : Rst;
+        XT vals[kVE];
+#pragma unroll
+        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? srcb[(v * kVE + k) * L::kLdX + t] : from_f<XT>(0.f);
+        *reinterpret_cast<uint4*>(fblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + v * kVE) =
+            *reinterpret_cast<const uint4*>(vals);
+      }
     }
     write_state_copies();
   }

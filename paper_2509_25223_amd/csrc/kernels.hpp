@@ -42,11 +42,18 @@ struct OpParams {
   // workspace regions
   float* gate_ws = nullptr;     // [max_chunks][H][kGateBlock]
   void* mat_ws = nullptr;       // [max_chunks][H][kNumMats][64][64]  (mm type)
-  float* ck_S = nullptr;        // [max_chunks][H][DK][DV] chunk-start S
-  float* ck_R = nullptr;        // [max_chunks][H][DK][DV] chunk-start R
+  // chunk states saved for the gradient kernel, [max_chunks][H][DK][DV]: fp32
+  // for fp32 inputs; fp16 for bf16 inputs, each (row, 32 columns) scaled by a
+  // power of two held in the matching *_sc array [max_chunks][H][DK][DV / 32]
+  void* ck_S = nullptr;         // chunk-start S
+  void* ck_R = nullptr;         // chunk-start R
+  void* dS_ws = nullptr;        // grad of chunk-end S
+  void* dR_ws = nullptr;        // grad of chunk-end R
+  float* ck_S_sc = nullptr;
+  float* ck_R_sc = nullptr;
+  float* dS_sc = nullptr;
+  float* dR_sc = nullptr;
   uint8_t* ck_mask = nullptr;   // [ntok][H][DV] 1 where |x| <= clip
-  float* dS_ws = nullptr;       // [max_chunks][H][DK][DV] grad of chunk-end S
-  float* dR_ws = nullptr;       // [max_chunks][H][DK][DV] grad of chunk-end R
   // per-token blocks saved for the gradient kernel, [max_chunks][H][3][64][DV]
   // (mm type, token-major, rows past the end of a sequence are zero):
   void* fwd_blk = nullptr;      // U, UR, r (clipped residual) from the forward scan
