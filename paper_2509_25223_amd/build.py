@@ -21,6 +21,10 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     # packed-fp32 instructions are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # no mixed-precision FMAs: the backend would otherwise fold an fp32 product
+    # into its fp16 conversion (one rounding instead of two) in some template
+    # instances and not others, so the saving and plain forwards could differ
+    "-Xclang", "-target-feature", "-Xclang", "-fma-mix-insts",
     # fused multiply-adds only where one source expression asks for them, so
     # that every template instantiation of a kernel rounds alike (the default,
     # fast contraction, lets the backend fuse differently per instantiation)

@@ -382,7 +382,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
             const float sc = pow2_scale(group_max<4>(mx)), inv = 1.f / sc;
             f16x8 hv;
 #pragma unroll
-            for (int k = 0; k < kVE; ++k) hv[k] = (f16)(x[k] * inv);
+            for (int k = 0; k < kVE; ++k) hv[k] = to_f16(x[k] * inv);
             f16* dst = reinterpret_cast<f16*>(sidx == 0 ? p.dS_ws : p.dR_ws);
             *reinterpret_cast<f16x8*>(dst + off + (int64_t)i * DV + v * kVE) = hv;
             float* scd = sidx == 0 ? p.dS_sc : p.dR_sc;

@@ -34,7 +34,11 @@ template <> __device__ __forceinline__ float to_f<f16>(f16 x) { return (float)x;
 template <typename T> __device__ __forceinline__ T from_f(float x);
 template <> __device__ __forceinline__ float from_f<float>(float x) { return x; }
 template <> __device__ __forceinline__ u16 from_f<u16>(float x) { return f2bf(x); }
-template <> __device__ __forceinline__ f16 from_f<f16>(float x) { return (f16)x; }
+// fp32 -> fp16, round to nearest even.  (The build disables the mixed-precision
+// FMA instructions, so a preceding fp32 product is never folded into the
+// conversion with a single rounding in some template instances only.)
+__device__ __forceinline__ f16 to_f16(float x) { return (f16)x; }
+template <> __device__ __forceinline__ f16 from_f<f16>(float x) { return to_f16(x); }
 
 // bf16 residual of x after its bf16 rounding hi: x ~= hi + lo to ~16 bits,
 // with fp32 range.  Used for state operands (split-bf16 products).
@@ -222,15 +226,18 @@ __device__ __forceinline__ void dma16(const void* src, void* lds) {
                                    reinterpret_cast<char*>(lds), 16, 0, 0);
 }
 
-// DMA of one row-major 64 x 64 matrix (global) into a swizzled LDS tile; every
-// wave issues kDmaPerWave instructions.  Completion: s_waitcnt vmcnt + barrier.
-template <typename T>
+// DMA of one row-major 64 x 64 matrix (global) into a swizzled LDS tile; each
+// of the NW waves of the workgroup issues an equal share of the 1 KiB
+// instructions.  Completion: s_waitcnt vmcnt + barrier.
+template <typename T, int NW = kWaves>
 __device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds) {
   typedef Swz<T> S;
+  constexpr int kPerWave = S::kBytes / 1024 / NW;
+  static_assert(kPerWave * NW * 1024 == S::kBytes, "equal DMA share per wave");
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
-  for (int m = 0; m < S::kDmaPerWave; ++m) {
-    const int blk = w * S::kDmaPerWave + m;
+  for (int m = 0; m < kPerWave; ++m) {
+    const int blk = w * kPerWave + m;
     const int P = blk * 64 + lane;                 // physical chunk index
     const int r = P / S::kCpr, pc = P % S::kCpr;
     const int c = pc ^ (r & (S::kCpr - 1));        // logical chunk stored there
