@@ -84,9 +84,11 @@ struct Tile {
 
 // token blocks in LDS
 enum { bDO = 0, bU, bUR, bDX, bDY, bDYR, kNumTokBlk };
-// per-token sums (LDS, fp32, one set per wave): direct gate terms of
-// g_t, g_{t-1}, h_t, beta, gamma; row / column sums of the Z matrices
-enum { sGS = 0, sGSP, sGR, sB, sGM, sZRS, sZCS, sZRP, sZCP, sZRR, sZCR, kNumSums };
+// per-token sums (LDS, fp32, one set per wave, each entry written once so
+// that plain stores suffice): direct gate terms of g_t, g_{t-1}, h_t, beta,
+// gamma from the F contractions; row / column sums of the Z matrices and the
+// beta / gamma terms of the decay-matrix products
+enum { sGS = 0, sGSP, sGR, sB, sGM, sZRS, sZCS, sZRP, sZCP, sZRR, sZCR, sZB, sZGM, kNumSums };
 
 template <typename IN, int DK, int DV>
 struct GradLayout {
@@ -113,7 +115,8 @@ struct GradLayout {
   static constexpr int kGates = kBlkEnd > kOvlEnd ? kBlkEnd : kOvlEnd;
   static constexpr int kNumGateArrays = 11;
   static constexpr int kSums = kGates + kNumGateArrays * kChunk * 4;
-  static constexpr int kRed = kSums + kNW * kNumSums * kChunk * 4;   // per-wave sums
+  static constexpr int kElem = kSums + kNW * kNumSums * kChunk * 4;  // per-wave sums
+  static constexpr int kRed = kElem + 2 * kChunk * 4;   // elementwise beta / gamma sums
   static constexpr int kBytes = kRed + 16 * 4;
   static_assert(kBytes <= 160 * 1024, "gradient kernel LDS");
 };
@@ -125,25 +128,20 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-// Per-wave per-token sums in LDS, updated branch-free: all lanes that hold
-// the same sum write the same value to the same address.
+// Per-wave per-token sums in LDS, written branch-free: all lanes that hold
+// the same sum store the same value to the same address.
 // Row sums of a tile quantity (lane: rows 4*(lane>>4)+r) into dst[t0 + row].
-__device__ __forceinline__ void acc_rows(float* dst, int t0, const float (&v)[4]) {
+__device__ __forceinline__ void put_rows(float* dst, int t0, const float (&v)[4]) {
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float s = group_sum<16>(v[r]);
-    float* a = dst + t0 + acc_row(r);
-    *a = *a + s;
-  }
+  for (int r = 0; r < 4; ++r) dst[t0 + acc_row(r)] = group_sum<16>(v[r]);
 }
 
 // Column sums of a tile quantity (lane: column lane & 15) into dst[s0 + column].
-__device__ __forceinline__ void acc_cols(float* dst, int s0, const float (&v)[4]) {
+__device__ __forceinline__ void put_cols(float* dst, int s0, const float (&v)[4]) {
   float s = v[0] + v[1] + v[2] + v[3];
   s += __shfl_xor(s, 16, 64);
   s += __shfl_xor(s, 32, 64);
-  float* a = dst + s0 + (threadIdx.x & 15);
-  *a = *a + s;
+  dst[s0 + (threadIdx.x & 15)] = s;
 }
 
 template <typename IN, int DK, int DV, bool RDN, typename OT>
@@ -183,6 +181,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   float* grv = gspv + kChunk;   // h_t
   float* edge = grv + kChunk;   // e^{g_C}, e^{h_C}
   float* sums = reinterpret_cast<float*>(smem + L::kSums);   // [wave][kNumSums][64]
+  float* esum = reinterpret_cast<float*>(smem + L::kElem);   // [2][64]: dY.V, dYR.r
   float* red = reinterpret_cast<float*>(smem + L::kRed);
 
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
@@ -208,6 +207,38 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   const int64_t soff = ((int64_t)c * H + h) * DK * DV;
 
   // ---------------- phase 0: staging ----------------
+  // A state's rows i0 .. i0+15 as MFMA B fragments (row = lane & 15), with
+  // the power-of-two scale of each (row, 32-column k-step) for fp16 states.
+  struct StateRows {
+    Frag fr[KSV];
+    float sc[KSV];
+  };
+  const void* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
+  const float* scs[4] = {p.ck_S_sc, p.ck_R_sc, p.dS_sc, p.dR_sc};
+  const int64_t sco = ((int64_t)c * H + h) * DK * (DV / 32);
+  auto load_rows = [&](StateRows& x, int st, int i0) {
+    const int i = i0 + (lane & 15);
+    if constexpr (BF) {
+      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * DV;
+      const float* scp = scs[st] + sco + (int64_t)i * (DV / 32);
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) {
+        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + ks * M::kStep + 8 * (lane >> 4));
+        x.sc[ks] = scp[ks];
+      }
+    } else {
+      const float* rowp = reinterpret_cast<const float*>(srcs[st]) + soff + (int64_t)i * DV;
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) {
+        x.fr[ks] = rowp[ks * M::kStep + (lane >> 4)];
+        x.sc[ks] = 1.f;
+      }
+    }
+  };
+  // the first state rows stream in while the chunk's blocks are staged
+  StateRows rowA, rowB;
+  load_rows(rowA, 0, 16 * w);
+  load_rows(rowB, 2, 16 * w);
   TV::template dma64<NW>(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
   TV::template dma64<NW>(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
   TV::template dma64<NW>(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
@@ -309,8 +340,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       }
       s1 = group_sum<kPerRow>(s1);
       s2 = group_sum<kPerRow>(s2);
-      sum_row(sB)[t] += s1;
-      sum_row(sGM)[t] += s2;
+      esum[t] = s1;
+      esum[kChunk + t] = s2;
     }
   }
 
@@ -322,34 +353,6 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     for (int tt = 0; tt < 4; ++tt) { dQ[m][tt] = zero4(); dK[m][tt] = zero4(); }
   float gsC = 0.f, grC = 0.f;
 
-  // A state's rows i0 .. i0+15 as MFMA B fragments (row = lane & 15), with
-  // the power-of-two scale of each (row, 32-column k-step) for fp16 states.
-  struct StateRows {
-    Frag fr[KSV];
-    float sc[KSV];
-  };
-  const void* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
-  const float* scs[4] = {p.ck_S_sc, p.ck_R_sc, p.dS_sc, p.dR_sc};
-  const int64_t sco = ((int64_t)c * H + h) * DK * (DV / 32);
-  auto load_rows = [&](StateRows& x, int st, int i0) {
-    const int i = i0 + (lane & 15);
-    if constexpr (BF) {
-      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * DV;
-      const float* scp = scs[st] + sco + (int64_t)i * (DV / 32);
-#pragma unroll
-      for (int ks = 0; ks < KSV; ++ks) {
-        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + ks * M::kStep + 8 * (lane >> 4));
-        x.sc[ks] = scp[ks];
-      }
-    } else {
-      const float* rowp = reinterpret_cast<const float*>(srcs[st]) + soff + (int64_t)i * DV;
-#pragma unroll
-      for (int ks = 0; ks < KSV; ++ks) {
-        x.fr[ks] = rowp[ks * M::kStep + (lane >> 4)];
-        x.sc[ks] = 1.f;
-      }
-    }
-  };
   // sum over this lane's elements of a (.) b
   auto frag_dot = [&](const StateRows& a, const StateRows& b) {
     float s = 0.f;
@@ -381,9 +384,6 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 
   // per d_k tile: S0 with dS1, then R0 with dR1; the next pair's rows are
   // loaded while the current pair's products run
-  StateRows rowA, rowB;
-  load_rows(rowA, 0, 16 * w);
-  load_rows(rowB, 2, 16 * w);
 #pragma unroll
   for (int m = 0; m < kIT; ++m) {
     // the token-block fragments are reloaded per d_k tile: keeping them
@@ -433,9 +433,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
             ab[r] = kq[r] * e2;
           }
         }
-        acc_rows(sum_row(sGS), 16 * tt, ags);
-        acc_rows(sum_row(sGSP), 16 * tt, agsp);
-        if constexpr (RDN) acc_rows(sum_row(sB), 16 * tt, ab);
+        put_rows(sum_row(sGS), 16 * tt, ags);
+        put_rows(sum_row(sGSP), 16 * tt, agsp);
+        if constexpr (RDN) put_rows(sum_row(sB), 16 * tt, ab);
       }
     }
     // ---- R0 (rowA) and dR1 (rowB) ----
@@ -472,8 +472,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
             agm[r] += kq[r] * e5;
           }
         }
-        acc_rows(sum_row(sGR), 16 * tt, agr);
-        acc_rows(sum_row(sGM), 16 * tt, agm);
+        put_rows(sum_row(sGR), 16 * tt, agr);
+        put_rows(sum_row(sGM), 16 * tt, agm);
       }
     }
   }
@@ -561,14 +561,14 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
           dGm[t * ldp + t] = from_f<XT>(0.f);
         }
       }
-      acc_rows(sum_row(sZRS), 16 * tt, zs);
-      acc_rows(sum_row(sZRP), 16 * tt, zp);
-      acc_rows(sum_row(sZRR), 16 * tt, zr);
-      acc_rows(sum_row(sB), 16 * tt, zb);
-      acc_rows(sum_row(sGM), 16 * tt, zg);
-      acc_cols(sum_row(sZCS), 16 * st, zs);
-      acc_cols(sum_row(sZCP), 16 * st, zp);
-      acc_cols(sum_row(sZCR), 16 * st, zr);
+      put_rows(sum_row(sZRS), 16 * tt, zs);
+      put_rows(sum_row(sZRP), 16 * tt, zp);
+      put_rows(sum_row(sZRR), 16 * tt, zr);
+      put_rows(sum_row(sZB), 16 * tt, zb);
+      put_rows(sum_row(sZGM), 16 * tt, zg);
+      put_cols(sum_row(sZCS), 16 * st, zs);
+      put_cols(sum_row(sZCP), 16 * st, zp);
+      put_cols(sum_row(sZCR), 16 * st, zr);
     }
   }
   // dP above the diagonal and dP^T below it are zero: the 6 upper tiles
@@ -620,8 +620,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       const float as = p.alpha_s[gi], ar = p.alpha_r[gi];
       p.dalpha_s[gi] = as >= 1.17549435e-38f ? ss / as : 0.f;
       p.dalpha_r[gi] = ar >= 1.17549435e-38f ? sr / ar : 0.f;
-      p.dbeta[gi] = total(sB, t);
-      p.dgamma[gi] = total(sGM, t);
+      p.dbeta[gi] = esum[t] + total(sB, t) + total(sZB, t);
+      p.dgamma[gi] = esum[kChunk + t] + total(sGM, t) + total(sZGM, t);
     }
   }
 #pragma unroll
