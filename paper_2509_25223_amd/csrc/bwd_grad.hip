@@ -345,6 +345,87 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     }
   }
 
+  // ---------------- phase 2: W, G, P on the lower token tiles ----------------
+  constexpr int kMyTiles = (10 + NW - 1) / NW;   // share of the 10 lower tiles per wave
+  floatx4 tW1[kMyTiles], tW2[kMyTiles], tW3[kMyTiles], tW4[kMyTiles], tW5[kMyTiles];
+  floatx4 tG[kMyTiles], tP[kMyTiles];
+  auto tile_of = [](int idx, int& tt, int& st) {   // lower tiles, row by row
+    tt = idx >= 6 ? 3 : idx >= 3 ? 2 : idx >= 1 ? 1 : 0;
+    st = idx - (tt * (tt + 1)) / 2;
+  };
+#pragma unroll
+  for (int x = 0; x < kMyTiles; ++x) {
+    asm volatile("" ::: "memory");
+    const int idx = w + NW * x;
+    tW1[x] = zero4(); tW2[x] = zero4(); tW3[x] = zero4(); tW4[x] = zero4(); tW5[x] = zero4();
+    tG[x] = zero4(); tP[x] = zero4();
+    if (idx < 10) {
+      int tt, st;
+      tile_of(idx, tt, st);
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) {
+        const int k0 = ks * M::kStep;
+        const Frag fo = TV::template frag<M>(tokblk(bDO), 16 * tt, k0);
+        const Frag fx = TV::template frag<M>(tokblk(bDX), 16 * tt, k0);
+        const Frag fu = TV::template frag<M>(tokblk(bU), 16 * st, k0);
+        const Frag fur = TV::template frag<M>(tokblk(bUR), 16 * st, k0);
+        tW1[x] = M::mma(fo, fu, tW1[x]);
+        tW2[x] = M::mma(fo, fur, tW2[x]);
+        tW3[x] = M::mma(fx, fu, tW3[x]);
+        if constexpr (RDN) {
+          tW4[x] = M::mma(TV::template frag<M>(tokblk(bDY), 16 * tt, k0), fu, tW4[x]);
+          tW5[x] = M::mma(TV::template frag<M>(tokblk(bDYR), 16 * tt, k0), fur, tW5[x]);
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KSK; ++ks) {
+        const int k0 = ks * M::kStep;
+        const Frag fk = TK::template frag<M>(Kl, 16 * st, k0);
+        tG[x] = M::mma(TK::template frag<M>(Kl, 16 * tt, k0), fk, tG[x]);
+        tP[x] = M::mma(TK::template frag<M>(Ql, 16 * tt, k0), fk, tP[x]);
+      }
+    }
+  }
+  // ---- dP, dG (into registers) and the sums over the decay-matrix products ----
+  float edp[kMyTiles][4], edg[kMyTiles][4];
+#pragma unroll
+  for (int x = 0; x < kMyTiles; ++x) {
+    const int idx = w + NW * x;
+    if (idx < 10) {
+      int tt, st;
+      tile_of(idx, tt, st);
+      float zs[4], zp[4], zr[4], zb[4], zg[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
+        const bool lower = s < t, diag = s <= t;
+        const float es = __expf(fminf(gsv[t] - gsv[s], 0.f));
+        const float ep = __expf(fminf(gspv[t] - gsv[s], 0.f));
+        const float er = __expf(fminf(grv[t] - grv[s], 0.f));
+        const float W1 = tW1[x][r], W2 = tW2[x][r], W3 = tW3[x][r];
+        const float G = tG[x][r], P = tP[x][r];
+        const float dAs = RDN ? -tW4[x][r] : 0.f, dAr = RDN ? -tW5[x][r] : 0.f;
+        const float gw2 = ggm[t] * W2;
+        const float dp = (lower ? es * W1 : 0.f) + (diag ? er * gw2 : 0.f);
+        const float dg = lower ? (-ep * W3 + gbt[t] * es * dAs + ggm[t] * er * dAr) : 0.f;
+        zs[r] = lower ? es * (P * W1 + gbt[t] * G * dAs) : 0.f;
+        zp[r] = lower ? -ep * G * W3 : 0.f;
+        zr[r] = (diag ? er * P * gw2 : 0.f) + (lower ? ggm[t] * er * G * dAr : 0.f);
+        zb[r] = lower ? dAs * es * G : 0.f;
+        zg[r] = (lower ? dAr * er * G : 0.f) + (diag ? er * P * W2 : 0.f);
+        edp[x][r] = dp;
+        edg[x][r] = dg;
+      }
+      put_rows(sum_row(sZRS), 16 * tt, zs);
+      put_rows(sum_row(sZRP), 16 * tt, zp);
+      put_rows(sum_row(sZRR), 16 * tt, zr);
+      put_rows(sum_row(sZB), 16 * tt, zb);
+      put_rows(sum_row(sZGM), 16 * tt, zg);
+      put_cols(sum_row(sZCS), 16 * st, zs);
+      put_cols(sum_row(sZCP), 16 * st, zp);
+      put_cols(sum_row(sZCR), 16 * st, zr);
+    }
+  }
   // ---------------- phase 1: contractions over the value dimension ----------------
   floatx4 dQ[kIT][4], dK[kIT][4];
 #pragma unroll
@@ -482,50 +563,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     if (lane == 0) { red[w] = a; red[NW + w] = b; }
   }
 
-  // ---------------- phase 2: W, G, P on the lower token tiles ----------------
-  constexpr int kMyTiles = (10 + NW - 1) / NW;   // share of the 10 lower tiles per wave
-  floatx4 tW1[kMyTiles], tW2[kMyTiles], tW3[kMyTiles], tW4[kMyTiles], tW5[kMyTiles];
-  floatx4 tG[kMyTiles], tP[kMyTiles];
-  auto tile_of = [](int idx, int& tt, int& st) {   // lower tiles, row by row
-    tt = idx >= 6 ? 3 : idx >= 3 ? 2 : idx >= 1 ? 1 : 0;
-    st = idx - (tt * (tt + 1)) / 2;
-  };
-#pragma unroll
-  for (int x = 0; x < kMyTiles; ++x) {
-    asm volatile("" ::: "memory");
-    const int idx = w + NW * x;
-    tW1[x] = zero4(); tW2[x] = zero4(); tW3[x] = zero4(); tW4[x] = zero4(); tW5[x] = zero4();
-    tG[x] = zero4(); tP[x] = zero4();
-    if (idx < 10) {
-      int tt, st;
-      tile_of(idx, tt, st);
-#pragma unroll
-      for (int ks = 0; ks < KSV; ++ks) {
-        const int k0 = ks * M::kStep;
-        const Frag fo = TV::template frag<M>(tokblk(bDO), 16 * tt, k0);
-        const Frag fx = TV::template frag<M>(tokblk(bDX), 16 * tt, k0);
-        const Frag fu = TV::template frag<M>(tokblk(bU), 16 * st, k0);
-        const Frag fur = TV::template frag<M>(tokblk(bUR), 16 * st, k0);
-        tW1[x] = M::mma(fo, fu, tW1[x]);
-        tW2[x] = M::mma(fo, fur, tW2[x]);
-        tW3[x] = M::mma(fx, fu, tW3[x]);
-        if constexpr (RDN) {
-          tW4[x] = M::mma(TV::template frag<M>(tokblk(bDY), 16 * tt, k0), fu, tW4[x]);
-          tW5[x] = M::mma(TV::template frag<M>(tokblk(bDYR), 16 * tt, k0), fur, tW5[x]);
-        }
-      }
-#pragma unroll
-      for (int ks = 0; ks < KSK; ++ks) {
-        const int k0 = ks * M::kStep;
-        const Frag fk = TK::template frag<M>(Kl, 16 * st, k0);
-        tG[x] = M::mma(TK::template frag<M>(Kl, 16 * tt, k0), fk, tG[x]);
-        tP[x] = M::mma(TK::template frag<M>(Ql, 16 * tt, k0), fk, tP[x]);
-      }
-    }
-  }
   barrier_lds();   // token blocks dead: their region becomes dP, dP^T, dG + dG^T, K^T, Q^T
 
-  // ---- dP, dG and the sums over the decay-matrix products ----
+  // ---- dP, dP^T and dG + dG^T (kept in registers since the decay step) ----
   constexpr int ldp = L::kLdP;
 #pragma unroll
   for (int x = 0; x < kMyTiles; ++x) {
@@ -533,42 +573,18 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     if (idx < 10) {
       int tt, st;
       tile_of(idx, tt, st);
-      float zs[4], zp[4], zr[4], zb[4], zg[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
-        const bool lower = s < t, diag = s <= t;
-        const float es = __expf(fminf(gsv[t] - gsv[s], 0.f));
-        const float ep = __expf(fminf(gspv[t] - gsv[s], 0.f));
-        const float er = __expf(fminf(grv[t] - grv[s], 0.f));
-        const float W1 = tW1[x][r], W2 = tW2[x][r], W3 = tW3[x][r];
-        const float G = tG[x][r], P = tP[x][r];
-        const float dAs = RDN ? -tW4[x][r] : 0.f, dAr = RDN ? -tW5[x][r] : 0.f;
-        const float gw2 = ggm[t] * W2;
-        const float dp = (lower ? es * W1 : 0.f) + (diag ? er * gw2 : 0.f);
-        const float dg = lower ? (-ep * W3 + gbt[t] * es * dAs + ggm[t] * er * dAr) : 0.f;
-        zs[r] = lower ? es * (P * W1 + gbt[t] * G * dAs) : 0.f;
-        zp[r] = lower ? -ep * G * W3 : 0.f;
-        zr[r] = (diag ? er * P * gw2 : 0.f) + (lower ? ggm[t] * er * G * dAr : 0.f);
-        zb[r] = lower ? dAs * es * G : 0.f;
-        zg[r] = (lower ? dAr * er * G : 0.f) + (diag ? er * P * W2 : 0.f);
-        dPm[t * ldp + s] = from_f<XT>(dp);
-        dPTm[s * ldp + t] = from_f<XT>(dp);
-        if (lower) {   // dG + dG^T: the two halves have disjoint supports
-          dGm[t * ldp + s] = from_f<XT>(dg);
-          dGm[s * ldp + t] = from_f<XT>(dg);
+        dPm[t * ldp + s] = from_f<XT>(edp[x][r]);
+        dPTm[s * ldp + t] = from_f<XT>(edp[x][r]);
+        if (s < t) {   // dG + dG^T: the two halves have disjoint supports
+          dGm[t * ldp + s] = from_f<XT>(edg[x][r]);
+          dGm[s * ldp + t] = from_f<XT>(edg[x][r]);
         } else if (s == t) {
           dGm[t * ldp + t] = from_f<XT>(0.f);
         }
       }
-      put_rows(sum_row(sZRS), 16 * tt, zs);
-      put_rows(sum_row(sZRP), 16 * tt, zp);
-      put_rows(sum_row(sZRR), 16 * tt, zr);
-      put_rows(sum_row(sZB), 16 * tt, zb);
-      put_rows(sum_row(sZGM), 16 * tt, zg);
-      put_cols(sum_row(sZCS), 16 * st, zs);
-      put_cols(sum_row(sZCP), 16 * st, zp);
-      put_cols(sum_row(sZCR), 16 * st, zr);
     }
   }
   // dP above the diagonal and dP^T below it are zero: the 6 upper tiles
