@@ -174,7 +174,9 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   //   T^R, mask: after P3;  MG, MP: after P4;  T^S: after P5 (their last uses)
   // bf16 inputs; fp32 inputs single-buffer every matrix and move them all
   // after the chunk's last barrier.
-  constexpr int kOPerThread = kChunk * BV / kThreads;
+  // dO block: one 16-byte vector per thread, token = lane, columns of wave w
+  constexpr int kOPerThread = 16 / (int)sizeof(IN);
+  static_assert(kChunk * BV == kThreads * kOPerThread, "one dO vector per thread");
   typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];
   IN on[kOPerThread];
   auto chunk_len = [&](int c) { return min(kChunk, si.len - c * kChunk); };
@@ -188,10 +190,13 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
     load_rowfrags<IN, DK>(Kn, t < len ? kg + roff : nullptr);
     load_rowfrags<IN, DK>(Qn, t < len ? qg + roff : nullptr);
+    {
+      typedef IN INV __attribute__((ext_vector_type(kOPerThread)));
+      const int tt = lane, j = w * kOPerThread;
+      INV v = {};
+      if (tt < len) v = *reinterpret_cast<const INV*>(dog + ((tok + tt) * H + h) * (int64_t)DV + j0 + j);
 #pragma unroll
-    for (int u = 0; u < kOPerThread; ++u) {
-      const int e = tid + u * kThreads, tt = e / BV, j = e % BV;
-      on[u] = tt < len ? dog[((tok + tt) * H + h) * (int64_t)DV + j0 + j] : from_f<IN>(0.f);
+      for (int u = 0; u < kOPerThread; ++u) on[u] = v[u];
     }
   };
   auto issue_gates = [&](int c) {
@@ -303,10 +308,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       }
       XT* dbT = blk(bDB_DKS);
 #pragma unroll
-      for (int u = 0; u < kOPerThread; ++u) {
-        const int e = tid + u * kThreads, tt = e / BV, j = e % BV;
-        dbT[j * L::kLdX + tt] = from_f<XT>(to_f<IN>(on[u]));
-      }
+      for (int u = 0; u < kOPerThread; ++u)   // lanes write consecutive tokens
+        dbT[(w * kOPerThread + u) * L::kLdX + lane] = from_f<XT>(to_f<IN>(on[u]));
       if (tid < kChunk) {
         const int tt = tid;
         const float gs = graw[tt], gsp = tt > 0 ? graw[tt - 1] : 0.f, gsl = graw[kChunk - 1];
@@ -352,47 +355,18 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       store_acc_t<XT>(blk(bQDB) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdb);
       store_acc_t<XT>(blk(bQDC) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdc);
     }
-    // gradient w.r.t. this chunk's end states for the gradient kernel, read
-    // back from the state copies (rows i of [BV][DK]) and written row-major in
-    // 16-byte vectors; bf16 inputs: fp16 scaled per (row, 32 columns)
+    // gradient w.r.t. this chunk's end states for the gradient kernel,
+    // straight from the accumulators (bf16 inputs: fp16 scaled per (row, 32
+    // columns))
     {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
-      constexpr int kVE = BF ? 8 : 4;            // elements per vector
-      constexpr int kVPR = BV / kVE;             // vectors per state row
-      constexpr int kItems = DK * kVPR / kThreads;
-#pragma unroll
-      for (int sidx = 0; sidx < 2; ++sidx) {
-        const IN* hi = sidx == 0 ? dShi : dRhi;
-        const IN* lo = sidx == 0 ? dSlo : dRlo;
-#pragma unroll
-        for (int u = 0; u < kItems; ++u) {
-          const int e = tid + u * kThreads, i = e / kVPR, v = e % kVPR;
-          float x[kVE];
-#pragma unroll
-          for (int k = 0; k < kVE; ++k) {
-            const int o2 = (v * kVE + k) * L::kLdS + i;
-            x[k] = to_f<IN>(hi[o2]);
-            if constexpr (BF) x[k] += to_f<IN>(lo[o2]);
-          }
-          if constexpr (BF) {
-            static_assert(kVPR == 4, "one 32-column scale block = 4 lanes");
-            float mx = 0.f;
-#pragma unroll
-            for (int k = 0; k < kVE; ++k) mx = fmaxf(mx, fabsf(x[k]));
-            const float sc = pow2_scale(group_max<4>(mx)), inv = 1.f / sc;
-            f16x8 hv;
-#pragma unroll
-            for (int k = 0; k < kVE; ++k) hv[k] = to_f16(x[k] * inv);
-            f16* dst = reinterpret_cast<f16*>(sidx == 0 ? p.dS_ws : p.dR_ws);
-            *reinterpret_cast<f16x8*>(dst + off + (int64_t)i * DV + v * kVE) = hv;
-            float* scd = sidx == 0 ? p.dS_sc : p.dR_sc;
-            scd[((int64_t)gc * H + h) * DK * (DV / 32) + (int64_t)i * (DV / 32) + j0 / 32] = sc;
-          } else {
-            float* dst = reinterpret_cast<float*>(sidx == 0 ? p.dS_ws : p.dR_ws);
-            *reinterpret_cast<float4*>(dst + off + (int64_t)i * DV + v * kVE) =
-                float4{x[0], x[1], x[2], x[3]};
-          }
-        }
+      if constexpr (BF) {
+        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
+        save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + off, DV, p.dS_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + off, DV, p.dR_sc + so, DV / 32, w * (DK / 4));
+      } else {
+        save_state_f32<IT, JT>(dS, reinterpret_cast<float*>(p.dS_ws) + off, DV, w * (DK / 4));
+        save_state_f32<IT, JT>(dR, reinterpret_cast<float*>(p.dR_ws) + off, DV, w * (DK / 4));
       }
     }
 
@@ -509,7 +483,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       constexpr int kVE = 16 / (int)sizeof(XT);
       constexpr int kVPR = BV / kVE;
       static_assert(kChunk * kVPR == kThreads, "one block vector per thread");
-      const int t = tid / kVPR, v = tid % kVPR;
+      const int t = lane, v = w;   // lanes read consecutive tokens: no bank conflicts
 #pragma unroll
       for (int b = 0; b < 3; ++b) {
         const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;

@@ -19,6 +19,7 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef u16 u16x4 __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef u16 u16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ float bf2f(u16 x) { return __uint_as_float(((uint32_t)x) << 16); }
@@ -203,18 +204,24 @@ __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f};
 // ---------------------------------------------------------------------------
 // 64 x 64 matrices staged in LDS by LDS-DMA (global_load_lds_dwordx4): the
 // hardware writes lane i's 16 bytes at base + 16 i, so a tile is stored
-// unpadded, and the 16-byte chunks of row r are XOR-swizzled with r so that
-// 16 rows read at the same column hit distinct banks.
-//   logical (row r, chunk c) -> physical byte r * kRowB + ((c ^ (r & (kCpr-1))) << 4)
+// unpadded, and the 16-byte chunks of row r are XOR-swizzled with sw(r):
+//   logical (row r, chunk c) -> physical byte r * kRowB + ((c ^ sw(r)) << 4)
+// For 2-byte elements sw(r) = (r & 7) ^ ((r >> 2) & 6): 8 consecutive rows
+// read at one column (row fragments) hit 8 distinct chunks, and so do the
+// column gathers of transposed fragments, whose lane groups read rows 8 apart
+// (the second term separates those).  Wider elements: sw(r) = r mod chunks.
 // ---------------------------------------------------------------------------
 template <typename T> struct Swz {
   static constexpr int kRowB = kChunk * (int)sizeof(T);   // bytes per row
   static constexpr int kCpr = kRowB / 16;                 // 16-byte chunks per row
   static constexpr int kBytes = kChunk * kRowB;
   static constexpr int kDmaPerWave = kBytes / 1024 / kWaves;   // 1 KiB per instruction
+  __device__ __forceinline__ static int sw(int r) {
+    return kCpr == 8 ? (r & 7) ^ ((r >> 2) & 6) : r & (kCpr - 1);
+  }
   __device__ __forceinline__ static int off(int r, int col) {   // byte offset of element
     const int c = (col * (int)sizeof(T)) >> 4, inside = (col * (int)sizeof(T)) & 15;
-    return r * kRowB + ((c ^ (r & (kCpr - 1))) << 4) + inside;
+    return r * kRowB + ((c ^ sw(r)) << 4) + inside;
   }
 };
 
@@ -240,7 +247,7 @@ __device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds) {
     const int blk = w * kPerWave + m;
     const int P = blk * 64 + lane;                 // physical chunk index
     const int r = P / S::kCpr, pc = P % S::kCpr;
-    const int c = pc ^ (r & (S::kCpr - 1));        // logical chunk stored there
+    const int c = pc ^ S::sw(r);                   // logical chunk stored there
     const char* src = reinterpret_cast<const char*>(gsrc) + r * S::kRowB + c * 16;
     dma16(src, reinterpret_cast<char*>(lds) + blk * 1024);
   }
@@ -350,17 +357,109 @@ __device__ __forceinline__ float group_max(float x) {
   return x;
 }
 
-// Power-of-two scale s for a block of values with largest magnitude mx:
-// mx / s lies in [2^13, 2^14), so the block stored as fp16 (x / s) keeps
-// fp16's full relative precision for its largest entries and cannot overflow.
-// Blocks of zeros (or non-finite maxima) get s = 1.
-__device__ __forceinline__ float pow2_scale(float mx) {
-  if (!(mx > 0.f) || !(mx < __builtin_inff())) return 1.f;
-  int e;
-  frexpf(mx, &e);   // mx in [2^(e-1), 2^e)
-  e = e - 14;
-  e = e < -126 ? -126 : e > 127 ? 127 : e;
-  return ldexpf(1.f, e);
+// Power-of-two scale 2^e for a block of values whose largest magnitude has
+// the fp32 bit pattern mbits: e = (biased exponent) - 140, so that the largest
+// magnitude over 2^e lies in [2^13, 2^14) and the block stored as fp16 keeps
+// fp16's full relative precision for its largest entries without overflow.
+// e is at least -126; blocks of zeros (or subnormals only) get e = 0.
+__device__ __forceinline__ int pow2_scale_exp(uint32_t mbits) {
+  const int be = (int)(mbits >> 23);
+  return be == 0 ? 0 : max(be - 140, -126);
+}
+__device__ __forceinline__ float exp2_int(int e) {   // 2^e, -126 <= e <= 127
+  return __uint_as_float((uint32_t)(e + 127) << 23);
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+
+// Largest |x| over a 16-lane row, as an fp32 bit pattern (unsigned compares
+// of the magnitude bits, which fold into DPP max instructions).
+__device__ __forceinline__ uint32_t row16_absmax_bits(float a, float b) {
+  uint32_t m = max(__float_as_uint(a) & 0x7FFFFFFFu, __float_as_uint(b) & 0x7FFFFFFFu);
+  m = max(m, dpp_u32<0xB1>(m));
+  m = max(m, dpp_u32<0x4E>(m));
+  m = max(m, dpp_u32<0x141>(m));
+  return max(m, dpp_u32<0x140>(m));
+}
+
+__device__ __forceinline__ uint32_t cvt_pk_f16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, f16x2{to_f16(a), to_f16(b)});
+}
+
+// Saves one 32-column block of a state held in MFMA accumulators: tile
+// acc[it][jt] holds rows row0 + 16 it + acc_row(r) and columns
+// 16 jt + acc_col().  Each row is divided by its power-of-two scale
+// (pow2_scale_exp of the row's largest magnitude), stored as fp16 row-major
+// (row stride ld), and the scale goes to sc[row * sc_ld].  Two DPP exchanges
+// inside lane quads turn a lane's 4 rows x 1 column into 1 row x 4 columns,
+// so the rows leave in 8-byte stores.  Branch-free (lanes holding the same
+// row store its scale alike), so it can interleave with matrix work.
+template <int IT>
+__device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16* dst, int64_t ld,
+                                               float* sc, int64_t sc_ld, int row0) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const int c = threadIdx.x & 15, q = (threadIdx.x & 63) >> 4;
+  const bool odd = c & 1, upper = c & 2;
+  const int rho = ((c & 1) << 1) | ((c >> 1) & 1);   // row of the quad this lane stores
+  // v_perm byte selectors over {recv:keep}: even lanes (keep, recv), odd (recv, keep)
+  const uint32_t selA = odd ? 0x01000504u : 0x05040100u;
+  const uint32_t selB = odd ? 0x03020706u : 0x07060302u;
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    int e[4];
+    float inv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      e[r] = pow2_scale_exp(row16_absmax_bits(acc[it][0][r], acc[it][1][r]));
+      inv[r] = exp2_int(-e[r]);
+    }
+    const int64_t row = row0 + 16 * it + 4 * q + rho;
+#pragma unroll
+    for (int jt = 0; jt < 2; ++jt) {
+      const uint32_t p01 = cvt_pk_f16(acc[it][jt][0] * inv[0], acc[it][jt][1] * inv[1]);
+      const uint32_t p23 = cvt_pk_f16(acc[it][jt][2] * inv[2], acc[it][jt][3] * inv[3]);
+      // round 1, lanes c and c^1: even lanes end with rows 0, 1 and odd
+      // lanes with rows 2, 3, each as a column pair
+      const uint32_t keep = odd ? p23 : p01;
+      const uint32_t recv = dpp_u32<0xB1>(odd ? p01 : p23);
+      const uint32_t a = __builtin_amdgcn_perm(recv, keep, selA);
+      const uint32_t b = __builtin_amdgcn_perm(recv, keep, selB);
+      // round 2, lanes c and c^2: each lane ends with one row, 4 columns
+      const uint32_t recv2 = dpp_u32<0x4E>(upper ? a : b);
+      const u32x2 out = upper ? u32x2{recv2, b} : u32x2{a, recv2};
+      *reinterpret_cast<u32x2*>(dst + row * ld + 16 * jt + (c & ~3)) = out;
+    }
+    const int er = odd ? (upper ? e[3] : e[2]) : (upper ? e[1] : e[0]);   // e[rho]
+    sc[row * sc_ld] = exp2_int(er);
+  }
+}
+
+// Scheduling hint for the enclosing basic block: alternate one LDS read, two
+// MFMAs and VALU_PER vector instructions, NMFMA / 2 times.
+template <int NMFMA, int VALU_PER>
+__device__ __forceinline__ void interleave_mfma_valu() {
+#pragma unroll
+  for (int i = 0; i < NMFMA / 2; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);        // DS read
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);        // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, VALU_PER, 0); // VALU
+  }
+}
+
+// fp32 counterpart of save_state_f16 (no scales): dst[row * ld + col].
+template <int IT, int JT>
+__device__ __forceinline__ void save_state_f32(const floatx4 (&acc)[IT][JT], float* dst, int64_t ld,
+                                               int row0) {
+#pragma unroll
+  for (int it = 0; it < IT; ++it)
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        dst[(int64_t)(row0 + 16 * it + acc_row(r)) * ld + 16 * jt + acc_col()] = acc[it][jt][r];
 }
 
 // Stores the 4 accumulator rows of this lane, column-major into LDS as a

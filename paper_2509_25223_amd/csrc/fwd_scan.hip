@@ -298,48 +298,21 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         mma_rega<IN, DK, true>(QR[jt], Qf, Rlo + o, L::kLdS);
       }
     }
-    // chunk-start states for the gradient kernel, read back from the state
-    // copies (rows i of [BV][DK]) and written row-major in 16-byte vectors;
-    // bf16 inputs: fp16 scaled by a power of two per (row, 32 columns)
+    // chunk-start states for the gradient kernel, straight from the
+    // accumulators (bf16 inputs: fp16 scaled per (row, 32 columns))
     if constexpr (CKPT) {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
-      constexpr int kVE = BF ? 8 : 4;            // elements per vector
-      constexpr int kVPR = BV / kVE;             // vectors per state row
-      constexpr int kItems = DK * kVPR / kThreads;
-#pragma unroll
-      for (int sidx = 0; sidx < 2; ++sidx) {
-        const IN* hi = sidx == 0 ? Shi : Rhi;
-        const IN* lo = sidx == 0 ? Slo : Rlo;
-#pragma unroll
-        for (int u = 0; u < kItems; ++u) {
-          const int e = tid + u * kThreads, i = e / kVPR, v = e % kVPR;
-          float x[kVE];
-#pragma unroll
-          for (int k = 0; k < kVE; ++k) {
-            const int o2 = (v * kVE + k) * L::kLdS + i;
-            x[k] = to_f<IN>(hi[o2]);
-            if constexpr (BF) x[k] += to_f<IN>(lo[o2]);
-          }
-          if constexpr (BF) {
-            static_assert(kVPR == 4, "one 32-column scale block = 4 lanes");
-            float mx = 0.f;
-#pragma unroll
-            for (int k = 0; k < kVE; ++k) mx = fmaxf(mx, fabsf(x[k]));
-            const float sc = pow2_scale(group_max<4>(mx)), inv = 1.f / sc;
-            f16x8 hv;
-#pragma unroll
-            for (int k = 0; k < kVE; ++k) hv[k] = (f16)(x[k] * inv);
-            f16* dst = reinterpret_cast<f16*>(sidx == 0 ? p.ck_S : p.ck_R);
-            *reinterpret_cast<f16x8*>(dst + off + (int64_t)i * DV + v * kVE) = hv;
-            float* scd = sidx == 0 ? p.ck_S_sc : p.ck_R_sc;
-            scd[((int64_t)gc * H + h) * DK * (DV / 32) + (int64_t)i * (DV / 32) + j0 / 32] = sc;
-          } else {
-            float* dst = reinterpret_cast<float*>(sidx == 0 ? p.ck_S : p.ck_R);
-            *reinterpret_cast<float4*>(dst + off + (int64_t)i * DV + v * kVE) =
-                float4{x[0], x[1], x[2], x[3]};
-          }
-        }
+      if constexpr (BF) {
+        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
+        save_state_f16<IT>(Sacc, reinterpret_cast<f16*>(p.ck_S) + off, DV, p.ck_S_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(Racc, reinterpret_cast<f16*>(p.ck_R) + off, DV, p.ck_R_sc + so, DV / 32, w * (DK / 4));
+      } else {
+        save_state_f32<IT, JT>(Sacc, reinterpret_cast<float*>(p.ck_S) + off, DV, w * (DK / 4));
+        save_state_f32<IT, JT>(Racc, reinterpret_cast<float*>(p.ck_R) + off, DV, w * (DK / 4));
       }
+      // the checkpoint's vector work fills the gaps between P1's matrix
+      // products, which wait on their LDS operands
+      if constexpr (BF) interleave_mfma_valu<KS_STEPS * JT * 4, 8>();
     }
     float vloc[JT][4];
 #pragma unroll
@@ -496,7 +469,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
       constexpr int kVE = 16 / (int)sizeof(XT);
       constexpr int kVPR = BV / kVE;
       static_assert(kChunk * kVPR == kThreads, "one block vector per thread");
-      const int t = tid / kVPR, v = tid % kVPR;
+      const int t = lane, v = w;   // lanes read consecutive tokens: no bank conflicts
 #pragma unroll
       for (int b = 0; b < 3; ++b) {
         const XT* srcb = b == 0 ? Ut : b == 1 ? URt : Rst;
