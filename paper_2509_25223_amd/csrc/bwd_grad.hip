@@ -41,47 +41,6 @@ namespace rla {
 
 namespace {
 
-// A [rows][COLS] tile in LDS with the 16-byte chunks of row r XOR-swizzled by
-// r, so that 16 rows read at one column hit distinct banks.
-template <typename T, int COLS>
-struct Tile {
-  static constexpr int kRowB = COLS * (int)sizeof(T);
-  static constexpr int kCpr = kRowB / 16;
-  static_assert((kCpr & (kCpr - 1)) == 0, "power-of-two chunks per row");
-  __device__ __forceinline__ static int off(int r, int col) {   // byte offset
-    const int b = col * (int)sizeof(T);
-    return r * kRowB + (((b >> 4) ^ (r & (kCpr - 1))) << 4) + (b & 15);
-  }
-  // MFMA fragment of rows r0 .. r0+15 at k = k0 (k contiguous in a row)
-  template <typename M>
-  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0) {
-    constexpr int kPL = M::kStep / 4;   // k-values per lane
-    const int lane = threadIdx.x & 63;
-    const char* b = reinterpret_cast<const char*>(base);
-    return *reinterpret_cast<const typename M::frag*>(
-        b + off(r0 + (lane & 15), k0 + kPL * (lane >> 4)));
-  }
-  __device__ __forceinline__ static T at(const void* base, int r, int col) {
-    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + off(r, col));
-  }
-  // LDS-DMA of 64 contiguous rows (global, unswizzled) into the swizzled tile;
-  // each of the NW waves issues an equal share.  Completion: wait_vmem + barrier.
-  template <int NW>
-  __device__ __forceinline__ static void dma64(const T* gsrc, void* lds) {
-    constexpr int kInst = kChunk * kRowB / 1024;
-    static_assert(kInst % NW == 0, "equal DMA share per wave");
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-#pragma unroll
-    for (int m = 0; m < kInst / NW; ++m) {
-      const int blk = w * (kInst / NW) + m;
-      const int P = blk * 64 + lane;   // physical 16-byte chunk
-      const int r = P / kCpr, c = (P % kCpr) ^ (r & (kCpr - 1));
-      dma16(reinterpret_cast<const char*>(gsrc) + r * kRowB + c * 16,
-            reinterpret_cast<char*>(lds) + blk * 1024);
-    }
-  }
-};
-
 // token blocks in LDS
 enum { bDO = 0, bU, bUR, bDX, bDY, bDYR, kNumTokBlk };
 // per-token sums (LDS, fp32, one set per wave, each entry written once so
@@ -239,11 +198,11 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   StateRows rowA, rowB;
   load_rows(rowA, 0, 16 * w);
   load_rows(rowB, 2, 16 * w);
-  TV::template dma64<NW>(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
-  TV::template dma64<NW>(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
-  TV::template dma64<NW>(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
-  TV::template dma64<NW>(bb + blk_off(c, h, H, 1, DV), tokblk(bDY));
-  TV::template dma64<NW>(bb + blk_off(c, h, H, 2, DV), tokblk(bDYR));
+  dma_tile64<TV, NW>(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
+  dma_tile64<TV, NW>(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
+  dma_tile64<TV, NW>(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
+  dma_tile64<TV, NW>(bb + blk_off(c, h, H, 1, DV), tokblk(bDY));
+  dma_tile64<TV, NW>(bb + blk_off(c, h, H, 2, DV), tokblk(bDYR));
 
   // V and r rows for the elementwise sums (consumed after the staging barrier)
   constexpr int kVV = kChunk * DV / kE / NT;

@@ -33,9 +33,11 @@ template <typename IN, int DK, int BV, bool RDN>
 struct BwdScanLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
   typedef typename std::conditional<kBF, f16, float>::type XT;
-  static constexpr int kPad = kBF ? 8 : 4;
-  static constexpr int kLdX = kChunk + kPad;
-  static constexpr int kLdS = DK + kPad;
+  // LDS buffers as padded rows (measured faster here than the swizzled
+  // tiles, whose element-wise addressing costs this kernel registers):
+  typedef PadRows<XT, kChunk, kBF ? 8 : 4> TT;    // per-token blocks [BV][64]
+  typedef PadRows<XT, kChunk, kBF ? 8 : 4> TKQ;   // K^T, Q^T [DK][64]
+  typedef PadRows<IN, DK, kBF ? 8 : 4> TSC;       // gradient-state copies [BV][DK]
   // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs MR
   // (first used) is double-buffered
   static constexpr bool kDB = kBF;
@@ -43,17 +45,17 @@ struct BwdScanLayout {
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kNumBufs = 6;
   static constexpr int kKT = 0;
-  static constexpr int kQT = kKT + DK * kLdX * (int)sizeof(XT);
-  static constexpr int kCopies = kQT + DK * kLdX * (int)sizeof(XT);
-  static constexpr int kCopyBytes = BV * kLdS * (int)sizeof(IN);
+  static constexpr int kQT = kKT + DK * TKQ::kRowB;
+  static constexpr int kCopies = kQT + DK * TKQ::kRowB;
+  static constexpr int kCopyBytes = BV * TSC::kRowB;
   static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
   static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
-  static constexpr int kBufBytes = BV * kLdX * (int)sizeof(XT);
+  static constexpr int kBufBytes = BV * TT::kRowB;
   static constexpr int kMask = kBufs + kNumBufs * kBufBytes;
   static constexpr int kMaskBytes = kChunk * BV;
   static constexpr int kGraw = kMask + kMaskBytes;
   static constexpr int kGates = kGraw + kGateBlock * 4;
-  static constexpr int kYst = kGates + 10 * kChunk * 4;   // dYR staging [BV][kLdX]
+  static constexpr int kYst = kGates + 10 * kChunk * 4;   // dYR staging (token tile)
   static constexpr int kBytes = kYst + kBufBytes;
   static_assert(kMaskBytes % 1024 == 0, "mask block moved in whole DMA instructions");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
@@ -78,21 +80,24 @@ struct BwdScanLayout {
 // P4.  RLA keeps dKS in the dKR slot (dKR = 0 there).
 enum { bDB_DKS = 0, bDC_DX = 1, bQDB = 2, bQDC = 3, bDUR_DU = 4, bDKR = 5 };
 
-template <typename IN>
-__device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int ld, floatx4 v) {
-  const int off = acc_col() * ld + acc_row(0);
+// Writes this lane's 4 accumulator rows of a gradient-state tile into the
+// transposed copies (tile rows r0 + column, columns c0 + row): hi (and, for
+// bf16, the residual lo).
+template <class TL, typename IN>
+__device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0, floatx4 v) {
+  // r0, c0 multiples of 16
+  const int o = TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(IN), c0 * (int)sizeof(IN));
   if constexpr (sizeof(IN) == 2) {   // 8-byte stores of 4 consecutive rows
     u16x4 h4, l4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      h4[r] = f2bf(v[r]);
-      l4[r] = bf16_lo(v[r], h4[r]);
+    for (int k = 0; k < 4; ++k) {
+      h4[k] = f2bf(v[k]);
+      l4[k] = bf16_lo(v[k], h4[k]);
     }
-    *reinterpret_cast<u16x4*>(hi + off) = h4;
-    *reinterpret_cast<u16x4*>(lo + off) = l4;
+    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(hi) + o) = h4;
+    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(lo) + o) = l4;
   } else {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) hi[off + r] = v[r];
+    *reinterpret_cast<floatx4*>(reinterpret_cast<char*>(hi) + o) = v;
   }
 }
 
@@ -101,10 +106,17 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   typedef BwdScanLayout<IN, DK, BV, RDN> L;
   typedef typename L::XT XT;
   typedef Mfma<IN> MI;
+  typedef typename L::TT TT;
+  typedef typename L::TKQ TKQ;
+  typedef typename L::TSC TSC;
   constexpr bool BF = L::kBF;
   constexpr int JT = BV / 16;
   constexpr int IT = DK / 64;
   constexpr int KS_STEPS = DK / MI::kStep;
+  // store instructions per wave of the two checkpointed gradient states
+  // (save_state_f16: two row stores and one scale store per 16-row tile;
+  // fp32: one per row)
+  constexpr int kCkptStores = 2 * (BF ? 3 * IT : 4 * IT * JT);
   extern __shared__ __align__(16) unsigned char smem[];
   XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
   XT* QT = reinterpret_cast<XT*>(smem + L::kQT);
@@ -155,9 +167,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     for (int it = 0; it < IT; ++it)
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
-        const int o = (jt * 16) * L::kLdS + w * (DK / 4) + it * 16;
-        store_state_copy<IN>(dShi + o, dSlo + o, L::kLdS, dS[it][jt]);
-        store_state_copy<IN>(dRhi + o, dRlo + o, L::kLdS, dR[it][jt]);
+        store_state_copy<TSC>(dShi, dSlo, jt * 16, w * (DK / 4) + it * 16, dS[it][jt]);
+        store_state_copy<TSC>(dRhi, dRlo, jt * 16, w * (DK / 4) + it * 16, dR[it][jt]);
       }
   };
   write_copies();
@@ -284,6 +295,22 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       }
     };
 
+    // gradient w.r.t. this chunk's end states for the gradient kernel,
+    // straight from the accumulators (bf16 inputs: fp16 scaled per (row, 32
+    // columns)).  Stored after the chunk's last prefetch, so that the wait
+    // for the prefetched data at the chunk's end leaves these stores in flight.
+    auto save_ckpt = [&]() {
+      const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
+      if constexpr (BF) {
+        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
+        save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + off, DV, p.dS_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + off, DV, p.dR_sc + so, DV / 32, w * (DK / 4));
+      } else {
+        save_state_f32<IT, JT>(dS, reinterpret_cast<float*>(p.dS_ws) + off, DV, w * (DK / 4));
+        save_state_f32<IT, JT>(dR, reinterpret_cast<float*>(p.dR_ws) + off, DV, w * (DK / 4));
+      }
+    };
+
     // ---- commit: K fragments, K^T and Q^T (XT), dO^T, gate vectors ----
     typename MI::frag Kf[KS_STEPS];
     {
@@ -297,19 +324,19 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
             const int i = s2 * 32 + (lane >> 4) * 8 + e;
-            KT[i * L::kLdX + t] = from_f<XT>(bf2f(kv[e]));
-            QT[i * L::kLdX + t] = from_f<XT>(bf2f(qv[e]));
+            *TKQ::ptr(KT, i, t) = from_f<XT>(bf2f(kv[e]));
+            *TKQ::ptr(QT, i, t) = from_f<XT>(bf2f(qv[e]));
           }
         } else {
           const int i = s2 * 4 + (lane >> 4);
-          KT[i * L::kLdX + t] = Kn[s2];
-          QT[i * L::kLdX + t] = Qn[s2];
+          *TKQ::ptr(KT, i, t) = Kn[s2];
+          *TKQ::ptr(QT, i, t) = Qn[s2];
         }
       }
       XT* dbT = blk(bDB_DKS);
 #pragma unroll
       for (int u = 0; u < kOPerThread; ++u)   // lanes write consecutive tokens
-        dbT[(w * kOPerThread + u) * L::kLdX + lane] = from_f<XT>(to_f<IN>(on[u]));
+        *TT::ptr(dbT, w * kOPerThread + u, lane) = from_f<XT>(to_f<IN>(on[u]));
       if (tid < kChunk) {
         const int tt = tid;
         const float gs = graw[tt], gsp = tt > 0 ? graw[tt - 1] : 0.f, gsl = graw[kChunk - 1];
@@ -335,41 +362,28 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     for (int jt = 0; jt < JT; ++jt) {
       KdS[jt] = zero4();
       KdR[jt] = zero4();
-      const int o = jt * 16 * L::kLdS;
-      mma_rega<IN, DK, true>(KdS[jt], Kf, dShi + o, L::kLdS);
-      mma_rega<IN, DK, true>(KdR[jt], Kf, dRhi + o, L::kLdS);
+      mma_rega_tile<IN, DK, TSC>(KdS[jt], Kf, dShi, jt * 16);
+      mma_rega_tile<IN, DK, TSC>(KdR[jt], Kf, dRhi, jt * 16);
       if constexpr (BF) {
-        mma_rega<IN, DK, true>(KdS[jt], Kf, dSlo + o, L::kLdS);
-        mma_rega<IN, DK, true>(KdR[jt], Kf, dRlo + o, L::kLdS);
+        mma_rega_tile<IN, DK, TSC>(KdS[jt], Kf, dSlo, jt * 16);
+        mma_rega_tile<IN, DK, TSC>(KdR[jt], Kf, dRlo, jt * 16);
       }
       floatx4 dc, qdb, qdc;
+      const floatx4 o4 = load_acc_tile<TT>(blk(bDB_DKS), jt * 16, 16 * w);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int t = 16 * w + acc_row(r), j = jt * 16 + acc_col();
-        const float o2 = to_f<XT>(blk(bDB_DKS)[j * L::kLdX + t]);
-        dc[r] = ggm[t] * o2;
-        qdb[r] = egs[t] * o2;
+        const int t = 16 * w + acc_row(r);
+        dc[r] = ggm[t] * o4[r];
+        qdb[r] = egs[t] * o4[r];
         qdc[r] = egr[t] * dc[r];
       }
-      store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dc);
-      store_acc_t<XT>(blk(bQDB) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdb);
-      store_acc_t<XT>(blk(bQDC) + jt * 16 * L::kLdX + 16 * w, L::kLdX, qdc);
+      store_acc_tile<TT>(blk(bDC_DX), jt * 16, 16 * w, dc);
+      store_acc_tile<TT>(blk(bQDB), jt * 16, 16 * w, qdb);
+      store_acc_tile<TT>(blk(bQDC), jt * 16, 16 * w, qdc);
     }
-    // gradient w.r.t. this chunk's end states for the gradient kernel,
-    // straight from the accumulators (bf16 inputs: fp16 scaled per (row, 32
-    // columns))
-    {
-      const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
-      if constexpr (BF) {
-        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
-        save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + off, DV, p.dS_sc + so, DV / 32, w * (DK / 4));
-        save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + off, DV, p.dR_sc + so, DV / 32, w * (DK / 4));
-      } else {
-        save_state_f32<IT, JT>(dS, reinterpret_cast<float*>(p.dS_ws) + off, DV, w * (DK / 4));
-        save_state_f32<IT, JT>(dR, reinterpret_cast<float*>(p.dR_ws) + off, DV, w * (DK / 4));
-      }
-    }
-
+    // the transposed matrices' fragments are loaded ahead of the barriers
+    // that precede their products (every matrix landed in an earlier chunk)
+    const MatFrags<XT> aMR = swz_cols_frags<XT>(mat(kMatMR, buf), 16 * w);
     barrier_lds();
     if (c > 0) {
       issue_regs(c - 1);
@@ -381,11 +395,13 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       floatx4 a = zero4();
-      mma_swz_cols<XT>(a, mat(kMatMR, buf), 16 * w, blk(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+      mma_frags<XT, TT>(a, aMR, blk(bDC_DX), jt * 16);
 #pragma unroll
       for (int r = 0; r < 4; ++r) dUR[jt][r] = dlr[16 * w + acc_row(r)] * KdR[jt][r] + a[r];
-      if constexpr (RDN) store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dUR[jt]);
+      if constexpr (RDN) store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * w, dUR[jt]);
     }
+    MatFrags<XT> aTR;
+    if constexpr (RDN) aTR = swz_cols_frags<XT>(mat(kMatTR, 0), 16 * w);
     barrier_lds();
 
     // ---- P3: dYR, dX, dKR (RLA: dKS) ----
@@ -395,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       floatx4 dYR = dUR[jt];
       if constexpr (RDN) {
         dYR = zero4();
-        mma_swz_cols<XT>(dYR, mat(kMatTR, 0), 16 * w, blk(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+        mma_frags<XT, TT>(dYR, aTR, blk(bDUR_DU), jt * 16);
       }
       floatx4 dkr, dks;
 #pragma unroll
@@ -405,30 +421,36 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         dkr[r] = -ggm[t] * egr[t] * dYR[r];
         dks[r] = -egsp[t] * dX[jt][r];
       }
-      store_acc_t<XT>(blk(bDC_DX) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dX[jt]);
-      store_acc_t<XT>(blk(bDKR) + jt * 16 * L::kLdX + 16 * w, L::kLdX, RDN ? dkr : dks);
-      store_acc_t<XT>(Yst + jt * 16 * L::kLdX + 16 * w, L::kLdX, dYR);
+      store_acc_tile<TT>(blk(bDC_DX), jt * 16, 16 * w, dX[jt]);
+      store_acc_tile<TT>(blk(bDKR), jt * 16, 16 * w, RDN ? dkr : dks);
+      store_acc_tile<TT>(Yst, jt * 16, 16 * w, dYR);
     }
+    const MatFrags<XT> aMP = swz_cols_frags<XT>(mat(kMatMP, 0), 16 * w);
+    const MatFrags<XT> aMG = swz_cols_frags<XT>(mat(kMatMG, 0), 16 * w);
     barrier_lds();
     if (c > 0) issue_mid(c - 1);
 
     // ---- P4: dU = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX ----
+    floatx4 dU[JT];   // RLA: U = diag(b) V, so dV gets b dU
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
-      floatx4 a = zero4(), b = zero4(), du;
-      mma_swz_cols<XT>(a, mat(kMatMP, 0), 16 * w, blk(bDB_DKS) + jt * 16 * L::kLdX, L::kLdX);
-      mma_swz_cols<XT>(b, mat(kMatMG, 0), 16 * w, blk(bDC_DX) + jt * 16 * L::kLdX, L::kLdX);
+      floatx4 a = zero4(), b = zero4();
+      mma_frags<XT, TT>(a, aMP, blk(bDB_DKS), jt * 16);
+      mma_frags<XT, TT>(b, aMG, blk(bDC_DX), jt * 16);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
-      if constexpr (RDN) {
-        store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-      } else {   // RLA: U = diag(b) V, so dV gets b dU; dU is kept for the block store
-        store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
-        store_dv(jt, dX[jt], du);
-      }
+      for (int r = 0; r < 4; ++r) dU[jt][r] = dls[16 * w + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
+      // RLA keeps dU there for the block store
+      store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * w, dU[jt]);
     }
+    MatFrags<XT> aTS;
+    if constexpr (RDN) aTS = swz_cols_frags<XT>(mat(kMatTS, 0), 16 * w);
     barrier_lds();
     if (c > 0) issue_late(c - 1);
+    if constexpr (!RDN) {   // last prefetch issued: dv and checkpoint stores
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) store_dv(jt, dX[jt], dU[jt]);
+      save_ckpt();
+    }
     if constexpr (RDN) {
       // ---- P5: dY = T^S^T dU, dKS ----
       floatx4 dY[JT];
@@ -436,21 +458,24 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 dks;
         dY[jt] = zero4();
-        mma_swz_cols<XT>(dY[jt], mat(kMatTS, 0), 16 * w, blk(bDUR_DU) + jt * 16 * L::kLdX, L::kLdX);
+        mma_frags<XT, TT>(dY[jt], aTS, blk(bDUR_DU), jt * 16);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
           dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[jt][r];
         }
-        store_acc_t<XT>(blk(bDB_DKS) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dks);
-        store_dv(jt, dX[jt], dY[jt]);
+        store_acc_tile<TT>(blk(bDB_DKS), jt * 16, 16 * w, dks);
       }
       barrier_lds();
       if (c > 0) issue_after5(c - 1);
+      // last prefetch issued: dv and checkpoint stores
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) store_dv(jt, dX[jt], dY[jt]);
+      save_ckpt();
       // dU is dead: its slot keeps dY for the block store (P6 does not read it)
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt)
-        store_acc_t<XT>(blk(bDUR_DU) + jt * 16 * L::kLdX + 16 * w, L::kLdX, dY[jt]);
+        store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * w, dY[jt]);
     }
 
     // ---- P6: state gradients at the chunk start ----
@@ -462,20 +487,20 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       for (int jt = 0; jt < JT; ++jt) {
         dS[it][jt] *= eS;
         dR[it][jt] *= eR;
-        const int bo = jt * 16 * L::kLdX;
-        mma_tile<XT, kChunk, true, true>(dS[it][jt], QT + i0 * L::kLdX, L::kLdX, blk(bQDB) + bo, L::kLdX);
-        mma_tile<XT, kChunk, true, true>(dS[it][jt], KT + i0 * L::kLdX, L::kLdX,
-                                         blk(RDN ? bDB_DKS : bDKR) + bo, L::kLdX);
-        mma_tile<XT, kChunk, true, true>(dR[it][jt], QT + i0 * L::kLdX, L::kLdX, blk(bQDC) + bo, L::kLdX);
-        if constexpr (RDN)
-          mma_tile<XT, kChunk, true, true>(dR[it][jt], KT + i0 * L::kLdX, L::kLdX, blk(bDKR) + bo, L::kLdX);
+        mma_tiles<XT, kChunk, TKQ, TT>(dS[it][jt], QT, i0, blk(bQDB), jt * 16);
+        mma_tiles<XT, kChunk, TKQ, TT>(dS[it][jt], KT, i0, blk(RDN ? bDB_DKS : bDKR), jt * 16);
+        mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], QT, i0, blk(bQDC), jt * 16);
+        if constexpr (RDN) mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], KT, i0, blk(bDKR), jt * 16);
       }
     }
     barrier_lds();
     if constexpr (!L::kDB) {
       if (c > 0) issue_all_single(c - 1);
     }
-    wait_vmem();
+    // the next chunk's DMA data must have landed before anyone reads it (with
+    // bf16 inputs the checkpoint stores are issued last and may still be in
+    // flight; single-buffered fp32 issues its DMAs after them)
+    wait_vmem_but<L::kDB ? kCkptStores : 0>();
     barrier_lds();
     {   // this chunk's dX, dY, dYR (value-major in LDS) as token-major rows in
         // 16-byte stores; rows past the end are zero.  The buffers are next
@@ -489,7 +514,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
         XT vals[kVE];
 #pragma unroll
-        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? srcb[(v * kVE + k) * L::kLdX + t] : from_f<XT>(0.f);
+        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? TT::at(srcb, v * kVE + k, t) : from_f<XT>(0.f);
         *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + v * kVE) =
             *reinterpret_cast<const uint4*>(vals);
       }

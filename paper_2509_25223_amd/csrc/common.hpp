@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace rla {
 
 constexpr int kChunk = 64;      // tokens per chunk
@@ -202,26 +204,80 @@ __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f};
 
 
 // ---------------------------------------------------------------------------
-// 64 x 64 matrices staged in LDS by LDS-DMA (global_load_lds_dwordx4): the
-// hardware writes lane i's 16 bytes at base + 16 i, so a tile is stored
-// unpadded, and the 16-byte chunks of row r are XOR-swizzled with sw(r):
+// Row-major LDS tiles without padding: rows of COLS elements of T whose
+// 16-byte chunks are XOR-swizzled with sw(row):
 //   logical (row r, chunk c) -> physical byte r * kRowB + ((c ^ sw(r)) << 4)
-// For 2-byte elements sw(r) = (r & 7) ^ ((r >> 2) & 6): 8 consecutive rows
-// read at one column (row fragments) hit 8 distinct chunks, and so do the
-// column gathers of transposed fragments, whose lane groups read rows 8 apart
-// (the second term separates those).  Wider elements: sw(r) = r mod chunks.
+// 128-byte rows: sw(r) = (r & 7) ^ ((r >> 2) & 6); longer rows: sw(r) = r mod
+// chunks.  On gfx950 (measured with the LDS bank-conflict counter) this keeps
+// conflict-free both the 16-byte MFMA fragment reads (16 rows at one chunk)
+// and the 2-byte column gathers of transposed fragments (lane groups reading
+// rows 8 apart), where padded rows conflict 2-way.  The swizzle moves whole
+// chunks, so 8- and 16-byte pieces stay contiguous.  64 x 64 matrices are
+// staged into such tiles by LDS-DMA (the hardware writes lane i's 16 bytes at
+// base + 16 i; the lanes pick their global sources to match).
 // ---------------------------------------------------------------------------
-template <typename T> struct Swz {
-  static constexpr int kRowB = kChunk * (int)sizeof(T);   // bytes per row
+template <typename T, int COLS> struct Tile {
+  static constexpr int kRowB = COLS * (int)sizeof(T);     // bytes per row
   static constexpr int kCpr = kRowB / 16;                 // 16-byte chunks per row
-  static constexpr int kBytes = kChunk * kRowB;
-  static constexpr int kDmaPerWave = kBytes / 1024 / kWaves;   // 1 KiB per instruction
+  static_assert(kCpr >= 4 && (kCpr & (kCpr - 1)) == 0, "power-of-two chunks per row");
+  static constexpr int kBytes = kChunk * kRowB;           // a 64-row tile
   __device__ __forceinline__ static int sw(int r) {
     return kCpr == 8 ? (r & 7) ^ ((r >> 2) & 6) : r & (kCpr - 1);
   }
   __device__ __forceinline__ static int off(int r, int col) {   // byte offset of element
-    const int c = (col * (int)sizeof(T)) >> 4, inside = (col * (int)sizeof(T)) & 15;
-    return r * kRowB + ((c ^ sw(r)) << 4) + inside;
+    const int b = col * (int)sizeof(T);
+    return r * kRowB + (((b >> 4) ^ sw(r)) << 4) + (b & 15);
+  }
+  // For r0 a multiple of 16 and n < 16: sw(r0 + n) = sw(n) ^ sw_hi(r0).
+  __device__ __forceinline__ static int sw_hi(int r0) { return kCpr == 8 ? (r0 >> 2) & 4 : 0; }
+  // Byte offset of element (r0 + n, column byte cb_lane + cb_uni), r0 a
+  // multiple of 16, n < 16, cb_uni a multiple of 16 whose chunk bits do not
+  // overlap those of cb_lane: a per-lane part XOR a per-block part, so that
+  // every fragment of a tile is one lane offset, one XOR with a wave-uniform
+  // value and an immediate offset.
+  __device__ __forceinline__ static int off_split(int r0, int n, int cb_lane, int cb_uni) {
+    const int lane = n * kRowB + (((cb_lane >> 4) ^ sw(n)) << 4) + (cb_lane & 15);
+    return r0 * kRowB + (lane ^ (((cb_uni >> 4) ^ sw_hi(r0)) << 4));
+  }
+  __device__ __forceinline__ static T* ptr(void* base, int r, int col) {
+    return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off(r, col));
+  }
+  __device__ __forceinline__ static T at(const void* base, int r, int col) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + off(r, col));
+  }
+  // MFMA fragment of rows r0 .. r0+15 (r0 a multiple of 16) at k = k0 (k runs
+  // along a row, k0 a multiple of the MFMA k-step)
+  template <typename M>
+  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0) {
+    constexpr int kPL = M::kStep / 4;   // k-values per lane
+    const int lane = threadIdx.x & 63;
+    return *reinterpret_cast<const typename M::frag*>(
+        reinterpret_cast<const char*>(base) +
+        off_split(r0, lane & 15, kPL * (lane >> 4) * (int)sizeof(T), k0 * (int)sizeof(T)));
+  }
+};
+template <typename T> using Swz = Tile<T, kChunk>;   // 64 x 64 matrices
+
+// Same interface over plain rows padded to COLS + PAD elements: cheaper
+// addressing for buffers written element by element (transposes).
+template <typename T, int COLS, int PAD> struct PadRows {
+  static constexpr int kRowB = (COLS + PAD) * (int)sizeof(T);
+  __device__ __forceinline__ static int off(int r, int col) { return r * kRowB + col * (int)sizeof(T); }
+  __device__ __forceinline__ static int off_split(int r0, int n, int cb_lane, int cb_uni) {
+    return (r0 + n) * kRowB + cb_lane + cb_uni;
+  }
+  __device__ __forceinline__ static T* ptr(void* base, int r, int col) {
+    return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off(r, col));
+  }
+  __device__ __forceinline__ static T at(const void* base, int r, int col) {
+    return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + off(r, col));
+  }
+  template <typename M>
+  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0) {
+    constexpr int kPL = M::kStep / 4;
+    const int lane = threadIdx.x & 63;
+    return *reinterpret_cast<const typename M::frag*>(
+        reinterpret_cast<const char*>(base) + off(r0 + (lane & 15), k0 + kPL * (lane >> 4)));
   }
 };
 
@@ -233,24 +289,29 @@ __device__ __forceinline__ void dma16(const void* src, void* lds) {
                                    reinterpret_cast<char*>(lds), 16, 0, 0);
 }
 
-// DMA of one row-major 64 x 64 matrix (global) into a swizzled LDS tile; each
-// of the NW waves of the workgroup issues an equal share of the 1 KiB
+// LDS-DMA of 64 contiguous rows (global, row-major, unswizzled) into a tile;
+// each of the NW waves of the workgroup issues an equal share of the 1 KiB
 // instructions.  Completion: s_waitcnt vmcnt + barrier.
-template <typename T, int NW = kWaves>
-__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds) {
-  typedef Swz<T> S;
-  constexpr int kPerWave = S::kBytes / 1024 / NW;
-  static_assert(kPerWave * NW * 1024 == S::kBytes, "equal DMA share per wave");
+template <class TL, int NW>
+__device__ __forceinline__ void dma_tile64(const void* gsrc, void* lds) {
+  constexpr int kInst = kChunk * TL::kRowB / 1024;
+  static_assert(kInst % NW == 0, "equal DMA share per wave");
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
-  for (int m = 0; m < kPerWave; ++m) {
-    const int blk = w * kPerWave + m;
-    const int P = blk * 64 + lane;                 // physical chunk index
-    const int r = P / S::kCpr, pc = P % S::kCpr;
-    const int c = pc ^ S::sw(r);                   // logical chunk stored there
-    const char* src = reinterpret_cast<const char*>(gsrc) + r * S::kRowB + c * 16;
-    dma16(src, reinterpret_cast<char*>(lds) + blk * 1024);
+  for (int m = 0; m < kInst / NW; ++m) {
+    const int blk = w * (kInst / NW) + m;
+    const int P = blk * 64 + lane;                  // physical 16-byte chunk
+    const int r = P / TL::kCpr, c = (P % TL::kCpr) ^ TL::sw(r);   // logical chunk stored there
+    dma16(reinterpret_cast<const char*>(gsrc) + r * TL::kRowB + c * 16,
+          reinterpret_cast<char*>(lds) + blk * 1024);
   }
+}
+
+// DMA of one row-major 64 x 64 matrix (global) into a swizzled LDS tile by
+// the NW waves of the workgroup.
+template <typename T, int NW = kWaves>
+__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds) {
+  dma_tile64<Swz<T>, NW>(gsrc, lds);
 }
 
 // DMA of `bytes` contiguous bytes (a multiple of 1 KiB) by wave `wave` only.
@@ -264,6 +325,18 @@ __device__ __forceinline__ void dma_linear_wave(const void* gsrc, void* lds, int
 // and LDS-DMA): s_waitcnt vmcnt(0).  A barrier afterwards makes every wave's
 // DMA data visible.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// s_waitcnt vmcnt(N): waits until at most N of this wave's vector memory
+// operations are outstanding.  They complete in issue order (loads, stores
+// and LDS-DMA share the counter), so with the last N operations being stores
+// this waits for every earlier load but not for those stores' acknowledgement.
+template <int N>
+__device__ __forceinline__ void wait_vmem_but() {
+  static_assert(N >= 0 && N < 64, "vmcnt field");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+  asm volatile("" ::: "memory");
+}
 
 // Workgroup barrier for LDS data: waits for this wave's LDS operations
 // (lgkmcnt(0)) and meets the other waves, but leaves global loads, stores and
@@ -309,22 +382,70 @@ __device__ __forceinline__ typename Mfma<T>::frag swz_load_cols(const T* base, i
   }
 }
 
-// acc += M[r0.., :] * B   (M swizzled 64 x 64, B given as [n][k] rows with ld)
-template <typename T>
-__device__ __forceinline__ void mma_swz_rows(floatx4& acc, const T* M, int r0, const T* B, int ldb) {
+// acc += M[r0.., :] * B, M a swizzled 64 x 64 matrix, B^T rows b0.. of a
+// 64-token tile (row n of B^T = column n of B)
+template <typename T, class TB = Swz<T>>
+__device__ __forceinline__ void mma_swz_rows(floatx4& acc, const T* M, int r0, const void* B, int b0) {
   typedef Mfma<T> F;
 #pragma unroll
   for (int k0 = 0; k0 < kChunk; k0 += F::kStep)
-    acc = F::mma(swz_load_rows<T>(M, r0, k0), F::template load<true>(B, ldb, k0), acc);
+    acc = F::mma(swz_load_rows<T>(M, r0, k0), TB::template frag<F>(B, b0, k0), acc);
 }
 
 // acc += M^T[t0.., :] * B
-template <typename T>
-__device__ __forceinline__ void mma_swz_cols(floatx4& acc, const T* M, int t0, const T* B, int ldb) {
+template <typename T, class TB = Swz<T>>
+__device__ __forceinline__ void mma_swz_cols(floatx4& acc, const T* M, int t0, const void* B, int b0) {
   typedef Mfma<T> F;
 #pragma unroll
   for (int k0 = 0; k0 < kChunk; k0 += F::kStep)
-    acc = F::mma(swz_load_cols<T>(M, t0, k0), F::template load<true>(B, ldb, k0), acc);
+    acc = F::mma(swz_load_cols<T>(M, t0, k0), TB::template frag<F>(B, b0, k0), acc);
+}
+
+// The A fragments of rows r0..r0+15 of a swizzled 64 x 64 matrix (or of its
+// transpose), every k-step, loaded ahead of use (e.g. before a barrier).
+template <typename T> struct MatFrags {
+  typename Mfma<T>::frag f[kChunk / Mfma<T>::kStep];
+};
+template <typename T>
+__device__ __forceinline__ MatFrags<T> swz_rows_frags(const T* M, int r0) {
+  MatFrags<T> a;
+#pragma unroll
+  for (int s = 0; s < kChunk / Mfma<T>::kStep; ++s) a.f[s] = swz_load_rows<T>(M, r0, s * Mfma<T>::kStep);
+  return a;
+}
+template <typename T>
+__device__ __forceinline__ MatFrags<T> swz_cols_frags(const T* M, int t0) {
+  MatFrags<T> a;
+#pragma unroll
+  for (int s = 0; s < kChunk / Mfma<T>::kStep; ++s) a.f[s] = swz_load_cols<T>(M, t0, s * Mfma<T>::kStep);
+  return a;
+}
+// acc += A * B with A from MatFrags and B^T rows b0.. of a 64-token tile
+template <typename T, class TB = Swz<T>>
+__device__ __forceinline__ void mma_frags(floatx4& acc, const MatFrags<T>& a, const void* B, int b0) {
+  typedef Mfma<T> F;
+#pragma unroll
+  for (int s = 0; s < kChunk / F::kStep; ++s)
+    acc = F::mma(a.f[s], TB::template frag<F>(B, b0, s * F::kStep), acc);
+}
+
+// acc += A(rows a0.., :K) * B(rows b0.., :K)^T with both operands in tiles
+template <typename T, int K, class TA, class TB>
+__device__ __forceinline__ void mma_tiles(floatx4& acc, const void* A, int a0, const void* B, int b0) {
+  typedef Mfma<T> F;
+#pragma unroll
+  for (int k0 = 0; k0 < K; k0 += F::kStep)
+    acc = F::mma(TA::template frag<F>(A, a0, k0), TB::template frag<F>(B, b0, k0), acc);
+}
+
+// acc += A * B(rows b0.., :K)^T with the A fragments in registers (afr[k-step])
+template <typename T, int K, class TB>
+__device__ __forceinline__ void mma_rega_tile(floatx4& acc, const typename Mfma<T>::frag* afr,
+                                              const void* B, int b0) {
+  typedef Mfma<T> F;
+#pragma unroll
+  for (int s = 0; s < K / F::kStep; ++s)
+    acc = F::mma(afr[s], TB::template frag<F>(B, b0, s * F::kStep), acc);
 }
 
 // Row (inside a 16-row tile) and column of accumulator element r of this lane.
@@ -477,6 +598,36 @@ __device__ __forceinline__ void store_acc_t(T* dst, int ld, floatx4 v) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) p[r] = from_f<T>(v[r]);
   }
+}
+
+// Stores the 4 accumulator rows of this lane transposed into a tile: element
+// (row, col) of the accumulator tile goes to tile row r0 + col, column
+// c0 + row (4 consecutive elements, one 8- or 16-byte store).
+// r0 a multiple of 16, c0 a multiple of 16 elements.
+template <class TL>
+__device__ __forceinline__ void store_acc_tile(void* base, int r0, int c0, floatx4 v) {
+  typedef typename std::remove_pointer<decltype(TL::ptr(nullptr, 0, 0))>::type T;
+  T* p = reinterpret_cast<T*>(reinterpret_cast<char*>(base) +
+                              TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(T), c0 * (int)sizeof(T)));
+  typedef T T4 __attribute__((ext_vector_type(4)));
+  T4 w;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) w[r] = from_f<T>(v[r]);
+  *reinterpret_cast<T4*>(p) = w;
+}
+
+// Inverse of store_acc_tile: the accumulator-layout values of tile rows
+// r0 + column, columns c0 + row (one 8- or 16-byte read).
+template <class TL>
+__device__ __forceinline__ floatx4 load_acc_tile(const void* base, int r0, int c0) {
+  typedef typename std::remove_pointer<decltype(TL::ptr(nullptr, 0, 0))>::type T;
+  typedef T T4 __attribute__((ext_vector_type(4)));
+  const T4 w = *reinterpret_cast<const T4*>(reinterpret_cast<const char*>(base) +
+                                            TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(T), c0 * (int)sizeof(T)));
+  floatx4 v;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) v[r] = to_f<T>(w[r]);
+  return v;
 }
 
 // Stores the 4 accumulator rows of this lane into LDS row-major: dst[row * ld + col].

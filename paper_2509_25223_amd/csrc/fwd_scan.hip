@@ -36,26 +36,25 @@ template <typename IN, int DK, int BV, bool RDN>
 struct FwdLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
   typedef typename std::conditional<kBF, f16, float>::type XT;
-  static constexpr int kPad = kBF ? 8 : 4;
-  static constexpr int kLdX = kChunk + kPad;    // K^T rows, per-token blocks
-  static constexpr int kLdS = DK + kPad;        // state copies [BV][DK]
+  typedef Tile<XT, kChunk> TT;   // token tiles: K^T [DK][64], per-token blocks [BV][64]
+  typedef Tile<IN, DK> TSC;      // state copies [BV][DK]
   // matrix slots (swizzled 64 x 64 tiles filled by LDS-DMA); with bf16 inputs
   // T^R and MR are double-buffered so the next chunk's copies land early
   static constexpr bool kDB = kBF;
   static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 4 : 3);
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kKT = 0;
-  static constexpr int kCopies = kKT + DK * kLdX * (int)sizeof(XT);
-  static constexpr int kCopyBytes = BV * kLdS * (int)sizeof(IN);
+  static constexpr int kCopies = kKT + DK * TT::kRowB;
+  static constexpr int kCopyBytes = BV * TSC::kRowB;
   static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
   static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
-  static constexpr int kBufBytes = BV * kLdX * (int)sizeof(XT);
+  static constexpr int kBufBytes = BV * TT::kRowB;
   static constexpr int kVc = kBufs + 5 * kBufBytes;
   static constexpr int kVBytes = kChunk * BV * (int)sizeof(IN);
   static constexpr int kGraw = kVc + kVBytes;
   static constexpr int kGates = kGraw + kGateBlock * 4;
   // output staging, so that o, the clip mask and r leave in 16-byte stores:
-  // r value-major [BV][kLdX] (XT), mask token-major [64][BV] bytes, o
+  // r value-major (token tile), mask token-major [64][BV] bytes, o
   // token-major [64][BV + 4] fp32
   static constexpr int kRst = kGates + 10 * kChunk * 4;
   static constexpr int kMst = kRst + kBufBytes;
@@ -80,22 +79,23 @@ struct FwdLayout {
 };
 
 // Writes this lane's 4 accumulator rows of a state tile into the transposed
-// state copy: hi (and, for bf16, the residual lo).
-template <typename IN>
-__device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int ld, floatx4 v) {
-  const int off = acc_col() * ld + acc_row(0);
+// state copies (tile rows r0 + column, columns c0 + row): hi (and, for bf16,
+// the residual lo).
+template <class TL, typename IN>
+__device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0, floatx4 v) {
+  // r0, c0 multiples of 16
+  const int o = TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(IN), c0 * (int)sizeof(IN));
   if constexpr (sizeof(IN) == 2) {   // 8-byte stores of 4 consecutive rows
     u16x4 h4, l4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      h4[r] = f2bf(v[r]);
-      l4[r] = bf16_lo(v[r], h4[r]);
+    for (int k = 0; k < 4; ++k) {
+      h4[k] = f2bf(v[k]);
+      l4[k] = bf16_lo(v[k], h4[k]);
     }
-    *reinterpret_cast<u16x4*>(hi + off) = h4;
-    *reinterpret_cast<u16x4*>(lo + off) = l4;
+    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(hi) + o) = h4;
+    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(lo) + o) = l4;
   } else {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) hi[off + r] = v[r];
+    *reinterpret_cast<floatx4*>(reinterpret_cast<char*>(hi) + o) = v;
   }
 }
 
@@ -104,10 +104,14 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
   typedef typename L::XT XT;
   typedef Mfma<IN> MI;
+  typedef typename L::TT TT;
   constexpr bool BF = L::kBF;
   constexpr int JT = BV / 16;        // value tiles per block
   constexpr int IT = DK / 64;        // state row tiles per wave
   constexpr int KS_STEPS = DK / MI::kStep;
+  // store instructions per wave of the two checkpointed states (save_state_f16:
+  // two row stores and one scale store per 16-row tile; fp32: one per row)
+  constexpr int kCkptStores = 2 * (BF ? 3 * IT : 4 * IT * JT);
   extern __shared__ __align__(16) unsigned char smem[];
   XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
   IN* Shi = reinterpret_cast<IN*>(smem + L::kCopies);
@@ -167,9 +171,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     for (int it = 0; it < IT; ++it)
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
-        const int o = (jt * 16) * L::kLdS + w * (DK / 4) + it * 16;
-        store_state_copy<IN>(Shi + o, Slo + o, L::kLdS, Sacc[it][jt]);
-        store_state_copy<IN>(Rhi + o, Rlo + o, L::kLdS, Racc[it][jt]);
+        store_state_copy<typename L::TSC>(Shi, Slo, jt * 16, w * (DK / 4) + it * 16, Sacc[it][jt]);
+        store_state_copy<typename L::TSC>(Rhi, Rlo, jt * 16, w * (DK / 4) + it * 16, Racc[it][jt]);
       }
   };
   write_state_copies();
@@ -257,9 +260,9 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
           const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s2]);
 #pragma unroll
           for (int e = 0; e < 8; ++e)
-            KT[(s2 * 32 + (lane >> 4) * 8 + e) * L::kLdX + t] = from_f<XT>(bf2f(kv[e]));
+            *TT::ptr(KT, s2 * 32 + (lane >> 4) * 8 + e, t) = from_f<XT>(bf2f(kv[e]));
         } else {
-          KT[(s2 * 4 + (lane >> 4)) * L::kLdX + t] = Kf[s2];
+          *TT::ptr(KT, s2 * 4 + (lane >> 4), t) = Kf[s2];
         }
       }
       if (tid < kChunk) {
@@ -286,33 +289,17 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       KS[jt] = zero4(); QS[jt] = zero4(); KR[jt] = zero4(); QR[jt] = zero4();
-      const int o = jt * 16 * L::kLdS;
-      mma_rega<IN, DK, true>(KS[jt], Kf, Shi + o, L::kLdS);
-      mma_rega<IN, DK, true>(QS[jt], Qf, Shi + o, L::kLdS);
-      mma_rega<IN, DK, true>(KR[jt], Kf, Rhi + o, L::kLdS);
-      mma_rega<IN, DK, true>(QR[jt], Qf, Rhi + o, L::kLdS);
+      typedef typename L::TSC TSC;
+      mma_rega_tile<IN, DK, TSC>(KS[jt], Kf, Shi, jt * 16);
+      mma_rega_tile<IN, DK, TSC>(QS[jt], Qf, Shi, jt * 16);
+      mma_rega_tile<IN, DK, TSC>(KR[jt], Kf, Rhi, jt * 16);
+      mma_rega_tile<IN, DK, TSC>(QR[jt], Qf, Rhi, jt * 16);
       if constexpr (BF) {
-        mma_rega<IN, DK, true>(KS[jt], Kf, Slo + o, L::kLdS);
-        mma_rega<IN, DK, true>(QS[jt], Qf, Slo + o, L::kLdS);
-        mma_rega<IN, DK, true>(KR[jt], Kf, Rlo + o, L::kLdS);
-        mma_rega<IN, DK, true>(QR[jt], Qf, Rlo + o, L::kLdS);
+        mma_rega_tile<IN, DK, TSC>(KS[jt], Kf, Slo, jt * 16);
+        mma_rega_tile<IN, DK, TSC>(QS[jt], Qf, Slo, jt * 16);
+        mma_rega_tile<IN, DK, TSC>(KR[jt], Kf, Rlo, jt * 16);
+        mma_rega_tile<IN, DK, TSC>(QR[jt], Qf, Rlo, jt * 16);
       }
-    }
-    // chunk-start states for the gradient kernel, straight from the
-    // accumulators (bf16 inputs: fp16 scaled per (row, 32 columns))
-    if constexpr (CKPT) {
-      const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
-      if constexpr (BF) {
-        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
-        save_state_f16<IT>(Sacc, reinterpret_cast<f16*>(p.ck_S) + off, DV, p.ck_S_sc + so, DV / 32, w * (DK / 4));
-        save_state_f16<IT>(Racc, reinterpret_cast<f16*>(p.ck_R) + off, DV, p.ck_R_sc + so, DV / 32, w * (DK / 4));
-      } else {
-        save_state_f32<IT, JT>(Sacc, reinterpret_cast<float*>(p.ck_S) + off, DV, w * (DK / 4));
-        save_state_f32<IT, JT>(Racc, reinterpret_cast<float*>(p.ck_R) + off, DV, w * (DK / 4));
-      }
-      // the checkpoint's vector work fills the gaps between P1's matrix
-      // products, which wait on their LDS operands
-      if constexpr (BF) interleave_mfma_valu<KS_STEPS * JT * 4, 8>();
     }
     float vloc[JT][4];
 #pragma unroll
@@ -325,14 +312,22 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         y[r] = RDN ? gbt[t] * __builtin_fmaf(-egs[t], KS[jt][r], vloc[jt][r]) : gbt[t] * vloc[jt][r];
       }
       if constexpr (RDN) {
-        store_acc_t<XT>(Yt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
+        store_acc_tile<TT>(Yt, jt * 16, 16 * w, y);
       } else {
         floatx4 du;
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * y[r];
-        store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
-        store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        store_acc_tile<TT>(Ut, jt * 16, 16 * w, y);
+        store_acc_tile<TT>(DUt, jt * 16, 16 * w, du);
       }
+    }
+    // matrix fragments are loaded ahead of the barriers that precede their
+    // products (each matrix landed in an earlier chunk)
+    MatFrags<XT> aTS, aMG, aMP;
+    if constexpr (RDN) aTS = swz_rows_frags<XT>(mat(kMatTS, 0), 16 * w);
+    else {
+      aMG = swz_rows_frags<XT>(mat(kMatMG, 0), 16 * w);
+      aMP = swz_rows_frags<XT>(mat(kMatMP, 0), 16 * w);
     }
     barrier_lds();
     if (c + 1 < nch) {
@@ -344,13 +339,15 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 u = zero4();
-        mma_swz_rows<XT>(u, mat(kMatTS, 0), 16 * w, Yt + jt * 16 * L::kLdX, L::kLdX);
+        mma_frags<XT>(u, aTS, Yt, jt * 16);
         floatx4 du;
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dls[16 * w + acc_row(r)] * u[r];
-        store_acc_t<XT>(Ut + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
-        store_acc_t<XT>(DUt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        store_acc_tile<TT>(Ut, jt * 16, 16 * w, u);
+        store_acc_tile<TT>(DUt, jt * 16, 16 * w, du);
       }
+      aMG = swz_rows_frags<XT>(mat(kMatMG, 0), 16 * w);
+      aMP = swz_rows_frags<XT>(mat(kMatMP, 0), 16 * w);
       barrier_lds();
     }
 
@@ -360,8 +357,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       floatx4 mgu = zero4(), mpu = zero4();
-      mma_swz_rows<XT>(mgu, mat(kMatMG, 0), 16 * w, Ut + jt * 16 * L::kLdX, L::kLdX);
-      mma_swz_rows<XT>(mpu, mat(kMatMP, 0), 16 * w, Ut + jt * 16 * L::kLdX, L::kLdX);
+      mma_frags<XT>(mgu, aMG, Ut, jt * 16);
+      mma_frags<XT>(mpu, aMP, Ut, jt * 16);
       floatx4 y, rv;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -374,31 +371,56 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         y[r] = RDN ? ggm[t] * __builtin_fmaf(-egr[t], KR[jt][r], rr) : ggm[t] * rr;
       }
       if constexpr (RDN) {
-        store_acc_t<XT>(Yt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
+        store_acc_tile<TT>(Yt, jt * 16, 16 * w, y);
       } else {
         floatx4 du;
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * y[r];
-        store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, y);
-        store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        store_acc_tile<TT>(URt, jt * 16, 16 * w, y);
+        store_acc_tile<TT>(DURt, jt * 16, 16 * w, du);
       }
-      if constexpr (CKPT) store_acc_t<XT>(Rst + jt * 16 * L::kLdX + 16 * w, L::kLdX, rv);
+      if constexpr (CKPT) store_acc_tile<TT>(Rst, jt * 16, 16 * w, rv);
+    }
+    MatFrags<XT> aTR, aMR;
+    if constexpr (L::kDB) {   // double-buffered: landed in the previous chunk
+      if constexpr (RDN) aTR = swz_rows_frags<XT>(mat(kMatTR, buf), 16 * w);
+      else aMR = swz_rows_frags<XT>(mat(kMatMR, buf), 16 * w);
     }
     if constexpr (!L::kDB) wait_vmem();   // single-buffered T^R / MR of this chunk
     barrier_lds();
     if (c + 1 < nch) issue_late(c + 1);
+    // chunk-start states for the gradient kernel, straight from the
+    // accumulators (bf16 inputs: fp16 scaled per (row, 32 columns)).  Stored
+    // after the chunk's last prefetch, so that the wait for the prefetched
+    // data at the chunk's end does not also wait for these stores.
+    if constexpr (CKPT) {
+      const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
+      if constexpr (BF) {
+        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
+        save_state_f16<IT>(Sacc, reinterpret_cast<f16*>(p.ck_S) + off, DV, p.ck_S_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(Racc, reinterpret_cast<f16*>(p.ck_R) + off, DV, p.ck_R_sc + so, DV / 32, w * (DK / 4));
+      } else {
+        save_state_f32<IT, JT>(Sacc, reinterpret_cast<float*>(p.ck_S) + off, DV, w * (DK / 4));
+        save_state_f32<IT, JT>(Racc, reinterpret_cast<float*>(p.ck_R) + off, DV, w * (DK / 4));
+      }
+    }
+    if constexpr (!L::kDB) {
+      if constexpr (RDN) aTR = swz_rows_frags<XT>(mat(kMatTR, buf), 16 * w);
+      else aMR = swz_rows_frags<XT>(mat(kMatMR, buf), 16 * w);
+    }
 
     if constexpr (RDN) {   // ---- P4: UR = T^R YR ----
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 u = zero4();
-        mma_swz_rows<XT>(u, mat(kMatTR, buf), 16 * w, Yt + jt * 16 * L::kLdX, L::kLdX);
+        mma_frags<XT>(u, aTR, Yt, jt * 16);
         floatx4 du;
 #pragma unroll
         for (int r = 0; r < 4; ++r) du[r] = dlr[16 * w + acc_row(r)] * u[r];
-        store_acc_t<XT>(URt + jt * 16 * L::kLdX + 16 * w, L::kLdX, u);
-        store_acc_t<XT>(DURt + jt * 16 * L::kLdX + 16 * w, L::kLdX, du);
+        store_acc_tile<TT>(URt, jt * 16, 16 * w, u);
+        store_acc_tile<TT>(DURt, jt * 16, 16 * w, du);
       }
+      aMR = swz_rows_frags<XT>(mat(kMatMR, buf), 16 * w);
       barrier_lds();
     }
 
@@ -407,7 +429,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 mru = zero4();
-        mma_swz_rows<XT>(mru, mat(kMatMR, buf), 16 * w, URt + jt * 16 * L::kLdX, L::kLdX);
+        mma_frags<XT>(mru, aMR, URt, jt * 16);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
@@ -421,17 +443,18 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     const float eS = edge[0], eR = edge[1];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const XT* Ai = KT + (w * (DK / 4) + it * 16) * L::kLdX;
+      const int i0 = w * (DK / 4) + it * 16;
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         Sacc[it][jt] *= eS;
         Racc[it][jt] *= eR;
-        mma_tile<XT, kChunk, true, true>(Sacc[it][jt], Ai, L::kLdX, DUt + jt * 16 * L::kLdX, L::kLdX);
-        mma_tile<XT, kChunk, true, true>(Racc[it][jt], Ai, L::kLdX, DURt + jt * 16 * L::kLdX, L::kLdX);
+        mma_tiles<XT, kChunk, TT, TT>(Sacc[it][jt], KT, i0, DUt, jt * 16);
+        mma_tiles<XT, kChunk, TT, TT>(Racc[it][jt], KT, i0, DURt, jt * 16);
       }
     }
-    // the next chunk's DMA data must have landed before anyone reads it
-    wait_vmem();
+    // the next chunk's DMA data must have landed before anyone reads it (the
+    // checkpoint stores, issued last, may still be in flight)
+    wait_vmem_but<CKPT ? kCkptStores : 0>();
     barrier_lds();
     if (c + 1 < nch) issue_tail(c + 1);   // single-buffered T^R / MR: waited at P3
     // ---- this chunk's staged outputs, in 16-byte stores (the buffers are
@@ -475,7 +498,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         const XT* srcb = b == 0 ? Ut : b == 1 ? URt : Rst;
         XT vals[kVE];
 #pragma unroll
-        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? srcb[(v * kVE + k) * L::kLdX + t] : from_f<XT>(0.f);
+        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? TT::at(srcb, v * kVE + k, t) : from_f<XT>(0.f);
         *reinterpret_cast<uint4*>(fblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + v * kVE) =
             *reinterpret_cast<const uint4*>(vals);
       }
