@@ -23,36 +23,39 @@ namespace rla {
 
 namespace {
 
+constexpr int kLdA = kChunk + 4;   // fp32 64 x 64 scratch row stride
+
 template <typename T, int DK>
 struct PrepLayout {
   static constexpr int kLdK = DK + (sizeof(T) == 2 ? 8 : 4);   // Kc / Qc row stride
-  static constexpr int kLdA = kChunk + 1;                       // fp32 64x64 scratch stride
+  static constexpr int kLdA = rla::kLdA;
   // region 0: Kc, Qc (T) -- later reused by As, Ar, Ts, Tr (fp32)
   static constexpr int kBytesKQ = 2 * kChunk * kLdK * (int)sizeof(T);
   static constexpr int kBytesA = 4 * kChunk * kLdA * 4;
   static constexpr int kBytes0 = kBytesKQ > kBytesA ? kBytesKQ : kBytesA;
-  static constexpr int kBytesW = 6 * 256 * 4;                   // block products
+  static constexpr int kBytesW = 6 * 256 * 4;                   // per-wave block products
   static constexpr int kBytesGates = 5 * kChunk * 4;
   static constexpr int kBytes = kBytes0 + kBytesW + kBytesGates;
   static_assert(kBytes <= 160 * 1024, "prep LDS");
 };
 
-// Inverse of the unit lower-triangular I + A (A strictly lower, fp32, ld = kLdA)
-// for two matrices at once: A0 -> T0, A1 -> T1.  256 threads.
+// Inverse T = (I + A)^{-1} of a unit lower-triangular 64 x 64 matrix (A
+// strictly lower, fp32, row stride kLdA) for two matrices at once (A0 -> T0,
+// A1 -> T1), in 16 x 16 blocks: the diagonal blocks T_ii = (I + A_ii)^{-1} by
+// forward substitution (one lane per column), then each block column j by
+//   T_ij = -T_ii * sum_{m=j}^{i-1} A_im T_mj        (i = j+1 .. 3)
+// on fp32 MFMA.  Wave w takes matrix w >> 1 and block column 0 (w even) or
+// block columns 1 and 2 (w odd); a column only reads its own blocks and the
+// diagonal ones, so one barrier separates the two phases.  Blocks above the
+// diagonal are not written.  P: 4 x 256 floats of per-wave scratch.
 __device__ void invert_unit_lower_pair(const float* A0, const float* A1, float* T0, float* T1,
-                                       float* W) {
-  constexpr int ld = kChunk + 1;
-  const int tid = threadIdx.x;
-  // zero both inverses
-  for (int e = tid; e < kChunk * kChunk; e += kThreads) {
-    const int r = e / kChunk, c = e % kChunk;
-    T0[r * ld + c] = 0.f;
-    T1[r * ld + c] = 0.f;
-  }
-  __syncthreads();
-  // diagonal 16 x 16 blocks: thread = (matrix, block, column)
-  if (tid < 128) {
-    const int mat = tid >> 6, blk = (tid >> 4) & 3, c = tid & 15;
+                                       float* P) {
+  constexpr int ld = kLdA;
+  typedef Mfma<float> F;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  // ---- diagonal blocks: lanes 0..31 of wave w solve blocks 2w and 2w+1 ----
+  if (lane < 32) {
+    const int b = 2 * w + (lane >> 4), mat = b >> 2, blk = b & 3, c = lane & 15;
     const float* A = (mat ? A1 : A0) + (16 * blk) * ld + 16 * blk;
     float* T = (mat ? T1 : T0) + (16 * blk) * ld + 16 * blk;
     float x[16];
@@ -60,43 +63,44 @@ __device__ void invert_unit_lower_pair(const float* A0, const float* A1, float* 
     for (int i = 0; i < 16; ++i) {
       float acc = (i == c) ? 1.f : 0.f;
 #pragma unroll
-      for (int k = 0; k < i; ++k) acc -= A[i * ld + k] * x[k];
+      for (int k = 0; k < i; ++k) acc = __builtin_fmaf(-A[i * ld + k], x[k], acc);
       x[i] = (i < c) ? 0.f : acc;
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) T[i * ld + c] = x[i];
   }
   __syncthreads();
-  // block rows bi = 1..3: T[bi][bj] = -T[bi][bi] * sum_{m=bj}^{bi-1} A[bi][m] T[m][bj]
-  for (int bi = 1; bi < 4; ++bi) {
-    const int nblk = 2 * bi;   // (matrix, bj) pairs
-    for (int e = tid; e < nblk * 256; e += kThreads) {
-      const int blk = e >> 8, mat = blk / bi, bj = blk % bi;
-      const int r = (e >> 4) & 15, c = e & 15;
-      const float* A = mat ? A1 : A0;
-      const float* T = mat ? T1 : T0;
-      float acc = 0.f;
-      for (int m = bj; m < bi; ++m) {
-        const float* arow = A + (16 * bi + r) * ld + 16 * m;
-        const float* tcol = T + (16 * m) * ld + 16 * bj + c;
+  // ---- off-diagonal blocks, one block column chain per wave ----
+  const float* A = (w >> 1) ? A1 : A0;
+  float* T = (w >> 1) ? T1 : T0;
+  float* Pw = P + w * 256;   // [16][16], k-major rows
+  const int n = lane & 15, kg = lane >> 4;
+  // acc += X[rows 16 xi.., cols 16 xm..] * Y[rows 16 ym.., cols 16 yj..] (16 x 16 x 16)
+  auto mm = [&](floatx4& acc, const float* X, int xi, int xm, const float* Y, int ym, int yj, int ldy) {
 #pragma unroll
-        for (int kk = 0; kk < 16; ++kk) acc += arow[kk] * tcol[kk * ld];
-      }
-      W[e] = acc;
-    }
-    __syncthreads();
-    for (int e = tid; e < nblk * 256; e += kThreads) {
-      const int blk = e >> 8, mat = blk / bi, bj = blk % bi;
-      const int r = (e >> 4) & 15, c = e & 15;
-      float* T = mat ? T1 : T0;
-      const float* trow = T + (16 * bi + r) * ld + 16 * bi;
-      const float* w = W + (blk << 8) + c;
-      float acc = 0.f;
+    for (int k0 = 0; k0 < 16; k0 += F::kStep)
+      acc = F::mma(X[(16 * xi + n) * ld + 16 * xm + k0 + kg], Y[(16 * ym + k0 + kg) * ldy + 16 * yj + n], acc);
+  };
+  auto solve_block = [&](int i, int j) {   // T_ij from T_jj .. T_{i-1,j}
+    floatx4 s = zero4();
+    for (int m = j; m < i; ++m) mm(s, A, i, m, T, m, j, ld);
 #pragma unroll
-      for (int kk = 0; kk < 16; ++kk) acc += trow[kk] * w[kk * 16];
-      T[(16 * bi + r) * ld + 16 * bj + c] = -acc;
-    }
-    __syncthreads();
+    for (int r = 0; r < 4; ++r) Pw[(4 * kg + r) * 16 + n] = s[r];
+    floatx4 t = zero4();
+#pragma unroll
+    for (int k0 = 0; k0 < 16; k0 += F::kStep)   // T_ii * P (wave-local LDS order)
+      t = F::mma(T[(16 * i + n) * ld + 16 * i + k0 + kg], Pw[(k0 + kg) * 16 + n], t);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) T[(16 * i + 4 * kg + r) * ld + 16 * j + n] = -t[r];
+  };
+  if ((w & 1) == 0) {
+    solve_block(1, 0);
+    solve_block(2, 0);
+    solve_block(3, 0);
+  } else {
+    solve_block(2, 1);
+    solve_block(3, 2);
+    solve_block(3, 1);
   }
 }
 
@@ -206,10 +210,12 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   if constexpr (RDN) {
     __syncthreads();
     invert_unit_lower_pair(As, Ar, Ts, Tr, W);
+    __syncthreads();
     for (int e = tid; e < kMatElems; e += kThreads) {
       const int t = e / kChunk, s = e % kChunk;
-      mats[kMatTS * kMatElems + e] = from_f<XT>(Ts[t * L::kLdA + s]);
-      mats[kMatTR * kMatElems + e] = from_f<XT>(Tr[t * L::kLdA + s]);
+      const bool upper = (s >> 4) > (t >> 4);   // blocks above the diagonal are zero
+      mats[kMatTS * kMatElems + e] = from_f<XT>(upper ? 0.f : Ts[t * L::kLdA + s]);
+      mats[kMatTR * kMatElems + e] = from_f<XT>(upper ? 0.f : Tr[t * L::kLdA + s]);
     }
   }
 }
