@@ -32,7 +32,8 @@
 //
 // Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation.  The
 // scans store the states in fp16 scaled by a power of two per (row, 32
-// columns); a contraction applies each k-step's scale to the accumulator.
+// columns); here each row is brought to one scale (its largest) when loaded,
+// and a contraction multiplies its result by that scale.
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -168,9 +169,13 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   // ---------------- phase 0: staging ----------------
   // A state's rows i0 .. i0+15 as MFMA B fragments (row = lane & 15), with
   // the power-of-two scale of each (row, 32-column k-step) for fp16 states.
+  // The row's fp16 blocks are brought to one scale, the largest of its blocks
+  // (power-of-two factors <= 1, applied in fp16): a block 2^10 or more below
+  // the row's largest loses only entries under 2^-14 of that scale, far below
+  // what fp16 operands resolve in the contraction.
   struct StateRows {
     Frag fr[KSV];
-    float sc[KSV];
+    float sc;         // the row's scale
   };
   const void* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
   const float* scs[4] = {p.ck_S_sc, p.ck_R_sc, p.dS_sc, p.dR_sc};
@@ -180,18 +185,29 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     if constexpr (BF) {
       const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * DV;
       const float* scp = scs[st] + sco + (int64_t)i * (DV / 32);
+      float sc[KSV], mx = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks) {
         x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + ks * M::kStep + 8 * (lane >> 4));
-        x.sc[ks] = scp[ks];
+        sc[ks] = scp[ks];
+        mx = fmaxf(mx, sc[ks]);
       }
+      // sc / mx: exact power of two <= 1 (from the exponent bits; f16 0 below 2^-24)
+      const uint32_t emx = __float_as_uint(mx) >> 23;
+#pragma unroll
+      for (int ks = 0; ks < KSV; ++ks) {
+        const int d = (int)(__float_as_uint(sc[ks]) >> 23) - (int)emx;   // <= 0
+        const f16 f = d < -24 ? (f16)0.f : (f16)__uint_as_float((uint32_t)(127 + d) << 23);
+        x.fr[ks] = x.fr[ks] * f;
+      }
+      x.sc = mx;
     } else {
       const float* rowp = reinterpret_cast<const float*>(srcs[st]) + soff + (int64_t)i * DV;
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks) {
         x.fr[ks] = rowp[ks * M::kStep + (lane >> 4)];
-        x.sc[ks] = 1.f;
       }
+      x.sc = 1.f;
     }
   };
   // the first state rows stream in while the chunk's blocks are staged
@@ -398,16 +414,14 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     float s = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KSV; ++ks) {
-      float d = 0.f;
       if constexpr (BF) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) d += (float)a.fr[ks][e] * (float)b.fr[ks][e];
+        for (int e = 0; e < 8; ++e) s += (float)a.fr[ks][e] * (float)b.fr[ks][e];
       } else {
-        d = a.fr[ks] * b.fr[ks];
+        s += a.fr[ks] * b.fr[ks];
       }
-      s += d * (a.sc[ks] * b.sc[ks]);
     }
-    return s;
+    return s * (a.sc * b.sc);
   };
   // [16 tokens x 16 state rows] tile: token block rows 16 tt times the state
   // rows, contracted over the value dimension; each k-step's scale is applied
@@ -416,10 +430,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     floatx4 acc = zero4();
 #pragma unroll
     for (int ks = 0; ks < KSV; ++ks) {
-      if (ks > 0) acc *= x.sc[ks - 1] * (1.f / x.sc[ks]);
       acc = M::mma(TV::template frag<M>(tokblk(b), 16 * tt, ks * M::kStep), x.fr[ks], acc);
     }
-    return acc * x.sc[KSV - 1];
+    return BF ? acc * x.sc : acc;
   };
 
   // per d_k tile: S0 with dS1, then R0 with dR1; the next pair's rows are
