@@ -5,10 +5,11 @@ At the end of every chunk the scans publish the next chunk's LDS-DMA data
 with `s_waitcnt vmcnt(N)` followed by a barrier, N > 0 leaving that many of
 the wave's newest vector-memory operations in flight.  Vector memory
 operations complete in issue order, so this is correct only if those N
-newest operations are stores (the chunk's checkpoint stores), never a load
-or a DMA.  This test compiles both scan kernels and checks, for every such
-wait in every template instance, that the vector-memory instructions between
-the last load and the wait are at least N stores.
+newest operations were all issued after the last LDS-DMA (they are register
+prefetches and stores, whose own uses the compiler waits for).  This test
+compiles both scan kernels and checks, for every such wait in every template
+instance, that at least N vector-memory instructions lie between the last
+LDS-DMA instruction and the wait.
 """
 import os
 import re
@@ -34,7 +35,7 @@ def _asm(src: str) -> str:
 
 
 def _publishing_waits(body):
-    """(N, trailing stores, instance-local index) for each vmcnt(N > 0) wait
+    """(N, ops after the last LDS-DMA, index) for each vmcnt(N > 0) wait
     that reaches a barrier before any other vector-memory op or vmcnt wait."""
     out = []
     for k, line in enumerate(body):
@@ -51,21 +52,21 @@ def _publishing_waits(body):
                 break
         if not publishes:
             continue
-        stores = 0
+        after = 0
         for x in reversed(body[:k]):
             op = x.split()[0]
             if op.startswith(("global_", "buffer_")):
-                if "load" in op or "atomic" in op:
+                if "_lds" in op:
                     break
-                stores += 1
-        out.append((int(m.group(1)), stores, k))
+                after += 1
+        out.append((int(m.group(1)), after, k))
     return out
 
 
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not available")
 @pytest.mark.parametrize("src,kernel", [("fwd_scan.hip", "fwd_scan_kernel"),
                                         ("bwd_scan.hip", "bwd_scan_kernel")])
-def test_partial_waits_leave_only_stores_in_flight(src, kernel):
+def test_partial_waits_leave_no_dma_in_flight(src, kernel):
     s = _asm(src)
     names = re.findall(r"^(_Z\w*%s\w*):" % kernel, s, re.M)
     assert names, "no %s instances found" % kernel
@@ -76,7 +77,7 @@ def test_partial_waits_leave_only_stores_in_flight(src, kernel):
         body = [l.strip() for l in s[i:j].split("\n")
                 if l.strip() and not l.strip().startswith((";", "."))
                 and not l.strip().endswith(":")]
-        for n, stores, _ in _publishing_waits(body):
-            assert stores >= n, (name, n, stores)
+        for n, after, _ in _publishing_waits(body):
+            assert after >= n, (name, n, after)
             checked += 1
     assert checked > 0
