@@ -41,10 +41,10 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("563cc1bd7280f056", ("bwd_grad.hip", "common.hpp", "kernels.hpp"), 1883479626, 424625152),
-    "bwd_scan": ("6c3058f8dc931fe6", ("bwd_scan.hip", "common.hpp", "kernels.hpp"), 407247528, 880806502),
-    "fwd_scan": ("7dbbe0ab6b90d766", ("fwd_scan.hip", "common.hpp", "kernels.hpp"), 373586733, 905978675),
-    "prep": ("04b8f825e0b2d63a", ("prep.hip", "common.hpp", "kernels.hpp"), 150075069, 172199117),
+    "bwd_grad": ("e13371c0605273d4", ("bwd_grad.hip", "common.hpp", "kernels.hpp"), 1279757515, 322540501),
+    "bwd_scan": ("10e4bebe306ccf75", ("bwd_scan.hip", "common.hpp", "kernels.hpp"), 407276559, 637578544),
+    "fwd_scan": ("e25fde891f48e0e3", ("fwd_scan.hip", "common.hpp", "kernels.hpp"), 373594974, 654311545),
+    "prep": ("5aeaa998c6e4e057", ("prep.hip", "common.hpp", "kernels.hpp"), 153261552, 172847589),
 }
 
 
