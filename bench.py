@@ -17,7 +17,11 @@ launch time), and the fp64 CPU oracle timed on a bounded sample of the same
 workload on this host.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
-                    [--copy-calibration-mib M]
+                    [--copy-calibration-mib M] [--op fwdbwd|decode]
+
+--op decode instead times the recurrent decoding step (one token for each of
+256 sequences, H=16, d=128, states resident in HBM and updated in place),
+an HBM-bound kernel reported against the 8 TB/s peak.
 """
 from __future__ import annotations
 
@@ -45,6 +49,7 @@ MEASURED_TRAFFIC = {
     "bwd_scan": ("10e4bebe306ccf75", ("bwd_scan.hip", "common.hpp", "kernels.hpp"), 407276559, 637578544),
     "fwd_scan": ("e25fde891f48e0e3", ("fwd_scan.hip", "common.hpp", "kernels.hpp"), 373594974, 654311545),
     "prep": ("5aeaa998c6e4e057", ("prep.hip", "common.hpp", "kernels.hpp"), 153261552, 172847589),
+    "decode": ("c28ceaa8e700b72f", ("decode.hip", "common.hpp", "kernels.hpp"), 542727091, 539545242),
 }
 
 
@@ -100,6 +105,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--op", choices=("fwdbwd", "decode"), default="fwdbwd",
+                    help="fwdbwd: the RDN training step (default); decode: the RDN recurrent "
+                         "step, one token for each of 256 sequences from resident states")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a kernel of "
                          "known traffic, for scaling hardware byte counters)")
@@ -110,6 +118,24 @@ def main() -> int:
               file=sys.stderr)
         return 2
 
+    if args.op == "decode":
+        return run_decode(args)
+    return run_fwdbwd(args)
+
+
+def copy_calibration(mib: int, dev) -> None:
+    """One device-to-device copy of known size, for scaling byte counters."""
+    import torch
+    if mib <= 0:
+        return
+    n = mib * (1 << 20) // 4
+    src_ = torch.ones(n, dtype=torch.float32, device=dev)
+    dst_ = torch.empty_like(src_)
+    dst_.copy_(src_)
+    torch.cuda.synchronize()
+
+
+def run_fwdbwd(args) -> int:
     import numpy as np
     import torch
     import datagen
@@ -145,13 +171,7 @@ def main() -> int:
         fwd()
         bwd()
 
-    if args.copy_calibration_mib > 0:
-        n = args.copy_calibration_mib * (1 << 20) // 4
-        src_ = torch.ones(n, dtype=torch.float32, device=dev)
-        dst_ = torch.empty_like(src_)
-        dst_.copy_(src_)
-        torch.cuda.synchronize()
-        del src_, dst_
+    copy_calibration(args.copy_calibration_mib, dev)
 
     for _ in range(args.warmup):
         step()
@@ -191,6 +211,7 @@ def main() -> int:
         for i, name in enumerate(names):
             stage_ms[tag + name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
     units = B * ((T + CHUNK - 1) // CHUNK) * H   # (chunk, head) pairs per launch
+    step_flops = sum(stage_model(st, d)[0] for st in fwd_stages + bwd_stages) * units
     stages = {}
     for key, ms in stage_ms.items():
         fl, by = stage_model(key.split(".", 1)[1], d)
@@ -232,7 +253,7 @@ def main() -> int:
                          "backward, fp64 token recurrence (%.1f s wall)" % (B, T, H, c1 - c0)}
 
     line = {
-        "metric": "RDN fwd+bwd tokens/sec on 1 MI355X (H=16,d=128,T=4096)",
+        "metric": "RDN fwd+bwd tokens/sec on 1 MI355X (H=16,d=128,T=4096); % bf16 MFMA peak",
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -247,7 +268,112 @@ def main() -> int:
         "config": {"workload": wl.name, "B": B, "T": T, "H": H, "d_k": d, "d_v": d,
                    "chunk": CHUNK, "clip": wl.clip, "outputs": "fp32",
                    "parallelism": "single GPU"},
+        # algorithmic flops of the whole step (every stage's count model) over
+        # the step time, as a fraction of the dense bf16 MFMA peak
+        "step_mfma_frac": round(step_flops / (ms_per_step * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
         "stages": stages,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+DECODE_B = 256   # sequences decoded together (one token each per step)
+
+
+def decode_bytes(dk: int, dv: int) -> int:
+    """Algorithmic HBM bytes of one (sequence, head) of a one-token decode
+    step: S and R read and written (fp32), q k v in (bf16), o out (fp32), four
+    fp32 gates."""
+    return 4 * dk * dv * 4 + (2 * dk + dv) * 2 + dv * 4 + 4 * 4
+
+
+def run_decode(args) -> int:
+    import numpy as np
+    import torch
+    import datagen
+    import paper_2509_25223_amd as rla
+
+    dev = torch.device("cuda:0")
+    B, H, d = DECODE_B, 16, 128
+    wl = datagen.small("rdn_fwd", "bf16", [1] * B, H=H, d=d, varlen=False)
+    seed = 6 if args.seed is None else args.seed
+    inp = datagen.make_inputs(wl, seed=seed)
+    S0, R0 = datagen.random_states(seed, B, H, d, d)
+
+    def to_dev(a, dtype, shape):
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev, dtype).view(*shape)
+
+    q, k, v = (to_dev(inp[n], torch.bfloat16, (B, 1, H, d)) for n in ("q", "k", "v"))
+    gates = [to_dev(inp[n], torch.float32, (B, 1, H)) for n in ("alpha_s", "beta", "alpha_r", "gamma")]
+    S, R = to_dev(S0, torch.float32, S0.shape), to_dev(R0, torch.float32, R0.shape)
+    o = torch.empty(v.shape, dtype=torch.float32, device=dev)
+    copy_calibration(args.copy_calibration_mib, dev)
+
+    def step():   # in place: the states advance by one token per step
+        rla.rdn_decode(q, k, v, *gates, clip=wl.clip, S_in=S, R_in=R, S_out=S, R_out=R, out=o)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed * 1e3 / args.steps
+
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for s_ in range(args.steps):
+        rla.rla_set_stage_events(ev[s_])
+        step()
+    rla.rla_set_stage_events(None)
+    torch.cuda.synchronize()
+    kms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    units = B * H
+    by = decode_bytes(d, d) * units
+    gbs = by / (kms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("decode"),
+                "bytes_per_launch": by,
+                "kernel": "decode_kernel", "launch_ms": round(kms, 4), "units_per_launch": units}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        names = ("q", "k", "v", "alpha_s", "beta", "alpha_r", "gamma")
+        reps = 0
+        c0 = time.perf_counter()
+        while True:   # repeat the same step for about 10 s of oracle time
+            oracle.forward("rdn", *[inp[n] for n in names], clip=wl.clip, S0=S0, R0=R0,
+                           cu_seqlens=wl.cu_seqlens())
+            reps += 1
+            if time.perf_counter() - c0 > 10.0:
+                break
+        c1 = time.perf_counter()
+        cpu = {"value": round(B * reps / (c1 - c0), 2), "unit": "tokens/s",
+               "cores": oracle.threads(), "kind": "oracle",
+               "sample": "%d repetitions of the whole decode step (%d sequences x 1 token, %d "
+                         "heads, states in and out), fp64 token recurrence (%.1f s wall)"
+                         % (reps, B, H, c1 - c0)}
+
+    line = {
+        "metric": "RDN decode-step tokens/sec on 1 MI355X (B=256 sequences, H=16, d=128)",
+        "value": round(B / (ms_per_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 in, fp32 states and arithmetic, fp32 out",
+        "data": "synthetic",
+        "config": {"workload": "rdn_decode_bf16_B256_H16_d128", "B": B, "T": 1, "H": H,
+                   "d_k": d, "d_v": d, "clip": wl.clip, "states": "fp32, updated in place",
+                   "parallelism": "single GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

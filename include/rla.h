@@ -49,7 +49,8 @@
  *   sequences.  Tokens outside every sequence get zero outputs/gradients.
  *   Launch failures return RLA_ERR_HIP.  No call aborts or throws.
  * Supported shapes.  bf16: d_k, d_v in {64, 128}.  fp32: d_k = 64,
- *   d_v in {64, 128} for the forward; the backward (and a forward with
+ *   d_v in {64, 128} for the chunked forward (the decoding step below takes
+ *   d_k in {64, 128}); the backward (and a forward with
  *   RLA_FLAG_SAVE_FOR_BACKWARD) in fp32 needs d_v = 64 and returns
  *   RLA_ERR_UNSUPPORTED otherwise.  Any B, T >= 0, H >= 1.  Internally the sequence is
  *   processed in chunks of 64 tokens; results do not depend on B or packing.
@@ -192,6 +193,41 @@ rla_status rla_backward(const rla_problem *problem,
                         float *dalpha_s, float *dbeta, float *dalpha_r, float *dgamma,
                         float *dS0, float *dR0,
                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Recurrent step for decoding (the token recurrence of Sec. 3.4 evaluated
+ * directly, as in the paper's recurrent pseudo-code of App. D): advances the
+ * states of B = problem.batch sequences by T = problem.seq_len tokens each
+ * and writes the T outputs.  Meant for small T (T = 1 per generated token);
+ * the chunked rla_forward / rdn_forward serve long sequences.
+ *   q, k [B, T, H, d_k], v [B, T, H, d_v]      problem.dtype
+ *   alpha_s, beta, alpha_r, gamma [B, T, H]     fp32 gate values
+ *   o [B, T, H, d_v]                            problem.out_dtype
+ *   S_in, R_in [B, H, d_k, d_v] fp32, or NULL for zero states
+ *   S_out, R_out [B, H, d_k, d_v] fp32, required, 16-byte aligned; S_out may
+ *     be the same pointer as S_in (in-place update), likewise R_out and R_in;
+ *     any other overlap among the four state buffers is rejected.
+ * No workspace.  problem.cu_seqlens must be NULL (RLA_ERR_UNSUPPORTED) and
+ * problem.flags 0.  bf16 and fp32 inputs both support d_k, d_v in {64, 128};
+ * all arithmetic is fp32 (bf16 inputs are widened exactly).  Decays are used
+ * as given (no 2^-126 floor is needed here).  T = 0 copies S_in, R_in (or
+ * zeros) to S_out, R_out.  Each (sequence, head) reads its states once and
+ * writes them once, so a step moves 16 d_k d_v bytes per (sequence, head).
+ */
+rla_status rla_decode(const rla_problem *problem,
+                      const void *q, const void *k, const void *v,
+                      const float *alpha_s, const float *beta,
+                      const float *alpha_r, const float *gamma,
+                      const float *S_in, const float *R_in,
+                      void *o, float *S_out, float *R_out, void *stream);
+
+/* RDN recurrent step (Sec. 3.4, right box); arguments as for rla_decode. */
+rla_status rdn_decode(const rla_problem *problem,
+                      const void *q, const void *k, const void *v,
+                      const float *alpha_s, const float *beta,
+                      const float *alpha_r, const float *gamma,
+                      const float *S_in, const float *R_in,
+                      void *o, float *S_out, float *R_out, void *stream);
 
 #ifdef __cplusplus
 }

@@ -29,7 +29,7 @@ RLA_F32, RLA_BF16 = 0, 1
 RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD, RLA_OP_RLA_BACKWARD = 0, 1, 2, 3
 
 SYMBOLS = ("rla_workspace_size", "rla_status_string", "rla_forward", "rdn_forward",
-           "rla_backward", "rdn_backward", "rla_set_stage_events")
+           "rla_backward", "rdn_backward", "rla_set_stage_events", "rla_decode", "rdn_decode")
 
 
 class rla_problem(ctypes.Structure):
@@ -69,6 +69,10 @@ def load_library():
     for name in ("rla_forward", "rdn_forward"):
         f = getattr(lib, name)
         f.argtypes = fwd_args
+        f.restype = ctypes.c_int
+    for name in ("rla_decode", "rdn_decode"):
+        f = getattr(lib, name)
+        f.argtypes = [pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp]
         f.restype = ctypes.c_int
     for name in ("rla_backward", "rdn_backward"):
         f = getattr(lib, name)
@@ -300,3 +304,52 @@ def rla_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, 
     return _backward("rla_backward", RLA_OP_RLA_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
                      out_dtype, use_saved)
+
+
+def _decode(name, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in, S_out, R_out, out,
+            stream, out_dtype):
+    torch = _torch()
+    lib = load_library()
+    if q.dim() != 4:
+        raise ValueError("decoding takes q, k, v as [B, T, H, d] (T tokens per sequence)")
+    problem = make_problem(q, v, None, clip, out_dtype, 0)
+    dev = q.device
+    _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
+                S_in=S_in, R_in=R_in, S_out=S_out, R_out=R_out), dev)
+    for t in (alpha_s, beta, alpha_r, gamma, S_in, R_in, S_out, R_out):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError("gates and states must be float32")
+    shape = (problem.batch, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
+    if S_out is None:
+        S_out = torch.empty(shape, dtype=torch.float32, device=dev)
+    if R_out is None:
+        R_out = torch.empty(shape, dtype=torch.float32, device=dev)
+    for nm, t in (("S_in", S_in), ("R_in", R_in), ("S_out", S_out), ("R_out", R_out)):
+        if t is not None and tuple(t.shape) != shape:
+            raise ValueError("%s must have shape %s" % (nm, shape))
+    odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
+    o = torch.empty(v.shape, dtype=odt, device=dev) if out is None else out
+    if o.dtype != odt or o.shape != v.shape:
+        raise ValueError("out must be %s with shape %s" % (odt, tuple(v.shape)))
+    st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
+                            _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S_in), _ptr(R_in),
+                            _ptr(o), _ptr(S_out), _ptr(R_out), _stream_handle(stream))
+    if st != RLA_OK:
+        raise RLAError(st, name)
+    return o, S_out, R_out
+
+
+def rla_decode(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S_in=None, R_in=None,
+               S_out=None, R_out=None, out=None, stream=None, out_dtype=None):
+    """RLA recurrent step (Sec. 3.4, left box, evaluated token by token):
+    q, k, v [B, T, H, d] with small T, gates [B, T, H].  Returns (o, S_out,
+    R_out); pass S_out=S_in, R_out=R_in to update the states in place."""
+    return _decode("rla_decode", q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in,
+                   S_out, R_out, out, stream, out_dtype)
+
+
+def rdn_decode(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S_in=None, R_in=None,
+               S_out=None, R_out=None, out=None, stream=None, out_dtype=None):
+    """RDN recurrent step (Sec. 3.4, right box); arguments as rla_decode."""
+    return _decode("rdn_decode", q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in,
+                   S_out, R_out, out, stream, out_dtype)

@@ -41,7 +41,8 @@ struct Workspace {
   size_t ckS_sc = 0, ckR_sc = 0, dS_sc = 0, dR_sc = 0;
 };
 
-rla_status check_problem(const rla_problem* pp, Problem& pr) {
+// recurrent: the decoding step, whose kernel has no fp32 d_k restriction
+rla_status check_problem(const rla_problem* pp, Problem& pr, bool recurrent = false) {
   if (!pp) return RLA_ERR_NULL_ARG;
   if (pp->dtype != RLA_F32 && pp->dtype != RLA_BF16) return RLA_ERR_DTYPE;
   if (pp->batch < 0 || pp->seq_len < 0 || pp->num_heads < 1) return RLA_ERR_SHAPE;
@@ -49,7 +50,7 @@ rla_status check_problem(const rla_problem* pp, Problem& pr) {
   const bool dk_ok = pp->head_dim_k == 64 || pp->head_dim_k == 128;
   const bool dv_ok = pp->head_dim_v == 64 || pp->head_dim_v == 128;
   if (!dk_ok || !dv_ok) return RLA_ERR_SHAPE;
-  if (pp->dtype == RLA_F32 && pp->head_dim_k != 64) return RLA_ERR_DTYPE;
+  if (!recurrent && pp->dtype == RLA_F32 && pp->head_dim_k != 64) return RLA_ERR_DTYPE;
   if (pp->out_dtype != RLA_F32 && pp->out_dtype != RLA_BF16) return RLA_ERR_DTYPE;
   if (pp->dtype == RLA_F32 && pp->out_dtype != RLA_F32) return RLA_ERR_DTYPE;
   if (isnan(pp->clip) || pp->clip < 0.f) return RLA_ERR_VALUE;
@@ -287,6 +288,62 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   return to_status(e);
 }
 
+
+// Byte ranges [a, a + bytes) and [b, b + bytes) intersect (NULL never does).
+bool ranges_overlap(const void* a, const void* b, size_t bytes) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  if (!a || !b) return false;
+  return x < y + bytes && y < x + bytes;
+}
+
+rla_status decode(bool rdn, const rla_problem* problem, const void* q, const void* k,
+                  const void* v, const float* alpha_s, const float* beta, const float* alpha_r,
+                  const float* gamma, const float* S_in, const float* R_in, void* o,
+                  float* S_out, float* R_out, void* stream_) {
+  Problem pr;
+  rla_status st = check_problem(problem, pr, /*recurrent=*/true);
+  if (st != RLA_OK) return st;
+  if (pr.varlen) return RLA_ERR_UNSUPPORTED;
+  if (pr.save || pr.use_saved) return RLA_ERR_VALUE;
+  if (pr.N * pr.H == 0) return RLA_OK;
+  if (!S_out || !R_out) return RLA_ERR_NULL_ARG;
+  if (pr.ntok > 0 && (!q || !k || !v || !alpha_s || !beta || !alpha_r || !gamma || !o))
+    return RLA_ERR_NULL_ARG;
+  if (pr.ntok > 0 && (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)))
+    return RLA_ERR_VALUE;
+  if ((S_in && !aligned16(S_in)) || (R_in && !aligned16(R_in)) || !aligned16(S_out) ||
+      !aligned16(R_out))
+    return RLA_ERR_VALUE;
+  const size_t sbytes = (size_t)pr.N * pr.H * pr.DK * pr.DV * sizeof(float);
+  // outputs may alias their own input exactly (in-place), nothing else
+  if ((S_in != S_out && ranges_overlap(S_in, S_out, sbytes)) ||
+      (R_in != R_out && ranges_overlap(R_in, R_out, sbytes)) ||
+      ranges_overlap(S_out, R_out, sbytes) || ranges_overlap(S_in, R_out, sbytes) ||
+      ranges_overlap(R_in, S_out, sbytes))
+    return RLA_ERR_VALUE;
+  if ((int64_t)pr.N * pr.H > INT32_MAX / 4 || pr.T > INT32_MAX) return RLA_ERR_SHAPE;
+
+  OpParams p;
+  p.H = (int32_t)pr.H;
+  p.DK = (int32_t)pr.DK;
+  p.DV = (int32_t)pr.DV;
+  p.ntok = pr.ntok;
+  p.clip = pr.clip;
+  p.rdn = rdn ? 1 : 0;
+  p.out_bf16 = pr.out_bf16 ? 1 : 0;
+  p.st.nseq = (int32_t)pr.N;
+  p.st.dense_T = pr.T;
+  p.q = q; p.k = k; p.v = v;
+  p.alpha_s = alpha_s; p.beta = beta; p.alpha_r = alpha_r; p.gamma = gamma;
+  p.S0 = S_in; p.R0 = R_in;
+  p.o = o; p.S_fin = S_out; p.R_fin = R_out;
+  hipStream_t stream = reinterpret_cast<hipStream_t>(stream_);
+  hipError_t e = mark_stage(stream, true);
+  if (e == hipSuccess) e = launch_decode(p, pr.bf16, stream);
+  if (e == hipSuccess) e = mark_stage(stream, false);
+  return to_status(e);
+}
+
 }  // namespace
 }  // namespace rla
 
@@ -361,6 +418,22 @@ rla_status rdn_backward(const rla_problem* problem, const void* q, const void* k
   return backward(true, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, dO, dS_final,
                   dR_final, dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0, workspace,
                   workspace_bytes, stream);
+}
+
+rla_status rla_decode(const rla_problem* problem, const void* q, const void* k, const void* v,
+                      const float* alpha_s, const float* beta, const float* alpha_r,
+                      const float* gamma, const float* S_in, const float* R_in, void* o,
+                      float* S_out, float* R_out, void* stream) {
+  return decode(false, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S_in, R_in, o, S_out,
+                R_out, stream);
+}
+
+rla_status rdn_decode(const rla_problem* problem, const void* q, const void* k, const void* v,
+                      const float* alpha_s, const float* beta, const float* alpha_r,
+                      const float* gamma, const float* S_in, const float* R_in, void* o,
+                      float* S_out, float* R_out, void* stream) {
+  return decode(true, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S_in, R_in, o, S_out,
+                R_out, stream);
 }
 
 }  // extern "C"

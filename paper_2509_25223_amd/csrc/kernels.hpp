@@ -95,4 +95,8 @@ hipError_t launch_bwd_scan(const OpParams& p, bool bf16, hipStream_t stream);
 // Chunk-parallel gradient contractions.
 hipError_t launch_bwd_grad(const OpParams& p, bool bf16, hipStream_t stream);
 
+// Recurrent step over T tokens per sequence (dense layout, st.dense_T = T,
+// st.nseq = B) with S0/R0 in (NULL = zeros) and S_fin/R_fin out.
+hipError_t launch_decode(const OpParams& p, bool bf16, hipStream_t stream);
+
 }  // namespace rla

@@ -123,3 +123,40 @@ def test_status_strings(lib):
     for s in range(8):
         assert rla.status_string(s)
     assert "workspace" in rla.status_string(5)
+
+
+def call_dec(lib, p, name="rdn_decode", **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, a=FAKE, b=FAKE, ar=FAKE, g=FAKE, Si=FAKE, Ri=FAKE + (1 << 30),
+             o=FAKE, So=FAKE, Ro=FAKE + (1 << 30))
+    a.update(kw)
+    return getattr(lib, name)(ctypes.byref(p) if p is not None else None, a["q"], a["k"], a["v"],
+                              a["a"], a["b"], a["ar"], a["g"], a["Si"], a["Ri"], a["o"],
+                              a["So"], a["Ro"], None)
+
+
+@pytest.mark.parametrize("name", ["rla_decode", "rdn_decode"])
+def test_decode_validation_errors(lib, name):
+    """The recurrent step validates on the host like the chunked calls; the
+    state buffers may alias exactly (in-place update) but not partially."""
+    p = prob(T=1)
+    assert call_dec(lib, None, name) == 1
+    assert call_dec(lib, p, name, So=None) == 1
+    assert call_dec(lib, p, name, Ro=None) == 1
+    assert call_dec(lib, p, name, q=None) == 1
+    assert call_dec(lib, prob(T=1, dk=96), name) == 2
+    assert call_dec(lib, prob(T=1, clip=-2.0), name) == 6
+    assert call_dec(lib, prob(B=1, T=1, cu=FAKE, N=1), name) == 4      # dense layout only
+    pf = prob(T=1)
+    pf.flags = rla.RLA_FLAG_SAVE_FOR_BACKWARD
+    assert call_dec(lib, pf, name) == 6
+    assert call_dec(lib, p, name, So=FAKE + 8) == 6                    # misaligned state
+    assert call_dec(lib, p, name, So=FAKE + 256) == 6                  # partial overlap with S_in
+    assert call_dec(lib, p, name, Ro=FAKE) == 6                        # S_out == R_out
+    # fp32 inputs with d_k = 128 are accepted by the recurrent step (validation
+    # passes and the call would launch), unlike the chunked forward: check the
+    # failure comes from a later argument instead
+    assert call_dec(lib, prob(T=1, dtype=rla.RLA_F32, dk=128), name, So=None) == 1
+    # an empty batch is a no-op that touches nothing
+    assert call_dec(lib, prob(B=0, T=1), name, So=None, Ro=None) == 0
+    # an output may not alias the other state's input
+    assert call_dec(lib, p, name, Ri=FAKE + (1 << 31), So=FAKE + (1 << 31)) == 6
