@@ -100,9 +100,9 @@ Workspace plan(const Problem& pr, int op) {
   w.gates = take(sizeof(float) * mc * H * kGateBlock);
   w.mats = take((pr.bf16 ? 2 : 4) * mc * H * kNumMats * kMatElems);
   if (op == RLA_OP_RDN_BACKWARD || op == RLA_OP_RLA_BACKWARD) {
-    // states: fp16 with per-(row, 32 columns) scales for bf16 inputs, fp32 otherwise
+    // states: fp16 with per-(16 rows, 32 columns) scales for bf16 inputs, fp32 otherwise
     const size_t st = (pr.bf16 ? 2 : 4) * mc * H * (size_t)pr.DK * (size_t)pr.DV;
-    const size_t sc = pr.bf16 ? sizeof(float) * mc * H * (size_t)pr.DK * (size_t)(pr.DV / 32) : 0;
+    const size_t sc = pr.bf16 ? sizeof(float) * mc * H * (size_t)(pr.DK / 16) * (size_t)(pr.DV / 32) : 0;
     w.ckS = take(st);
     w.ckR = take(st);
     w.mask = take((size_t)pr.ntok * H * (size_t)pr.DV);

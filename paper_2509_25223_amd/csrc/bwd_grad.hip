@@ -31,7 +31,7 @@
 // fragments; the token blocks are moved into LDS by LDS-DMA.
 //
 // Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation.  The
-// scans store the states in fp16 scaled by a power of two per (row, 32
+// scans store the states in fp16 scaled by a power of two per (16 rows, 32
 // columns); here each row is brought to one scale (its largest) when loaded,
 // and a contraction multiplies its result by that scale.
 #include <type_traits>
@@ -168,7 +168,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 
   // ---------------- phase 0: staging ----------------
   // A state's rows i0 .. i0+15 as MFMA B fragments (row = lane & 15), with
-  // the power-of-two scale of each (row, 32-column k-step) for fp16 states.
+  // the power-of-two scale of each (16-row tile, 32-column k-step) for fp16
+  // states.
   // The row's fp16 blocks are brought to one scale, the largest of its blocks
   // (power-of-two factors <= 1, applied in fp16): a block 2^10 or more below
   // the row's largest loses only entries under 2^-14 of that scale, far below
@@ -179,12 +180,12 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   };
   const void* srcs[4] = {p.ck_S, p.ck_R, p.dS_ws, p.dR_ws};
   const float* scs[4] = {p.ck_S_sc, p.ck_R_sc, p.dS_sc, p.dR_sc};
-  const int64_t sco = ((int64_t)c * H + h) * DK * (DV / 32);
+  const int64_t sco = ((int64_t)c * H + h) * (DK / 16) * (DV / 32);
   auto load_rows = [&](StateRows& x, int st, int i0) {
     const int i = i0 + (lane & 15);
     if constexpr (BF) {
       const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * DV;
-      const float* scp = scs[st] + sco + (int64_t)i * (DV / 32);
+      const float* scp = scs[st] + sco + (int64_t)(i >> 4) * (DV / 32);
       float sc[KSV], mx = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks) {

@@ -114,9 +114,9 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   constexpr int IT = DK / 64;
   constexpr int KS_STEPS = DK / MI::kStep;
   // store instructions per wave of the two checkpointed gradient states
-  // (save_state_f16: two row stores and one scale store per 16-row tile;
+  // (save_state_f16: one row store and one scale store per 16-row tile;
   // fp32: one per row)
-  constexpr int kCkptStores = 2 * (BF ? 3 * IT : 4 * IT * JT);
+  constexpr int kCkptStores = 2 * (BF ? 2 * IT : 4 * IT * JT);
   extern __shared__ __align__(16) unsigned char smem[];
   XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
   XT* QT = reinterpret_cast<XT*>(smem + L::kQT);
@@ -296,13 +296,13 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     };
 
     // gradient w.r.t. this chunk's end states for the gradient kernel,
-    // straight from the accumulators (bf16 inputs: fp16 scaled per (row, 32
-    // columns)).  Stored after the chunk's last prefetch, so that the wait
+    // straight from the accumulators (bf16 inputs: fp16 scaled per (16 rows,
+    // 32 columns)).  Stored after the chunk's last prefetch, so that the wait
     // for the prefetched data at the chunk's end leaves these stores in flight.
     auto save_ckpt = [&]() {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
       if constexpr (BF) {
-        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
+        const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
         save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + off, DV, p.dS_sc + so, DV / 32, w * (DK / 4));
         save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + off, DV, p.dR_sc + so, DV / 32, w * (DK / 4));
       } else {

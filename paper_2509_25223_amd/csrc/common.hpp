@@ -512,36 +512,49 @@ __device__ __forceinline__ uint32_t cvt_pk_f16(float a, float b) {
 
 // Saves one 32-column block of a state held in MFMA accumulators: tile
 // acc[it][jt] holds rows row0 + 16 it + acc_row(r) and columns
-// 16 jt + acc_col().  Each row is divided by its power-of-two scale
-// (pow2_scale_exp of the row's largest magnitude), stored as fp16 row-major
-// (row stride ld), and the scale goes to sc[row * sc_ld].  Two DPP exchanges
-// inside lane quads turn a lane's 4 rows x 1 column into 1 row x 4 columns,
-// so the rows leave in 8-byte stores.  Branch-free (lanes holding the same
-// row store its scale alike), so it can interleave with matrix work.
+// 16 jt + acc_col().  Each 16-row x 32-column tile is divided by one power of
+// two (pow2_scale_exp of the tile's largest magnitude) and stored as fp16
+// row-major (row stride ld); the scale goes to sc[(row0 / 16 + it) * sc_ld].
+// fp16 keeps 11 significant bits for every value within 2^-28 of the tile's
+// largest, so one scale per tile loses nothing a per-row scale would keep
+// for states whose rows span fewer than ~28 binades.  Three DPP exchanges
+// (lanes c^1, c^2 inside quads, then c^4 inside rows) turn a lane's 4 rows x
+// 1 column of both column tiles into 1 row x 8 consecutive columns, so each
+// tile leaves in one 16-byte store per lane (a wave writes 16 rows x 64 B).
 template <int IT>
 __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16* dst, int64_t ld,
                                                float* sc, int64_t sc_ld, int row0) {
   typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-  const int c = threadIdx.x & 15, q = (threadIdx.x & 63) >> 4;
-  const bool odd = c & 1, upper = c & 2;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63, c = lane & 15, q = lane >> 4, g = c >> 2;
+  const bool odd = c & 1, upper = c & 2, hi4 = g & 1;
   const int rho = ((c & 1) << 1) | ((c >> 1) & 1);   // row of the quad this lane stores
   // v_perm byte selectors over {recv:keep}: even lanes (keep, recv), odd (recv, keep)
   const uint32_t selA = odd ? 0x01000504u : 0x05040100u;
   const uint32_t selB = odd ? 0x03020706u : 0x07060302u;
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
-    int e[4];
-    float inv[4];
+    // tile maximum: in-lane, over the 16-lane row (DPP), over the 4 rows
+    uint32_t m = 0;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      e[r] = pow2_scale_exp(row16_absmax_bits(acc[it][0][r], acc[it][1][r]));
-      inv[r] = exp2_int(-e[r]);
-    }
-    const int64_t row = row0 + 16 * it + 4 * q + rho;
+    for (int jt = 0; jt < 2; ++jt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m = max(m, __float_as_uint(acc[it][jt][r]) & 0x7FFFFFFFu);
+    m = max(m, dpp_u32<0xB1>(m));
+    m = max(m, dpp_u32<0x4E>(m));
+    m = max(m, dpp_u32<0x141>(m));
+    m = max(m, dpp_u32<0x140>(m));
+    const uint32_t mt = max(max((uint32_t)__builtin_amdgcn_readlane((int)m, 0),
+                                (uint32_t)__builtin_amdgcn_readlane((int)m, 16)),
+                            max((uint32_t)__builtin_amdgcn_readlane((int)m, 32),
+                                (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
+    const int e = pow2_scale_exp(mt);
+    const float inv = exp2_int(-e);
+    u32x2 out[2];
 #pragma unroll
     for (int jt = 0; jt < 2; ++jt) {
-      const uint32_t p01 = cvt_pk_f16(acc[it][jt][0] * inv[0], acc[it][jt][1] * inv[1]);
-      const uint32_t p23 = cvt_pk_f16(acc[it][jt][2] * inv[2], acc[it][jt][3] * inv[3]);
+      const uint32_t p01 = cvt_pk_f16(acc[it][jt][0] * inv, acc[it][jt][1] * inv);
+      const uint32_t p23 = cvt_pk_f16(acc[it][jt][2] * inv, acc[it][jt][3] * inv);
       // round 1, lanes c and c^1: even lanes end with rows 0, 1 and odd
       // lanes with rows 2, 3, each as a column pair
       const uint32_t keep = odd ? p23 : p01;
@@ -550,11 +563,20 @@ __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16*
       const uint32_t b = __builtin_amdgcn_perm(recv, keep, selB);
       // round 2, lanes c and c^2: each lane ends with one row, 4 columns
       const uint32_t recv2 = dpp_u32<0x4E>(upper ? a : b);
-      const u32x2 out = upper ? u32x2{recv2, b} : u32x2{a, recv2};
-      *reinterpret_cast<u32x2*>(dst + row * ld + 16 * jt + (c & ~3)) = out;
+      out[jt] = upper ? u32x2{recv2, b} : u32x2{a, recv2};
     }
-    const int er = odd ? (upper ? e[3] : e[2]) : (upper ? e[1] : e[0]);   // e[rho]
-    sc[row * sc_ld] = exp2_int(er);
+    // round 3, lanes c and c^4 (column groups g, g^1): the lower lane keeps
+    // its tile-0 columns and takes its partner's, the upper lane the same
+    // for tile 1 (row_shl:4 / row_shr:4 stay inside the 16-lane row)
+    const u32x2 snd = hi4 ? out[0] : out[1];
+    const uint32_t fromR0 = dpp_u32<0x104>(snd.x), fromR1 = dpp_u32<0x104>(snd.y);   // lane c + 4
+    const uint32_t fromL0 = dpp_u32<0x114>(snd.x), fromL1 = dpp_u32<0x114>(snd.y);   // lane c - 4
+    const u32x4 v = hi4 ? u32x4{fromL0, fromL1, out[1].x, out[1].y}
+                        : u32x4{out[0].x, out[0].y, fromR0, fromR1};
+    const int64_t row = row0 + 16 * it + 4 * q + rho;
+    const int col = hi4 ? 16 + 4 * (g - 1) : 4 * g;
+    *reinterpret_cast<u32x4*>(dst + row * ld + col) = v;
+    if (lane == 0) sc[(int64_t)(row0 / 16 + it) * sc_ld] = exp2_int(e);
   }
 }
 

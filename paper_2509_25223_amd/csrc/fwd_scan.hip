@@ -110,8 +110,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   constexpr int IT = DK / 64;        // state row tiles per wave
   constexpr int KS_STEPS = DK / MI::kStep;
   // store instructions per wave of the two checkpointed states (save_state_f16:
-  // two row stores and one scale store per 16-row tile; fp32: one per row)
-  constexpr int kCkptStores = 2 * (BF ? 3 * IT : 4 * IT * JT);
+  // one row store and one scale store per 16-row tile; fp32: one per row)
+  constexpr int kCkptStores = 2 * (BF ? 2 * IT : 4 * IT * JT);
   extern __shared__ __align__(16) unsigned char smem[];
   XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
   IN* Shi = reinterpret_cast<IN*>(smem + L::kCopies);
@@ -390,13 +390,13 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     barrier_lds();
     if (c + 1 < nch) issue_late(c + 1);
     // chunk-start states for the gradient kernel, straight from the
-    // accumulators (bf16 inputs: fp16 scaled per (row, 32 columns)).  Stored
+    // accumulators (bf16 inputs: fp16 scaled per (16 rows, 32 columns)).  Stored
     // after the chunk's last prefetch, so that the wait for the prefetched
     // data at the chunk's end does not also wait for these stores.
     if constexpr (CKPT) {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
       if constexpr (BF) {
-        const int64_t so = ((int64_t)gc * H + h) * DK * (DV / 32) + j0 / 32;
+        const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
         save_state_f16<IT>(Sacc, reinterpret_cast<f16*>(p.ck_S) + off, DV, p.ck_S_sc + so, DV / 32, w * (DK / 4));
         save_state_f16<IT>(Racc, reinterpret_cast<f16*>(p.ck_R) + off, DV, p.ck_R_sc + so, DV / 32, w * (DK / 4));
       } else {
