@@ -184,12 +184,14 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   auto load_rows = [&](StateRows& x, int st, int i0) {
     const int i = i0 + (lane & 15);
     if constexpr (BF) {
-      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * DV;
+      // blocked layout [DV / 32][DK][32]: k-step ks is column block ks
+      static_assert(M::kStep == 32, "one 32-column block per k-step");
+      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * 32;
       const float* scp = scs[st] + sco + (int64_t)(i >> 4) * (DV / 32);
       float sc[KSV], mx = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks) {
-        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + ks * M::kStep + 8 * (lane >> 4));
+        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + (int64_t)ks * DK * 32 + 8 * (lane >> 4));
         sc[ks] = scp[ks];
         mx = fmaxf(mx, sc[ks]);
       }

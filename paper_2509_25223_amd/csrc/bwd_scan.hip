@@ -301,10 +301,11 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     // for the prefetched data at the chunk's end leaves these stores in flight.
     auto save_ckpt = [&]() {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
-      if constexpr (BF) {
+      if constexpr (BF) {   // blocked [DV / 32][DK][32]: each wave store is 1 KiB contiguous
+        const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
         const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
-        save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + off, DV, p.dS_sc + so, DV / 32, w * (DK / 4));
-        save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + off, DV, p.dR_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + ob, 32, p.dS_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + ob, 32, p.dR_sc + so, DV / 32, w * (DK / 4));
       } else {
         save_state_f32<IT, JT>(dS, reinterpret_cast<float*>(p.dS_ws) + off, DV, w * (DK / 4));
         save_state_f32<IT, JT>(dR, reinterpret_cast<float*>(p.dR_ws) + off, DV, w * (DK / 4));

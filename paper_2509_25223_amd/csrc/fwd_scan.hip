@@ -395,10 +395,11 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     // data at the chunk's end does not also wait for these stores.
     if constexpr (CKPT) {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
-      if constexpr (BF) {
+      if constexpr (BF) {   // blocked [DV / 32][DK][32]: each wave store is 1 KiB contiguous
+        const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
         const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
-        save_state_f16<IT>(Sacc, reinterpret_cast<f16*>(p.ck_S) + off, DV, p.ck_S_sc + so, DV / 32, w * (DK / 4));
-        save_state_f16<IT>(Racc, reinterpret_cast<f16*>(p.ck_R) + off, DV, p.ck_R_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(Sacc, reinterpret_cast<f16*>(p.ck_S) + ob, 32, p.ck_S_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16<IT>(Racc, reinterpret_cast<f16*>(p.ck_R) + ob, 32, p.ck_R_sc + so, DV / 32, w * (DK / 4));
       } else {
         save_state_f32<IT, JT>(Sacc, reinterpret_cast<float*>(p.ck_S) + off, DV, w * (DK / 4));
         save_state_f32<IT, JT>(Racc, reinterpret_cast<float*>(p.ck_R) + off, DV, w * (DK / 4));
