@@ -34,6 +34,12 @@ _lib = None
 
 RLA = 0
 RDN = 1
+# variant bits (combine with `flags=`): the log-cosh residual r = c tanh(x / c)
+# (App. B), the ungated output S_{t-1} q + R_t q (Sec. 4.3 ablation), the
+# decayed residual x = v - aS S_{t-1} k (Table 1's gated prediction)
+TANH = 2
+UNGATED = 4
+DECAYED = 8
 
 
 def build(force: bool = True) -> str:
@@ -77,11 +83,13 @@ def threads() -> int:
     return int(_load().orc_threads())
 
 
-def _variant(name) -> int:
+def _variant(name, flags: int = 0) -> int:
+    if flags & ~(TANH | UNGATED | DECAYED):
+        raise ValueError("unknown variant flags")
     if name in ("rdn", RDN):
-        return RDN
+        return RDN | flags
     if name in ("rla", RLA):
-        return RLA
+        return RLA | flags
     raise ValueError("variant must be 'rla' or 'rdn'")
 
 
@@ -130,14 +138,15 @@ def _clip_arg(clip: float) -> float:
 
 
 def forward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, clip=1.0,
-            S0=None, R0=None, cu_seqlens=None):
-    """Token-recurrent fp64 forward.  Returns (o, S_final, R_final)."""
+            S0=None, R0=None, cu_seqlens=None, flags=0):
+    """Token-recurrent fp64 forward.  Returns (o, S_final, R_final).
+    flags: any of TANH, UNGATED, DECAYED."""
     lib = _load()
     p = _Prob(q, k, v, (alpha_s, beta, alpha_r, gamma), cu_seqlens, S0, R0)
     o = np.zeros((p.ntok, p.H, p.dv))
     Sf = np.zeros((p.N, p.H, p.dk, p.dv))
     Rf = np.zeros((p.N, p.H, p.dk, p.dv))
-    rc = lib.orc_forward(_variant(variant), p.N, _ptr(p.cu), p.ntok, p.H, p.dk, p.dv,
+    rc = lib.orc_forward(_variant(variant, flags), p.N, _ptr(p.cu), p.ntok, p.H, p.dk, p.dv,
                          _ptr(p.q), _ptr(p.k), _ptr(p.v), *[_ptr(g) for g in p.gates],
                          _clip_arg(clip), _ptr(p.S0), _ptr(p.R0), _ptr(o), _ptr(Sf), _ptr(Rf))
     if rc != 0:
@@ -146,7 +155,7 @@ def forward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, clip=1.0,
 
 
 def backward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip=1.0,
-             S0=None, R0=None, dS_final=None, dR_final=None, cu_seqlens=None):
+             S0=None, R0=None, dS_final=None, dR_final=None, cu_seqlens=None, flags=0):
     """Adjoint of ``forward`` for L = <dO,o> + <dS_final,S_T> + <dR_final,R_T>.
 
     Returns a dict with dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0.
@@ -162,7 +171,7 @@ def backward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip=1.0,
                dbeta=np.zeros((p.ntok, p.H)), dalpha_r=np.zeros((p.ntok, p.H)),
                dgamma=np.zeros((p.ntok, p.H)), dS0=np.zeros((p.N, p.H, p.dk, p.dv)),
                dR0=np.zeros((p.N, p.H, p.dk, p.dv)))
-    rc = lib.orc_backward(_variant(variant), p.N, _ptr(p.cu), p.ntok, p.H, p.dk, p.dv,
+    rc = lib.orc_backward(_variant(variant, flags), p.N, _ptr(p.cu), p.ntok, p.H, p.dk, p.dv,
                           _ptr(p.q), _ptr(p.k), _ptr(p.v), *[_ptr(g) for g in p.gates],
                           _clip_arg(clip), _ptr(p.S0), _ptr(p.R0), _ptr(dO_), _ptr(dSf),
                           _ptr(dRf), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
@@ -176,7 +185,7 @@ def backward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip=1.0,
 
 
 def nudge_margin(variant, q, k, v, alpha_s, beta, alpha_r, gamma, clip=1.0, S0=None, R0=None,
-                 cu_seqlens=None, margin=1e-2, grid="bf16"):
+                 cu_seqlens=None, margin=1e-2, grid="bf16", flags=0):
     """Returns (v_moved, count): v moved so that every pre-clip residual stays
     at least ``margin`` away from the clip kink |x| = c, with moved values kept
     on the input dtype's grid (grid in {'bf16', 'f32', 'f64'}).  Gradient
@@ -186,7 +195,7 @@ def nudge_margin(variant, q, k, v, alpha_s, beta, alpha_r, gamma, clip=1.0, S0=N
     p = _Prob(q, k, v, (alpha_s, beta, alpha_r, gamma), cu_seqlens, S0, R0)
     vv = p.v.copy()
     bits = {"bf16": 16, "f32": 0, "f64": 64}[grid]
-    moved = lib.orc_nudge_margin(_variant(variant), p.N, _ptr(p.cu), p.ntok, p.H, p.dk, p.dv,
+    moved = lib.orc_nudge_margin(_variant(variant, flags), p.N, _ptr(p.cu), p.ntok, p.H, p.dk, p.dv,
                                  _ptr(p.q), _ptr(p.k), _ptr(vv), *[_ptr(g) for g in p.gates],
                                  _clip_arg(clip), _ptr(p.S0), _ptr(p.R0), float(margin), bits)
     if moved < 0:

@@ -27,6 +27,13 @@ local index t = 1..C, start states S0, R0):
       o_t = b_t + gamma_t c_t
   Chunk-end states: S_C = e^{g_C} S0 + sum_i e^{g_C-g_i} u_i k_i^T, same for R.
   RLA: T = I on both paths, u_t = b_t v_t and uR_t = gamma_t r_t.
+Variants (keyword flags):
+  tanh     r_t = c tanh(x_t / c) instead of the clip (log-cosh loss, App. B);
+  ungated  o_t = S_{t-1} q_t + R_t q_t: the read-out of S uses the same
+           decays as p_t, b'_t = e^{g_{t-1}} S0 q_t + sum_{i<t} e^{g_{t-1}-g_i} P_ti u_i,
+           and o_t = b'_t + c_t;
+  decayed  x_t = v_t - aS_t S_{t-1} k_t: the prediction uses the decays of b_t,
+           p~_t = e^{g_t} S0 k_t + sum_{i<t} e^{g_t-g_i} G_ti u_i.
 """
 from __future__ import annotations
 
@@ -39,6 +46,14 @@ def _clip(x, c):
     return x if (c is None or math.isinf(c)) else np.clip(x, -c, c)
 
 
+def _tanh_resid(x, c):
+    if c is None or math.isinf(c):
+        return x
+    if c == 0:
+        return np.zeros_like(x)
+    return c * np.tanh(x / c)
+
+
 def _solve_unit_lower(A, rhs):
     """(I + A) X = rhs for strictly-lower A, by forward substitution."""
     C = A.shape[0]
@@ -48,7 +63,8 @@ def _solve_unit_lower(A, rhs):
     return X
 
 
-def chunk_step(variant, Q, K, V, aS, b, aR, g, clip, S0, R0):
+def chunk_step(variant, Q, K, V, aS, b, aR, g, clip, S0, R0, tanh=False, ungated=False,
+               decayed=False):
     """One chunk.  Q, K: [C, dk]; V: [C, dv]; gates: [C]; S0, R0: [dv, dk]
     (paper orientation).  Returns (O [C, dv], S_C, R_C)."""
     C = Q.shape[0]
@@ -71,23 +87,29 @@ def chunk_step(variant, Q, K, V, aS, b, aR, g, clip, S0, R0):
         U = _solve_unit_lower(A, b[:, None] * (V - np.exp(gs)[:, None] * KS))
     else:
         U = b[:, None] * V
-    p = np.exp(gs_prev)[:, None] * KS + (dec_s_prev * G * lower_strict) @ U
-    base = np.exp(gs)[:, None] * QS + (dec_s * P * lower_strict) @ U
-    r = _clip(V - p, clip)
+    if decayed:
+        p = np.exp(gs)[:, None] * KS + (dec_s * G * lower_strict) @ U
+    else:
+        p = np.exp(gs_prev)[:, None] * KS + (dec_s_prev * G * lower_strict) @ U
+    if ungated:
+        base = np.exp(gs_prev)[:, None] * QS + (dec_s_prev * P * lower_strict) @ U
+    else:
+        base = np.exp(gs)[:, None] * QS + (dec_s * P * lower_strict) @ U
+    r = _tanh_resid(V - p, clip) if tanh else _clip(V - p, clip)
     if variant == "rdn":
         AR = g[:, None] * dec_r * G * lower_strict
         UR = _solve_unit_lower(AR, g[:, None] * (r - np.exp(gr)[:, None] * KR))
     else:
         UR = g[:, None] * r
     corr = np.exp(gr)[:, None] * QR + (dec_r * P * lower) @ UR
-    O = base + g[:, None] * corr
+    O = base + (corr if ungated else g[:, None] * corr)
     S1 = math.exp(gs[-1]) * S0 + (np.exp(gs[-1] - gs)[:, None] * U).T @ K
     R1 = math.exp(gr[-1]) * R0 + (np.exp(gr[-1] - gr)[:, None] * UR).T @ K
     return O, S1, R1
 
 
 def forward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, clip=1.0, S0=None, R0=None,
-            cu_seqlens=None, chunk=64):
+            cu_seqlens=None, chunk=64, **flags):
     """Chunked forward with the same conventions as ``oracle.forward``:
     q, k [ntok, H, dk], v [ntok, H, dv], gates [ntok, H], states [N, H, dk, dv]
     (transposed storage).  Chunks restart at every sequence start; the last
@@ -109,7 +131,7 @@ def forward(variant, q, k, v, alpha_s, beta, alpha_r, gamma, clip=1.0, S0=None, 
                 c1 = min(c0 + chunk, int(cu[n + 1]))
                 sl = slice(c0, c1)
                 O, S, R = chunk_step(variant, q[sl, h], k[sl, h], v[sl, h],
-                                     *[gg[sl, h] for gg in gates], clip, S, R)
+                                     *[gg[sl, h] for gg in gates], clip, S, R, **flags)
                 o[sl, h] = O
             Sf[n, h] = S.T
             Rf[n, h] = R.T

@@ -47,6 +47,22 @@
  *             dv += b w ;  dk += -aS b (S_{t-1}^T w + dS_t^T S_{t-1} k) + b dS_t^T v
  * (RLA drops every term that comes from the (I - . k k^T) factors.)
  * The clip's derivative is taken as 1 on the closed interval [-c, c].
+ *
+ * Variants (bits of `variant` above bit 0, which selects RDN over RLA):
+ *   ORC_TANH     r_t = c tanh(x_t / c): the negative gradient of the scaled
+ *                log-cosh loss c^2 log cosh((v - v_hat) / c), the robust
+ *                alternative to the clipped residual of App. B (c = 1 is the
+ *                paper's plain tanh; c = inf gives r = x, c = 0 gives r = 0).
+ *                Its derivative 1 - tanh^2(x / c) replaces the clip mask.
+ *   ORC_UNGATED  o_t = S_{t-1} q_t + R_t q_t, the ungated output combination
+ *                of the ablation in Sec. 4.3.
+ *   ORC_DECAYED  x_t = v_t - aS_t S_{t-1} k_t, the residual of the decayed
+ *                prediction (the prediction of Table 1's gated rows) in place
+ *                of the boxed v_t - S_{t-1} k_t.
+ * Backward with the variants: the output adjoint loses its aS and g factors
+ * (UNGATED); dx = phi'(x) dr with phi' the derivative of the residual
+ * function (TANH); the residual's adjoint carries the factor aS and adds
+ * daS -= dx.(S_{t-1} k) (DECAYED).
  */
 #include <math.h>
 #include <stdint.h>
@@ -55,6 +71,9 @@
 
 #define ORC_RLA 0
 #define ORC_RDN 1
+#define ORC_TANH 2
+#define ORC_UNGATED 4
+#define ORC_DECAYED 8
 #define CKPT 64
 
 static double clip_value(double x, double c) {
@@ -67,6 +86,23 @@ static double clip_value(double x, double c) {
 static int clip_passes(double x, double c) {
     if (c < 0.0) return 1;
     return (x >= -c && x <= c) ? 1 : 0;
+}
+
+/* residual function r = phi(x) and its derivative phi'(x) */
+static double resid_value(int variant, double x, double c) {
+    if (!(variant & ORC_TANH)) return clip_value(x, c);
+    if (c < 0.0) return x;
+    if (c == 0.0) return 0.0;
+    return c * tanh(x / c);
+}
+
+static double resid_slope(int variant, double x, double c) {
+    double th;
+    if (!(variant & ORC_TANH)) return clip_passes(x, c) ? 1.0 : 0.0;
+    if (c < 0.0) return 1.0;
+    if (c == 0.0) return 0.0;
+    th = tanh(x / c);
+    return 1.0 - th * th;
 }
 
 /* Scratch for one (sequence, head) pair. */
@@ -91,16 +127,18 @@ static void forward_token(int variant, int64_t dk, int64_t dv,
                           double aS, double b, double aR, double g, double c,
                           double *S, double *R, double *o, fwd_scratch *w) {
     int64_t i, j;
-    /* S_{t-1} k_t and the residual x_t = v_t - S_{t-1} k_t, then r_t. */
+    const double eps = (variant & ORC_DECAYED) ? aS : 1.0;
+    /* S_{t-1} k_t and the residual x_t = v_t - S_{t-1} k_t (DECAYED:
+       v_t - aS_t S_{t-1} k_t), then r_t = phi(x_t). */
     for (j = 0; j < dv; ++j) {
         double acc = 0.0;
         for (i = 0; i < dk; ++i) acc += S[i * dv + j] * k[i];
         w->Sk[j] = acc;
-        w->x[j] = v[j] - acc;
-        w->r[j] = clip_value(w->x[j], c);
+        w->x[j] = v[j] - eps * acc;
+        w->r[j] = resid_value(variant, w->x[j], c);
     }
     /* R_t from R_{t-1}. */
-    if (variant == ORC_RDN) {
+    if (variant & ORC_RDN) {
         for (j = 0; j < dv; ++j) {
             double acc = 0.0;
             for (i = 0; i < dk; ++i) acc += R[i * dv + j] * k[i];
@@ -114,7 +152,7 @@ static void forward_token(int variant, int64_t dk, int64_t dv,
             for (j = 0; j < dv; ++j)
                 R[i * dv + j] = aR * R[i * dv + j] + g * k[i] * w->r[j];
     }
-    /* o_t = aS S_{t-1} q_t + g R_t q_t. */
+    /* o_t = aS S_{t-1} q_t + g R_t q_t (UNGATED: S_{t-1} q_t + R_t q_t). */
     if (o) {
         for (j = 0; j < dv; ++j) {
             double sq = 0.0, rq = 0.0;
@@ -122,11 +160,11 @@ static void forward_token(int variant, int64_t dk, int64_t dv,
                 sq += S[i * dv + j] * q[i];
                 rq += R[i * dv + j] * q[i];
             }
-            o[j] = aS * sq + g * rq;
+            o[j] = (variant & ORC_UNGATED) ? sq + rq : aS * sq + g * rq;
         }
     }
     /* S_t from S_{t-1}. */
-    if (variant == ORC_RDN) {
+    if (variant & ORC_RDN) {
         for (i = 0; i < dk; ++i)
             for (j = 0; j < dv; ++j)
                 S[i * dv + j] = aS * (S[i * dv + j] - b * k[i] * w->Sk[j]) + b * k[i] * v[j];
@@ -226,7 +264,7 @@ int64_t orc_nudge_margin(int variant, int64_t nseq, const int64_t *cu, int64_t n
     int64_t moved = 0;
     int failed = 0;
     int64_t pair;
-    if (clip < 0.0) return 0;
+    if (clip < 0.0 || (variant & ORC_TANH)) return 0;   /* no kink */
 #pragma omp parallel for schedule(dynamic, 1) reduction(+ : moved) reduction(| : failed)
     for (pair = 0; pair < nseq * H; ++pair) {
         int64_t n = pair / H, h = pair % H, t, i, j;
@@ -246,6 +284,7 @@ int64_t orc_nudge_margin(int variant, int64_t nseq, const int64_t *cu, int64_t n
                 double p = 0.0;
                 int tries;
                 for (i = 0; i < dk; ++i) p += S[i * dv + j] * kt[i];
+                if (variant & ORC_DECAYED) p *= alpha_s[th];
                 for (tries = 0; tries < 8; ++tries) {
                     double x = vt[j] - p, ax = fabs(x), target_x, nv;
                     if (fabs(ax - clip) >= margin) break;
@@ -355,6 +394,9 @@ int orc_backward(int variant, int64_t nseq, const int64_t *cu, int64_t ntok,
                 double aS = alpha_s[th], b = beta[th], aR = alpha_r[th], g = gamma[th];
                 double *dqt = dq + th * dk, *dkt = dk_out + th * dk, *dvt = dv_out + th * dv;
                 double das = 0.0, dbb = 0.0, dar = 0.0, dg = 0.0;
+                const double eps = (variant & ORC_DECAYED) ? aS : 1.0;
+                const double wS = (variant & ORC_UNGATED) ? 1.0 : aS;   /* output weights */
+                const double wR = (variant & ORC_UNGATED) ? 1.0 : g;
                 /* recompute this token's forward quantities */
                 for (j = 0; j < dv; ++j) {
                     double sk = 0.0, rk = 0.0, sq = 0.0;
@@ -364,12 +406,12 @@ int orc_backward(int variant, int64_t nseq, const int64_t *cu, int64_t ntok,
                         sq += Sp[i * dv + j] * qt[i];
                     }
                     Sk[j] = sk; Rk[j] = rk; Sq[j] = sq;
-                    x[j] = vt[j] - sk;
-                    r[j] = clip_value(x[j], clip);
+                    x[j] = vt[j] - eps * sk;
+                    r[j] = resid_value(variant, x[j], clip);
                 }
                 for (i = 0; i < dk; ++i)
                     for (j = 0; j < dv; ++j) {
-                        if (variant == ORC_RDN)
+                        if (variant & ORC_RDN)
                             Rn[i * dv + j] = aR * (Rp[i * dv + j] - g * kt[i] * Rk[j]) + g * kt[i] * r[j];
                         else
                             Rn[i * dv + j] = aR * Rp[i * dv + j] + g * kt[i] * r[j];
@@ -379,23 +421,25 @@ int orc_backward(int variant, int64_t nseq, const int64_t *cu, int64_t ntok,
                     for (i = 0; i < dk; ++i) rq += Rn[i * dv + j] * qt[i];
                     Rq[j] = rq;
                 }
-                /* output o_t = aS S_{t-1} q + g R_t q */
+                /* output o_t = wS S_{t-1} q + wR R_t q (wS = aS, wR = g; UNGATED: 1, 1) */
                 for (i = 0; i < dk; ++i) {
                     double a1 = 0.0, a2 = 0.0;
                     for (j = 0; j < dv; ++j) {
                         a1 += Sp[i * dv + j] * dot[j];
                         a2 += Rn[i * dv + j] * dot[j];
                     }
-                    dqt[i] += aS * a1 + g * a2;
+                    dqt[i] += wS * a1 + wR * a2;
                 }
-                for (j = 0; j < dv; ++j) {
-                    das += dot[j] * Sq[j];
-                    dg += dot[j] * Rq[j];
+                if (!(variant & ORC_UNGATED)) {
+                    for (j = 0; j < dv; ++j) {
+                        das += dot[j] * Sq[j];
+                        dg += dot[j] * Rq[j];
+                    }
                 }
                 for (i = 0; i < dk; ++i)
                     for (j = 0; j < dv; ++j) {
-                        DR[i * dv + j] = dR[i * dv + j] + g * qt[i] * dot[j];
-                        dSp[i * dv + j] = aS * qt[i] * dot[j];
+                        DR[i * dv + j] = dR[i * dv + j] + wR * qt[i] * dot[j];
+                        dSp[i * dv + j] = wS * qt[i] * dot[j];
                     }
                 /* R update */
                 for (j = 0; j < dv; ++j) {
@@ -404,7 +448,7 @@ int orc_backward(int variant, int64_t nseq, const int64_t *cu, int64_t ntok,
                     z[j] = acc;
                     dr[j] = g * acc;
                 }
-                if (variant == ORC_RDN) {
+                if (variant & ORC_RDN) {
                     for (i = 0; i < dk; ++i) {
                         double rz = 0.0, drrk = 0.0, drr = 0.0;
                         for (j = 0; j < dv; ++j) {
@@ -432,18 +476,19 @@ int orc_backward(int variant, int64_t nseq, const int64_t *cu, int64_t ntok,
                     for (i = 0; i < dk; ++i)
                         for (j = 0; j < dv; ++j) dR[i * dv + j] = aR * DR[i * dv + j];
                 }
-                /* clip */
+                /* residual function, then x = v - eps S_{t-1} k */
                 for (j = 0; j < dv; ++j) {
-                    dx[j] = clip_passes(x[j], clip) ? dr[j] : 0.0;
+                    dx[j] = resid_slope(variant, x[j], clip) * dr[j];
                     dvt[j] += dx[j];
+                    if (variant & ORC_DECAYED) das -= dx[j] * Sk[j];
                 }
                 for (i = 0; i < dk; ++i) {
                     double acc = 0.0;
                     for (j = 0; j < dv; ++j) {
-                        dSp[i * dv + j] -= kt[i] * dx[j];
+                        dSp[i * dv + j] -= eps * kt[i] * dx[j];
                         acc += Sp[i * dv + j] * dx[j];
                     }
-                    dkt[i] -= acc;
+                    dkt[i] -= eps * acc;
                 }
                 /* S update */
                 for (j = 0; j < dv; ++j) {
@@ -451,7 +496,7 @@ int orc_backward(int variant, int64_t nseq, const int64_t *cu, int64_t ntok,
                     for (i = 0; i < dk; ++i) acc += dS[i * dv + j] * kt[i];
                     ww[j] = acc;
                 }
-                if (variant == ORC_RDN) {
+                if (variant & ORC_RDN) {
                     for (i = 0; i < dk; ++i) {
                         double sw = 0.0, dssk = 0.0, dsv = 0.0;
                         for (j = 0; j < dv; ++j) {
