@@ -119,6 +119,25 @@ typedef struct {
 #define RLA_FLAG_SAVE_FOR_BACKWARD 1u
 #define RLA_FLAG_USE_SAVED 2u
 
+/*
+ * Variants of the operator (flags, any combination; every entry point
+ * supports them, forward, backward and decoding alike):
+ *   RLA_FLAG_RESIDUAL_TANH    r_t = c tanh(x_t / c): the negative gradient of
+ *       the log-cosh loss c^2 log cosh((v - v_hat) / c), the robust
+ *       alternative to the clip of App. B (c = 1 is the paper's plain tanh;
+ *       c = +INFINITY gives r = x, c = 0 gives r = 0).
+ *   RLA_FLAG_UNGATED_OUTPUT   o_t = S_{t-1} q_t + R_t q_t, the ungated output
+ *       combination of the ablation in Sec. 4.3.
+ *   RLA_FLAG_DECAYED_RESIDUAL x_t = v_t - aS_t S_{t-1} k_t, the residual of
+ *       the decayed prediction (the gated rows of Table 1) instead of the
+ *       boxed v_t - S_{t-1} k_t.
+ * A backward with RLA_FLAG_USE_SAVED must carry the variant flags of the
+ * saving forward.
+ */
+#define RLA_FLAG_RESIDUAL_TANH 4u
+#define RLA_FLAG_UNGATED_OUTPUT 8u
+#define RLA_FLAG_DECAYED_RESIDUAL 16u
+
 /* Bytes of workspace the operation needs for this problem (0 if the problem
  * is invalid).  Pure host function. */
 size_t rla_workspace_size(const rla_problem *problem, int op);

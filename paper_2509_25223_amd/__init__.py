@@ -25,6 +25,8 @@ LIB_PATH = os.path.join(_HERE, "librla_mi355x.so")
 
 RLA_OK = 0
 RLA_FLAG_SAVE_FOR_BACKWARD, RLA_FLAG_USE_SAVED = 1, 2
+# variants (include/rla.h): log-cosh residual, ungated output, decayed residual
+RLA_FLAG_RESIDUAL_TANH, RLA_FLAG_UNGATED_OUTPUT, RLA_FLAG_DECAYED_RESIDUAL = 4, 8, 16
 RLA_F32, RLA_BF16 = 0, 1
 RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD, RLA_OP_RLA_BACKWARD = 0, 1, 2, 3
 
@@ -193,12 +195,20 @@ def _workspace(problem, op, device, workspace):
     return torch.empty(max(need, 1), dtype=torch.uint8, device=device), need
 
 
+def _variant_bits(variants: int) -> int:
+    if variants & ~(RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT | RLA_FLAG_DECAYED_RESIDUAL):
+        raise ValueError("variants must combine RLA_FLAG_RESIDUAL_TANH, "
+                         "RLA_FLAG_UNGATED_OUTPUT and RLA_FLAG_DECAYED_RESIDUAL")
+    return int(variants)
+
+
 def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_seqlens,
-             out, workspace, stream, return_states, out_dtype, save_for_backward):
+             out, workspace, stream, return_states, out_dtype, save_for_backward, variants=0):
     torch = _torch()
     lib = load_library()
     problem = make_problem(q, v, cu_seqlens, clip, out_dtype,
-                           RLA_FLAG_SAVE_FOR_BACKWARD if save_for_backward else 0)
+                           (RLA_FLAG_SAVE_FOR_BACKWARD if save_for_backward else 0) |
+                           _variant_bits(variants))
     if save_for_backward:
         op = RLA_OP_RDN_BACKWARD if op == RLA_OP_RDN_FORWARD else RLA_OP_RLA_BACKWARD
     dev = q.device
@@ -228,35 +238,37 @@ def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_
 
 def rla_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
                 cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
-                out_dtype=None, save_for_backward=False):
+                out_dtype=None, save_for_backward=False, variants=0):
     """RLA forward (Sec. 3.4, left box).  Returns (o, S_final, R_final).
     With save_for_backward the (backward-sized) workspace keeps what the
-    matching backward call with use_saved=True reads instead of recomputing."""
+    matching backward call with use_saved=True reads instead of recomputing.
+    variants: RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT |
+    RLA_FLAG_DECAYED_RESIDUAL bits (include/rla.h)."""
     return _forward("rla_forward", RLA_OP_RLA_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                     clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
-                    save_for_backward)
+                    save_for_backward, variants)
 
 
 def rdn_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
                 cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
-                out_dtype=None, save_for_backward=False):
+                out_dtype=None, save_for_backward=False, variants=0):
     """RDN forward (Sec. 3.4, right box).  Returns (o, S_final, R_final).
     With save_for_backward the (backward-sized) workspace keeps what the
     matching backward call with use_saved=True reads instead of recomputing."""
     return _forward("rdn_forward", RLA_OP_RDN_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                     clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
-                    save_for_backward)
+                    save_for_backward, variants)
 
 
 def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None, use_saved=False):
+                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0):
     torch = _torch()
     lib = load_library()
     if use_saved and workspace is None:
         raise ValueError("use_saved needs the workspace of the saving forward call")
     problem = make_problem(q, v, cu_seqlens, clip, out_dtype,
-                           RLA_FLAG_USE_SAVED if use_saved else 0)
+                           (RLA_FLAG_USE_SAVED if use_saved else 0) | _variant_bits(variants))
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S0=S0, R0=R0, dO=dO, dS_final=dS_final, dR_final=dR_final), dev)
@@ -288,31 +300,31 @@ def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float 
 
 def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None, use_saved=False):
+                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0):
     """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rdn_forward.
     Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0.
     use_saved: read what rdn_forward(save_for_backward=True) left in `workspace`."""
     return _backward("rdn_backward", RLA_OP_RDN_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
-                     out_dtype, use_saved)
+                     out_dtype, use_saved, variants)
 
 
 def rla_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None, use_saved=False):
+                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0):
     """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rla_forward."""
     return _backward("rla_backward", RLA_OP_RLA_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
-                     out_dtype, use_saved)
+                     out_dtype, use_saved, variants)
 
 
 def _decode(name, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in, S_out, R_out, out,
-            stream, out_dtype):
+            stream, out_dtype, variants=0):
     torch = _torch()
     lib = load_library()
     if q.dim() != 4:
         raise ValueError("decoding takes q, k, v as [B, T, H, d] (T tokens per sequence)")
-    problem = make_problem(q, v, None, clip, out_dtype, 0)
+    problem = make_problem(q, v, None, clip, out_dtype, _variant_bits(variants))
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S_in=S_in, R_in=R_in, S_out=S_out, R_out=R_out), dev)
@@ -340,16 +352,16 @@ def _decode(name, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in, S_ou
 
 
 def rla_decode(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S_in=None, R_in=None,
-               S_out=None, R_out=None, out=None, stream=None, out_dtype=None):
+               S_out=None, R_out=None, out=None, stream=None, out_dtype=None, variants=0):
     """RLA recurrent step (Sec. 3.4, left box, evaluated token by token):
     q, k, v [B, T, H, d] with small T, gates [B, T, H].  Returns (o, S_out,
     R_out); pass S_out=S_in, R_out=R_in to update the states in place."""
     return _decode("rla_decode", q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in,
-                   S_out, R_out, out, stream, out_dtype)
+                   S_out, R_out, out, stream, out_dtype, variants)
 
 
 def rdn_decode(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S_in=None, R_in=None,
-               S_out=None, R_out=None, out=None, stream=None, out_dtype=None):
+               S_out=None, R_out=None, out=None, stream=None, out_dtype=None, variants=0):
     """RDN recurrent step (Sec. 3.4, right box); arguments as rla_decode."""
     return _decode("rdn_decode", q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in,
-                   S_out, R_out, out, stream, out_dtype)
+                   S_out, R_out, out, stream, out_dtype, variants)

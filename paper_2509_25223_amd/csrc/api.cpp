@@ -31,6 +31,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 struct Problem {
   int64_t B = 0, T = 0, H = 0, DK = 0, DV = 0, N = 0, ntok = 0, max_chunks = 0;
   bool varlen = false, bf16 = false, out_bf16 = false, save = false, use_saved = false;
+  int32_t vflags = 0;   // kVar* bits
   const int32_t* cu = nullptr;
   float clip = -1.f;
 };
@@ -54,7 +55,13 @@ rla_status check_problem(const rla_problem* pp, Problem& pr, bool recurrent = fa
   if (pp->out_dtype != RLA_F32 && pp->out_dtype != RLA_BF16) return RLA_ERR_DTYPE;
   if (pp->dtype == RLA_F32 && pp->out_dtype != RLA_F32) return RLA_ERR_DTYPE;
   if (isnan(pp->clip) || pp->clip < 0.f) return RLA_ERR_VALUE;
-  if (pp->flags & ~(RLA_FLAG_SAVE_FOR_BACKWARD | RLA_FLAG_USE_SAVED)) return RLA_ERR_VALUE;
+  constexpr uint32_t kKnown = RLA_FLAG_SAVE_FOR_BACKWARD | RLA_FLAG_USE_SAVED |
+                              RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT |
+                              RLA_FLAG_DECAYED_RESIDUAL;
+  if (pp->flags & ~kKnown) return RLA_ERR_VALUE;
+  pr.vflags = ((pp->flags & RLA_FLAG_RESIDUAL_TANH) ? kVarTanh : 0) |
+              ((pp->flags & RLA_FLAG_UNGATED_OUTPUT) ? kVarUngated : 0) |
+              ((pp->flags & RLA_FLAG_DECAYED_RESIDUAL) ? kVarDecayed : 0);
   pr.save = (pp->flags & RLA_FLAG_SAVE_FOR_BACKWARD) != 0;
   pr.use_saved = (pp->flags & RLA_FLAG_USE_SAVED) != 0;
   pr.B = pp->batch;
@@ -135,6 +142,7 @@ OpParams make_params(const Problem& pr, const Workspace& w, unsigned char* ws, b
   p.ntok = pr.ntok;
   p.clip = pr.clip;
   p.rdn = rdn ? 1 : 0;
+  p.vflags = pr.vflags;
   p.out_bf16 = pr.out_bf16 ? 1 : 0;
   p.max_chunks = (int32_t)pr.max_chunks;
   p.st.nseq = (int32_t)pr.N;
@@ -330,6 +338,7 @@ rla_status decode(bool rdn, const rla_problem* problem, const void* q, const voi
   p.ntok = pr.ntok;
   p.clip = pr.clip;
   p.rdn = rdn ? 1 : 0;
+  p.vflags = pr.vflags;
   p.out_bf16 = pr.out_bf16 ? 1 : 0;
   p.st.nseq = (int32_t)pr.N;
   p.st.dense_T = pr.T;

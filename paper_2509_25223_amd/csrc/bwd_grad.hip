@@ -16,6 +16,12 @@
 //   dP = E^S (.) W1 (.) L- + diag(gamma) E^R (.) W2 (.) L
 //   dG = [-E' (.) W3 - diag(b) E^S (.) W4 - diag(gamma) E^R (.) W5] (.) L-
 // (dA^S = -W4 and dA^R = -W5 are the gradients of the triangular systems.)
+// Variants: the ungated output weights its S0 and U read-out by e^{g_{t-1}}
+// (E' in dP, F1 with e^{g_{t-1}}: their gate terms move to g_{t-1}) and drops
+// gamma from the output (dQ's F2 term, dP's W2 term and dgamma's output
+// terms); the decayed residual weights FK1 and W3 by e^{g} and E^S (their
+// gate terms move from g_{t-1} to g_t).  The log-cosh residual changes
+// nothing here: the reverse scan applied its slope to dX.
 // The gate gradients need per-token sums over the value dimension of
 // products of a backward and a forward quantity.  Those that involve a state
 // are row-dots of Q or K with the F matrices above, e.g.
@@ -104,7 +110,9 @@ __device__ __forceinline__ void put_cols(float* dst, int s0, const float (&v)[4]
   dst[s0 + (threadIdx.x & 15)] = s;
 }
 
-template <typename IN, int DK, int DV, bool RDN, typename OT>
+// VAR: an instance that reads the variant flags (the default instance
+// compiles them away)
+template <typename IN, int DK, int DV, bool RDN, typename OT, bool VAR>
 __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   typedef GradLayout<IN, DK, DV> L;
   constexpr int NW = L::kNW, NT = L::kNT;
@@ -140,6 +148,10 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   float* gspv = gsv + kChunk;   // g_{t-1}
   float* grv = gspv + kChunk;   // h_t
   float* edge = grv + kChunk;   // e^{g_C}, e^{h_C}
+  const int vf = VAR ? p.vflags : 0;
+  const bool ung = (vf & kVarUngated) != 0, dec = (vf & kVarDecayed) != 0;
+  const float* eqb = ung ? egsp : egs;   // S0 factor of the base read-out
+  const float* ekp = dec ? egs : egsp;   // S0 factor of the residual
   float* sums = reinterpret_cast<float*>(smem + L::kSums);   // [wave][kNumSums][64]
   float* esum = reinterpret_cast<float*>(smem + L::kElem);   // [2][64]: dY.V, dYR.r
   float* red = reinterpret_cast<float*>(smem + L::kRed);
@@ -383,14 +395,19 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
         const float W1 = tW1[x][r], W2 = tW2[x][r], W3 = tW3[x][r];
         const float G = tG[x][r], P = tP[x][r];
         const float dAs = RDN ? -tW4[x][r] : 0.f, dAr = RDN ? -tW5[x][r] : 0.f;
-        const float gw2 = ggm[t] * W2;
-        const float dp = (lower ? es * W1 : 0.f) + (diag ? er * gw2 : 0.f);
-        const float dg = lower ? (-ep * W3 + gbt[t] * es * dAs + ggm[t] * er * dAr) : 0.f;
-        zs[r] = lower ? es * (P * W1 + gbt[t] * G * dAs) : 0.f;
-        zp[r] = lower ? -ep * G * W3 : 0.f;
+        // decays of the base read-out (W1) and residual (W3) terms: e^{g_t - g_s}
+        // or e^{g_{t-1} - g_s}, by variant; their gate terms follow them to
+        // the g_t (zs) or the g_{t-1} (zp) sums
+        const float ew1 = ung ? ep : es, ew3 = dec ? es : ep;
+        const float gw2 = (ung ? 1.f : ggm[t]) * W2;
+        const float dp = (lower ? ew1 * W1 : 0.f) + (diag ? er * gw2 : 0.f);
+        const float dg = lower ? (-ew3 * W3 + gbt[t] * es * dAs + ggm[t] * er * dAr) : 0.f;
+        const float t1 = lower ? ew1 * P * W1 : 0.f, t3 = lower ? -ew3 * G * W3 : 0.f;
+        zs[r] = (lower ? es * gbt[t] * G * dAs : 0.f) + (ung ? 0.f : t1) + (dec ? t3 : 0.f);
+        zp[r] = (ung ? t1 : 0.f) + (dec ? 0.f : t3);
         zr[r] = (diag ? er * P * gw2 : 0.f) + (lower ? ggm[t] * er * G * dAr : 0.f);
         zb[r] = lower ? dAs * es * G : 0.f;
-        zg[r] = (lower ? dAr * er * G : 0.f) + (diag ? er * P * W2 : 0.f);
+        zg[r] = (lower ? dAr * er * G : 0.f) + ((diag && !ung) ? er * P * W2 : 0.f);
         edp[x][r] = dp;
         edg[x][r] = dg;
       }
@@ -475,11 +492,12 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * tt + acc_row(r);
-          const float c1 = egs[t] * F1[r], c2 = -egsp[t] * FK1[r], c6 = dls[t] * FK4[r];
+          const float c1 = eqb[t] * F1[r], c2 = -ekp[t] * FK1[r], c6 = dls[t] * FK4[r];
           dQ[m][tt][r] += c1;
           dK[m][tt][r] += c2 + c6;
-          ags[r] = qq[r] * c1 - kq[r] * c6;
-          agsp[r] = kq[r] * c2;
+          // c1 is a g_t term (g_{t-1} when ungated), c2 a g_{t-1} term (g_t when decayed)
+          ags[r] = (ung ? 0.f : qq[r] * c1) + (dec ? kq[r] * c2 : 0.f) - kq[r] * c6;
+          agsp[r] = (ung ? qq[r] * c1 : 0.f) + (dec ? 0.f : kq[r] * c2);
           gsC += kq[r] * c6;
           ab[r] = 0.f;
           if constexpr (RDN) {
@@ -515,11 +533,11 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * tt + acc_row(r);
-          const float e4 = egr[t] * F2[r], c4 = ggm[t] * e4, c7 = dlr[t] * FK5[r];
+          const float e4 = egr[t] * F2[r], c4 = (ung ? 1.f : ggm[t]) * e4, c7 = dlr[t] * FK5[r];
           dQ[m][tt][r] += c4;
           dK[m][tt][r] += c7;
           agr[r] = qq[r] * c4 - kq[r] * c7;
-          agm[r] = qq[r] * e4;
+          agm[r] = ung ? 0.f : qq[r] * e4;   // gamma's output term
           grC += kq[r] * c7;
           if constexpr (RDN) {
             const float e5 = -egr[t] * FK3[r], c5 = ggm[t] * e5;
@@ -651,7 +669,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 template <typename IN, int DK, int DV, bool RDN, typename OT>
 hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
   typedef GradLayout<IN, DK, DV> L;
-  auto kern = bwd_grad_kernel<IN, DK, DV, RDN, OT>;
+  auto kern = p.vflags ? bwd_grad_kernel<IN, DK, DV, RDN, OT, true> : bwd_grad_kernel<IN, DK, DV, RDN, OT, false>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;

@@ -17,6 +17,10 @@
 //   dR_start = e^{h_C} dR_end + Q^T diag(e^{h}) dc + K^T dKR
 // Also written per chunk: dv = dX + diag(b) dY (RLA: dX + diag(b) dU), and
 // the blocks dX, dY (RLA: dU), dYR (RLA: dUR) for the gradient kernel.
+// Variants: ungated output db = e^{g_{t-1}}-weighted (the S_{t-1} q read-out)
+// and dc = dO; decayed residual dKS with e^{g} in place of e^{g_{t-1}};
+// log-cosh residual dX = (1 - (r / c)^2) gamma dYR, r read from the forward's
+// saved block instead of the clip mask.
 // Every column of dS, dR only sees its own value column, so value blocks are
 // independent here as in the forward.  Operand precision as in the forward
 // scan: K x (dS, dR) uses bf16 K with the gradient state split into bf16
@@ -29,7 +33,7 @@ namespace rla {
 
 namespace {
 
-template <typename IN, int DK, int BV, bool RDN>
+template <typename IN, int DK, int BV, bool RDN, bool VAR>
 struct BwdScanLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
   typedef typename std::conditional<kBF, f16, float>::type XT;
@@ -52,7 +56,9 @@ struct BwdScanLayout {
   static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
   static constexpr int kBufBytes = BV * TT::kRowB;
   static constexpr int kMask = kBufs + kNumBufs * kBufBytes;
-  static constexpr int kMaskBytes = kChunk * BV;
+  // the clip mask (BV bytes per token) or, in the variant instance (log-cosh
+  // residual), the forward's r block (BV operand-type values per token)
+  static constexpr int kMaskBytes = kChunk * BV * (VAR ? (int)sizeof(XT) : 1);
   static constexpr int kGraw = kMask + kMaskBytes;
   static constexpr int kGates = kGraw + kGateBlock * 4;
   static constexpr int kYst = kGates + 10 * kChunk * 4;   // dYR staging (token tile)
@@ -101,9 +107,11 @@ __device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0,
   }
 }
 
-template <typename IN, int DK, int BV, bool RDN>
+// VAR: an instance that reads the variant flags (the default instance
+// compiles them away)
+template <typename IN, int DK, int BV, bool RDN, bool VAR>
 __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
-  typedef BwdScanLayout<IN, DK, BV, RDN> L;
+  typedef BwdScanLayout<IN, DK, BV, RDN, VAR> L;
   typedef typename L::XT XT;
   typedef Mfma<IN> MI;
   typedef typename L::TT TT;
@@ -138,6 +146,15 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   float* dls = egr + kChunk;
   float* dlr = dls + kChunk;
   float* edge = dlr + kChunk;
+  // output weight of c: gamma (ungated: 1); the default instance reads gamma
+  float* gout = VAR ? edge + kChunk : ggm;
+  const int vf = VAR ? p.vflags : 0;
+  const float* ekp = (vf & kVarDecayed) ? egs : egsp;   // S0 factor of the residual
+  const float* eqb = (vf & kVarUngated) ? egsp : egs;   // S0 factor of the base read-out
+  const bool tanh_resid = (vf & kVarTanh) != 0;
+  // log-cosh slope 1 - (r / c)^2 = s0 (1 - (r invc)^2): c = inf -> 1, c = 0 -> 0
+  const float invc = p.clip > 0.f ? 1.f / p.clip : 0.f;
+  const float s0 = p.clip == 0.f ? 0.f : 1.f;
   XT* Yst = reinterpret_cast<XT*>(smem + L::kYst);   // dYR of this chunk
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
@@ -216,11 +233,20 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
                       kGateBlock * 4);
   };
   auto issue_mask = [&](int c) {   // rows of BV bytes; padding rows read row 0 (masked by 0 grads)
+    if (tanh_resid) {   // the r block rows of this value block (rows past the end are zero)
+      constexpr int kPerRow = BV * (int)sizeof(XT) / 16;
+      static_assert(kChunk * kPerRow == kThreads, "r block = one DMA instruction per wave");
+      const int P = w * 64 + lane, t = P / kPerRow, cc = P % kPerRow;
+      const XT* src = reinterpret_cast<const XT*>(p.fwd_blk) + blk_off(si.chunk0 + c, h, H, 2, DV) +
+                      (int64_t)t * DV + j0 + cc * (16 / (int)sizeof(XT));
+      dma16(src, mask + w * 1024);
+      return;
+    }
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
     constexpr int kPerRow = BV / 16;
 #pragma unroll
-    for (int m = 0; m < L::kMaskBytes / 1024; ++m) {
+    for (int m = 0; m < kChunk * BV / 1024; ++m) {
       if (w == m) {
         const int P = m * 64 + lane, t = P / kPerRow, cc = P % kPerRow;
         const int ts = t < len ? t : 0;
@@ -344,6 +370,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         const float gr = graw[64 + tt], grl = graw[64 + kChunk - 1];
         gbt[tt] = graw[128 + tt];
         ggm[tt] = graw[192 + tt];
+        if constexpr (VAR) gout[tt] = (vf & kVarUngated) ? 1.f : graw[192 + tt];
         egs[tt] = __expf(gs);
         egsp[tt] = __expf(gsp);
         egr[tt] = __expf(gr);
@@ -374,8 +401,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r);
-        dc[r] = ggm[t] * o4[r];
-        qdb[r] = egs[t] * o4[r];
+        dc[r] = gout[t] * o4[r];
+        qdb[r] = eqb[t] * o4[r];
         qdc[r] = egr[t] * dc[r];
       }
       store_acc_tile<TT>(blk(bDC_DX), jt * 16, 16 * w, dc);
@@ -418,9 +445,20 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r), j = jt * 16 + acc_col();
-        dX[jt][r] = mask[t * BV + j] ? ggm[t] * dYR[r] : 0.f;
+        if constexpr (VAR) {
+          float slope;
+          if (tanh_resid) {
+            const float rn = to_f<XT>(reinterpret_cast<const XT*>(mask)[t * BV + j]) * invc;
+            slope = s0 * __builtin_fmaf(-rn, rn, 1.f);
+          } else {
+            slope = mask[t * BV + j] ? 1.f : 0.f;
+          }
+          dX[jt][r] = slope * (ggm[t] * dYR[r]);
+        } else {
+          dX[jt][r] = mask[t * BV + j] ? ggm[t] * dYR[r] : 0.f;
+        }
         dkr[r] = -ggm[t] * egr[t] * dYR[r];
-        dks[r] = -egsp[t] * dX[jt][r];
+        dks[r] = -ekp[t] * dX[jt][r];
       }
       store_acc_tile<TT>(blk(bDC_DX), jt * 16, 16 * w, dX[jt]);
       store_acc_tile<TT>(blk(bDKR), jt * 16, 16 * w, RDN ? dkr : dks);
@@ -463,7 +501,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
-          dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[jt][r];
+          dks[r] = -ekp[t] * dX[jt][r] - gbt[t] * egs[t] * dY[jt][r];
         }
         store_acc_tile<TT>(blk(bDB_DKS), jt * 16, 16 * w, dks);
       }
@@ -537,10 +575,10 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   }
 }
 
-template <typename IN, int DK, int BV, bool RDN>
-hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
-  typedef BwdScanLayout<IN, DK, BV, RDN> L;
-  auto kern = bwd_scan_kernel<IN, DK, BV, RDN>;
+template <typename IN, int DK, int BV, bool RDN, bool VAR>
+hipError_t launch_bwd_scan_v(const OpParams& p, hipStream_t stream) {
+  typedef BwdScanLayout<IN, DK, BV, RDN, VAR> L;
+  auto kern = bwd_scan_kernel<IN, DK, BV, RDN, VAR>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;
@@ -550,6 +588,12 @@ hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
   if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), L::kBytes, stream, p);
   return hipGetLastError();
+}
+
+template <typename IN, int DK, int BV, bool RDN>
+hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
+  return p.vflags ? launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream)
+                  : launch_bwd_scan_v<IN, DK, BV, RDN, false>(p, stream);
 }
 
 }  // namespace

@@ -506,6 +506,13 @@ __device__ __forceinline__ uint32_t row16_absmax_bits(float a, float b) {
   return max(m, dpp_u32<0x140>(m));
 }
 
+// Log-cosh residual r = c tanh(x / c) (c < 0: no bound, r = x; c = 0: r = 0).
+__device__ __forceinline__ float resid_tanh(float x, float c) {
+  if (c < 0.f) return x;
+  if (c == 0.f) return 0.f;
+  return c * tanhf(x / c);
+}
+
 __device__ __forceinline__ uint32_t cvt_pk_f16(float a, float b) {
   return __builtin_bit_cast(uint32_t, f16x2{to_f16(a), to_f16(b)});
 }

@@ -24,7 +24,8 @@
 //   o = aS Sq + gamma (aR Rq + gamma (k.q) b)           (= aS S_{t-1} q + gamma R_t q)
 // which is the boxed update S_t = aS S_{t-1}(I - beta k k^T) + beta v k^T
 // (RDN) or aS S_{t-1} + beta v k^T (RLA), and likewise for R with (aR, gamma,
-// r), written in the transposed storage.
+// r), written in the transposed storage.  Variants: x = v - aS Sk (decayed
+// residual), r = c tanh(x / c) (log-cosh residual), o = Sq + R_t q (ungated).
 #include "kernels.hpp"
 
 namespace rla {
@@ -136,14 +137,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(OpParams p) {
       }
       const float aS = sg[b][0], aR = sg[b][2], gm = sg[b][3];
       const float vj = sv[b][j];
-      const float x = vj - Sk;
-      const float r = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
+      const float x = (p.vflags & kVarDecayed) ? __builtin_fmaf(-aS, Sk, vj) : vj - Sk;
+      const float r = (p.vflags & kVarTanh) ? resid_tanh(x, clip)
+                                            : (clip < 0.f ? x : fminf(fmaxf(x, -clip), clip));
       const float ca = RDN ? __builtin_fmaf(-aS, Sk, vj) : vj;
       const float cb = RDN ? __builtin_fmaf(-aR, Rk, r) : r;
       coef[0][j] = ca;
       coef[1][j] = cb;
       const float rq = __builtin_fmaf(gm * skq, cb, aR * Rq);   // R_t q
-      const float oj = __builtin_fmaf(gm, rq, aS * Sq);
+      const bool ung = (p.vflags & kVarUngated) != 0;
+      const float oj = __builtin_fmaf(ung ? 1.f : gm, rq, ung ? Sq : aS * Sq);
       const int64_t oo = (tok * H + h) * DV + j0 + j;
       if constexpr (sizeof(OT) == 4) og[oo] = oj;
       else og[oo] = f2bf(oj);

@@ -15,6 +15,9 @@
 //   c_t = e^{h} QR + MR UR              = R_t q_t
 //   o   = b + diag(gamma) c
 //   S  <- e^{g_C} S + K^T diag(e^{g_C - g}) U,  R likewise with (h, UR)
+// Variants: decayed residual p = e^{g} KS + MG U (= aS_t S_{t-1} k_t, MG with
+// e^{g_t - g_s}); ungated output b = e^{g_{t-1}} QS + MP U (= S_{t-1} q_t, MP
+// with e^{g_{t-1} - g_s}) and o = b + c; log-cosh residual r = c tanh(x / c).
 //
 // Operand precision (bf16 inputs; fp32 inputs use fp32 MFMA throughout):
 //   K, Q x state: bf16 K/Q fragments (exact inputs, loaded from HBM straight
@@ -99,7 +102,9 @@ __device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0,
   }
 }
 
-template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT>
+// VAR: an instance that reads the variant flags (the default instance
+// compiles them away, so the boxed operator keeps its register budget)
+template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT, bool VAR>
 __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
   typedef typename L::XT XT;
@@ -136,6 +141,13 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   float* dls = egr + kChunk;        // e^{g_C - g_t}
   float* dlr = dls + kChunk;        // e^{h_C - h_t}
   float* edge = dlr + kChunk;       // [0] = e^{g_C}, [1] = e^{h_C}
+  // output weight of c: gamma (ungated: 1); the default instance reads gamma
+  float* gout = VAR ? edge + kChunk : ggm;
+  // per-token factors of S0 in the residual's and the base read-out's terms
+  const int vf = VAR ? p.vflags : 0;
+  const float* ekp = (vf & kVarDecayed) ? egs : egsp;
+  const float* eqb = (vf & kVarUngated) ? egsp : egs;
+  const bool tanh_resid = (vf & kVarTanh) != 0;
   XT* Rst = reinterpret_cast<XT*>(smem + L::kRst);            // r (saving mode)
   uint8_t* Mst = reinterpret_cast<uint8_t*>(smem + L::kMst);  // clip mask (saving mode)
   float* Ost = reinterpret_cast<float*>(smem + L::kOst);      // o
@@ -271,6 +283,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         const float gr = graw[64 + tt], grl = graw[64 + kChunk - 1];
         gbt[tt] = graw[128 + tt];
         ggm[tt] = graw[192 + tt];
+        if constexpr (VAR) gout[tt] = (vf & kVarUngated) ? 1.f : graw[192 + tt];
         egs[tt] = __expf(gs);
         egsp[tt] = __expf(gsp);
         egr[tt] = __expf(gr);
@@ -363,11 +376,12 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r);
-        const float x = __builtin_fmaf(-egsp[t], KS[jt][r], vloc[jt][r]) - mgu[r];
-        const float rr = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
+        const float x = __builtin_fmaf(-ekp[t], KS[jt][r], vloc[jt][r]) - mgu[r];
+        const float rr = tanh_resid ? resid_tanh(x, clip)
+                                    : (clip < 0.f ? x : fminf(fmaxf(x, -clip), clip));
         rv[r] = rr;
         if constexpr (CKPT) Mst[t * BV + jt * 16 + acc_col()] = (clip < 0.f || fabsf(x) <= clip) ? 1 : 0;
-        base[jt][r] = __builtin_fmaf(egs[t], QS[jt][r], mpu[r]);
+        base[jt][r] = __builtin_fmaf(eqb[t], QS[jt][r], mpu[r]);
         y[r] = RDN ? ggm[t] * __builtin_fmaf(-egr[t], KR[jt][r], rr) : ggm[t] * rr;
       }
       if constexpr (RDN) {
@@ -435,7 +449,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) {
           const int t = 16 * w + acc_row(r);
           Ost[t * L::kLdO + jt * 16 + acc_col()] =
-              __builtin_fmaf(ggm[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
+              __builtin_fmaf(gout[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
         }
       }
     }
@@ -524,7 +538,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT>
 hipError_t launch_fwd_t(const OpParams& p, hipStream_t stream) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
-  auto kern = fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT>;
+  auto kern = p.vflags ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
+                       : fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, false>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;

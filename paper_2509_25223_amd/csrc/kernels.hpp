@@ -15,12 +15,19 @@ __host__ __device__ inline int64_t blk_off(int64_t gc, int h, int H, int b, int 
   return ((gc * H + h) * kNumBlk + b) * (int64_t)kChunk * DV;
 }
 
+// Variants of the residual and of the output (bits of OpParams::vflags):
+//   kVarTanh     r = c tanh(x / c) instead of the clip (c < 0: r = x; c = 0: r = 0)
+//   kVarUngated  o = S_{t-1} q + R_t q
+//   kVarDecayed  x = v - aS S_{t-1} k
+constexpr int kVarTanh = 1, kVarUngated = 2, kVarDecayed = 4;
+
 // Everything a launch needs; passed by value to the kernels.
 struct OpParams {
   int32_t H = 0, DK = 0, DV = 0;
   int64_t ntok = 0;
   float clip = -1.f;            // < 0: no clipping
   int32_t rdn = 1;              // 1: RDN, 0: RLA
+  int32_t vflags = 0;           // kVar* bits
   int32_t out_bf16 = 0;         // o, dq, dk, dv in bf16 (else fp32)
   int32_t max_chunks = 0;       // upper bound on chunks (grid size of chunk-parallel kernels)
   SeqTable st{};

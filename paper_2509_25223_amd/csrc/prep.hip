@@ -9,6 +9,8 @@
 //   MG[t][s] = e^{g_{t-1}-g_s} G[t][s]  (s < t)   -> S_{t-1} k_t read-out
 //   MP[t][s] = e^{g_t - g_s}   P[t][s]  (s < t)   -> aS_t S_{t-1} q_t read-out
 //   MR[t][s] = e^{h_t - h_s}   P[t][s]  (s <= t)  -> R_t q_t read-out
+//   (decayed residual: MG with e^{g_t - g_s}, the aS_t S_{t-1} k_t read-out;
+//    ungated output: MP with e^{g_{t-1} - g_s}, the S_{t-1} q_t read-out)
 //   RDN only: the delta rule S_t = aS_t S_{t-1}(I - b_t k_t k_t^T) + b_t v_t k_t^T
 //   makes the chunk's corrections U solve (I + A^S) U = rhs with
 //   A^S[t][s] = b_t e^{g_t-g_s} G[t][s] (s < t); likewise A^R with (gamma, h).
@@ -198,8 +200,10 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
       const float esp = __expf(fminf(gsp[t] - gs[s], 0.f));
       const float er = __expf(fminf(gr[t] - gr[s], 0.f));
       const bool lower = s < t;
-      mats[kMatMG * kMatElems + t * kChunk + s] = from_f<XT>(lower ? esp * g : 0.f);
-      mats[kMatMP * kMatElems + t * kChunk + s] = from_f<XT>(lower ? es * pq : 0.f);
+      const float eg = (p.vflags & kVarDecayed) ? es : esp;
+      const float ep = (p.vflags & kVarUngated) ? esp : es;
+      mats[kMatMG * kMatElems + t * kChunk + s] = from_f<XT>(lower ? eg * g : 0.f);
+      mats[kMatMP * kMatElems + t * kChunk + s] = from_f<XT>(lower ? ep * pq : 0.f);
       mats[kMatMR * kMatElems + t * kChunk + s] = from_f<XT>(s <= t ? er * pq : 0.f);
       if constexpr (RDN) {
         As[t * L::kLdA + s] = lower ? bt[t] * es * g : 0.f;

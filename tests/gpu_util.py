@@ -10,6 +10,14 @@ import paper_2509_25223_amd as rla
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
+# library variant bits -> the oracle's own variant bits
+LIB_TO_ORACLE = ((rla.RLA_FLAG_RESIDUAL_TANH, oracle.TANH), (rla.RLA_FLAG_UNGATED_OUTPUT, oracle.UNGATED),
+                 (rla.RLA_FLAG_DECAYED_RESIDUAL, oracle.DECAYED))
+
+
+def oracle_flags(variants):
+    return sum(o for lib, o in LIB_TO_ORACLE if variants & lib)
+
 
 def torch_dtype(dt):
     import torch
@@ -35,7 +43,7 @@ def rel_err(x, ref):
     return float(np.max(np.abs(np.asarray(x, np.float64) - ref))) / rms
 
 
-def gpu_forward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dense_B=None):
+def gpu_forward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dense_B=None, variants=0):
     """Runs rla_forward / rdn_forward on packed inputs [ntok, H, d].  With
     dense_B the tokens are viewed as [B, T, H, d] (equal lengths), else
     cu_seqlens from inp is used."""
@@ -54,15 +62,15 @@ def gpu_forward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dense_B
     else:
         cu = torch.from_numpy(np.asarray(inp["cu_seqlens"], dtype=np.int32)).to(device)
     fn = rla.rdn_forward if variant == "rdn" else rla.rla_forward
-    o, Sf, Rf = fn(q, k, v, *gates, clip=clip, S0=S0d, R0=R0d, cu_seqlens=cu)
+    o, Sf, Rf = fn(q, k, v, *gates, clip=clip, S0=S0d, R0=R0d, cu_seqlens=cu, variants=variants)
     torch.cuda.synchronize()
     return host(o).reshape(-1, *o.shape[-2:]), host(Sf), host(Rf)
 
 
-def oracle_forward(variant, inp, clip=1.0, S0=None, R0=None):
+def oracle_forward(variant, inp, clip=1.0, S0=None, R0=None, variants=0):
     return oracle.forward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
                           inp["alpha_r"], inp["gamma"], clip=clip, S0=S0, R0=R0,
-                          cu_seqlens=inp["cu_seqlens"])
+                          cu_seqlens=inp["cu_seqlens"], flags=oracle_flags(variants))
 
 
 def select(inp, seqs, heads):
@@ -80,7 +88,7 @@ def select(inp, seqs, heads):
 
 
 def gpu_backward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dS_final=None,
-                 dR_final=None, dense_B=None, out_dtype=None):
+                 dR_final=None, dense_B=None, out_dtype=None, variants=0):
     """Runs rla_backward / rdn_backward on packed inputs; returns numpy grads."""
     import torch
     td = torch_dtype(dtype)
@@ -97,7 +105,7 @@ def gpu_backward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dS_fin
         cu = torch.from_numpy(np.asarray(inp["cu_seqlens"], dtype=np.int32)).to(device)
     fn = rla.rdn_backward if variant == "rdn" else rla.rla_backward
     g = fn(q, k, v, *gates, dO, clip=clip, S0=opt(S0), R0=opt(R0), dS_final=opt(dS_final),
-           dR_final=opt(dR_final), cu_seqlens=cu, out_dtype=out_dtype)
+           dR_final=opt(dR_final), cu_seqlens=cu, out_dtype=out_dtype, variants=variants)
     torch.cuda.synchronize()
     out = {}
     for key, t in g.items():
@@ -110,13 +118,15 @@ def gpu_backward(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dS_fin
     return out
 
 
-def oracle_backward(variant, inp, clip=1.0, S0=None, R0=None, dS_final=None, dR_final=None):
+def oracle_backward(variant, inp, clip=1.0, S0=None, R0=None, dS_final=None, dR_final=None,
+                    variants=0):
     return oracle.backward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
                            inp["alpha_r"], inp["gamma"], inp["dO"], clip=clip, S0=S0, R0=R0,
-                           dS_final=dS_final, dR_final=dR_final, cu_seqlens=inp["cu_seqlens"])
+                           dS_final=dS_final, dR_final=dR_final, cu_seqlens=inp["cu_seqlens"],
+                           flags=oracle_flags(variants))
 
 
-def nudge(variant, inp, dtype, clip=1.0, S0=None, R0=None, margin=None):
+def nudge(variant, inp, dtype, clip=1.0, S0=None, R0=None, margin=None, variants=0):
     """Moves v (on its dtype's grid) so no pre-clip residual is within `margin`
     of the clip kink; masks taken in two precisions then agree."""
     if margin is None:
@@ -124,7 +134,8 @@ def nudge(variant, inp, dtype, clip=1.0, S0=None, R0=None, margin=None):
     v, moved = oracle.nudge_margin(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"],
                                    inp["beta"], inp["alpha_r"], inp["gamma"], clip=clip, S0=S0,
                                    R0=R0, cu_seqlens=inp["cu_seqlens"], margin=margin,
-                                   grid="bf16" if dtype == "bf16" else "f32")
+                                   grid="bf16" if dtype == "bf16" else "f32",
+                                   flags=oracle_flags(variants))
     out = dict(inp)
     out["v"] = v.astype(np.float32)
     return out, moved

@@ -160,3 +160,16 @@ def test_decode_validation_errors(lib, name):
     assert call_dec(lib, prob(B=0, T=1), name, So=None, Ro=None) == 0
     # an output may not alias the other state's input
     assert call_dec(lib, p, name, Ri=FAKE + (1 << 31), So=FAKE + (1 << 31)) == 6
+
+
+def test_variant_flags_validated(lib):
+    """The three variant bits are accepted by every entry point; any other
+    unknown bit is rejected before any HIP call."""
+    p = prob()
+    p.flags = rla.RLA_FLAG_RESIDUAL_TANH | rla.RLA_FLAG_UNGATED_OUTPUT | rla.RLA_FLAG_DECAYED_RESIDUAL
+    assert call_fwd(lib, p, ws=None) == 5   # passes flag validation, stops at the workspace
+    p.flags = 32
+    assert call_fwd(lib, p) == 6
+    pd = prob(T=1)
+    pd.flags = 32
+    assert call_dec(lib, pd) == 6

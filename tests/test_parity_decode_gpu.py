@@ -13,7 +13,7 @@ pytestmark = pytest.mark.gpu
 
 
 def gpu_decode(variant, inp, dtype, device, B, clip=1.0, S0=None, R0=None, steps=1,
-               out_dtype=None, in_place=False):
+               out_dtype=None, in_place=False, variants=0):
     """Runs the packed inputs (B sequences of equal length T) through `steps`
     decode calls of T / steps tokens each, carrying the states between calls."""
     import torch
@@ -34,9 +34,11 @@ def gpu_decode(variant, inp, dtype, device, B, clip=1.0, S0=None, R0=None, steps
         sl = slice(s * per, (s + 1) * per)
         args = [x[:, sl].contiguous() for x in (q, k, v)] + [g[:, sl].contiguous() for g in gates]
         if in_place and Sd is not None:
-            o, Sd, Rd = fn(*args, clip=clip, S_in=Sd, R_in=Rd, S_out=Sd, R_out=Rd, out_dtype=out_dtype)
+            o, Sd, Rd = fn(*args, clip=clip, S_in=Sd, R_in=Rd, S_out=Sd, R_out=Rd,
+                           out_dtype=out_dtype, variants=variants)
         else:
-            o, Sd, Rd = fn(*args, clip=clip, S_in=Sd, R_in=Rd, out_dtype=out_dtype)
+            o, Sd, Rd = fn(*args, clip=clip, S_in=Sd, R_in=Rd, out_dtype=out_dtype,
+                           variants=variants)
         outs.append(o)
     o = torch.cat(outs, dim=1) if outs else torch.empty(0)
     torch.cuda.synchronize()
