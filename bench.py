@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("e13371c0605273d4", ("bwd_grad.hip", "common.hpp", "kernels.hpp"), 1279757515, 322540501),
-    "bwd_scan": ("10e4bebe306ccf75", ("bwd_scan.hip", "common.hpp", "kernels.hpp"), 407276559, 637578544),
-    "fwd_scan": ("e25fde891f48e0e3", ("fwd_scan.hip", "common.hpp", "kernels.hpp"), 373594974, 654311545),
-    "prep": ("5aeaa998c6e4e057", ("prep.hip", "common.hpp", "kernels.hpp"), 153261552, 172847589),
-    "decode": ("c28ceaa8e700b72f", ("decode.hip", "common.hpp", "kernels.hpp"), 542727091, 539545242),
+    "bwd_grad": ("c1d6ba926a99f799", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1248319538, 323097952),
+    "bwd_scan": ("781ba65aac8e4d79", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407416491, 615846336),
+    "fwd_scan": ("bb002e34f51ba4d9", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373598123, 638584243),
+    "prep": ("07f0b0dc559f5fe8", ('prep.hip', 'common.hpp', 'kernels.hpp'), 165154987, 173150746),
+    "decode": ("e6c80c09961cc3cf", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542727091, 539545242),
 }
 
 
@@ -108,6 +108,9 @@ def main() -> int:
     ap.add_argument("--op", choices=("fwdbwd", "decode"), default="fwdbwd",
                     help="fwdbwd: the RDN training step (default); decode: the RDN recurrent "
                          "step, one token for each of 256 sequences from resident states")
+    ap.add_argument("--variants", default="",
+                    help="comma list of operator variants to switch on: tanh (log-cosh "
+                         "residual), ungated (output), decayed (residual), or all")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run one device-to-device copy of this many MiB (a kernel of "
                          "known traffic, for scaling hardware byte counters)")
@@ -121,6 +124,18 @@ def main() -> int:
     if args.op == "decode":
         return run_decode(args)
     return run_fwdbwd(args)
+
+
+def variant_bits(spec: str) -> tuple:
+    """(flag bits, names) for --variants."""
+    import paper_2509_25223_amd as rla
+    table = {"tanh": rla.RLA_FLAG_RESIDUAL_TANH, "ungated": rla.RLA_FLAG_UNGATED_OUTPUT,
+             "decayed": rla.RLA_FLAG_DECAYED_RESIDUAL}
+    names = sorted(table) if spec == "all" else [x for x in spec.split(",") if x]
+    for n in names:
+        if n not in table:
+            raise SystemExit("unknown variant %r (choose from %s or all)" % (n, ", ".join(table)))
+    return sum(table[n] for n in names), names
 
 
 def copy_calibration(mib: int, dev) -> None:
@@ -154,18 +169,19 @@ def run_fwdbwd(args) -> int:
 
     q, k, v, dO = (to_dev(n, torch.bfloat16) for n in ("q", "k", "v", "dO"))
     gates = [to_dev(n, torch.float32) for n in ("alpha_s", "beta", "alpha_r", "gamma")]
+    vbits, vnames = variant_bits(args.variants)
     prob = rla.make_problem(q, v, clip=wl.clip)
     ws_b = torch.empty(rla.rla_workspace_size(prob, rla.RLA_OP_RDN_BACKWARD), dtype=torch.uint8, device=dev)
     o = torch.empty(v.shape, dtype=torch.float32, device=dev)
-    grads = rla.rdn_backward(q, k, v, *gates, dO, clip=wl.clip, workspace=ws_b)
+    grads = rla.rdn_backward(q, k, v, *gates, dO, clip=wl.clip, workspace=ws_b, variants=vbits)
 
     def fwd():
         rla.rdn_forward(q, k, v, *gates, clip=wl.clip, out=o, workspace=ws_b, return_states=False,
-                        save_for_backward=True)
+                        save_for_backward=True, variants=vbits)
 
     def bwd():
         rla.rdn_backward(q, k, v, *gates, dO, clip=wl.clip, workspace=ws_b, grads=grads,
-                         use_saved=True)
+                         use_saved=True, variants=vbits)
 
     def step():
         fwd()
@@ -220,7 +236,7 @@ def run_fwdbwd(args) -> int:
         stages[key] = {"ms": round(ms, 4), "tflops": round(tf, 2), "gbs": round(gb, 1),
                        "mfma_frac": round(tf / PEAK_MFMA_TFLOPS, 4),
                        "hbm_frac": round(gb / PEAK_HBM_GBS, 4),
-                       "traffic": measured_traffic(key.split(".", 1)[1])}
+                       "traffic": None if vnames else measured_traffic(key.split(".", 1)[1])}
     dom = max(stage_ms, key=stage_ms.get)
     ds = stages[dom]
     kernel_names = {"prep": "prep_kernel", "fwd_scan": "fwd_scan_kernel (saving)",
@@ -243,9 +259,11 @@ def run_fwdbwd(args) -> int:
         import oracle
         names = ("q", "k", "v", "alpha_s", "beta", "alpha_r", "gamma", "dO")
         cu = wl.cu_seqlens()
+        oflags = sum(f for n, f in (("tanh", oracle.TANH), ("ungated", oracle.UNGATED),
+                                    ("decayed", oracle.DECAYED)) if n in vnames)
         c0 = time.perf_counter()
-        oracle.forward("rdn", *[inp[n] for n in names[:7]], clip=wl.clip, cu_seqlens=cu)
-        oracle.backward("rdn", *[inp[n] for n in names], clip=wl.clip, cu_seqlens=cu)
+        oracle.forward("rdn", *[inp[n] for n in names[:7]], clip=wl.clip, cu_seqlens=cu, flags=oflags)
+        oracle.backward("rdn", *[inp[n] for n in names], clip=wl.clip, cu_seqlens=cu, flags=oflags)
         c1 = time.perf_counter()
         cpu = {"value": round(B * T / (c1 - c0), 2), "unit": "tokens/s",
                "cores": oracle.threads(), "kind": "oracle",
@@ -265,9 +283,9 @@ def run_fwdbwd(args) -> int:
         "vs_baseline": None,
         "dtype": "bf16 in, fp16/bf16 MFMA, fp32 acc+out",
         "data": "synthetic",
-        "config": {"workload": wl.name, "B": B, "T": T, "H": H, "d_k": d, "d_v": d,
-                   "chunk": CHUNK, "clip": wl.clip, "outputs": "fp32",
-                   "parallelism": "single GPU"},
+        "config": dict({"workload": wl.name, "B": B, "T": T, "H": H, "d_k": d, "d_v": d,
+                        "chunk": CHUNK, "clip": wl.clip, "outputs": "fp32",
+                        "parallelism": "single GPU"}, **({"variants": vnames} if vnames else {})),
         # algorithmic flops of the whole step (every stage's count model) over
         # the step time, as a fraction of the dense bf16 MFMA peak
         "step_mfma_frac": round(step_flops / (ms_per_step * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
