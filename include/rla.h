@@ -35,9 +35,9 @@
  *   sequence n is tokens [cu_seqlens[n], cu_seqlens[n+1]); states reset at
  *   every sequence start.  Without it N = B sequences of length T.
  *   q, k, v, o, dO, dq, dk, dv must be 16-byte aligned.
- * Gates.  Gate values, not logits: aS, aR in (0, 1], b, g in [0, 1] are
- *   preconditions not checked on the device.  Decays below 2^-126 are
- *   treated as 2^-126.
+ * Gates.  Gate values, not logits (unless RLA_FLAG_GATE_PREACT): aS, aR in
+ *   (0, 1], b, g in [0, 1] are preconditions not checked on the device.
+ *   Decays below 2^-126 are treated as 2^-126.
  * Clip.  clip >= 0; +INFINITY disables clipping.  The clip's derivative is
  *   taken as 1 on the closed interval [-clip, clip].
  * Errors.  Argument, shape and workspace errors are detected on the host
@@ -104,6 +104,9 @@ typedef struct {
   float clip;               /* c >= 0, or +INFINITY for no clipping */
   int32_t out_dtype;        /* rla_dtype of o, dq, dk, dv (fp32 inputs: fp32 only) */
   uint32_t flags;           /* RLA_FLAG_* bits, 0 by default */
+  const float *decay_param; /* device [2][H]: a (> 0) then b, read with RLA_FLAG_GATE_PREACT */
+  float *decay_param_grad;  /* device [2][H]: d/da then d/db, written by a backward with
+                               RLA_FLAG_GATE_PREACT (may be NULL: not written) */
 } rla_problem;
 
 /*
@@ -137,6 +140,24 @@ typedef struct {
 #define RLA_FLAG_RESIDUAL_TANH 4u
 #define RLA_FLAG_UNGATED_OUTPUT 8u
 #define RLA_FLAG_DECAYED_RESIDUAL 16u
+
+/*
+ * Input pre-processing inside the operator (the closing paragraph of
+ * Sec. 3.4 and the caption of the architecture figure; any combination, every
+ * entry point; gradients are with respect to the raw inputs):
+ *   RLA_FLAG_QK_SILU_L2NORM  q and k are raw projections: each token-head row
+ *       becomes y / max(||y||, 1e-12) with y = SiLU(x) before the recurrence
+ *       (the torch F.normalize convention).  bf16 inputs: the normalised rows
+ *       are rounded to bf16 once.  Needs workspace (rla_workspace_size).
+ *   RLA_FLAG_GATE_PREACT  alpha_s, alpha_r, beta, gamma hold pre-activations z:
+ *       aS = exp(-a_h softplus(z + b_h)) (likewise aR, with the same per-head
+ *       (a_h, b_h) from problem.decay_param: the Mamba-2 re-parameterisation),
+ *       beta = sigmoid(z), gamma = sigmoid(z).  The backward returns the
+ *       gradients of the pre-activations and, in problem.decay_param_grad,
+ *       of (a_h, b_h) summed over every token and both decays.
+ */
+#define RLA_FLAG_QK_SILU_L2NORM 32u
+#define RLA_FLAG_GATE_PREACT 64u
 
 /* Bytes of workspace the operation needs for this problem (0 if the problem
  * is invalid).  Pure host function. */

@@ -3,12 +3,15 @@
 The paper's attention block (Sec. 3.4, closing paragraph, and the caption of
 its architecture figure) feeds the recurrences with
   q_t, k_t  after a SiLU activation and L2 normalisation over the head
-            dimension (x / ||x||);
+            dimension, y / max(||y||, 1e-12) (the torch F.normalize form);
   alpha_t = exp(-a softplus(z^alpha_t + b)), the Mamba-2 re-parameterisation
             with learnable scalars a > 0, b (here one pair per head, shared by
             the decays of S and R; pass the same pre-activations for both to
             tie the decays as the paper does);
   beta_t = sigmoid(z^beta_t),  gamma_t = sigmoid(z^gamma_t).
+With bf16 inputs the operator stores the normalised rows in bf16 once
+(``qk_round="bf16"``: round to nearest even), as the recurrences of the plain
+path read bf16 inputs; the gradient passes that rounding straight through.
 ``forward`` applies these steps to raw inputs and calls the recurrent oracle;
 ``backward`` calls the recurrent oracle's adjoint on the transformed inputs
 and applies the chain rule of each step, so it returns gradients with respect
@@ -34,21 +37,36 @@ def _softplus(x):
     return np.logaddexp(0.0, x)
 
 
+NORM_EPS = 1e-12
+
+
+def _round_bf16(x):
+    """Round-to-nearest-even onto the bf16 grid (the upper 16 bits of fp32)."""
+    a = np.ascontiguousarray(np.asarray(x, np.float64).astype(np.float32))
+    u = a.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
 def qk_transform(x):
-    """q_hat = SiLU(x) / ||SiLU(x)|| over the last axis (fp64)."""
+    """q_hat = SiLU(x) / max(||SiLU(x)||, 1e-12) over the last axis (fp64)."""
     y = _silu(np.asarray(x, np.float64))
-    return y / np.linalg.norm(y, axis=-1, keepdims=True)
+    return y / np.maximum(np.linalg.norm(y, axis=-1, keepdims=True), NORM_EPS)
 
 
 def qk_transform_grad(x, dxhat):
     """Gradient w.r.t. x of <dxhat, qk_transform(x)>: through the norm
-    (dy = (dxhat - xhat (xhat . dxhat)) / ||y||) and SiLU' = s (1 + x (1 - s))."""
+    (dy = (dxhat - xhat (xhat . dxhat)) / ||y||; below the floor the scale is
+    the constant 1 / 1e-12) and SiLU' = s (1 + x (1 - s))."""
     x = np.asarray(x, np.float64)
     s = _sigmoid(x)
     y = x * s
     n = np.linalg.norm(y, axis=-1, keepdims=True)
-    yh = y / n
-    dy = (dxhat - yh * np.sum(yh * dxhat, axis=-1, keepdims=True)) / n
+    floor = n < NORM_EPS
+    nn = np.maximum(n, NORM_EPS)
+    yh = y / nn
+    dy = np.where(floor, dxhat / NORM_EPS,
+                  (dxhat - yh * np.sum(yh * dxhat, axis=-1, keepdims=True)) / nn)
     return dy * s * (1.0 + x * (1.0 - s))
 
 
@@ -64,10 +82,13 @@ def decay_from_preact(z, a, b):
     return np.exp(-A * _softplus(z + Bb))
 
 
-def transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b, qk_norm=True, gate_preact=True):
+def transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b, qk_norm=True, gate_preact=True,
+                     qk_round=None):
     """The operator's inputs (q, k, alpha_s, beta, alpha_r, gamma) from raw ones."""
     if qk_norm:
         q, k = qk_transform(q), qk_transform(k)
+        if qk_round == "bf16":
+            q, k = _round_bf16(q), _round_bf16(k)
     if gate_preact:
         return (q, k, decay_from_preact(z_as, decay_a, decay_b), _sigmoid(np.asarray(z_b, np.float64)),
                 decay_from_preact(z_ar, decay_a, decay_b), _sigmoid(np.asarray(z_g, np.float64)))
@@ -75,22 +96,23 @@ def transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b, qk_norm=True,
 
 
 def forward(variant, q, k, v, z_as, z_b, z_ar, z_g, decay_a=None, decay_b=None, clip=1.0,
-            S0=None, R0=None, cu_seqlens=None, flags=0, qk_norm=True, gate_preact=True):
+            S0=None, R0=None, cu_seqlens=None, flags=0, qk_norm=True, gate_preact=True,
+            qk_round=None):
     """Forward from raw inputs: (o, S_final, R_final)."""
     qq, kk, aS, bb, aR, gg = transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b,
-                                             qk_norm, gate_preact)
+                                             qk_norm, gate_preact, qk_round)
     return oracle.forward(variant, qq, kk, v, aS, bb, aR, gg, clip=clip, S0=S0, R0=R0,
                           cu_seqlens=cu_seqlens, flags=flags)
 
 
 def backward(variant, q, k, v, z_as, z_b, z_ar, z_g, dO, decay_a=None, decay_b=None, clip=1.0,
              S0=None, R0=None, dS_final=None, dR_final=None, cu_seqlens=None, flags=0,
-             qk_norm=True, gate_preact=True):
+             qk_norm=True, gate_preact=True, qk_round=None):
     """Gradients w.r.t. the raw inputs: dq, dk (raw q, k), dv, dalpha_s, dbeta,
     dalpha_r, dgamma (pre-activations), dS0, dR0 and, with gate_preact,
     ddecay_a, ddecay_b [H] (summed over every token of both decays)."""
     qq, kk, aS, bb, aR, gg = transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b,
-                                             qk_norm, gate_preact)
+                                             qk_norm, gate_preact, qk_round)
     g = oracle.backward(variant, qq, kk, v, aS, bb, aR, gg, dO, clip=clip, S0=S0, R0=R0,
                         dS_final=dS_final, dR_final=dR_final, cu_seqlens=cu_seqlens, flags=flags)
     out = dict(g)

@@ -27,6 +27,8 @@ RLA_OK = 0
 RLA_FLAG_SAVE_FOR_BACKWARD, RLA_FLAG_USE_SAVED = 1, 2
 # variants (include/rla.h): log-cosh residual, ungated output, decayed residual
 RLA_FLAG_RESIDUAL_TANH, RLA_FLAG_UNGATED_OUTPUT, RLA_FLAG_DECAYED_RESIDUAL = 4, 8, 16
+# input pre-processing: SiLU + L2 norm of q, k; gates given as pre-activations
+RLA_FLAG_QK_SILU_L2NORM, RLA_FLAG_GATE_PREACT = 32, 64
 RLA_F32, RLA_BF16 = 0, 1
 RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD, RLA_OP_RLA_BACKWARD = 0, 1, 2, 3
 
@@ -40,7 +42,8 @@ class rla_problem(ctypes.Structure):
                 ("head_dim_v", ctypes.c_int64), ("num_seqs", ctypes.c_int64),
                 ("cu_seqlens", ctypes.c_void_p), ("dtype", ctypes.c_int32),
                 ("clip", ctypes.c_float), ("out_dtype", ctypes.c_int32),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("decay_param", ctypes.c_void_p),
+                ("decay_param_grad", ctypes.c_void_p)]
 
 
 class RLAError(RuntimeError):
@@ -146,7 +149,7 @@ def _dtype_code(dt):
 
 
 def make_problem(q, v, cu_seqlens=None, clip: float = 1.0, out_dtype=None,
-                 flags: int = 0) -> rla_problem:
+                 flags: int = 0, decay_param=None, decay_param_grad=None) -> rla_problem:
     """rla_problem for q [B,T,H,dk] / [T,H,dk] and v, with optional cu_seqlens.
     out_dtype (dtype of o, dq, dk, dv) defaults to float32."""
     torch = _torch()
@@ -172,7 +175,8 @@ def make_problem(q, v, cu_seqlens=None, clip: float = 1.0, out_dtype=None,
         N = cu_seqlens.numel() - 1
     c = math.inf if clip is None else float(clip)
     out = _dtype_code(torch.float32 if out_dtype is None else out_dtype)
-    return rla_problem(B, T, H, dk, dv, N, _ptr(cu_seqlens), dtype, c, out, flags)
+    return rla_problem(B, T, H, dk, dv, N, _ptr(cu_seqlens), dtype, c, out, flags,
+                       _ptr(decay_param), _ptr(decay_param_grad))
 
 
 def _check(tensors, device):
@@ -195,20 +199,36 @@ def _workspace(problem, op, device, workspace):
     return torch.empty(max(need, 1), dtype=torch.uint8, device=device), need
 
 
+_VARIANT_MASK = (RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT | RLA_FLAG_DECAYED_RESIDUAL |
+                 RLA_FLAG_QK_SILU_L2NORM | RLA_FLAG_GATE_PREACT)
+
+
 def _variant_bits(variants: int) -> int:
-    if variants & ~(RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT | RLA_FLAG_DECAYED_RESIDUAL):
-        raise ValueError("variants must combine RLA_FLAG_RESIDUAL_TANH, "
-                         "RLA_FLAG_UNGATED_OUTPUT and RLA_FLAG_DECAYED_RESIDUAL")
+    if variants & ~_VARIANT_MASK:
+        raise ValueError("variants must combine RLA_FLAG_RESIDUAL_TANH, RLA_FLAG_UNGATED_OUTPUT, "
+                         "RLA_FLAG_DECAYED_RESIDUAL, RLA_FLAG_QK_SILU_L2NORM and RLA_FLAG_GATE_PREACT")
     return int(variants)
 
 
+def _check_decay_param(variants, decay_param, H, device):
+    if variants & RLA_FLAG_GATE_PREACT:
+        if decay_param is None:
+            raise ValueError("RLA_FLAG_GATE_PREACT needs decay_param [2, H] (a then b)")
+        if decay_param.numel() != 2 * H or not decay_param.is_contiguous() or \
+                decay_param.device != device:
+            raise ValueError("decay_param must be a contiguous [2, H] tensor on %s" % device)
+    return decay_param
+
+
 def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_seqlens,
-             out, workspace, stream, return_states, out_dtype, save_for_backward, variants=0):
+             out, workspace, stream, return_states, out_dtype, save_for_backward, variants=0,
+             decay_param=None):
     torch = _torch()
     lib = load_library()
     problem = make_problem(q, v, cu_seqlens, clip, out_dtype,
                            (RLA_FLAG_SAVE_FOR_BACKWARD if save_for_backward else 0) |
-                           _variant_bits(variants))
+                           _variant_bits(variants),
+                           _check_decay_param(variants, decay_param, q.shape[-2], q.device))
     if save_for_backward:
         op = RLA_OP_RDN_BACKWARD if op == RLA_OP_RDN_FORWARD else RLA_OP_RLA_BACKWARD
     dev = q.device
@@ -238,7 +258,7 @@ def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_
 
 def rla_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
                 cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
-                out_dtype=None, save_for_backward=False, variants=0):
+                out_dtype=None, save_for_backward=False, variants=0, decay_param=None):
     """RLA forward (Sec. 3.4, left box).  Returns (o, S_final, R_final).
     With save_for_backward the (backward-sized) workspace keeps what the
     matching backward call with use_saved=True reads instead of recomputing.
@@ -246,29 +266,37 @@ def rla_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=No
     RLA_FLAG_DECAYED_RESIDUAL bits (include/rla.h)."""
     return _forward("rla_forward", RLA_OP_RLA_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                     clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
-                    save_for_backward, variants)
+                    save_for_backward, variants, decay_param)
 
 
 def rdn_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None, R0=None,
                 cu_seqlens=None, out=None, workspace=None, stream=None, return_states=True,
-                out_dtype=None, save_for_backward=False, variants=0):
+                out_dtype=None, save_for_backward=False, variants=0, decay_param=None):
     """RDN forward (Sec. 3.4, right box).  Returns (o, S_final, R_final).
     With save_for_backward the (backward-sized) workspace keeps what the
     matching backward call with use_saved=True reads instead of recomputing."""
     return _forward("rdn_forward", RLA_OP_RDN_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                     clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
-                    save_for_backward, variants)
+                    save_for_backward, variants, decay_param)
 
 
 def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0):
+                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0,
+                 decay_param=None):
     torch = _torch()
     lib = load_library()
     if use_saved and workspace is None:
         raise ValueError("use_saved needs the workspace of the saving forward call")
+    _check_decay_param(variants, decay_param, q.shape[-2], q.device)
+    ddp = None
+    if variants & RLA_FLAG_GATE_PREACT:
+        ddp = grads.get("ddecay_param") if grads is not None else None
+        if ddp is None:
+            ddp = torch.empty(2, q.shape[-2], dtype=torch.float32, device=q.device)
     problem = make_problem(q, v, cu_seqlens, clip, out_dtype,
-                           (RLA_FLAG_USE_SAVED if use_saved else 0) | _variant_bits(variants))
+                           (RLA_FLAG_USE_SAVED if use_saved else 0) | _variant_bits(variants),
+                           decay_param, ddp)
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S0=S0, R0=R0, dO=dO, dS_final=dS_final, dR_final=dR_final), dev)
@@ -285,6 +313,8 @@ def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float 
                      dalpha_r=torch.empty_like(alpha_r), dgamma=torch.empty_like(gamma),
                      dS0=torch.empty(shape, dtype=torch.float32, device=dev),
                      dR0=torch.empty(shape, dtype=torch.float32, device=dev))
+    if ddp is not None:
+        grads["ddecay_param"] = ddp
     ws, need = _workspace(problem, op, dev, workspace)
     g = grads
     st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
@@ -300,31 +330,34 @@ def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float 
 
 def rdn_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0):
+                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0,
+                 decay_param=None):
     """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rdn_forward.
     Returns a dict dq, dk, dv, dalpha_s, dbeta, dalpha_r, dgamma, dS0, dR0.
     use_saved: read what rdn_forward(save_for_backward=True) left in `workspace`."""
     return _backward("rdn_backward", RLA_OP_RDN_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
-                     out_dtype, use_saved, variants)
+                     out_dtype, use_saved, variants, decay_param)
 
 
 def rla_backward(q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,
                  R0=None, dS_final=None, dR_final=None, cu_seqlens=None, workspace=None,
-                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0):
+                 stream=None, grads=None, out_dtype=None, use_saved=False, variants=0,
+                 decay_param=None):
     """Gradients of <dO,o> + <dS_final,S_T> + <dR_final,R_T> for rla_forward."""
     return _backward("rla_backward", RLA_OP_RLA_BACKWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                      dO, clip, S0, R0, dS_final, dR_final, cu_seqlens, workspace, stream, grads,
-                     out_dtype, use_saved, variants)
+                     out_dtype, use_saved, variants, decay_param)
 
 
 def _decode(name, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in, S_out, R_out, out,
-            stream, out_dtype, variants=0):
+            stream, out_dtype, variants=0, decay_param=None):
     torch = _torch()
     lib = load_library()
     if q.dim() != 4:
         raise ValueError("decoding takes q, k, v as [B, T, H, d] (T tokens per sequence)")
-    problem = make_problem(q, v, None, clip, out_dtype, _variant_bits(variants))
+    problem = make_problem(q, v, None, clip, out_dtype, _variant_bits(variants),
+                           _check_decay_param(variants, decay_param, q.shape[-2], q.device))
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S_in=S_in, R_in=R_in, S_out=S_out, R_out=R_out), dev)
@@ -352,16 +385,18 @@ def _decode(name, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in, S_ou
 
 
 def rla_decode(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S_in=None, R_in=None,
-               S_out=None, R_out=None, out=None, stream=None, out_dtype=None, variants=0):
+               S_out=None, R_out=None, out=None, stream=None, out_dtype=None, variants=0,
+               decay_param=None):
     """RLA recurrent step (Sec. 3.4, left box, evaluated token by token):
     q, k, v [B, T, H, d] with small T, gates [B, T, H].  Returns (o, S_out,
     R_out); pass S_out=S_in, R_out=R_in to update the states in place."""
     return _decode("rla_decode", q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in,
-                   S_out, R_out, out, stream, out_dtype, variants)
+                   S_out, R_out, out, stream, out_dtype, variants, decay_param)
 
 
 def rdn_decode(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S_in=None, R_in=None,
-               S_out=None, R_out=None, out=None, stream=None, out_dtype=None, variants=0):
+               S_out=None, R_out=None, out=None, stream=None, out_dtype=None, variants=0,
+               decay_param=None):
     """RDN recurrent step (Sec. 3.4, right box); arguments as rla_decode."""
     return _decode("rdn_decode", q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in,
-                   S_out, R_out, out, stream, out_dtype, variants)
+                   S_out, R_out, out, stream, out_dtype, variants, decay_param)

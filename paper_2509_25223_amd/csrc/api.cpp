@@ -32,6 +32,8 @@ struct Problem {
   int64_t B = 0, T = 0, H = 0, DK = 0, DV = 0, N = 0, ntok = 0, max_chunks = 0;
   bool varlen = false, bf16 = false, out_bf16 = false, save = false, use_saved = false;
   int32_t vflags = 0;   // kVar* bits
+  const float* decay_param = nullptr;
+  float* decay_param_grad = nullptr;
   const int32_t* cu = nullptr;
   float clip = -1.f;
 };
@@ -40,6 +42,7 @@ struct Workspace {
   size_t seqs = 0, chunks = 0, nchunks = 0, order = 0, gates = 0, mats = 0;
   size_t ckS = 0, ckR = 0, mask = 0, dS = 0, dR = 0, fblk = 0, bblk = 0, total = 0;
   size_t ckS_sc = 0, ckR_sc = 0, dS_sc = 0, dR_sc = 0;
+  size_t qh = 0, kh = 0, dqh = 0, dkh = 0, dpart = 0;   // pre-processing
 };
 
 // recurrent: the decoding step, whose kernel has no fp32 d_k restriction
@@ -57,11 +60,17 @@ rla_status check_problem(const rla_problem* pp, Problem& pr, bool recurrent = fa
   if (isnan(pp->clip) || pp->clip < 0.f) return RLA_ERR_VALUE;
   constexpr uint32_t kKnown = RLA_FLAG_SAVE_FOR_BACKWARD | RLA_FLAG_USE_SAVED |
                               RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT |
-                              RLA_FLAG_DECAYED_RESIDUAL;
+                              RLA_FLAG_DECAYED_RESIDUAL | RLA_FLAG_QK_SILU_L2NORM |
+                              RLA_FLAG_GATE_PREACT;
   if (pp->flags & ~kKnown) return RLA_ERR_VALUE;
   pr.vflags = ((pp->flags & RLA_FLAG_RESIDUAL_TANH) ? kVarTanh : 0) |
               ((pp->flags & RLA_FLAG_UNGATED_OUTPUT) ? kVarUngated : 0) |
-              ((pp->flags & RLA_FLAG_DECAYED_RESIDUAL) ? kVarDecayed : 0);
+              ((pp->flags & RLA_FLAG_DECAYED_RESIDUAL) ? kVarDecayed : 0) |
+              ((pp->flags & RLA_FLAG_GATE_PREACT) ? kVarGatePreact : 0) |
+              ((pp->flags & RLA_FLAG_QK_SILU_L2NORM) ? kVarQkNorm : 0);
+  if ((pp->flags & RLA_FLAG_GATE_PREACT) && !pp->decay_param) return RLA_ERR_NULL_ARG;
+  pr.decay_param = pp->decay_param;
+  pr.decay_param_grad = pp->decay_param_grad;
   pr.save = (pp->flags & RLA_FLAG_SAVE_FOR_BACKWARD) != 0;
   pr.use_saved = (pp->flags & RLA_FLAG_USE_SAVED) != 0;
   pr.B = pp->batch;
@@ -105,6 +114,17 @@ Workspace plan(const Problem& pr, int op) {
     w.order = take(sizeof(int32_t) * (size_t)pr.N);
   }
   w.gates = take(sizeof(float) * mc * H * kGateBlock);
+  const bool bwd = op == RLA_OP_RDN_BACKWARD || op == RLA_OP_RLA_BACKWARD;
+  if (pr.vflags & kVarQkNorm) {   // normalised q, k (input type); backward: their fp32 gradients
+    const size_t rows = (size_t)pr.ntok * H * (size_t)pr.DK;
+    w.qh = take((pr.bf16 ? 2 : 4) * rows);
+    w.kh = take((pr.bf16 ? 2 : 4) * rows);
+    if (bwd) {
+      w.dqh = take(4 * rows);
+      w.dkh = take(4 * rows);
+    }
+  }
+  if ((pr.vflags & kVarGatePreact) && bwd) w.dpart = take(sizeof(float) * mc * H * 2);
   w.mats = take((pr.bf16 ? 2 : 4) * mc * H * kNumMats * kMatElems);
   if (op == RLA_OP_RDN_BACKWARD || op == RLA_OP_RLA_BACKWARD) {
     // states: fp16 with per-(16 rows, 32 columns) scales for bf16 inputs, fp32 otherwise
@@ -143,6 +163,7 @@ OpParams make_params(const Problem& pr, const Workspace& w, unsigned char* ws, b
   p.clip = pr.clip;
   p.rdn = rdn ? 1 : 0;
   p.vflags = pr.vflags;
+  p.decay_param = pr.decay_param;
   p.out_bf16 = pr.out_bf16 ? 1 : 0;
   p.max_chunks = (int32_t)pr.max_chunks;
   p.st.nseq = (int32_t)pr.N;
@@ -229,6 +250,11 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
     e = hipMemsetAsync(o, 0, (size_t)pr.ntok * pr.H * pr.DV * (pr.out_bf16 ? 2 : 4), stream);
   if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
   if (e == hipSuccess) e = mark_stage(stream, true);
+  if (e == hipSuccess && (pr.vflags & kVarQkNorm)) {   // q, k -> SiLU + L2 norm rows
+    e = launch_qk_norm_fwd(q, k, ws + w.qh, ws + w.kh, pr.ntok * pr.H, (int)pr.DK, pr.bf16, stream);
+    p.q = ws + w.qh;
+    p.k = ws + w.kh;
+  }
   if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
   if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/true, /*ckpt=*/pr.save, stream);
@@ -283,6 +309,27 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   }
   if (e == hipSuccess && !pr.use_saved) e = build_tables(pr, w, ws, stream);
   if (e == hipSuccess) e = mark_stage(stream, true);
+  const bool qkn = (pr.vflags & kVarQkNorm) != 0;
+  if (qkn) {   // the chunked path reads the normalised rows (saved by a saving forward)
+    if (e == hipSuccess && !pr.use_saved)
+      e = launch_qk_norm_fwd(q, k, ws + w.qh, ws + w.kh, pr.ntok * pr.H, (int)pr.DK, pr.bf16, stream);
+    p.q = ws + w.qh;
+    p.k = ws + w.kh;
+    // the gradient kernel writes d(normalised q, k) in fp32 into the workspace
+    p.dq = ws + w.dqh;
+    p.dk = ws + w.dkh;
+    if (e == hipSuccess && pr.varlen) {   // rows outside every sequence stay zero
+      const size_t bytes = (size_t)pr.ntok * pr.H * pr.DK * 4;
+      e = hipMemsetAsync(ws + w.dqh, 0, bytes, stream);
+      if (e == hipSuccess) e = hipMemsetAsync(ws + w.dkh, 0, bytes, stream);
+    }
+  }
+  const bool pre = (pr.vflags & kVarGatePreact) != 0;
+  if (pre) {
+    p.decay_partials = reinterpret_cast<float*>(ws + w.dpart);
+    if (e == hipSuccess)
+      e = hipMemsetAsync(ws + w.dpart, 0, sizeof(float) * (size_t)pr.max_chunks * pr.H * 2, stream);
+  }
   if (!pr.use_saved) {
     if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
     if (e == hipSuccess) e = mark_stage(stream, false);
@@ -291,7 +338,18 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   }
   if (e == hipSuccess) e = launch_bwd_scan(p, pr.bf16, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
-  if (e == hipSuccess) e = launch_bwd_grad(p, pr.bf16, stream);
+  {
+    OpParams pg = p;
+    if (qkn) pg.out_bf16 = 0;   // fp32 gradients of the normalised rows
+    if (e == hipSuccess) e = launch_bwd_grad(pg, pr.bf16, stream);
+  }
+  if (e == hipSuccess && qkn)
+    e = launch_qk_norm_bwd(q, k, reinterpret_cast<const float*>(ws + w.dqh),
+                           reinterpret_cast<const float*>(ws + w.dkh), dq, dk, pr.ntok * pr.H,
+                           (int)pr.DK, pr.bf16, pr.out_bf16, stream);
+  if (e == hipSuccess && pre && pr.decay_param_grad)
+    e = launch_decay_grad_reduce(p.decay_partials, (int)pr.max_chunks, (int)pr.H,
+                                 pr.decay_param_grad, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
   return to_status(e);
 }
@@ -339,6 +397,7 @@ rla_status decode(bool rdn, const rla_problem* problem, const void* q, const voi
   p.clip = pr.clip;
   p.rdn = rdn ? 1 : 0;
   p.vflags = pr.vflags;
+  p.decay_param = pr.decay_param;
   p.out_bf16 = pr.out_bf16 ? 1 : 0;
   p.st.nseq = (int32_t)pr.N;
   p.st.dense_T = pr.T;

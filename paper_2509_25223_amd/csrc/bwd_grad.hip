@@ -624,13 +624,39 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       const float a = __shfl_down(ss, off, 64), b = __shfl_down(sr, off, 64);
       if (t + off < 64) { ss += a; sr += b; }
     }
+    // ss, sr: gradients of log aS_t, log aR_t
+    float pa = 0.f, pb = 0.f;   // this token's share of d/da_h, d/db_h (pre-activations)
     if (t < len) {
       const int64_t gi = (tok + t) * H + h;
-      const float as = p.alpha_s[gi], ar = p.alpha_r[gi];
-      p.dalpha_s[gi] = as >= 1.17549435e-38f ? ss / as : 0.f;
-      p.dalpha_r[gi] = ar >= 1.17549435e-38f ? sr / ar : 0.f;
-      p.dbeta[gi] = esum[t] + total(sB, t) + total(sZB, t);
-      p.dgamma[gi] = esum[kChunk + t] + total(sGM, t) + total(sZGM, t);
+      const float db = esum[t] + total(sB, t) + total(sZB, t);
+      const float dgm = esum[kChunk + t] + total(sGM, t) + total(sZGM, t);
+      if (vf & kVarGatePreact) {
+        // log a = -A softplus(z + Bb): d/dz = -A sigmoid(z + Bb), d/dA = -softplus(z + Bb);
+        // beta = sigmoid(z): d/dz = beta (1 - beta), likewise gamma
+        const float A = p.decay_param[h], Bb = p.decay_param[H + h];
+        const float zs = p.alpha_s[gi] + Bb, zr = p.alpha_r[gi] + Bb;
+        const float dzs = ss * (-A * sigmoid_f(zs)), dzr = sr * (-A * sigmoid_f(zr));
+        p.dalpha_s[gi] = dzs;
+        p.dalpha_r[gi] = dzr;
+        pa = -(ss * softplus_f(zs) + sr * softplus_f(zr));
+        pb = dzs + dzr;
+        p.dbeta[gi] = db * gbt[t] * (1.f - gbt[t]);
+        p.dgamma[gi] = dgm * ggm[t] * (1.f - ggm[t]);
+      } else {
+        const float as = p.alpha_s[gi], ar = p.alpha_r[gi];
+        p.dalpha_s[gi] = as >= 1.17549435e-38f ? ss / as : 0.f;
+        p.dalpha_r[gi] = ar >= 1.17549435e-38f ? sr / ar : 0.f;
+        p.dbeta[gi] = db;
+        p.dgamma[gi] = dgm;
+      }
+    }
+    if (vf & kVarGatePreact) {   // the chunk's (a, b) partials, summed over its tokens
+      pa = wave_sum(pa);
+      pb = wave_sum(pb);
+      if (t == 0) {
+        p.decay_partials[((int64_t)c * H + h) * 2 + 0] = pa;
+        p.decay_partials[((int64_t)c * H + h) * 2 + 1] = pb;
+      }
     }
   }
 #pragma unroll
@@ -669,7 +695,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 template <typename IN, int DK, int DV, bool RDN, typename OT>
 hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
   typedef GradLayout<IN, DK, DV> L;
-  auto kern = p.vflags ? bwd_grad_kernel<IN, DK, DV, RDN, OT, true> : bwd_grad_kernel<IN, DK, DV, RDN, OT, false>;
+  auto kern = (p.vflags & (kVarOperator | kVarGatePreact)) ? bwd_grad_kernel<IN, DK, DV, RDN, OT, true>
+                                                            : bwd_grad_kernel<IN, DK, DV, RDN, OT, false>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;

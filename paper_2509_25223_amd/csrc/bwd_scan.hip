@@ -592,7 +592,7 @@ hipError_t launch_bwd_scan_v(const OpParams& p, hipStream_t stream) {
 
 template <typename IN, int DK, int BV, bool RDN>
 hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
-  return p.vflags ? launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream)
+  return (p.vflags & kVarOperator) ? launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream)
                   : launch_bwd_scan_v<IN, DK, BV, RDN, false>(p, stream);
 }
 

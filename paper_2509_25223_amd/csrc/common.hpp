@@ -721,6 +721,13 @@ __device__ __forceinline__ bool chunk_info(const SeqTable& t, int c, ChunkInfo& 
 // Decay logarithm with the documented floor 2^-126 on the decay.
 __device__ __forceinline__ float log_decay(float a) { return __logf(fmaxf(a, 1.17549435e-38f)); }
 
+// Gate activations of the pre-activation inputs (Mamba-2 decay, sigmoid
+// write strengths): softplus(z) = log(1 + e^z), sigmoid(z) = 1 / (1 + e^-z).
+__device__ __forceinline__ float softplus_f(float z) {
+  return z > 20.f ? z : log1pf(__expf(z));
+}
+__device__ __forceinline__ float sigmoid_f(float z) { return 1.f / (1.f + __expf(-z)); }
+
 // Inclusive prefix sum over the 64 lanes of a wave.
 __device__ __forceinline__ float wave_inclusive_scan(float x) {
   const int lane = threadIdx.x & 63;

@@ -26,6 +26,8 @@
 // (RDN) or aS S_{t-1} + beta v k^T (RLA), and likewise for R with (aR, gamma,
 // r), written in the transposed storage.  Variants: x = v - aS Sk (decayed
 // residual), r = c tanh(x / c) (log-cosh residual), o = Sq + R_t q (ungated).
+// Pre-processing: q, k rows through SiLU and x / max(||x||, 1e-12); gates from
+// pre-activations (aS, aR = exp(-a_h softplus(z + b_h)), beta, gamma = sigmoid).
 #include "kernels.hpp"
 
 namespace rla {
@@ -81,9 +83,30 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(OpParams p) {
     if (tid < BV) sv[b][tid] = to_f<IN>(vg[(tok * H + h) * DV + j0 + tid]);
     if (tid < 4) {
       const float* gp = tid == 0 ? p.alpha_s : tid == 1 ? p.beta : tid == 2 ? p.alpha_r : p.gamma;
-      sg[b][tid] = gp[tok * H + h];
+      float gv = gp[tok * H + h];
+      if (p.vflags & kVarGatePreact)
+        gv = (tid & 1) ? sigmoid_f(gv) : __expf(-p.decay_param[h] * softplus_f(gv + p.decay_param[H + h]));
+      sg[b][tid] = gv;
     }
     __syncthreads();
+    if (p.vflags & kVarQkNorm) {   // wave 0: q, wave 1: k
+      if (w < 2) {
+        float* x = w == 0 ? sq[b] : sk[b];
+        float y[DK / 64], ss = 0.f;
+#pragma unroll
+        for (int e = 0; e < DK / 64; ++e) {
+          const float v = x[lane + 64 * e];
+          y[e] = v / (1.f + __expf(-v));
+          ss = __builtin_fmaf(y[e], y[e], ss);
+        }
+#pragma unroll
+        for (int m = 1; m < 64; m <<= 1) ss += __shfl_xor(ss, m);
+        const float inv = 1.f / fmaxf(sqrtf(ss), 1e-12f);
+#pragma unroll
+        for (int e = 0; e < DK / 64; ++e) x[lane + 64 * e] = y[e] * inv;
+      }
+      __syncthreads();
+    }
 
     // ---- column sums over this thread's rows, then over the wave's row groups ----
     floatx4 pSk = zero4(), pSq = zero4(), pRk = zero4(), pRq = zero4();

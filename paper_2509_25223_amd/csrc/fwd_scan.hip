@@ -538,7 +538,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT>
 hipError_t launch_fwd_t(const OpParams& p, hipStream_t stream) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
-  auto kern = p.vflags ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
+  auto kern = (p.vflags & kVarOperator) ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
                        : fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, false>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);

@@ -19,7 +19,12 @@ __host__ __device__ inline int64_t blk_off(int64_t gc, int h, int H, int b, int 
 //   kVarTanh     r = c tanh(x / c) instead of the clip (c < 0: r = x; c = 0: r = 0)
 //   kVarUngated  o = S_{t-1} q + R_t q
 //   kVarDecayed  x = v - aS S_{t-1} k
+//   kVarGatePreact gates given as pre-activations (prep, gradient kernel, decoding)
+//   kVarQkNorm     q, k given raw: SiLU + L2 normalisation (decoding; the host
+//                  runs the pre-processing kernels for the chunked path)
 constexpr int kVarTanh = 1, kVarUngated = 2, kVarDecayed = 4;
+constexpr int kVarOperator = kVarTanh | kVarUngated | kVarDecayed;   // bits the scans read
+constexpr int kVarGatePreact = 8, kVarQkNorm = 16;
 
 // Everything a launch needs; passed by value to the kernels.
 struct OpParams {
@@ -41,6 +46,8 @@ struct OpParams {
   const float* gamma = nullptr;
   const float* S0 = nullptr;
   const float* R0 = nullptr;
+  const float* decay_param = nullptr;   // [2][H] a, b (kVarGatePreact)
+  float* decay_partials = nullptr;      // [max_chunks][H][2] per-chunk d/da, d/db (backward)
 
   void* o = nullptr;
   float* S_fin = nullptr;
@@ -101,6 +108,21 @@ hipError_t launch_bwd_scan(const OpParams& p, bool bf16, hipStream_t stream);
 
 // Chunk-parallel gradient contractions.
 hipError_t launch_bwd_grad(const OpParams& p, bool bf16, hipStream_t stream);
+
+// SiLU + L2 normalisation of the q and k rows ([rows][DK] each) into qh, kh.
+hipError_t launch_qk_norm_fwd(const void* q, const void* k, void* qh, void* kh, int64_t rows,
+                              int DK, bool bf16, hipStream_t stream);
+
+// Gradient through the SiLU + L2 normalisation: dq = J^T dqh (raw q, fp32
+// dqh), likewise k; dq, dk in the output type.
+hipError_t launch_qk_norm_bwd(const void* q, const void* k, const float* dqh, const float* dkh,
+                              void* dq, void* dk, int64_t rows, int DK, bool bf16, bool out_bf16,
+                              hipStream_t stream);
+
+// Sums the gradient kernel's per-chunk (a, b) partials over chunks per head:
+// out[h] = sum_c partials[c][h][0], out[H + h] = sum_c partials[c][h][1].
+hipError_t launch_decay_grad_reduce(const float* partials, int nch, int H, float* out,
+                                    hipStream_t stream);
 
 // Recurrent step over T tokens per sequence (dense layout, st.dense_T = T,
 // st.nseq = B) with S0/R0 in (NULL = zeros) and S_fin/R_fin out.

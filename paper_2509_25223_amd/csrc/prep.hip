@@ -151,20 +151,24 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
     }
   }
   // ---- gates: wave 0 scans log aS, wave 1 scans log aR ----
+  // (pre-activations: log a = -a_h softplus(z + b_h), beta = sigmoid(z),
+  //  gamma = sigmoid(z))
   if (tid < 128) {
     const int t = tid & 63;
     const bool valid = t < ci.len;
+    const bool pre = (p.vflags & kVarGatePreact) != 0;
     const int64_t gi = (ci.tok + t) * H + h;
     const float* a = tid < 64 ? p.alpha_s : p.alpha_r;
-    const float la = valid ? log_decay(a[gi]) : 0.f;
+    float la = 0.f;
+    if (valid) la = pre ? -p.decay_param[h] * softplus_f(a[gi] + p.decay_param[H + h]) : log_decay(a[gi]);
     const float cum = wave_inclusive_scan(la);
     if (tid < 64) {
       gs[t] = cum;
-      bt[t] = valid ? p.beta[gi] : 0.f;
+      bt[t] = valid ? (pre ? sigmoid_f(p.beta[gi]) : p.beta[gi]) : 0.f;
       gsp[t] = cum - la;
     } else {
       gr[t] = cum;
-      gm[t] = valid ? p.gamma[gi] : 0.f;
+      gm[t] = valid ? (pre ? sigmoid_f(p.gamma[gi]) : p.gamma[gi]) : 0.f;
     }
   }
   __syncthreads();

@@ -168,8 +168,21 @@ def test_variant_flags_validated(lib):
     p = prob()
     p.flags = rla.RLA_FLAG_RESIDUAL_TANH | rla.RLA_FLAG_UNGATED_OUTPUT | rla.RLA_FLAG_DECAYED_RESIDUAL
     assert call_fwd(lib, p, ws=None) == 5   # passes flag validation, stops at the workspace
-    p.flags = 32
+    p.flags = 1 << 12
     assert call_fwd(lib, p) == 6
     pd = prob(T=1)
-    pd.flags = 32
+    pd.flags = 1 << 12
     assert call_dec(lib, pd) == 6
+
+
+def test_preproc_flags_need_decay_param(lib):
+    """Gates given as pre-activations need the per-head (a, b) parameters."""
+    p = prob()
+    p.flags = rla.RLA_FLAG_GATE_PREACT
+    assert call_fwd(lib, p) == 1
+    p.decay_param = FAKE
+    assert call_fwd(lib, p, ws=None) == 5
+    p.flags = rla.RLA_FLAG_QK_SILU_L2NORM
+    p.decay_param = None
+    # q, k normalisation needs workspace for the normalised rows
+    assert rla.rla_workspace_size(p, rla.RLA_OP_RDN_FORWARD) > rla.rla_workspace_size(prob(), rla.RLA_OP_RDN_FORWARD)

@@ -22,6 +22,8 @@ def test_qk_transform_closed_forms():
     y = preproc.qk_transform(np.array([[1.0, 3.0]]))
     s1, s3 = 0.7310585786300049, 3.0 * 0.9525741268224334   # 1 sigma(1), 3 sigma(3)
     np.testing.assert_allclose(y, [[s1 / math.hypot(s1, s3), s3 / math.hypot(s1, s3)]], atol=1e-15)
+    # an all-zero row stays zero (the 1e-12 floor of x / max(||x||, eps))
+    np.testing.assert_array_equal(preproc.qk_transform(np.zeros((1, 3))), np.zeros((1, 3)))
 
 
 def test_decay_reparameterisation_closed_form():

@@ -1,0 +1,175 @@
+"""GPU parity of the in-operator input pre-processing (SiLU + L2 norm of q, k;
+gates from pre-activations with per-head Mamba-2 decay parameters) against
+the fp64 oracle's pre-processing (oracle/preproc.py): forward, backward
+(recomputing and saved), the (a, b) gradients, and decoding."""
+import math
+
+import numpy as np
+import pytest
+
+import datagen
+import oracle
+import paper_2509_25223_amd as rla
+from oracle import preproc
+from tests.gpu_util import GRAD_KEYS, TOL, dev, host, oracle_flags, rel_err
+
+pytestmark = pytest.mark.gpu
+
+QKN, PRE = rla.RLA_FLAG_QK_SILU_L2NORM, rla.RLA_FLAG_GATE_PREACT
+CASES = [QKN, PRE, QKN | PRE, QKN | PRE | rla.RLA_FLAG_RESIDUAL_TANH]
+NAMES = {QKN: "qknorm", PRE: "preact", QKN | PRE: "both",
+         QKN | PRE | rla.RLA_FLAG_RESIDUAL_TANH: "both+tanh"}
+
+
+def raw_inputs(seed, lens, H, d, dtype, flags, grads=False):
+    """Raw inputs: q, k ~ N(0, 1) unnormalised (with QKN), else normalised;
+    gate pre-activations z ~ N(-3, 1) for the decays (then aS ~ 0.9 for a ~ 1),
+    N(0, 1) for beta and gamma (with PRE), else datagen's gate values."""
+    wl = datagen.small("rdn_fwdbwd" if grads else "rdn_fwd", dtype, lens, H=H, d=d)
+    inp = datagen.make_inputs(wl, seed=seed, grads=grads)
+    rng = np.random.default_rng(seed + 1000)
+    n = inp["q"].shape[0]
+    rnd = datagen.round_to_bf16 if dtype == "bf16" else (lambda a: a.astype(np.float32))
+    if flags & QKN:
+        inp["q"] = rnd(rng.standard_normal((n, H, d)).astype(np.float32))
+        inp["k"] = rnd(rng.standard_normal((n, H, d)).astype(np.float32))
+    if flags & PRE:
+        inp["alpha_s"] = (rng.standard_normal((n, H)) - 3.0).astype(np.float32)
+        inp["alpha_r"] = (rng.standard_normal((n, H)) - 3.0).astype(np.float32)
+        inp["beta"] = rng.standard_normal((n, H)).astype(np.float32)
+        inp["gamma"] = rng.standard_normal((n, H)).astype(np.float32)
+    dp = np.stack([rng.uniform(0.5, 1.5, H), rng.normal(0.0, 0.5, H)]).astype(np.float32)
+    return inp, dp
+
+
+def oracle_args(inp, dp, flags, dtype="bf16"):
+    return dict(decay_a=dp[0], decay_b=dp[1], qk_norm=bool(flags & QKN), gate_preact=bool(flags & PRE),
+                flags=oracle_flags(flags), qk_round="bf16" if dtype == "bf16" else None)
+
+
+def nudged(variant, inp, dp, flags, dtype, S0=None, R0=None):
+    """Kink margin on the transformed inputs (only v moves), as for the plain tests."""
+    if flags & rla.RLA_FLAG_RESIDUAL_TANH:
+        return inp
+    qq, kk, aS, bb, aR, gg = preproc.transform_inputs(inp["q"], inp["k"], inp["alpha_s"], inp["beta"],
+                                                       inp["alpha_r"], inp["gamma"], dp[0], dp[1],
+                                                       bool(flags & QKN), bool(flags & PRE),
+                                                       "bf16" if dtype == "bf16" else None)
+    v, _ = oracle.nudge_margin(variant, qq, kk, inp["v"], aS, bb, aR, gg, clip=1.0, S0=S0, R0=R0,
+                               cu_seqlens=inp["cu_seqlens"], margin=2e-2 if dtype == "bf16" else 1e-4,
+                               grid="bf16" if dtype == "bf16" else "f32", flags=oracle_flags(flags))
+    out = dict(inp)
+    out["v"] = v.astype(np.float32)
+    return out
+
+
+def to_gpu(inp, dtype, device):
+    import torch
+    td = torch.bfloat16 if dtype == "bf16" else torch.float32
+    t = {n: dev(inp[n], td, device) for n in ("q", "k", "v") + (("dO",) if "dO" in inp else ())}
+    t.update({n: dev(inp[n], torch.float32, device) for n in ("alpha_s", "beta", "alpha_r", "gamma")})
+    t["cu"] = torch.from_numpy(np.asarray(inp["cu_seqlens"], np.int32)).to(device)
+    return t
+
+
+def report(tag, errs, tol):
+    print("[%s] %s" % (tag, " ".join("%s=%.2e" % kv for kv in errs.items())), flush=True)
+    for key, e in errs.items():
+        assert e <= tol, (key, e)
+
+
+@pytest.mark.parametrize("flags", CASES, ids=[NAMES[f] for f in CASES])
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_forward(device, variant, dtype, d, flags):
+    import torch
+    lens = [1, 64, 0, 130, 65]
+    inp, dp = raw_inputs(401, lens, 2, d, dtype, flags)
+    S0, R0 = datagen.random_states(41, len(lens), 2, d, d)
+    t = to_gpu(inp, dtype, device)
+    fn = rla.rdn_forward if variant == "rdn" else rla.rla_forward
+    o, Sf, Rf = fn(t["q"], t["k"], t["v"], t["alpha_s"], t["beta"], t["alpha_r"], t["gamma"],
+                   S0=dev(S0, torch.float32, device), R0=dev(R0, torch.float32, device),
+                   cu_seqlens=t["cu"], variants=flags, decay_param=dev(dp, torch.float32, device))
+    torch.cuda.synchronize()
+    ro, rS, rR = preproc.forward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
+                                 inp["alpha_r"], inp["gamma"], S0=S0, R0=R0,
+                                 cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags, dtype))
+    report("fwd %s %s %s" % (variant, dtype, NAMES[flags]),
+           dict(o=rel_err(host(o), ro), S=rel_err(host(Sf), rS), R=rel_err(host(Rf), rR)), TOL[dtype])
+
+
+@pytest.mark.parametrize("flags", CASES, ids=[NAMES[f] for f in CASES])
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 128)])
+def test_backward(device, variant, dtype, d, flags):
+    import torch
+    lens = [64, 130, 5]
+    inp, dp = raw_inputs(402, lens, 2, d, dtype, flags, grads=True)
+    S0, R0 = datagen.random_states(42, len(lens), 2, d, d)
+    inp = nudged(variant, inp, dp, flags, dtype, S0, R0)
+    t = to_gpu(inp, dtype, device)
+    bwd = rla.rdn_backward if variant == "rdn" else rla.rla_backward
+    g = bwd(t["q"], t["k"], t["v"], t["alpha_s"], t["beta"], t["alpha_r"], t["gamma"], t["dO"],
+            S0=dev(S0, torch.float32, device), R0=dev(R0, torch.float32, device), cu_seqlens=t["cu"],
+            variants=flags, decay_param=dev(dp, torch.float32, device))
+    torch.cuda.synchronize()
+    ref = preproc.backward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
+                           inp["alpha_r"], inp["gamma"], inp["dO"], S0=S0, R0=R0,
+                           cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags, dtype))
+    errs = {}
+    for key in GRAD_KEYS:
+        a = host(g[key])
+        errs[key] = rel_err(a.reshape(ref[key].shape), ref[key])
+    if flags & PRE:
+        ddp = host(g["ddecay_param"])
+        errs["da"] = rel_err(ddp[0], ref["ddecay_a"])
+        errs["db"] = rel_err(ddp[1], ref["ddecay_b"])
+    report("bwd %s %s %s" % (variant, dtype, NAMES[flags]), errs, TOL[dtype])
+
+
+def test_saved_forward_path_is_identical(device):
+    import torch
+    flags = QKN | PRE
+    inp, dp = raw_inputs(403, [200, 200], 2, 128, "bf16", flags, grads=True)
+    B, T, H, d = 2, 200, 2, 128
+    q, k, v, dO = (dev(inp[n], torch.bfloat16, device).view(B, T, H, d) for n in ("q", "k", "v", "dO"))
+    gates = [dev(inp[n], torch.float32, device).view(B, T, H)
+             for n in ("alpha_s", "beta", "alpha_r", "gamma")]
+    dpg = dev(dp, torch.float32, device)
+    prob = rla.make_problem(q, v, flags=flags, decay_param=dpg)
+    ws = torch.empty(rla.rla_workspace_size(prob, rla.RLA_OP_RDN_BACKWARD), dtype=torch.uint8, device=device)
+    rla.rdn_forward(q, k, v, *gates, workspace=ws, save_for_backward=True, variants=flags, decay_param=dpg)
+    g1 = rla.rdn_backward(q, k, v, *gates, dO, workspace=ws, use_saved=True, variants=flags, decay_param=dpg)
+    g2 = rla.rdn_backward(q, k, v, *gates, dO, variants=flags, decay_param=dpg)
+    torch.cuda.synchronize()
+    for key in list(GRAD_KEYS) + ["ddecay_param"]:
+        assert torch.equal(g1[key], g2[key]), key
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+def test_decode(device, variant):
+    import torch
+    flags = QKN | PRE
+    B, T, H, d = 3, 5, 2, 128
+    inp, dp = raw_inputs(404, [T] * B, H, d, "bf16", flags)
+    S0, R0 = datagen.random_states(44, B, H, d, d)
+    t = {n: dev(inp[n], torch.bfloat16, device).view(B, T, H, d) for n in ("q", "k", "v")}
+    gates = [dev(inp[n], torch.float32, device).view(B, T, H) for n in ("alpha_s", "beta", "alpha_r", "gamma")]
+    Sd, Rd = dev(S0, torch.float32, device), dev(R0, torch.float32, device)
+    fn = rla.rdn_decode if variant == "rdn" else rla.rla_decode
+    outs = []
+    for s in range(T):
+        sl = slice(s, s + 1)
+        o, Sd, Rd = fn(*[t[n][:, sl].contiguous() for n in ("q", "k", "v")],
+                       *[g[:, sl].contiguous() for g in gates], S_in=Sd, R_in=Rd, S_out=Sd, R_out=Rd,
+                       variants=flags, decay_param=dev(dp, torch.float32, device))
+        outs.append(o)
+    o = torch.cat(outs, dim=1)
+    torch.cuda.synchronize()
+    ro, rS, rR = preproc.forward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
+                                 inp["alpha_r"], inp["gamma"], S0=S0, R0=R0,
+                                 cu_seqlens=inp["cu_seqlens"],
+                                 **oracle_args(inp, dp, flags, "fp32 rows"))   # decoding keeps the rows in fp32
+    report("decode %s both" % variant, dict(o=rel_err(host(o).reshape(-1, H, d), ro),
+                                            S=rel_err(host(Sd), rS), R=rel_err(host(Rd), rR)), TOL["bf16"])
