@@ -517,6 +517,47 @@ __device__ __forceinline__ uint32_t cvt_pk_f16(float a, float b) {
   return __builtin_bit_cast(uint32_t, f16x2{to_f16(a), to_f16(b)});
 }
 
+// Packs two adjacent 16 x 16 accumulator tiles (a0: columns 0..15, a1:
+// columns 16..31 of a 16-row strip), each value times `scale` and rounded to
+// fp16, into one 16-byte piece per lane holding 8 consecutive columns of one
+// row: on return `row` (0..15) and `col` (0, 8, 16 or 24) say where the piece
+// goes.  Three DPP exchanges (lanes c^1 and c^2 inside quads, then c^4 inside
+// rows) turn a lane's 4 rows x 1 column of both tiles into 1 row x 8 columns.
+__device__ __forceinline__ uint4 pack_strip_f16(const floatx4& a0, const floatx4& a1, float scale,
+                                                int& row, int& col) {
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+  const int lane = threadIdx.x & 63, c = lane & 15, q = lane >> 4, g = c >> 2;
+  const bool odd = c & 1, upper = c & 2, hi4 = g & 1;
+  // v_perm byte selectors over {recv:keep}: even lanes (keep, recv), odd (recv, keep)
+  const uint32_t selA = odd ? 0x01000504u : 0x05040100u;
+  const uint32_t selB = odd ? 0x03020706u : 0x07060302u;
+  u32x2 out[2];
+#pragma unroll
+  for (int jt = 0; jt < 2; ++jt) {
+    const floatx4& a = jt ? a1 : a0;
+    const uint32_t p01 = cvt_pk_f16(a[0] * scale, a[1] * scale);
+    const uint32_t p23 = cvt_pk_f16(a[2] * scale, a[3] * scale);
+    // round 1, lanes c and c^1: even lanes end with rows 0, 1 and odd
+    // lanes with rows 2, 3, each as a column pair
+    const uint32_t keep = odd ? p23 : p01;
+    const uint32_t recv = dpp_u32<0xB1>(odd ? p01 : p23);
+    const uint32_t x = __builtin_amdgcn_perm(recv, keep, selA);
+    const uint32_t y = __builtin_amdgcn_perm(recv, keep, selB);
+    // round 2, lanes c and c^2: each lane ends with one row, 4 columns
+    const uint32_t recv2 = dpp_u32<0x4E>(upper ? x : y);
+    out[jt] = upper ? u32x2{recv2, y} : u32x2{x, recv2};
+  }
+  // round 3, lanes c and c^4 (column groups g, g^1): the lower lane keeps its
+  // tile-0 columns and takes its partner's, the upper lane the same for tile
+  // 1 (row_shl:4 / row_shr:4 stay inside the 16-lane row)
+  const u32x2 snd = hi4 ? out[0] : out[1];
+  const uint32_t fromR0 = dpp_u32<0x104>(snd.x), fromR1 = dpp_u32<0x104>(snd.y);   // lane c + 4
+  const uint32_t fromL0 = dpp_u32<0x114>(snd.x), fromL1 = dpp_u32<0x114>(snd.y);   // lane c - 4
+  row = 4 * q + (((c & 1) << 1) | ((c >> 1) & 1));
+  col = hi4 ? 16 + 4 * (g - 1) : 4 * g;
+  return hi4 ? uint4{fromL0, fromL1, out[1].x, out[1].y} : uint4{out[0].x, out[0].y, fromR0, fromR1};
+}
+
 // Saves one 32-column block of a state held in MFMA accumulators: tile
 // acc[it][jt] holds rows row0 + 16 it + acc_row(r) and columns
 // 16 jt + acc_col().  Each 16-row x 32-column tile is divided by one power of
@@ -524,21 +565,12 @@ __device__ __forceinline__ uint32_t cvt_pk_f16(float a, float b) {
 // row-major (row stride ld); the scale goes to sc[(row0 / 16 + it) * sc_ld].
 // fp16 keeps 11 significant bits for every value within 2^-28 of the tile's
 // largest, so one scale per tile loses nothing a per-row scale would keep
-// for states whose rows span fewer than ~28 binades.  Three DPP exchanges
-// (lanes c^1, c^2 inside quads, then c^4 inside rows) turn a lane's 4 rows x
-// 1 column of both column tiles into 1 row x 8 consecutive columns, so each
-// tile leaves in one 16-byte store per lane (a wave writes 16 rows x 64 B).
+// for states whose rows span fewer than ~28 binades.  Each tile leaves in one
+// 16-byte store per lane (pack_strip_f16; a wave writes 16 rows x 64 B).
 template <int IT>
 __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16* dst, int64_t ld,
                                                float* sc, int64_t sc_ld, int row0) {
-  typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  const int lane = threadIdx.x & 63, c = lane & 15, q = lane >> 4, g = c >> 2;
-  const bool odd = c & 1, upper = c & 2, hi4 = g & 1;
-  const int rho = ((c & 1) << 1) | ((c >> 1) & 1);   // row of the quad this lane stores
-  // v_perm byte selectors over {recv:keep}: even lanes (keep, recv), odd (recv, keep)
-  const uint32_t selA = odd ? 0x01000504u : 0x05040100u;
-  const uint32_t selB = odd ? 0x03020706u : 0x07060302u;
+  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     // tile maximum: in-lane, over the 16-lane row (DPP), over the 4 rows
@@ -556,33 +588,9 @@ __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16*
                             max((uint32_t)__builtin_amdgcn_readlane((int)m, 32),
                                 (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
     const int e = pow2_scale_exp(mt);
-    const float inv = exp2_int(-e);
-    u32x2 out[2];
-#pragma unroll
-    for (int jt = 0; jt < 2; ++jt) {
-      const uint32_t p01 = cvt_pk_f16(acc[it][jt][0] * inv, acc[it][jt][1] * inv);
-      const uint32_t p23 = cvt_pk_f16(acc[it][jt][2] * inv, acc[it][jt][3] * inv);
-      // round 1, lanes c and c^1: even lanes end with rows 0, 1 and odd
-      // lanes with rows 2, 3, each as a column pair
-      const uint32_t keep = odd ? p23 : p01;
-      const uint32_t recv = dpp_u32<0xB1>(odd ? p01 : p23);
-      const uint32_t a = __builtin_amdgcn_perm(recv, keep, selA);
-      const uint32_t b = __builtin_amdgcn_perm(recv, keep, selB);
-      // round 2, lanes c and c^2: each lane ends with one row, 4 columns
-      const uint32_t recv2 = dpp_u32<0x4E>(upper ? a : b);
-      out[jt] = upper ? u32x2{recv2, b} : u32x2{a, recv2};
-    }
-    // round 3, lanes c and c^4 (column groups g, g^1): the lower lane keeps
-    // its tile-0 columns and takes its partner's, the upper lane the same
-    // for tile 1 (row_shl:4 / row_shr:4 stay inside the 16-lane row)
-    const u32x2 snd = hi4 ? out[0] : out[1];
-    const uint32_t fromR0 = dpp_u32<0x104>(snd.x), fromR1 = dpp_u32<0x104>(snd.y);   // lane c + 4
-    const uint32_t fromL0 = dpp_u32<0x114>(snd.x), fromL1 = dpp_u32<0x114>(snd.y);   // lane c - 4
-    const u32x4 v = hi4 ? u32x4{fromL0, fromL1, out[1].x, out[1].y}
-                        : u32x4{out[0].x, out[0].y, fromR0, fromR1};
-    const int64_t row = row0 + 16 * it + 4 * q + rho;
-    const int col = hi4 ? 16 + 4 * (g - 1) : 4 * g;
-    *reinterpret_cast<u32x4*>(dst + row * ld + col) = v;
+    int row, col;
+    const uint4 v = pack_strip_f16(acc[it][0], acc[it][1], exp2_int(-e), row, col);
+    *reinterpret_cast<uint4*>(dst + (int64_t)(row0 + 16 * it + row) * ld + col) = v;
     if (lane == 0) sc[(int64_t)(row0 / 16 + it) * sc_ld] = exp2_int(e);
   }
 }

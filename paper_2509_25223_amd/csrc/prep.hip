@@ -193,6 +193,7 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   __syncthreads();   // Kc/Qc dead: region 0 becomes As/Ar/Ts/Tr
 
   XT* mats = reinterpret_cast<XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
+  floatx4 mg[4], mp[4], mr[4];   // this wave's 16-row strips of MG, MP, MR
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
     const int s = 16 * ct + acc_col();
@@ -206,24 +207,60 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
       const bool lower = s < t;
       const float eg = (p.vflags & kVarDecayed) ? es : esp;
       const float ep = (p.vflags & kVarUngated) ? esp : es;
-      mats[kMatMG * kMatElems + t * kChunk + s] = from_f<XT>(lower ? eg * g : 0.f);
-      mats[kMatMP * kMatElems + t * kChunk + s] = from_f<XT>(lower ? ep * pq : 0.f);
-      mats[kMatMR * kMatElems + t * kChunk + s] = from_f<XT>(s <= t ? er * pq : 0.f);
+      mg[ct][r] = lower ? eg * g : 0.f;
+      mp[ct][r] = lower ? ep * pq : 0.f;
+      mr[ct][r] = s <= t ? er * pq : 0.f;
       if constexpr (RDN) {
         As[t * L::kLdA + s] = lower ? bt[t] * es * g : 0.f;
         Ar[t * L::kLdA + s] = lower ? gm[t] * er * g : 0.f;
       }
     }
   }
+  if constexpr (sizeof(XT) == 2) {   // fp16 rows leave in 16-byte stores (two strips of 32 columns)
+#pragma unroll
+    for (int m = 0; m < 3; ++m) {
+      const floatx4* x = m == 0 ? mg : m == 1 ? mp : mr;
+      XT* base = mats + (m == 0 ? kMatMG : m == 1 ? kMatMP : kMatMR) * kMatElems;
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        int row, col;
+        const uint4 v = pack_strip_f16(x[2 * half], x[2 * half + 1], 1.f, row, col);
+        *reinterpret_cast<uint4*>(base + (16 * w + row) * kChunk + 32 * half + col) = v;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = 16 * w + acc_row(r), s = 16 * ct + acc_col();
+        mats[kMatMG * kMatElems + t * kChunk + s] = mg[ct][r];
+        mats[kMatMP * kMatElems + t * kChunk + s] = mp[ct][r];
+        mats[kMatMR * kMatElems + t * kChunk + s] = mr[ct][r];
+      }
+  }
   if constexpr (RDN) {
     __syncthreads();
     invert_unit_lower_pair(As, Ar, Ts, Tr, W);
     __syncthreads();
-    for (int e = tid; e < kMatElems; e += kThreads) {
+    // 8 consecutive elements per thread and step (16-byte fp16 stores)
+    for (int e = 8 * tid; e < kMatElems; e += 8 * kThreads) {
       const int t = e / kChunk, s = e % kChunk;
       const bool upper = (s >> 4) > (t >> 4);   // blocks above the diagonal are zero
-      mats[kMatTS * kMatElems + e] = from_f<XT>(upper ? 0.f : Ts[t * L::kLdA + s]);
-      mats[kMatTR * kMatElems + e] = from_f<XT>(upper ? 0.f : Tr[t * L::kLdA + s]);
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const float* src = (m ? Tr : Ts) + t * L::kLdA + s;
+        XT vals[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) vals[k] = from_f<XT>(upper ? 0.f : src[k]);
+        XT* dst = mats + (m ? kMatTR : kMatTS) * kMatElems + e;
+        if constexpr (sizeof(XT) == 2) {
+          *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(vals);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) dst[k] = vals[k];
+        }
+      }
     }
   }
 }
