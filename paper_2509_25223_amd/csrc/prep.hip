@@ -132,22 +132,43 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   if (!chunk_info(p.st, c, ci)) return;
   const int H = p.H;
 
-  // ---- load K, Q rows (zero padding beyond the chunk) ----
+  // ---- every global load of the workgroup is issued before any is used:
+  //      the gates (waves 0, 1), then the K, Q rows (zero padding beyond the
+  //      chunk), so their latencies overlap ----
+  const bool pre = (p.vflags & kVarGatePreact) != 0;
+  float graw_a = 0.f, graw_b = 0.f;   // decay; beta (wave 0) or gamma (wave 1)
+  if (tid < 128) {
+    const int t = tid & 63;
+    if (t < ci.len) {
+      const int64_t gi = (ci.tok + t) * H + h;
+      graw_a = (tid < 64 ? p.alpha_s : p.alpha_r)[gi];
+      graw_b = (tid < 64 ? p.beta : p.gamma)[gi];
+    }
+  }
   {
     constexpr int kVec = 16 / sizeof(T);           // elements per 16-byte load
     constexpr int kPerRow = DK / kVec;
+    constexpr int kIter = kChunk * kPerRow / kThreads;
+    static_assert(kIter * kThreads == kChunk * kPerRow, "whole rows per step");
     const T* qg = reinterpret_cast<const T*>(p.q);
     const T* kg = reinterpret_cast<const T*>(p.k);
-    for (int e = tid; e < kChunk * kPerRow; e += kThreads) {
-      const int t = e / kPerRow, col = (e % kPerRow) * kVec;
-      uint4 kv = make_uint4(0, 0, 0, 0), qv = make_uint4(0, 0, 0, 0);
+    uint4 kv[kIter], qv[kIter];
+#pragma unroll
+    for (int u = 0; u < kIter; ++u) {
+      const int e = tid + u * kThreads, t = e / kPerRow, col = (e % kPerRow) * kVec;
+      kv[u] = make_uint4(0, 0, 0, 0);
+      qv[u] = make_uint4(0, 0, 0, 0);
       if (t < ci.len) {
         const int64_t off = ((ci.tok + t) * H + h) * (int64_t)DK + col;
-        kv = *reinterpret_cast<const uint4*>(kg + off);
-        qv = *reinterpret_cast<const uint4*>(qg + off);
+        kv[u] = *reinterpret_cast<const uint4*>(kg + off);
+        qv[u] = *reinterpret_cast<const uint4*>(qg + off);
       }
-      *reinterpret_cast<uint4*>(Kc + t * L::kLdK + col) = kv;
-      *reinterpret_cast<uint4*>(Qc + t * L::kLdK + col) = qv;
+    }
+#pragma unroll
+    for (int u = 0; u < kIter; ++u) {
+      const int e = tid + u * kThreads, t = e / kPerRow, col = (e % kPerRow) * kVec;
+      *reinterpret_cast<uint4*>(Kc + t * L::kLdK + col) = kv[u];
+      *reinterpret_cast<uint4*>(Qc + t * L::kLdK + col) = qv[u];
     }
   }
   // ---- gates: wave 0 scans log aS, wave 1 scans log aR ----
@@ -156,19 +177,17 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   if (tid < 128) {
     const int t = tid & 63;
     const bool valid = t < ci.len;
-    const bool pre = (p.vflags & kVarGatePreact) != 0;
-    const int64_t gi = (ci.tok + t) * H + h;
-    const float* a = tid < 64 ? p.alpha_s : p.alpha_r;
     float la = 0.f;
-    if (valid) la = pre ? -p.decay_param[h] * softplus_f(a[gi] + p.decay_param[H + h]) : log_decay(a[gi]);
+    if (valid) la = pre ? -p.decay_param[h] * softplus_f(graw_a + p.decay_param[H + h]) : log_decay(graw_a);
     const float cum = wave_inclusive_scan(la);
+    const float wb = valid ? (pre ? sigmoid_f(graw_b) : graw_b) : 0.f;
     if (tid < 64) {
       gs[t] = cum;
-      bt[t] = valid ? (pre ? sigmoid_f(p.beta[gi]) : p.beta[gi]) : 0.f;
+      bt[t] = wb;
       gsp[t] = cum - la;
     } else {
       gr[t] = cum;
-      gm[t] = valid ? (pre ? sigmoid_f(p.gamma[gi]) : p.gamma[gi]) : 0.f;
+      gm[t] = wb;
     }
   }
   __syncthreads();
