@@ -225,10 +225,36 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       x.sc = 1.f;
     }
   };
-  // the first state rows stream in while the chunk's blocks are staged
-  StateRows rowA, rowB;
-  load_rows(rowA, 0, 16 * w);
-  load_rows(rowB, 2, 16 * w);
+  // Every global load of the staging is issued at once: K, Q, dO rows and
+  // the gate block (converted / exponentiated before the barrier), the V and
+  // r rows (the elementwise sums) and the token blocks' LDS-DMA.  The
+  // compiler's waits for register loads issued alongside an LDS-DMA are full
+  // drains, so the first state rows are issued after the conversions and the
+  // drain: their latency then overlaps the barrier and the W / G / P products.
+  constexpr int kKV = kChunk * DK / kE / NT;
+  constexpr int kOV = kChunk * DV / kE / NT;
+  // Rows past the chunk's end (len >= 1) are read at the last row and zeroed
+  // where they are used: unconditional loads keep the waits for them at
+  // their uses.
+  auto in_row = [&](int t) { return t < len ? t : len - 1; };
+  uint4 kv[kKV], qv[kKV], ov[kOV];
+#pragma unroll
+  for (int u = 0; u < kKV; ++u) {
+    const int e = tid + u * NT, t = in_row(e / (DK / kE)), i = (e % (DK / kE)) * kE;
+    const int64_t off = ((tok + t) * H + h) * (int64_t)DK + i;
+    kv[u] = *reinterpret_cast<const uint4*>(kg + off);
+    qv[u] = *reinterpret_cast<const uint4*>(qg + off);
+  }
+#pragma unroll
+  for (int u = 0; u < kOV; ++u) {
+    const int e = tid + u * NT, t = in_row(e / (DV / kE)), j = (e % (DV / kE)) * kE;
+    ov[u] = *reinterpret_cast<const uint4*>(dog + ((tok + t) * H + h) * (int64_t)DV + j);
+  }
+  // the gate block (every wave reads it; wave 0 stores the derived arrays)
+  const float* gb = p.gate_ws + ((int64_t)c * H + h) * kGateBlock;
+  const float gs = gb[lane], gsl = gb[kChunk - 1], gspr = gb[lane > 0 ? lane - 1 : 0];
+  const float gr = gb[64 + lane], grl = gb[64 + kChunk - 1];
+  const float gbe = gb[128 + lane], ggme = gb[192 + lane];
   dma_tile64<TV, NW>(fb + blk_off(c, h, H, 0, DV), tokblk(bU));
   dma_tile64<TV, NW>(fb + blk_off(c, h, H, 1, DV), tokblk(bUR));
   dma_tile64<TV, NW>(bb + blk_off(c, h, H, 0, DV), tokblk(bDX));
@@ -241,28 +267,11 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
   for (int u = 0; u < kVV; ++u) {
     const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
-    vrow[u] = t < len ? *reinterpret_cast<const uint4*>(vg + ((tok + t) * H + h) * (int64_t)DV + j)
-                      : uint4{0, 0, 0, 0};
+    vrow[u] = *reinterpret_cast<const uint4*>(vg + ((tok + in_row(t)) * H + h) * (int64_t)DV + j);
     rrow[u] = *reinterpret_cast<const uint4*>(fb + blk_off(c, h, H, 2, DV) + t * DV + j);
   }
   // K, Q, dO rows: converted to the operand type, stored swizzled
   {
-    constexpr int kKV = kChunk * DK / kE / NT;
-    constexpr int kOV = kChunk * DV / kE / NT;
-    uint4 kv[kKV], qv[kKV], ov[kOV];
-#pragma unroll
-    for (int u = 0; u < kKV; ++u) {
-      const int e = tid + u * NT, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
-      const int64_t off = ((tok + t) * H + h) * (int64_t)DK + i;
-      kv[u] = t < len ? *reinterpret_cast<const uint4*>(kg + off) : uint4{0, 0, 0, 0};
-      qv[u] = t < len ? *reinterpret_cast<const uint4*>(qg + off) : uint4{0, 0, 0, 0};
-    }
-#pragma unroll
-    for (int u = 0; u < kOV; ++u) {
-      const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
-      ov[u] = t < len ? *reinterpret_cast<const uint4*>(dog + ((tok + t) * H + h) * (int64_t)DV + j)
-                      : uint4{0, 0, 0, 0};
-    }
     auto conv = [&](uint4 x) -> uint4 {
       if constexpr (BF) {
         const u16x8 a = __builtin_bit_cast(u16x8, x);
@@ -277,22 +286,20 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
     for (int u = 0; u < kKV; ++u) {
       const int e = tid + u * NT, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
-      *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(kv[u]);
-      *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(qv[u]);
+      *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(keep_if(kv[u], t < len));
+      *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(keep_if(qv[u], t < len));
     }
 #pragma unroll
     for (int u = 0; u < kOV; ++u) {
       const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
-      *reinterpret_cast<uint4*>(tokblk(bDO) + TV::off(t, j)) = conv(ov[u]);
+      *reinterpret_cast<uint4*>(tokblk(bDO) + TV::off(t, j)) = conv(keep_if(ov[u], t < len));
     }
   }
   if (tid < kChunk) {
-    const float* gb = p.gate_ws + ((int64_t)c * H + h) * kGateBlock;
     const int t = tid;
-    const float gs = gb[t], gsl = gb[kChunk - 1], gsp = t > 0 ? gb[t - 1] : 0.f;
-    const float gr = gb[64 + t], grl = gb[64 + kChunk - 1];
-    gbt[t] = gb[128 + t];
-    ggm[t] = gb[192 + t];
+    const float gsp = t > 0 ? gspr : 0.f;
+    gbt[t] = gbe;
+    ggm[t] = ggme;
     egs[t] = __expf(gs);
     egsp[t] = __expf(gsp);
     egr[t] = __expf(gr);
@@ -307,7 +314,11 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     }
   }
   for (int e = tid; e < NW * kNumSums * kChunk; e += NT) sums[e] = 0.f;
-  wait_vmem();
+  wait_vmem();   // this wave's DMAs have landed (published by the barrier)
+  asm volatile("" ::: "memory");
+  StateRows rowA, rowB;
+  load_rows(rowA, 0, 16 * w);
+  load_rows(rowB, 2, 16 * w);
   barrier_lds();
 
   // elementwise sums: dY . V (RLA: dU . V) for beta, dYR . r (RLA: dUR . r) for gamma
@@ -320,7 +331,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       const uint4 dyr = *reinterpret_cast<const uint4*>(tokblk(bDYR) + TV::off(t, j));
       const XT* a = reinterpret_cast<const XT*>(&dy);
       const XT* b = reinterpret_cast<const XT*>(&dyr);
-      const IN* x = reinterpret_cast<const IN*>(&vrow[u]);
+      const uint4 vr = keep_if(vrow[u], t < len);
+      const IN* x = reinterpret_cast<const IN*>(&vr);
       const XT* y = reinterpret_cast<const XT*>(&rrow[u]);
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll

@@ -202,6 +202,15 @@ __device__ __forceinline__ void load_rowfrags(typename Mfma<T>::frag* afr, const
 
 __device__ __forceinline__ floatx4 zero4() { return floatx4{0.f, 0.f, 0.f, 0.f}; }
 
+// x where ok, else zero, as four bitwise ANDs.  The mask is opaque to the
+// optimiser, which would otherwise turn the selection of a loaded value into
+// a branch and wait for every outstanding load at its join.
+__device__ __forceinline__ uint4 keep_if(uint4 x, bool ok) {
+  uint32_t m = ok ? 0xFFFFFFFFu : 0u;
+  asm volatile("" : "+v"(m));
+  return uint4{x.x & m, x.y & m, x.z & m, x.w & m};
+}
+
 
 // ---------------------------------------------------------------------------
 // Row-major LDS tiles without padding: rows of COLS elements of T whose
