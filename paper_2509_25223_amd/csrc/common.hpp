@@ -579,7 +579,6 @@ __device__ __forceinline__ uint4 pack_strip_f16(const floatx4& a0, const floatx4
 template <int IT>
 __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16* dst, int64_t ld,
                                                float* sc, int64_t sc_ld, int row0) {
-  const int lane = threadIdx.x & 63;
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     // tile maximum: in-lane, over the 16-lane row (DPP), over the 4 rows
@@ -600,7 +599,11 @@ __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16*
     int row, col;
     const uint4 v = pack_strip_f16(acc[it][0], acc[it][1], exp2_int(-e), row, col);
     *reinterpret_cast<uint4*>(dst + (int64_t)(row0 + 16 * it + row) * ld + col) = v;
-    if (lane == 0) sc[(int64_t)(row0 / 16 + it) * sc_ld] = exp2_int(e);
+    // every lane stores the (wave-uniform) scale to the same address: a
+    // store under a lane condition becomes a branch, after which the
+    // compiler can no longer count the wave's outstanding memory operations
+    // and drains them all at its next wait
+    sc[(int64_t)(row0 / 16 + it) * sc_ld] = exp2_int(e);
   }
 }
 
