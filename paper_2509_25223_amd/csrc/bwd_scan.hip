@@ -551,11 +551,16 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int b = 0; b < 3; ++b) {
         const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
-        XT vals[kVE];
+        uint4 x;
+        if constexpr (BF) {   // two transpose reads per 16-byte row piece
+          x = keep_if(tile_token_vec8<TT>(srcb, v * kVE), t < len);
+        } else {
+          XT vals[kVE];
 #pragma unroll
-        for (int k = 0; k < kVE; ++k) vals[k] = t < len ? TT::at(srcb, v * kVE + k, t) : from_f<XT>(0.f);
-        *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + v * kVE) =
-            *reinterpret_cast<const uint4*>(vals);
+          for (int k = 0; k < kVE; ++k) vals[k] = t < len ? TT::at(srcb, v * kVE + k, t) : from_f<XT>(0.f);
+          x = *reinterpret_cast<const uint4*>(vals);
+        }
+        *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + v * kVE) = x;
       }
     }
     write_copies();

@@ -267,6 +267,34 @@ template <typename T, int COLS> struct Tile {
 };
 template <typename T> using Swz = Tile<T, kChunk>;   // 64 x 64 matrices
 
+// LDS transpose read of 16-bit elements (gfx950 ds_read_b64_tr_b16).  In each
+// 16-lane group, the 8-byte pieces the lanes address form a 16 x 4 array D
+// (row j: the group's lane j); lane i of the group receives D[i / 4 + 4 e][i % 4]
+// for e = 0 .. 3.
+__device__ __forceinline__ u16x4 lds_read_tr16(const void* p) {
+  typedef short s16x4 __attribute__((ext_vector_type(4)));
+  const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(p));
+  return __builtin_bit_cast(u16x4, r);
+}
+
+// Token-major 16 bytes from a value-major tile of 16-bit elements (tile rows
+// = values, columns = 64 tokens): lane L receives rows j0 .. j0+7 of column L
+// (j0 a multiple of 4).  Two transpose reads: the group of lanes 16 g .. 16 g
+// + 15 addresses 4 rows x 16 columns from column 16 g, 4 columns per lane.
+template <class TL>
+__device__ __forceinline__ uint4 tile_token_vec8(const void* base, int j0) {
+  static_assert(sizeof(typename std::remove_pointer<decltype(TL::ptr(nullptr, 0, 0))>::type) == 2,
+                "16-bit tile");
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const int t = 16 * (lane >> 4) + 4 * (jj & 3), j = j0 + (jj >> 2);
+  const char* b = reinterpret_cast<const char*>(base);
+  const u16x4 a = lds_read_tr16(b + TL::off(j, t));
+  const u16x4 c = lds_read_tr16(b + TL::off(j + 4, t));
+  return uint4{a[0] | ((uint32_t)a[1] << 16), a[2] | ((uint32_t)a[3] << 16),
+               c[0] | ((uint32_t)c[1] << 16), c[2] | ((uint32_t)c[3] << 16)};
+}
+
 // Same interface over plain rows padded to COLS + PAD elements: cheaper
 // addressing for buffers written element by element (transposes).
 template <typename T, int COLS, int PAD> struct PadRows {
