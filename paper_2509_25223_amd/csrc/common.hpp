@@ -295,6 +295,39 @@ __device__ __forceinline__ uint4 tile_token_vec8(const void* base, int j0) {
                c[0] | ((uint32_t)c[1] << 16), c[2] | ((uint32_t)c[3] << 16)};
 }
 
+// A 64-row tile of 16-bit elements stored row-major (COLS per row, written
+// in 16-byte pieces) and read back as MFMA fragments of its transpose:
+// frag(base, r0, k0) holds rows r0 .. r0+15 of the transpose (tile columns)
+// at k = k0 .. k0+31 (tile rows), from two transpose reads.  The 16-byte
+// chunks of row r are XOR-swizzled by 2 (r & 7) (within the row's chunks):
+// the four rows that each 16-lane group of a transpose read touches, and
+// eight consecutive rows of one chunk column, fall in distinct banks.
+template <typename T, int COLS> struct TrTile {
+  static_assert(sizeof(T) == 2, "16-bit elements");
+  static constexpr int kRowB = COLS * 2;
+  static constexpr int kCpr = kRowB / 16;
+  static_assert(kCpr >= 8 && (kCpr & (kCpr - 1)) == 0, "power-of-two chunks per row");
+  __device__ __forceinline__ static int sw(int r) { return (2 * (r & 7)) & (kCpr - 1); }
+  __device__ __forceinline__ static int off(int r, int col) {
+    const int b = col * 2;
+    return r * kRowB + (((b >> 4) ^ sw(r)) << 4) + (b & 15);
+  }
+  __device__ __forceinline__ static T* ptr(void* base, int r, int col) {
+    return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off(r, col));
+  }
+  template <typename M>
+  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0) {
+    static_assert(M::kStep == 32, "8 k-values per lane");
+    const int lane = threadIdx.x & 63, jj = lane & 15;
+    const int row = k0 + 8 * (lane >> 4) + (jj >> 2), col = r0 + 4 * (jj & 3);
+    const char* b = reinterpret_cast<const char*>(base);
+    const u16x4 x = lds_read_tr16(b + off(row, col));
+    const u16x4 y = lds_read_tr16(b + off(row + 4, col));
+    const u16x8 v = {x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+    return __builtin_bit_cast(typename M::frag, v);
+  }
+};
+
 // Same interface over plain rows padded to COLS + PAD elements: cheaper
 // addressing for buffers written element by element (transposes).
 template <typename T, int COLS, int PAD> struct PadRows {

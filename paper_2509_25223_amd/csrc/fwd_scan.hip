@@ -39,7 +39,11 @@ template <typename IN, int DK, int BV, bool RDN>
 struct FwdLayout {
   static constexpr bool kBF = sizeof(IN) == 2;
   typedef typename std::conditional<kBF, f16, float>::type XT;
-  typedef Tile<XT, kChunk> TT;   // token tiles: K^T [DK][64], per-token blocks [BV][64]
+  typedef Tile<XT, kChunk> TT;   // token tiles: per-token blocks [BV][64]
+  // K for the state update's K^T operand: bf16 inputs keep K row-major [64][DK]
+  // (16-byte stores at the commit, transpose reads at the update); fp32
+  // inputs store K^T [DK][64]
+  typedef typename std::conditional<kBF, TrTile<XT, DK>, TT>::type TK;
   typedef Tile<IN, DK> TSC;      // state copies [BV][DK]
   // matrix slots (swizzled 64 x 64 tiles filled by LDS-DMA); with bf16 inputs
   // T^R and MR are double-buffered so the next chunk's copies land early
@@ -47,7 +51,7 @@ struct FwdLayout {
   static constexpr int kNumSlots = RDN ? (kDB ? 7 : 5) : (kDB ? 4 : 3);
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kKT = 0;
-  static constexpr int kCopies = kKT + DK * TT::kRowB;
+  static constexpr int kCopies = kKT + (kBF ? kChunk * TK::kRowB : DK * TT::kRowB);
   static constexpr int kCopyBytes = BV * TSC::kRowB;
   static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
   static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
@@ -110,6 +114,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   typedef typename L::XT XT;
   typedef Mfma<IN> MI;
   typedef typename L::TT TT;
+  typedef typename L::TK TK;
   constexpr bool BF = L::kBF;
   constexpr int JT = BV / 16;        // value tiles per block
   constexpr int IT = DK / 64;        // state row tiles per wave
@@ -268,11 +273,12 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
       for (int s2 = 0; s2 < KS_STEPS; ++s2) {
         Kf[s2] = Kn[s2];
         Qf[s2] = Qn[s2];
-        if constexpr (BF) {
+        if constexpr (BF) {   // row t, 8 columns: one 16-byte store
           const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s2]);
+          f16x8 kh;
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            *TT::ptr(KT, s2 * 32 + (lane >> 4) * 8 + e, t) = from_f<XT>(bf2f(kv[e]));
+          for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
+          *reinterpret_cast<f16x8*>(TK::ptr(KT, t, s2 * 32 + (lane >> 4) * 8)) = kh;
         } else {
           *TT::ptr(KT, s2 * 4 + (lane >> 4), t) = Kf[s2];
         }
@@ -455,6 +461,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     }
 
     // ---- state update: S <- e^{g_C} S + K^T DU, R <- e^{h_C} R + K^T DUR ----
+    // (the compiler drains the wave's outstanding memory operations before
+    // the first transpose read: the prefetch has landed by now)
     const float eS = edge[0], eR = edge[1];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
@@ -463,8 +471,8 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
       for (int jt = 0; jt < JT; ++jt) {
         Sacc[it][jt] *= eS;
         Racc[it][jt] *= eR;
-        mma_tiles<XT, kChunk, TT, TT>(Sacc[it][jt], KT, i0, DUt, jt * 16);
-        mma_tiles<XT, kChunk, TT, TT>(Racc[it][jt], KT, i0, DURt, jt * 16);
+        mma_tiles<XT, kChunk, TK, TT>(Sacc[it][jt], KT, i0, DUt, jt * 16);
+        mma_tiles<XT, kChunk, TK, TT>(Racc[it][jt], KT, i0, DURt, jt * 16);
       }
     }
     // the next chunk's DMA data must have landed before anyone reads it (the
