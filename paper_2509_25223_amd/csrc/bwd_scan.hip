@@ -40,7 +40,10 @@ struct BwdScanLayout {
   // LDS buffers as padded rows (measured faster here than the swizzled
   // tiles, whose element-wise addressing costs this kernel registers):
   typedef PadRows<XT, kChunk, kBF ? 8 : 4> TT;    // per-token blocks [BV][64]
-  typedef PadRows<XT, kChunk, kBF ? 8 : 4> TKQ;   // K^T, Q^T [DK][64]
+  // K, Q for the state-gradient update's K^T, Q^T operands: bf16 inputs keep
+  // them row-major [64][DK] (16-byte stores at the commit, transpose reads at
+  // the update); fp32 inputs store K^T, Q^T [DK][64]
+  typedef typename std::conditional<kBF, TrTile<XT, DK>, PadRows<XT, kChunk, 4>>::type TKQ;
   typedef PadRows<IN, DK, kBF ? 8 : 4> TSC;       // gradient-state copies [BV][DK]
   // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs MR
   // (first used) is double-buffered
@@ -49,8 +52,9 @@ struct BwdScanLayout {
   static constexpr int kNumCopies = kBF ? 4 : 2;
   static constexpr int kNumBufs = 6;
   static constexpr int kKT = 0;
-  static constexpr int kQT = kKT + DK * TKQ::kRowB;
-  static constexpr int kCopies = kQT + DK * TKQ::kRowB;
+  static constexpr int kKQBytes = kBF ? kChunk * TKQ::kRowB : DK * TKQ::kRowB;
+  static constexpr int kQT = kKT + kKQBytes;
+  static constexpr int kCopies = kQT + kKQBytes;
   static constexpr int kCopyBytes = BV * TSC::kRowB;
   static constexpr int kMats = kCopies + kNumCopies * kCopyBytes;
   static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
@@ -345,15 +349,18 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int s2 = 0; s2 < KS_STEPS; ++s2) {
         Kf[s2] = Kn[s2];
-        if constexpr (BF) {
+        if constexpr (BF) {   // row t, 8 columns: one 16-byte store each
           const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
           const u16x8 qv = __builtin_bit_cast(u16x8, Qn[s2]);
+          f16x8 kh, qh;
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            const int i = s2 * 32 + (lane >> 4) * 8 + e;
-            *TKQ::ptr(KT, i, t) = from_f<XT>(bf2f(kv[e]));
-            *TKQ::ptr(QT, i, t) = from_f<XT>(bf2f(qv[e]));
+            kh[e] = (f16)bf2f(kv[e]);
+            qh[e] = (f16)bf2f(qv[e]);
           }
+          const int i = s2 * 32 + (lane >> 4) * 8;
+          *reinterpret_cast<f16x8*>(TKQ::ptr(KT, t, i)) = kh;
+          *reinterpret_cast<f16x8*>(TKQ::ptr(QT, t, i)) = qh;
         } else {
           const int i = s2 * 4 + (lane >> 4);
           *TKQ::ptr(KT, i, t) = Kn[s2];
