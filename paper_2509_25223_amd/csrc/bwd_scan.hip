@@ -327,8 +327,9 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 
     // gradient w.r.t. this chunk's end states for the gradient kernel,
     // straight from the accumulators (bf16 inputs: fp16 scaled per (16 rows,
-    // 32 columns)).  Stored after the chunk's last prefetch, so that the wait
-    // for the prefetched data at the chunk's end leaves these stores in flight.
+    // 32 columns)), stored after the chunk's last prefetch (with bf16 inputs
+    // the update's transpose reads wait for them along with the prefetched
+    // data).
     auto save_ckpt = [&]() {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
       if constexpr (BF) {   // blocked [DV / 32][DK][32]: each wave store is 1 KiB contiguous
@@ -543,9 +544,10 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     if constexpr (!L::kDB) {
       if (c > 0) issue_all_single(c - 1);
     }
-    // the next chunk's DMA data must have landed before anyone reads it (with
-    // bf16 inputs the checkpoint stores are issued last and may still be in
-    // flight; single-buffered fp32 issues its DMAs after them)
+    // the next chunk's DMA data must have landed before anyone reads it (bf16
+    // inputs: the update's transpose reads have drained every operation of
+    // the wave; single-buffered fp32 issues its DMAs after the checkpoint
+    // stores)
     wait_vmem_but<L::kDB ? kCkptStores : 0>();
     barrier_lds();
     {   // this chunk's dX, dY, dYR (value-major in LDS) as token-major rows in

@@ -410,9 +410,10 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     barrier_lds();
     if (c + 1 < nch) issue_late(c + 1);
     // chunk-start states for the gradient kernel, straight from the
-    // accumulators (bf16 inputs: fp16 scaled per (16 rows, 32 columns)).  Stored
-    // after the chunk's last prefetch, so that the wait for the prefetched
-    // data at the chunk's end does not also wait for these stores.
+    // accumulators (bf16 inputs: fp16 scaled per (16 rows, 32 columns)),
+    // stored after the chunk's last prefetch.  With bf16 inputs the state
+    // update's transpose reads wait for them along with the prefetched data;
+    // fp32 inputs leave them in flight past the chunk's end.
     if constexpr (CKPT) {
       const int64_t off = ((int64_t)gc * H + h) * DK * DV + j0;
       if constexpr (BF) {   // blocked [DV / 32][DK][32]: each wave store is 1 KiB contiguous
@@ -475,8 +476,9 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         mma_tiles<XT, kChunk, TK, TT>(Racc[it][jt], KT, i0, DURt, jt * 16);
       }
     }
-    // the next chunk's DMA data must have landed before anyone reads it (the
-    // checkpoint stores, issued last, may still be in flight)
+    // the next chunk's DMA data must have landed before anyone reads it (with
+    // fp32 inputs the checkpoint stores, issued last, may still be in flight;
+    // with bf16 inputs the update's transpose reads have drained them)
     wait_vmem_but<CKPT ? kCkptStores : 0>();
     barrier_lds();
     if (c + 1 < nch) issue_tail(c + 1);   // single-buffered T^R / MR: waited at P3
