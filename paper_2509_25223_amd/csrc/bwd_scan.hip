@@ -129,37 +129,52 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   // (save_state_f16: one row store and one scale store per 16-row tile;
   // fp32: one per row)
   constexpr int kCkptStores = 2 * (BF ? 2 * IT : 4 * IT * JT);
-  extern __shared__ __align__(16) unsigned char smem[];
-  XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
-  XT* QT = reinterpret_cast<XT*>(smem + L::kQT);
-  IN* dShi = reinterpret_cast<IN*>(smem + L::kCopies);
-  IN* dRhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
-  IN* dSlo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);   // bf16 only
-  IN* dRlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);   // bf16 only
+  extern __shared__ __align__(16) unsigned char smem_[];
+  // LDS base, made opaque to the optimiser once per chunk (set_ptrs): the
+  // per-lane addresses of every tile are then formed inside the loop from a
+  // few per-lane offsets rather than each kept live across it
+  unsigned char* smem = smem_;
+  XT *KT, *QT, *Yst;
+  IN *dShi, *dRhi, *dSlo, *dRlo;
+  uint8_t* mask;
+  float *graw, *gbt, *ggm, *egs, *egsp, *egr, *dls, *dlr, *edge, *gout;
+  const float *ekp, *eqb;
+  const int vf = VAR ? p.vflags : 0;
+  auto set_ptrs = [&](bool opaque) {
+    __attribute__((address_space(3))) unsigned char* s3 = (__attribute__((address_space(3))) unsigned char*)smem_;
+    if (opaque) asm volatile("" : "+v"(s3));
+    smem = (unsigned char*)s3;
+    KT = reinterpret_cast<XT*>(smem + L::kKT);
+    QT = reinterpret_cast<XT*>(smem + L::kQT);
+    dShi = reinterpret_cast<IN*>(smem + L::kCopies);
+    dRhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
+    dSlo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);   // bf16 only
+    dRlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);   // bf16 only
+    mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
+    graw = reinterpret_cast<float*>(smem + L::kGraw);
+    gbt = reinterpret_cast<float*>(smem + L::kGates);
+    ggm = gbt + kChunk;
+    egs = ggm + kChunk;
+    egsp = egs + kChunk;
+    egr = egsp + kChunk;
+    dls = egr + kChunk;
+    dlr = dls + kChunk;
+    edge = dlr + kChunk;
+    // output weight of c: gamma (ungated: 1); the default instance reads gamma
+    gout = VAR ? edge + kChunk : ggm;
+    ekp = (vf & kVarDecayed) ? egs : egsp;   // S0 factor of the residual
+    eqb = (vf & kVarUngated) ? egsp : egs;   // S0 factor of the base read-out
+    Yst = reinterpret_cast<XT*>(smem + L::kYst);   // dYR of this chunk
+  };
+  set_ptrs(false);
   auto mat = [&](int m, int buf) {
     return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
   };
   auto blk = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBufs + b * L::kBufBytes); };
-  uint8_t* mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
-  float* graw = reinterpret_cast<float*>(smem + L::kGraw);
-  float* gbt = reinterpret_cast<float*>(smem + L::kGates);
-  float* ggm = gbt + kChunk;
-  float* egs = ggm + kChunk;
-  float* egsp = egs + kChunk;
-  float* egr = egsp + kChunk;
-  float* dls = egr + kChunk;
-  float* dlr = dls + kChunk;
-  float* edge = dlr + kChunk;
-  // output weight of c: gamma (ungated: 1); the default instance reads gamma
-  float* gout = VAR ? edge + kChunk : ggm;
-  const int vf = VAR ? p.vflags : 0;
-  const float* ekp = (vf & kVarDecayed) ? egs : egsp;   // S0 factor of the residual
-  const float* eqb = (vf & kVarUngated) ? egsp : egs;   // S0 factor of the base read-out
   const bool tanh_resid = (vf & kVarTanh) != 0;
   // log-cosh slope 1 - (r / c)^2 = s0 (1 - (r invc)^2): c = inf -> 1, c = 0 -> 0
   const float invc = p.clip > 0.f ? 1.f / p.clip : 0.f;
   const float s0 = p.clip == 0.f ? 0.f : 1.f;
-  XT* Yst = reinterpret_cast<XT*>(smem + L::kYst);   // dYR of this chunk
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int nvb = DV / BV;
@@ -307,6 +322,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   barrier_lds();
 
   for (int c = nch - 1; c >= 0; --c) {
+    set_ptrs(true);
     const int gc = si.chunk0 + c;
     const int buf = c & 1;
     const int len = chunk_len(c);
