@@ -327,17 +327,34 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     const int buf = c & 1;
     const int len = chunk_len(c);
     const int64_t tok = si.start + (int64_t)c * kChunk;
-    // dv = dX + diag(b) dV_tail, rows of this chunk only
-    auto store_dv = [&](int jt, const floatx4& dx, const floatx4& tail) {
+    // dv = dX + diag(b) dV_tail, rows of this chunk only: this lane's 4
+    // rows (one 16-byte read of b), all values formed before the stores
+    auto store_dv = [&](const floatx4 (&dx)[JT], const floatx4 (&tail)[JT]) {
+      const int t0 = 16 * w + acc_row(0);
+      const floatx4 b4 = *reinterpret_cast<const floatx4*>(gbt + t0);
+      float val[JT][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int t = 16 * w + acc_row(r);
-        if (t < len) {
-          const int64_t o = ((tok + t) * H + h) * (int64_t)DV + j0 + jt * 16 + acc_col();
-          const float val = __builtin_fmaf(gbt[t], tail[r], dx[r]);
-          if (p.out_bf16) reinterpret_cast<u16*>(p.dv)[o] = f2bf(val);
-          else reinterpret_cast<float*>(p.dv)[o] = val;
-        }
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) val[jt][r] = __builtin_fmaf(b4[r], tail[jt][r], dx[jt][r]);
+      const int64_t o0 = ((tok + t0) * H + h) * (int64_t)DV + j0 + acc_col();
+      const int64_t rs = (int64_t)H * DV;   // between consecutive tokens
+      if (p.out_bf16) {
+        u16* d = reinterpret_cast<u16*>(p.dv) + o0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (t0 + r < len) {
+#pragma unroll
+            for (int jt = 0; jt < JT; ++jt) d[r * rs + jt * 16] = f2bf(val[jt][r]);
+          }
+      } else {
+        float* d = reinterpret_cast<float*>(p.dv) + o0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (t0 + r < len) {
+#pragma unroll
+            for (int jt = 0; jt < JT; ++jt) d[r * rs + jt * 16] = val[jt][r];
+          }
       }
     };
 
@@ -510,8 +527,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     barrier_lds();
     if (c > 0) issue_late(c - 1);
     if constexpr (!RDN) {   // last prefetch issued: dv and checkpoint stores
-#pragma unroll
-      for (int jt = 0; jt < JT; ++jt) store_dv(jt, dX[jt], dU[jt]);
+      store_dv(dX, dU);
       save_ckpt();
     }
     if constexpr (RDN) {
@@ -532,8 +548,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       barrier_lds();
       if (c > 0) issue_after5(c - 1);
       // last prefetch issued: dv and checkpoint stores
-#pragma unroll
-      for (int jt = 0; jt < JT; ++jt) store_dv(jt, dX[jt], dY[jt]);
+      store_dv(dX, dY);
       save_ckpt();
       // dU is dead: its slot keeps dY for the block store (P6 does not read it)
 #pragma unroll
