@@ -118,6 +118,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   constexpr int NW = L::kNW, NT = L::kNT;
   typedef typename L::XT XT;
   typedef typename L::TK TK;
+  typedef PadRows<XT, kChunk, L::kLdP - kChunk> TDP;   // dP [64][kLdP]
   typedef typename L::TV TV;
   typedef Mfma<XT> M;
   typedef typename M::frag Frag;
@@ -582,7 +583,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
         dPm[t * ldp + s] = from_f<XT>(edp[x][r]);
-        dPTm[s * ldp + t] = from_f<XT>(edp[x][r]);
+        if constexpr (!BF) dPTm[s * ldp + t] = from_f<XT>(edp[x][r]);
         if (s < t) {   // dG + dG^T: the two halves have disjoint supports
           dGm[t * ldp + s] = from_f<XT>(edg[x][r]);
           dGm[s * ldp + t] = from_f<XT>(edg[x][r]);
@@ -600,10 +601,12 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     for (int r = 0; r < 4; ++r) {
       const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
       dPm[t * ldp + s] = from_f<XT>(0.f);
-      dPTm[s * ldp + t] = from_f<XT>(0.f);
+      if constexpr (!BF) dPTm[s * ldp + t] = from_f<XT>(0.f);
     }
   }
-  // K^T, Q^T for the final products
+  // K^T, Q^T for the final products (fp32; 16-bit operands read K, Q and
+  // dP transposed with transpose reads)
+  if constexpr (!BF)
   for (int e = tid; e < kChunk * DK / kE; e += NT) {
     const int s = e / (DK / kE), i = (e % (DK / kE)) * kE;
     const uint4 kv = *reinterpret_cast<const uint4*>(Kl + TK::off(s, i));
@@ -677,12 +680,21 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
     for (int ks = 0; ks < KSC; ++ks) {
       const int k0 = ks * M::kStep;
-      const Frag fk = M::template load<true>(KTm + i0 * ldp, ldp, k0);
-      const Frag fq = M::template load<true>(QTm + i0 * ldp, ldp, k0);
+      Frag fk, fq;
+      if constexpr (BF) {
+        fk = frag_tr<TK, M>(Kl, i0, k0);
+        fq = frag_tr<TK, M>(Ql, i0, k0);
+      } else {
+        fk = M::template load<true>(KTm + i0 * ldp, ldp, k0);
+        fq = M::template load<true>(QTm + i0 * ldp, ldp, k0);
+      }
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) {
+        Frag fpt;
+        if constexpr (BF) fpt = frag_tr<TDP, M>(dPm, 16 * tt, k0);   // dP^T rows from dP
+        else fpt = M::template load<true>(dPTm + 16 * tt * ldp, ldp, k0);
         dQ[m][tt] = M::mma(M::template load<true>(dPm + 16 * tt * ldp, ldp, k0), fk, dQ[m][tt]);
-        dK[m][tt] = M::mma(M::template load<true>(dPTm + 16 * tt * ldp, ldp, k0), fq, dK[m][tt]);
+        dK[m][tt] = M::mma(fpt, fq, dK[m][tt]);
         dK[m][tt] = M::mma(M::template load<true>(dGm + 16 * tt * ldp, ldp, k0), fk, dK[m][tt]);
       }
     }

@@ -316,17 +316,31 @@ template <typename T, int COLS> struct TrTile {
     return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off(r, col));
   }
   template <typename M>
-  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0) {
-    static_assert(M::kStep == 32, "8 k-values per lane");
-    const int lane = threadIdx.x & 63, jj = lane & 15;
-    const int row = k0 + 8 * (lane >> 4) + (jj >> 2), col = r0 + 4 * (jj & 3);
-    const char* b = reinterpret_cast<const char*>(base);
-    const u16x4 x = lds_read_tr16(b + off(row, col));
-    const u16x4 y = lds_read_tr16(b + off(row + 4, col));
-    const u16x8 v = {x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
-    return __builtin_bit_cast(typename M::frag, v);
-  }
+  __device__ __forceinline__ static typename M::frag frag(const void* base, int r0, int k0);
 };
+
+// MFMA fragment (16-bit, k-step 32) of the transpose of a row-major tile TL:
+// rows r0 .. r0+15 of the transpose (tile columns) at k = k0 .. k0+31 (tile
+// rows), from two transpose reads.  Lane j of each 16-lane group g addresses
+// tile row k0 + 8 g + j / 4 (and 4 rows further for the second read) at
+// columns r0 + 4 (j % 4) .. +3, which TL must keep in one aligned 8 bytes.
+template <class TL, typename M>
+__device__ __forceinline__ typename M::frag frag_tr(const void* base, int r0, int k0) {
+  static_assert(M::kStep == 32, "8 k-values per lane");
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const int row = k0 + 8 * (lane >> 4) + (jj >> 2), col = r0 + 4 * (jj & 3);
+  const char* b = reinterpret_cast<const char*>(base);
+  const u16x4 x = lds_read_tr16(b + TL::off(row, col));
+  const u16x4 y = lds_read_tr16(b + TL::off(row + 4, col));
+  const u16x8 v = {x[0], x[1], x[2], x[3], y[0], y[1], y[2], y[3]};
+  return __builtin_bit_cast(typename M::frag, v);
+}
+
+template <typename T, int COLS>
+template <typename M>
+__device__ __forceinline__ typename M::frag TrTile<T, COLS>::frag(const void* base, int r0, int k0) {
+  return frag_tr<TrTile<T, COLS>, M>(base, r0, k0);
+}
 
 // Same interface over plain rows padded to COLS + PAD elements: cheaper
 // addressing for buffers written element by element (transposes).
