@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("c1d6ba926a99f799", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1248319538, 323097952),
-    "bwd_scan": ("781ba65aac8e4d79", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407416491, 615846336),
-    "fwd_scan": ("bb002e34f51ba4d9", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373598123, 638584243),
-    "prep": ("07f0b0dc559f5fe8", ('prep.hip', 'common.hpp', 'kernels.hpp'), 165154987, 173150746),
-    "decode": ("e6c80c09961cc3cf", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542727091, 539545242),
+    "bwd_grad": ("6ae31052b44eaa55", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249547959, 321050613),
+    "bwd_scan": ("67a7ef433579ac0e", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407202438, 613495552),
+    "fwd_scan": ("5962a73091bae1a9", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373575611, 638583852),
+    "prep": ("e1142bf3755e3559", ('prep.hip', 'common.hpp', 'kernels.hpp'), 148910316, 171967872),
+    "decode": ("af432540746c491b", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542735767, 539510886),
 }
 
 
