@@ -177,6 +177,12 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   const float s0 = p.clip == 0.f ? 0.f : 1.f;
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  // transposed matrix fragments, loaded ahead of the barrier before their
+  // products (16-bit: transpose reads)
+  auto cols_frags = [&](const XT* m) {
+    if constexpr (BF) return swz_cols_frags_sync<XT>(m, 16 * w);
+    else return swz_cols_frags<XT>(m, 16 * w);
+  };
   const int nvb = DV / BV;
   const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   const int pair = (slot / nvb) * 8 + xcd, vb = slot % nvb;
@@ -452,7 +458,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     }
     // the transposed matrices' fragments are loaded ahead of the barriers
     // that precede their products (every matrix landed in an earlier chunk)
-    const MatFrags<XT> aMR = swz_cols_frags<XT>(mat(kMatMR, buf), 16 * w);
+    const MatFrags<XT> aMR = cols_frags(mat(kMatMR, buf));
     barrier_lds();
     if (c > 0) {
       issue_regs(c - 1);
@@ -470,7 +476,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       if constexpr (RDN) store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * w, dUR[jt]);
     }
     MatFrags<XT> aTR;
-    if constexpr (RDN) aTR = swz_cols_frags<XT>(mat(kMatTR, 0), 16 * w);
+    if constexpr (RDN) aTR = cols_frags(mat(kMatTR, 0));
     barrier_lds();
 
     // ---- P3: dYR, dX, dKR (RLA: dKS) ----
@@ -505,8 +511,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       store_acc_tile<TT>(blk(bDKR), jt * 16, 16 * w, RDN ? dkr : dks);
       store_acc_tile<TT>(Yst, jt * 16, 16 * w, dYR);
     }
-    const MatFrags<XT> aMP = swz_cols_frags<XT>(mat(kMatMP, 0), 16 * w);
-    const MatFrags<XT> aMG = swz_cols_frags<XT>(mat(kMatMG, 0), 16 * w);
+    const MatFrags<XT> aMP = cols_frags(mat(kMatMP, 0));
+    const MatFrags<XT> aMG = cols_frags(mat(kMatMG, 0));
     barrier_lds();
     if (c > 0) issue_mid(c - 1);
 
@@ -523,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * w, dU[jt]);
     }
     MatFrags<XT> aTS;
-    if constexpr (RDN) aTS = swz_cols_frags<XT>(mat(kMatTS, 0), 16 * w);
+    if constexpr (RDN) aTS = cols_frags(mat(kMatTS, 0));
     barrier_lds();
     if (c > 0) issue_late(c - 1);
     if constexpr (!RDN) {   // last prefetch issued: dv and checkpoint stores

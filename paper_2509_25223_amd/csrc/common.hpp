@@ -504,6 +504,39 @@ __device__ __forceinline__ MatFrags<T> swz_cols_frags(const T* M, int t0) {
   for (int s = 0; s < kChunk / Mfma<T>::kStep; ++s) a.f[s] = swz_load_cols<T>(M, t0, s * Mfma<T>::kStep);
   return a;
 }
+// The 16-bit transpose fragments of swz_cols_frags from transpose reads
+// (two per fragment instead of eight 16-bit gathers), issued as inline
+// assembly so that the compiler does not drain the wave's in-flight LDS-DMA
+// before them.  The compiler does not see these reads either, so the
+// function waits for them itself (lgkmcnt(0), tied to their registers so
+// that nothing reads them earlier); meant for fragments loaded just before a
+// barrier, which waits the same way.
+template <typename T>
+__device__ __forceinline__ MatFrags<T> swz_cols_frags_sync(const T* M, int t0) {
+  static_assert(sizeof(T) == 2 && Mfma<T>::kStep == 32 && kChunk == 64, "two 16-bit k-steps");
+  typedef Swz<T> TL;
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const int col = t0 + 4 * (jj & 3);
+  const char* b = reinterpret_cast<const char*>(M);
+  u16x4 x[2], y[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int row = 32 * s + 8 * (lane >> 4) + (jj >> 2);
+    const uint32_t a0 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(row, col));
+    const uint32_t a1 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(row + 4, col));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(x[s]) : "v"(a0));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(y[s]) : "v"(a1));
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(y[0]), "+v"(x[1]), "+v"(y[1]));
+  MatFrags<T> a;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const u16x8 v = {x[s][0], x[s][1], x[s][2], x[s][3], y[s][0], y[s][1], y[s][2], y[s][3]};
+    a.f[s] = __builtin_bit_cast(typename Mfma<T>::frag, v);
+  }
+  return a;
+}
 // acc += A * B with A from MatFrags and B^T rows b0.. of a 64-token tile
 template <typename T, class TB = Swz<T>>
 __device__ __forceinline__ void mma_frags(floatx4& acc, const MatFrags<T>& a, const void* B, int b0) {
