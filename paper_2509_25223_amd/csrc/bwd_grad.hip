@@ -479,10 +479,21 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     const int icol = i0 + (lane & 15);   // this lane's output column
     // K, Q at this lane's output positions of token tile tt
     auto kq_of = [&](int tt, float (&kq)[4], float (&qq)[4]) {
+      if constexpr (BF) {   // one transpose read each
+        // (whole-vector casts: a bit cast of one vector element miscompiles)
+        const f16x4 k4 = __builtin_bit_cast(f16x4, acc_tile_tr<TK>(Kl, 16 * tt, i0));
+        const f16x4 q4 = __builtin_bit_cast(f16x4, acc_tile_tr<TK>(Ql, 16 * tt, i0));
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        kq[r] = to_f<XT>(TK::at(Kl, 16 * tt + acc_row(r), icol));
-        qq[r] = to_f<XT>(TK::at(Ql, 16 * tt + acc_row(r), icol));
+        for (int r = 0; r < 4; ++r) {
+          kq[r] = (float)k4[r];
+          qq[r] = (float)q4[r];
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          kq[r] = to_f<XT>(TK::at(Kl, 16 * tt + acc_row(r), icol));
+          qq[r] = to_f<XT>(TK::at(Ql, 16 * tt + acc_row(r), icol));
+        }
       }
     };
     // ---- S0 (rowA) and dS1 (rowB) ----

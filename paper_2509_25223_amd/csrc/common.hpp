@@ -336,6 +336,17 @@ __device__ __forceinline__ typename M::frag frag_tr(const void* base, int r0, in
   return __builtin_bit_cast(typename M::frag, v);
 }
 
+// Rows r0 .. r0+15, columns c0 .. c0+15 of a row-major 16-bit tile TL in the
+// MFMA accumulator layout (lane: rows r0 + 4 (lane / 16) + 0..3, column
+// c0 + lane % 16), from one transpose read: lane j of group g addresses row
+// r0 + 4 g + j / 4 at columns c0 + 4 (j % 4) .. +3.
+template <class TL>
+__device__ __forceinline__ u16x4 acc_tile_tr(const void* base, int r0, int c0) {
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const int row = r0 + 4 * (lane >> 4) + (jj >> 2), col = c0 + 4 * (jj & 3);
+  return lds_read_tr16(reinterpret_cast<const char*>(base) + TL::off(row, col));
+}
+
 template <typename T, int COLS>
 template <typename M>
 __device__ __forceinline__ typename M::frag TrTile<T, COLS>::frag(const void* base, int r0, int k0) {
