@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("6ae31052b44eaa55", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249547959, 321050613),
-    "bwd_scan": ("67a7ef433579ac0e", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407202438, 613495552),
-    "fwd_scan": ("5962a73091bae1a9", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373575611, 638583852),
-    "prep": ("e1142bf3755e3559", ('prep.hip', 'common.hpp', 'kernels.hpp'), 148910316, 171967872),
-    "decode": ("af432540746c491b", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542735767, 539510886),
+    "bwd_grad": ("cc3e20a4a63d3541", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249552772, 321989546),
+    "bwd_scan": ("6db2094cbd753252", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407166075, 613416960),
+    "fwd_scan": ("62f7c2ce231f8029", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373574027, 638583020),
+    "prep": ("dc772e802826f175", ('prep.hip', 'common.hpp', 'kernels.hpp'), 148817029, 171967786),
+    "decode": ("be3c9a2e4d2ba3a4", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746884, 539537894),
 }
 
 
