@@ -213,6 +213,25 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
 
   XT* mats = reinterpret_cast<XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
   floatx4 mg[4], mp[4], mr[4];   // this wave's 16-row strips of MG, MP, MR
+  // the gate values of this lane's rows and columns, read once up front (a
+  // read needed only under a condition would become a branch with its own
+  // wait); masked entries are multiplied by 0
+  float gs_t[4], gsp_t[4], gr_t[4], bt_t[4], gm_t[4], gs_s[4], gr_s[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int t = 16 * w + acc_row(r);
+    gs_t[r] = gs[t];
+    gsp_t[r] = gsp[t];
+    gr_t[r] = gr[t];
+    bt_t[r] = bt[t];
+    gm_t[r] = gm[t];
+  }
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct) {
+    const int s = 16 * ct + acc_col();
+    gs_s[ct] = gs[s];
+    gr_s[ct] = gr[s];
+  }
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
     const int s = 16 * ct + acc_col();
@@ -220,18 +239,19 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
     for (int r = 0; r < 4; ++r) {
       const int t = 16 * w + acc_row(r);
       const float g = G[ct][r], pq = P[ct][r];
-      const float es = __expf(fminf(gs[t] - gs[s], 0.f));
-      const float esp = __expf(fminf(gsp[t] - gs[s], 0.f));
-      const float er = __expf(fminf(gr[t] - gr[s], 0.f));
+      const float es = __expf(fminf(gs_t[r] - gs_s[ct], 0.f));
+      const float esp = __expf(fminf(gsp_t[r] - gs_s[ct], 0.f));
+      const float er = __expf(fminf(gr_t[r] - gr_s[ct], 0.f));
       const bool lower = s < t;
+      const float lm = lower ? 1.f : 0.f;
       const float eg = (p.vflags & kVarDecayed) ? es : esp;
       const float ep = (p.vflags & kVarUngated) ? esp : es;
       mg[ct][r] = lower ? eg * g : 0.f;
       mp[ct][r] = lower ? ep * pq : 0.f;
       mr[ct][r] = s <= t ? er * pq : 0.f;
       if constexpr (RDN) {
-        As[t * L::kLdA + s] = lower ? bt[t] * es * g : 0.f;
-        Ar[t * L::kLdA + s] = lower ? gm[t] * er * g : 0.f;
+        As[t * L::kLdA + s] = lm * (bt_t[r] * es * g);
+        Ar[t * L::kLdA + s] = lm * (gm_t[r] * er * g);
       }
     }
   }
