@@ -288,10 +288,18 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
       const bool upper = (s >> 4) > (t >> 4);   // blocks above the diagonal are zero
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
+        // two 16-byte reads (blocks above the diagonal hold no values: their
+        // bits are cleared with a mask, not read under a condition)
         const float* src = (m ? Tr : Ts) + t * L::kLdA + s;
+        const uint4 b0 = keep_if(*reinterpret_cast<const uint4*>(src), !upper);
+        const uint4 b1 = keep_if(*reinterpret_cast<const uint4*>(src + 4), !upper);
+        const floatx4 f0 = __builtin_bit_cast(floatx4, b0), f1 = __builtin_bit_cast(floatx4, b1);
         XT vals[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) vals[k] = from_f<XT>(upper ? 0.f : src[k]);
+        for (int k = 0; k < 4; ++k) {
+          vals[k] = from_f<XT>(f0[k]);
+          vals[4 + k] = from_f<XT>(f1[k]);
+        }
         XT* dst = mats + (m ? kMatTR : kMatTS) * kMatElems + e;
         if constexpr (sizeof(XT) == 2) {
           *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(vals);
