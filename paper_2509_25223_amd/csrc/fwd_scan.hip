@@ -324,10 +324,15 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
       floatx4 y;
+      if constexpr (BF) {   // V at this lane's accumulator positions: one transpose read
+        const u16x4 v4 = acc_tile_tr<PadRows<IN, BV, 0>>(Vc, 16 * w, jt * 16);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) vloc[jt][r] = bf2f(v4[r]);
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r);
-        vloc[jt][r] = to_f<IN>(Vc[t * BV + jt * 16 + acc_col()]);
+        if constexpr (!BF) vloc[jt][r] = to_f<IN>(Vc[t * BV + jt * 16 + acc_col()]);
         y[r] = RDN ? gbt[t] * __builtin_fmaf(-egs[t], KS[jt][r], vloc[jt][r]) : gbt[t] * vloc[jt][r];
       }
       if constexpr (RDN) {
