@@ -44,12 +44,14 @@ struct BwdScanLayout {
   // them row-major [64][DK] (16-byte stores at the commit, transpose reads at
   // the update); fp32 inputs store K^T, Q^T [DK][64]
   typedef typename std::conditional<kBF, TrTile<XT, DK>, PadRows<XT, kChunk, 4>>::type TKQ;
-  typedef PadRows<IN, DK, kBF ? 8 : 4> TSC;       // gradient-state copies [BV][DK]
+  // gradient-state copies [BV][DK] in the operand type: bf16 inputs keep one
+  // fp16 copy of each state scaled by a power of two per chunk
+  typedef PadRows<XT, DK, kBF ? 8 : 4> TSC;
   // matrix slots (swizzled tiles filled by LDS-DMA); with bf16 inputs MR
   // (first used) is double-buffered
   static constexpr bool kDB = kBF;
   static constexpr int kNumSlots = RDN ? (kDB ? 6 : 5) : (kDB ? 4 : 3);
-  static constexpr int kNumCopies = kBF ? 4 : 2;
+  static constexpr int kNumCopies = 2;
   static constexpr int kNumBufs = 6;
   static constexpr int kKT = 0;
   static constexpr int kKQBytes = kBF ? kChunk * TKQ::kRowB : DK * TKQ::kRowB;
@@ -66,7 +68,8 @@ struct BwdScanLayout {
   static constexpr int kGraw = kMask + kMaskBytes;
   static constexpr int kGates = kGraw + kGateBlock * 4;
   static constexpr int kYst = kGates + 10 * kChunk * 4;   // dYR staging (token tile)
-  static constexpr int kBytes = kYst + kBufBytes;
+  static constexpr int kRed = kYst + kBufBytes;   // per-wave state maxima [2][4]
+  static constexpr int kBytes = kRed + 8 * 4;
   static_assert(kMaskBytes % 1024 == 0, "mask block moved in whole DMA instructions");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
   // RDN: TS MG MP TR MR[2]; RLA: MG MP MR[2]
@@ -91,23 +94,19 @@ struct BwdScanLayout {
 enum { bDB_DKS = 0, bDC_DX = 1, bQDB = 2, bQDC = 3, bDUR_DU = 4, bDKR = 5 };
 
 // Writes this lane's 4 accumulator rows of a gradient-state tile into the
-// transposed copies (tile rows r0 + column, columns c0 + row): hi (and, for
-// bf16, the residual lo).
-template <class TL, typename IN>
-__device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0, floatx4 v) {
+// transposed copy (tile rows r0 + column, columns c0 + row) in the operand
+// type: 4 consecutive elements, one 8-byte (fp16) or 16-byte (fp32) store.
+template <class TL, typename T>
+__device__ __forceinline__ void store_state_copy(T* dst, int r0, int c0, floatx4 v) {
   // r0, c0 multiples of 16
-  const int o = TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(IN), c0 * (int)sizeof(IN));
-  if constexpr (sizeof(IN) == 2) {   // 8-byte stores of 4 consecutive rows
-    u16x4 h4, l4;
+  const int o = TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(T), c0 * (int)sizeof(T));
+  if constexpr (sizeof(T) == 2) {
+    f16x4 x;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      h4[k] = f2bf(v[k]);
-      l4[k] = bf16_lo(v[k], h4[k]);
-    }
-    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(hi) + o) = h4;
-    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(lo) + o) = l4;
+    for (int k = 0; k < 4; ++k) x[k] = (f16)v[k];
+    *reinterpret_cast<f16x4*>(reinterpret_cast<char*>(dst) + o) = x;
   } else {
-    *reinterpret_cast<floatx4*>(reinterpret_cast<char*>(hi) + o) = v;
+    *reinterpret_cast<floatx4*>(reinterpret_cast<char*>(dst) + o) = v;
   }
 }
 
@@ -135,7 +134,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   // few per-lane offsets rather than each kept live across it
   unsigned char* smem = smem_;
   XT *KT, *QT, *Yst;
-  IN *dShi, *dRhi, *dSlo, *dRlo;
+  XT *dSc, *dRc;
+  uint32_t* smax;
   uint8_t* mask;
   float *graw, *gbt, *ggm, *egs, *egsp, *egr, *dls, *dlr, *edge, *gout;
   const float *ekp, *eqb;
@@ -146,10 +146,9 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     smem = (unsigned char*)s3;
     KT = reinterpret_cast<XT*>(smem + L::kKT);
     QT = reinterpret_cast<XT*>(smem + L::kQT);
-    dShi = reinterpret_cast<IN*>(smem + L::kCopies);
-    dRhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
-    dSlo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);   // bf16 only
-    dRlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);   // bf16 only
+    dSc = reinterpret_cast<XT*>(smem + L::kCopies);
+    dRc = reinterpret_cast<XT*>(smem + L::kCopies + L::kCopyBytes);
+    smax = reinterpret_cast<uint32_t*>(smem + L::kRed);
     mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
     graw = reinterpret_cast<float*>(smem + L::kGraw);
     gbt = reinterpret_cast<float*>(smem + L::kGates);
@@ -204,15 +203,50 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         dS[it][jt][r] = p.dS_fin ? p.dS_fin[state_off + (int64_t)i * DV + j] : 0.f;
         dR[it][jt][r] = p.dR_fin ? p.dR_fin[state_off + (int64_t)i * DV + j] : 0.f;
       }
-  auto write_copies = [&]() {
+  // Copies of the gradient states for the next chunk's K dS, K dR products.
+  // bf16 inputs: fp16, scaled by 2^-e with e from the largest magnitude of
+  // each whole state (the waves' maxima meet in LDS across a barrier); the
+  // products are multiplied back by 2^e (exact).  fp32 inputs: plain copies.
+  float scS = 1.f, scR = 1.f;
+  auto publish_state_max = [&]() {
+    if constexpr (BF) {
+      uint32_t ms = 0, mr = 0;
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            ms = max(ms, __float_as_uint(dS[it][jt][r]) & 0x7FFFFFFFu);
+            mr = max(mr, __float_as_uint(dR[it][jt][r]) & 0x7FFFFFFFu);
+          }
+      ms = wave_absmax_bits(ms);
+      mr = wave_absmax_bits(mr);
+      smax[w] = ms;   // every lane stores the wave-uniform value
+      smax[4 + w] = mr;
+    }
+  };
+  auto write_copies = [&]() {   // after a barrier that follows publish_state_max
+    float iS = 1.f, iR = 1.f;
+    if constexpr (BF) {
+      const uint32_t ms = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
+      const uint32_t mr = max(max(smax[4], smax[5]), max(smax[6], smax[7]));
+      const int es = pow2_scale_exp(ms), er = pow2_scale_exp(mr);
+      scS = exp2_int(es);
+      scR = exp2_int(er);
+      iS = exp2_int(-es);
+      iR = exp2_int(-er);
+    }
 #pragma unroll
     for (int it = 0; it < IT; ++it)
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
-        store_state_copy<TSC>(dShi, dSlo, jt * 16, w * (DK / 4) + it * 16, dS[it][jt]);
-        store_state_copy<TSC>(dRhi, dRlo, jt * 16, w * (DK / 4) + it * 16, dR[it][jt]);
+        store_state_copy<TSC>(dSc, jt * 16, w * (DK / 4) + it * 16, dS[it][jt] * iS);
+        store_state_copy<TSC>(dRc, jt * 16, w * (DK / 4) + it * 16, dR[it][jt] * iR);
       }
   };
+  publish_state_max();
+  barrier_lds();
   write_copies();
 
   const IN* qg = reinterpret_cast<const IN*>(p.q);
@@ -383,12 +417,12 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     };
 
     // ---- commit: K fragments, K^T and Q^T (XT), dO^T, gate vectors ----
-    typename MI::frag Kf[KS_STEPS];
+    typename Mfma<XT>::frag Kf[KS_STEPS];   // fp16 with bf16 inputs
     {
       const int t = 16 * w + (lane & 15);
 #pragma unroll
       for (int s2 = 0; s2 < KS_STEPS; ++s2) {
-        Kf[s2] = Kn[s2];
+        if constexpr (!BF) Kf[s2] = Kn[s2];
         if constexpr (BF) {   // row t, 8 columns: one 16-byte store each
           const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
           const u16x8 qv = __builtin_bit_cast(u16x8, Qn[s2]);
@@ -399,6 +433,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
             qh[e] = (f16)bf2f(qv[e]);
           }
           const int i = s2 * 32 + (lane >> 4) * 8;
+          Kf[s2] = kh;
           *reinterpret_cast<f16x8*>(TKQ::ptr(KT, t, i)) = kh;
           *reinterpret_cast<f16x8*>(TKQ::ptr(QT, t, i)) = qh;
         } else {
@@ -437,11 +472,11 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     for (int jt = 0; jt < JT; ++jt) {
       KdS[jt] = zero4();
       KdR[jt] = zero4();
-      mma_rega_tile<IN, DK, TSC>(KdS[jt], Kf, dShi, jt * 16);
-      mma_rega_tile<IN, DK, TSC>(KdR[jt], Kf, dRhi, jt * 16);
-      if constexpr (BF) {
-        mma_rega_tile<IN, DK, TSC>(KdS[jt], Kf, dSlo, jt * 16);
-        mma_rega_tile<IN, DK, TSC>(KdR[jt], Kf, dRlo, jt * 16);
+      mma_rega_tile<XT, DK, TSC>(KdS[jt], Kf, dSc, jt * 16);
+      mma_rega_tile<XT, DK, TSC>(KdR[jt], Kf, dRc, jt * 16);
+      if constexpr (BF) {   // undo the copies' scales (powers of two: exact)
+        KdS[jt] *= scS;
+        KdR[jt] *= scR;
       }
       floatx4 dc, qdb, qdc;
       const floatx4 o4 = load_acc_tile<TT>(blk(bDB_DKS), jt * 16, 16 * w);
@@ -577,6 +612,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
         if constexpr (RDN) mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], KT, i0, blk(bDKR), jt * 16);
       }
     }
+    publish_state_max();
     barrier_lds();
     if constexpr (!L::kDB) {
       if (c > 0) issue_all_single(c - 1);

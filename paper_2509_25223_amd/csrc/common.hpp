@@ -634,6 +634,17 @@ __device__ __forceinline__ uint32_t row16_absmax_bits(float a, float b) {
   return max(m, dpp_u32<0x140>(m));
 }
 
+// Largest |x| over a wave, as an fp32 bit pattern (wave-uniform): the lane's
+// own magnitudes m (bits), then over each 16-lane row and the four rows.
+__device__ __forceinline__ uint32_t wave_absmax_bits(uint32_t m) {
+  m = max(m, dpp_u32<0xB1>(m));
+  m = max(m, dpp_u32<0x4E>(m));
+  m = max(m, dpp_u32<0x141>(m));
+  m = max(m, dpp_u32<0x140>(m));
+  return max(max((uint32_t)__builtin_amdgcn_readlane((int)m, 0), (uint32_t)__builtin_amdgcn_readlane((int)m, 16)),
+             max((uint32_t)__builtin_amdgcn_readlane((int)m, 32), (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
+}
+
 // Log-cosh residual r = c tanh(x / c) (c < 0: no bound, r = x; c = 0: r = 0).
 __device__ __forceinline__ float resid_tanh(float x, float c) {
   if (c < 0.f) return x;
