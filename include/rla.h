@@ -57,8 +57,11 @@
  * Precision.  fp32 inputs: fp32 arithmetic throughout.  bf16 inputs: matrix
  *   products on MFMA with fp32 accumulation; products of q or k with a state
  *   use the state split into two bf16 terms (about 16 mantissa bits, fp32
- *   range); all other product operands are fp16 (intermediates bounded by
- *   the inputs, the clip and the gates).  States are carried in fp32.
+ *   range), except the backward's k dS and k dR, which use one fp16 copy of
+ *   each gradient state scaled by a power of two per chunk; all other
+ *   product operands are fp16 (intermediates bounded by the inputs, the clip
+ *   and the gates), so bf16 q and k are expected within fp16's range, as
+ *   L2-normalised rows are.  States are carried in fp32.
  *   out_dtype may be fp32 (no output rounding) or bf16 (for bf16 inputs).
  */
 #ifndef RLA_MI355X_RLA_H
