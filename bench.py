@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("cc3e20a4a63d3541", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249552772, 321989546),
-    "bwd_scan": ("6db2094cbd753252", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407166075, 613416960),
-    "fwd_scan": ("62f7c2ce231f8029", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373574027, 638583020),
-    "prep": ("dc772e802826f175", ('prep.hip', 'common.hpp', 'kernels.hpp'), 148817029, 171967786),
-    "decode": ("be3c9a2e4d2ba3a4", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746884, 539537894),
+    "bwd_grad": ("72743e201fdfebe9", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249550541, 322002560),
+    "bwd_scan": ("18b3df22ea63c874", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407183078, 613416960),
+    "fwd_scan": ("53673520b4e8fd72", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373583432, 638582860),
+    "prep": ("19280f9176a7eb72", ('prep.hip', 'common.hpp', 'kernels.hpp'), 147608512, 171966794),
+    "decode": ("ff21502440e74732", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542747069, 539547571),
 }
 
 
