@@ -208,20 +208,20 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   // each whole state (the waves' maxima meet in LDS across a barrier); the
   // products are multiplied back by 2^e (exact).  fp32 inputs: plain copies.
   float scS = 1.f, scR = 1.f;
+  // largest magnitude of each of this wave's 16-row checkpoint tiles of the
+  // current dS, dR (wave-uniform), kept for the next chunk's checkpoint
+  // stores, which save these same values
+  uint32_t tmS[IT], tmR[IT];
   auto publish_state_max = [&]() {
     if constexpr (BF) {
-      uint32_t ms = 0, mr = 0;
+      state_tile_absmax<IT>(dS, tmS);
+      state_tile_absmax<IT>(dR, tmR);
+      uint32_t ms = tmS[0], mr = tmR[0];
 #pragma unroll
-      for (int it = 0; it < IT; ++it)
-#pragma unroll
-        for (int jt = 0; jt < JT; ++jt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            ms = max(ms, __float_as_uint(dS[it][jt][r]) & 0x7FFFFFFFu);
-            mr = max(mr, __float_as_uint(dR[it][jt][r]) & 0x7FFFFFFFu);
-          }
-      ms = wave_absmax_bits(ms);
-      mr = wave_absmax_bits(mr);
+      for (int it = 1; it < IT; ++it) {
+        ms = max(ms, tmS[it]);
+        mr = max(mr, tmR[it]);
+      }
       smax[w] = ms;   // every lane stores the wave-uniform value
       smax[4 + w] = mr;
     }
@@ -408,8 +408,9 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       if constexpr (BF) {   // blocked [DV / 32][DK][32]: each wave store is 1 KiB contiguous
         const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
         const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
-        save_state_f16<IT>(dS, reinterpret_cast<f16*>(p.dS_ws) + ob, 32, p.dS_sc + so, DV / 32, w * (DK / 4));
-        save_state_f16<IT>(dR, reinterpret_cast<f16*>(p.dR_ws) + ob, 32, p.dR_sc + so, DV / 32, w * (DK / 4));
+        // tile maxima from publish_state_max: dS, dR are unchanged since
+        save_state_f16_max<IT>(dS, tmS, reinterpret_cast<f16*>(p.dS_ws) + ob, 32, p.dS_sc + so, DV / 32, w * (DK / 4));
+        save_state_f16_max<IT>(dR, tmR, reinterpret_cast<f16*>(p.dR_ws) + ob, 32, p.dR_sc + so, DV / 32, w * (DK / 4));
       } else {
         save_state_f32<IT, JT>(dS, reinterpret_cast<float*>(p.dS_ws) + off, DV, w * (DK / 4));
         save_state_f32<IT, JT>(dR, reinterpret_cast<float*>(p.dR_ws) + off, DV, w * (DK / 4));

@@ -645,6 +645,16 @@ __device__ __forceinline__ uint32_t wave_absmax_bits(uint32_t m) {
              max((uint32_t)__builtin_amdgcn_readlane((int)m, 32), (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
 }
 
+// Largest |x| over the 8 values of two accumulator tiles held by one lane, as
+// an fp32 bit pattern (float maxima of absolute values fold into v_max3_f32
+// with operand modifiers: one instruction per two values; a NaN is skipped).
+__device__ __forceinline__ uint32_t lane_absmax_bits(const floatx4& a, const floatx4& b) {
+  float m = fmaxf(fmaxf(fabsf(a[0]), fabsf(a[1])), fabsf(a[2]));
+  m = fmaxf(fmaxf(m, fabsf(a[3])), fabsf(b[0]));
+  m = fmaxf(fmaxf(m, fabsf(b[1])), fabsf(b[2]));
+  return __float_as_uint(fmaxf(m, fabsf(b[3])));
+}
+
 // Log-cosh residual r = c tanh(x / c) (c < 0: no bound, r = x; c = 0: r = 0).
 __device__ __forceinline__ float resid_tanh(float x, float c) {
   if (c < 0.f) return x;
@@ -706,26 +716,23 @@ __device__ __forceinline__ uint4 pack_strip_f16(const floatx4& a0, const floatx4
 // largest, so one scale per tile loses nothing a per-row scale would keep
 // for states whose rows span fewer than ~28 binades.  Each tile leaves in one
 // 16-byte store per lane (pack_strip_f16; a wave writes 16 rows x 64 B).
+// Largest magnitude of each 16-row x 32-column tile of such a state block
+// (wave-uniform fp32 bits): mt[it] for the tile of rows row0 + 16 it.
 template <int IT>
-__device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16* dst, int64_t ld,
-                                               float* sc, int64_t sc_ld, int row0) {
+__device__ __forceinline__ void state_tile_absmax(const floatx4 (&acc)[IT][2], uint32_t (&mt)[IT]) {
+#pragma unroll
+  for (int it = 0; it < IT; ++it) mt[it] = wave_absmax_bits(lane_absmax_bits(acc[it][0], acc[it][1]));
+}
+
+// save_state_f16 with the tile maxima already known (state_tile_absmax of the
+// same values).
+template <int IT>
+__device__ __forceinline__ void save_state_f16_max(const floatx4 (&acc)[IT][2], const uint32_t (&mt)[IT],
+                                                   f16* dst, int64_t ld, float* sc, int64_t sc_ld,
+                                                   int row0) {
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
-    // tile maximum: in-lane, over the 16-lane row (DPP), over the 4 rows
-    uint32_t m = 0;
-#pragma unroll
-    for (int jt = 0; jt < 2; ++jt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) m = max(m, __float_as_uint(acc[it][jt][r]) & 0x7FFFFFFFu);
-    m = max(m, dpp_u32<0xB1>(m));
-    m = max(m, dpp_u32<0x4E>(m));
-    m = max(m, dpp_u32<0x141>(m));
-    m = max(m, dpp_u32<0x140>(m));
-    const uint32_t mt = max(max((uint32_t)__builtin_amdgcn_readlane((int)m, 0),
-                                (uint32_t)__builtin_amdgcn_readlane((int)m, 16)),
-                            max((uint32_t)__builtin_amdgcn_readlane((int)m, 32),
-                                (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
-    const int e = pow2_scale_exp(mt);
+    const int e = pow2_scale_exp(mt[it]);
     int row, col;
     const uint4 v = pack_strip_f16(acc[it][0], acc[it][1], exp2_int(-e), row, col);
     *reinterpret_cast<uint4*>(dst + (int64_t)(row0 + 16 * it + row) * ld + col) = v;
@@ -735,6 +742,14 @@ __device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16*
     // and drains them all at its next wait
     sc[(int64_t)(row0 / 16 + it) * sc_ld] = exp2_int(e);
   }
+}
+
+template <int IT>
+__device__ __forceinline__ void save_state_f16(const floatx4 (&acc)[IT][2], f16* dst, int64_t ld,
+                                               float* sc, int64_t sc_ld, int row0) {
+  uint32_t mt[IT];
+  state_tile_absmax<IT>(acc, mt);
+  save_state_f16_max<IT>(acc, mt, dst, ld, sc, sc_ld, row0);
 }
 
 // Scheduling hint for the enclosing basic block: alternate one LDS read, two
