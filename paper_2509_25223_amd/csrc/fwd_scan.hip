@@ -283,22 +283,26 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
           *TT::ptr(KT, s2 * 4 + (lane >> 4), t) = Kf[s2];
         }
       }
-      if (tid < kChunk) {
-        const int tt = tid;
-        const float gs = graw[tt], gsp = tt > 0 ? graw[tt - 1] : 0.f, gsl = graw[kChunk - 1];
+      // gate vectors (lane = token), shared out over the four waves by a
+      // wave-uniform index; the chunk-edge factors are stored by every lane
+      // of their wave to one address
+      const int tt = lane, wu = __builtin_amdgcn_readfirstlane(w);
+      if (wu == 0) {
+        egs[tt] = __expf(graw[tt]);
+        egsp[tt] = tt > 0 ? __expf(graw[max(tt - 1, 0)]) : 1.f;
+      } else if (wu == 1) {
         const float gr = graw[64 + tt], grl = graw[64 + kChunk - 1];
+        egr[tt] = __expf(gr);
+        dlr[tt] = __expf(grl - gr);
+        edge[1] = __expf(grl);
+      } else if (wu == 2) {
+        const float gs = graw[tt], gsl = graw[kChunk - 1];
+        dls[tt] = __expf(gsl - gs);
+        edge[0] = __expf(gsl);
+      } else {
         gbt[tt] = graw[128 + tt];
         ggm[tt] = graw[192 + tt];
         if constexpr (VAR) gout[tt] = (vf & kVarUngated) ? 1.f : graw[192 + tt];
-        egs[tt] = __expf(gs);
-        egsp[tt] = __expf(gsp);
-        egr[tt] = __expf(gr);
-        dls[tt] = __expf(gsl - gs);
-        dlr[tt] = __expf(grl - gr);
-        if (tt == 0) {
-          edge[0] = __expf(gsl);
-          edge[1] = __expf(grl);
-        }
       }
     }
     barrier_lds();
