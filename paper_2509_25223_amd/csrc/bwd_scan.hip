@@ -368,33 +368,36 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     const int len = chunk_len(c);
     const int64_t tok = si.start + (int64_t)c * kChunk;
     // dv = dX + diag(b) dV_tail, rows of this chunk only: this lane's 4
-    // rows (one 16-byte read of b), all values formed before the stores
+    // rows (one 16-byte read of b), then a transpose within each lane quad so
+    // that lane 4g + i holds token t0 + i at columns 4g .. 4g + 3 of each
+    // 16-column tile: one 16-byte (fp32) or 8-byte (bf16) store per tile
     auto store_dv = [&](const floatx4 (&dx)[JT], const floatx4 (&tail)[JT]) {
       const int t0 = 16 * w + acc_row(0);
       const floatx4 b4 = *reinterpret_cast<const floatx4*>(gbt + t0);
-      float val[JT][4];
+      floatx4 val[JT];
 #pragma unroll
-      for (int jt = 0; jt < JT; ++jt)
+      for (int jt = 0; jt < JT; ++jt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) val[jt][r] = __builtin_fmaf(b4[r], tail[jt][r], dx[jt][r]);
-      const int64_t o0 = ((tok + t0) * H + h) * (int64_t)DV + j0 + acc_col();
-      const int64_t rs = (int64_t)H * DV;   // between consecutive tokens
-      if (p.out_bf16) {
-        u16* d = reinterpret_cast<u16*>(p.dv) + o0;
+        val[jt] = quad_transpose(val[jt]);
+      }
+      const int tq = t0 + (lane & 3);
+      const int64_t o0 = ((tok + tq) * H + h) * (int64_t)DV + j0 + 4 * ((lane & 15) >> 2);
+      if (tq < len) {
+        if (p.out_bf16) {
+          u16* d = reinterpret_cast<u16*>(p.dv) + o0;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (t0 + r < len) {
+          for (int jt = 0; jt < JT; ++jt) {
+            u16x4 b;
 #pragma unroll
-            for (int jt = 0; jt < JT; ++jt) d[r * rs + jt * 16] = f2bf(val[jt][r]);
+            for (int e = 0; e < 4; ++e) b[e] = f2bf(val[jt][e]);
+            *reinterpret_cast<u16x4*>(d + jt * 16) = b;
           }
-      } else {
-        float* d = reinterpret_cast<float*>(p.dv) + o0;
+        } else {
+          float* d = reinterpret_cast<float*>(p.dv) + o0;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (t0 + r < len) {
-#pragma unroll
-            for (int jt = 0; jt < JT; ++jt) d[r * rs + jt * 16] = val[jt][r];
-          }
+          for (int jt = 0; jt < JT; ++jt) *reinterpret_cast<floatx4*>(d + jt * 16) = val[jt];
+        }
       }
     };
 

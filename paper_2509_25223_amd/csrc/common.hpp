@@ -645,6 +645,32 @@ __device__ __forceinline__ uint32_t wave_absmax_bits(uint32_t m) {
              max((uint32_t)__builtin_amdgcn_readlane((int)m, 32), (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
 }
 
+// 4 x 4 transpose across the lanes of each quad (lanes 4g + i, i = 0..3): lane
+// i enters with x[r] = M[i][r] and leaves with x[r] = M[r][i].  Two exchange
+// rounds, with lane i ^ 1 for the registers whose index differs from i in bit
+// 0, then with lane i ^ 2 for bit 1; each lane sends two values per round.
+__device__ __forceinline__ floatx4 quad_transpose(floatx4 x) {
+  const int i = threadIdx.x & 3;
+  const bool odd = i & 1, hi = i & 2;
+  {
+    const float r0 = dpp<0xB1>(odd ? x[0] : x[1]);   // quad_perm [1,0,3,2]
+    const float r1 = dpp<0xB1>(odd ? x[2] : x[3]);
+    x[0] = odd ? r0 : x[0];
+    x[1] = odd ? x[1] : r0;
+    x[2] = odd ? r1 : x[2];
+    x[3] = odd ? x[3] : r1;
+  }
+  {
+    const float r0 = dpp<0x4E>(hi ? x[0] : x[2]);    // quad_perm [2,3,0,1]
+    const float r1 = dpp<0x4E>(hi ? x[1] : x[3]);
+    x[0] = hi ? r0 : x[0];
+    x[1] = hi ? r1 : x[1];
+    x[2] = hi ? x[2] : r0;
+    x[3] = hi ? x[3] : r1;
+  }
+  return x;
+}
+
 // Largest |x| over the 8 values of two accumulator tiles held by one lane, as
 // an fp32 bit pattern (float maxima of absolute values fold into v_max3_f32
 // with operand modifiers: one instruction per two values; a NaN is skipped).
