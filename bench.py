@@ -45,11 +45,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("72743e201fdfebe9", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249550541, 322002560),
-    "bwd_scan": ("18b3df22ea63c874", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407183078, 613416960),
-    "fwd_scan": ("53673520b4e8fd72", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373583432, 638582860),
-    "prep": ("19280f9176a7eb72", ('prep.hip', 'common.hpp', 'kernels.hpp'), 147608512, 171966794),
-    "decode": ("ff21502440e74732", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542747069, 539547571),
+    "bwd_grad": ("42f020ac9c630148", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249546473, 320918645),
+    "bwd_scan": ("d3c2963a85b9f99e", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407162643, 613416960),
+    "fwd_scan": ("25689f8b571ffdbe", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373572263, 638583296),
+    "prep": ("aaea8c87a79bdf3a", ('prep.hip', 'common.hpp', 'kernels.hpp'), 147792930, 171966677),
+    "decode": ("093edbbe40eefd13", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746642, 539571891),
 }
 
 
