@@ -31,9 +31,10 @@ template <typename T, int DK>
 struct PrepLayout {
   static constexpr int kLdK = DK + (sizeof(T) == 2 ? 8 : 4);   // Kc / Qc row stride
   static constexpr int kLdA = rla::kLdA;
-  // region 0: Kc, Qc (T) -- later reused by As, Ar, Ts, Tr (fp32)
+  // region 0: Kc, Qc (T) -- later reused by As, Ar (fp32), which the
+  // inversion overwrites with T^S, T^R
   static constexpr int kBytesKQ = 2 * kChunk * kLdK * (int)sizeof(T);
-  static constexpr int kBytesA = 4 * kChunk * kLdA * 4;
+  static constexpr int kBytesA = 2 * kChunk * kLdA * 4;
   static constexpr int kBytes0 = kBytesKQ > kBytesA ? kBytesKQ : kBytesA;
   static constexpr int kBytesW = 6 * 256 * 4;                   // per-wave block products
   static constexpr int kBytesGates = 5 * kChunk * 4;
@@ -41,25 +42,34 @@ struct PrepLayout {
   static_assert(kBytes <= 160 * 1024, "prep LDS");
 };
 
+// Offset (in floats, row stride kLdA) of 16 x 16 block (bi, bj), bi >= bj, of
+// an inverse T kept in the storage of its own A: diagonal blocks in place,
+// off-diagonal ones in the (unused) mirror position above the diagonal,
+// block (bi, bj) at (bj, bi), each block untransposed.
+__device__ __forceinline__ int tblk(int bi, int bj) {
+  return bi == bj ? 16 * bi * kLdA + 16 * bj : 16 * bj * kLdA + 16 * bi;
+}
+
 // Inverse T = (I + A)^{-1} of a unit lower-triangular 64 x 64 matrix (A
-// strictly lower, fp32, row stride kLdA) for two matrices at once (A0 -> T0,
-// A1 -> T1), in 16 x 16 blocks: the diagonal blocks T_ii = (I + A_ii)^{-1} by
-// forward substitution (one lane per column), then each block column j by
+// strictly lower, fp32, row stride kLdA) for two matrices at once (A0, A1),
+// in 16 x 16 blocks, each T written into the storage of its A (tblk): the
+// diagonal blocks T_ii = (I + A_ii)^{-1} by forward substitution (one lane
+// per column, every read of A_ii before the wave's writes), then each block
+// column j by
 //   T_ij = -T_ii * sum_{m=j}^{i-1} A_im T_mj        (i = j+1 .. 3)
-// on fp32 MFMA.  Wave w takes matrix w >> 1 and block column 0 (w even) or
-// block columns 1 and 2 (w odd); a column only reads its own blocks and the
-// diagonal ones, so one barrier separates the two phases.  Blocks above the
-// diagonal are not written.  P: 4 x 256 floats of per-wave scratch.
-__device__ void invert_unit_lower_pair(const float* A0, const float* A1, float* T0, float* T1,
-                                       float* P) {
+// on fp32 MFMA, which reads only the off-diagonal blocks of A below the
+// diagonal (never overwritten) and blocks of T.  Wave w takes matrix w >> 1
+// and block column 0 (w even) or block columns 1 and 2 (w odd); a column
+// only reads its own blocks and the diagonal ones, so one barrier separates
+// the two phases.  P: 4 x 256 floats of per-wave scratch.
+__device__ void invert_unit_lower_pair(float* A0, float* A1, float* P) {
   constexpr int ld = kLdA;
   typedef Mfma<float> F;
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   // ---- diagonal blocks: lanes 0..31 of wave w solve blocks 2w and 2w+1 ----
   if (lane < 32) {
     const int b = 2 * w + (lane >> 4), mat = b >> 2, blk = b & 3, c = lane & 15;
-    const float* A = (mat ? A1 : A0) + (16 * blk) * ld + 16 * blk;
-    float* T = (mat ? T1 : T0) + (16 * blk) * ld + 16 * blk;
+    float* A = (mat ? A1 : A0) + (16 * blk) * ld + 16 * blk;
     float x[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -69,31 +79,31 @@ __device__ void invert_unit_lower_pair(const float* A0, const float* A1, float* 
       x[i] = (i < c) ? 0.f : acc;
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) T[i * ld + c] = x[i];
+    for (int i = 0; i < 16; ++i) A[i * ld + c] = x[i];
   }
   __syncthreads();
   // ---- off-diagonal blocks, one block column chain per wave ----
-  const float* A = (w >> 1) ? A1 : A0;
-  float* T = (w >> 1) ? T1 : T0;
-  float* Pw = P + w * 256;   // [16][16], k-major rows
+  float* A = (w >> 1) ? A1 : A0;   // A below the diagonal, T per tblk
+  float* Pw = P + w * 256;         // [16][16], k-major rows
   const int n = lane & 15, kg = lane >> 4;
-  // acc += X[rows 16 xi.., cols 16 xm..] * Y[rows 16 ym.., cols 16 yj..] (16 x 16 x 16)
-  auto mm = [&](floatx4& acc, const float* X, int xi, int xm, const float* Y, int ym, int yj, int ldy) {
-#pragma unroll
-    for (int k0 = 0; k0 < 16; k0 += F::kStep)
-      acc = F::mma(X[(16 * xi + n) * ld + 16 * xm + k0 + kg], Y[(16 * ym + k0 + kg) * ldy + 16 * yj + n], acc);
-  };
   auto solve_block = [&](int i, int j) {   // T_ij from T_jj .. T_{i-1,j}
     floatx4 s = zero4();
-    for (int m = j; m < i; ++m) mm(s, A, i, m, T, m, j, ld);
+    for (int m = j; m < i; ++m) {   // s += A_im T_mj
+      const float* Y = A + tblk(m, j);
+#pragma unroll
+      for (int k0 = 0; k0 < 16; k0 += F::kStep)
+        s = F::mma(A[(16 * i + n) * ld + 16 * m + k0 + kg], Y[(k0 + kg) * ld + n], s);
+    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) Pw[(4 * kg + r) * 16 + n] = s[r];
     floatx4 t = zero4();
+    const float* Tii = A + tblk(i, i);
 #pragma unroll
     for (int k0 = 0; k0 < 16; k0 += F::kStep)   // T_ii * P (wave-local LDS order)
-      t = F::mma(T[(16 * i + n) * ld + 16 * i + k0 + kg], Pw[(k0 + kg) * 16 + n], t);
+      t = F::mma(Tii[n * ld + k0 + kg], Pw[(k0 + kg) * 16 + n], t);
+    float* Tij = A + tblk(i, j);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) T[(16 * i + 4 * kg + r) * ld + 16 * j + n] = -t[r];
+    for (int r = 0; r < 4; ++r) Tij[(4 * kg + r) * ld + n] = -t[r];
   };
   if ((w & 1) == 0) {
     solve_block(1, 0);
@@ -117,9 +127,7 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   T* Kc = reinterpret_cast<T*>(smem);
   T* Qc = Kc + kChunk * L::kLdK;
   float* As = reinterpret_cast<float*>(smem);   // reuses region 0 after G, P
-  float* Ar = As + kChunk * L::kLdA;
-  float* Ts = Ar + kChunk * L::kLdA;
-  float* Tr = Ts + kChunk * L::kLdA;
+  float* Ar = As + kChunk * L::kLdA;             // (then T^S, T^R: tblk)
   float* W = reinterpret_cast<float*>(smem + L::kBytes0);
   float* gs = W + 6 * 256;
   float* gr = gs + kChunk;
@@ -209,7 +217,7 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
     mma_tile<T, DK, true, true>(G[ct], Kc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
     mma_tile<T, DK, true, true>(P[ct], Qc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
   }
-  __syncthreads();   // Kc/Qc dead: region 0 becomes As/Ar/Ts/Tr
+  __syncthreads();   // Kc/Qc dead: region 0 becomes As/Ar
 
   XT* mats = reinterpret_cast<XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
   floatx4 mg[4], mp[4], mr[4];   // this wave's 16-row strips of MG, MP, MR
@@ -280,7 +288,7 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   }
   if constexpr (RDN) {
     __syncthreads();
-    invert_unit_lower_pair(As, Ar, Ts, Tr, W);
+    invert_unit_lower_pair(As, Ar, W);
     __syncthreads();
     // 8 consecutive elements per thread and step (16-byte fp16 stores)
     for (int e = 8 * tid; e < kMatElems; e += 8 * kThreads) {
@@ -288,9 +296,10 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
       const bool upper = (s >> 4) > (t >> 4);   // blocks above the diagonal are zero
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
-        // two 16-byte reads (blocks above the diagonal hold no values: their
-        // bits are cleared with a mask, not read under a condition)
-        const float* src = (m ? Tr : Ts) + t * L::kLdA + s;
+        // two 16-byte reads (blocks of T above the diagonal are zero: the
+        // bits read there are cleared with a mask, not read under a
+        // condition)
+        const float* src = (m ? Ar : As) + tblk(t >> 4, s >> 4) + (t & 15) * L::kLdA + (s & 15);
         const uint4 b0 = keep_if(*reinterpret_cast<const uint4*>(src), !upper);
         const uint4 b1 = keep_if(*reinterpret_cast<const uint4*>(src + 4), !upper);
         const floatx4 f0 = __builtin_bit_cast(floatx4, b0), f1 = __builtin_bit_cast(floatx4, b1);
