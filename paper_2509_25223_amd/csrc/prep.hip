@@ -36,10 +36,10 @@ struct PrepLayout {
   static constexpr int kBytesKQ = 2 * kChunk * kLdK * (int)sizeof(T);
   static constexpr int kBytesA = 2 * kChunk * kLdA * 4;
   static constexpr int kBytes0 = kBytesKQ > kBytesA ? kBytesKQ : kBytesA;
-  static constexpr int kBytesW = 6 * 256 * 4;                   // per-wave block products
+  static constexpr int kBytesW = 4 * 256 * 4;                   // per-wave block products
   static constexpr int kBytesGates = 5 * kChunk * 4;
   static constexpr int kBytes = kBytes0 + kBytesW + kBytesGates;
-  static_assert(kBytes <= 160 * 1024, "prep LDS");
+  static_assert(kBytes <= 40 * 1024, "prep LDS: four workgroups per CU");
 };
 
 // Offset (in floats, row stride kLdA) of 16 x 16 block (bi, bj), bi >= bj, of
@@ -129,7 +129,7 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   float* As = reinterpret_cast<float*>(smem);   // reuses region 0 after G, P
   float* Ar = As + kChunk * L::kLdA;             // (then T^S, T^R: tblk)
   float* W = reinterpret_cast<float*>(smem + L::kBytes0);
-  float* gs = W + 6 * 256;
+  float* gs = W + 4 * 256;
   float* gr = gs + kChunk;
   float* bt = gr + kChunk;
   float* gm = bt + kChunk;
