@@ -48,7 +48,7 @@ MEASURED_TRAFFIC = {
     "bwd_grad": ("42f020ac9c630148", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249546473, 320918645),
     "bwd_scan": ("d3c2963a85b9f99e", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407162643, 613416960),
     "fwd_scan": ("25689f8b571ffdbe", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373572263, 638583296),
-    "prep": ("aaea8c87a79bdf3a", ('prep.hip', 'common.hpp', 'kernels.hpp'), 147792930, 171966677),
+    "prep": ("72bae810063c3ecd", ('prep.hip', 'common.hpp', 'kernels.hpp'), 149294713, 171970410),
     "decode": ("093edbbe40eefd13", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746642, 539571891),
 }
 
