@@ -18,16 +18,31 @@ pytestmark = pytest.mark.gpu
 
 
 def check(variant, inp, dtype, device, clip=1.0, S0=None, R0=None, dSf=None, dRf=None,
-          dense_B=None, label=""):
+          dense_B=None, label="", out_dtype=None):
     inp, moved = nudge(variant, inp, dtype, clip=clip, S0=S0, R0=R0)
     g = gpu_backward(variant, inp, dtype, device, clip=clip, S0=S0, R0=R0, dS_final=dSf,
-                     dR_final=dRf, dense_B=dense_B)
+                     dR_final=dRf, dense_B=dense_B, out_dtype=out_dtype)
     ref = oracle_backward(variant, inp, clip=clip, S0=S0, R0=R0, dS_final=dSf, dR_final=dRf)
     errs = {key: rel_err(g[key], ref[key]) for key in GRAD_KEYS}
+    if out_dtype is not None:   # dq, dk, dv rounded once to bf16 on the way out
+        for key in ("dq", "dk", "dv"):
+            errs[key] = rel_err_rounded(g[key], ref[key], 2.0 ** -8)
     print("[%s %s %s moved=%d] %s" % (variant, dtype, label, moved,
                                       " ".join("%s=%.1e" % kv for kv in errs.items())))
     for key, e in errs.items():
         assert e <= TOL[dtype], (key, e)
+
+
+def rel_err_rounded(x, ref, half_ulp):
+    """max(|x - ref| - half_ulp |ref|, 0) / RMS(ref): what is left of the error
+    once each value's own rounding to the output format (relative half-ulp
+    half_ulp: 2^-8 for bf16's 8 significant bits) is set aside.  A plain
+    max|x - ref| / RMS would be dominated by that rounding of the largest
+    gradients (about 10x the RMS), which the computation cannot avoid."""
+    ref = np.asarray(ref, dtype=np.float64)
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    d = np.abs(np.asarray(x, np.float64) - ref) - half_ulp * np.abs(ref)
+    return float(np.max(np.maximum(d, 0.0))) / rms
 
 
 @pytest.mark.parametrize("variant", ["rdn", "rla"])
@@ -58,6 +73,19 @@ def test_varlen_edges(device, variant, dtype, d):
     inp = datagen.make_inputs(wl, seed=203)
     S0, R0 = datagen.random_states(11, len(lens), 2, d, d)
     check(variant, inp, dtype, device, S0=S0, R0=R0, label="varlen")
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
+def test_bf16_outputs(device, variant):
+    """dq, dk, dv returned in bf16 (out_dtype): the same gradients rounded once
+    to bf16, compared with the bound after setting that rounding aside
+    (rel_err_rounded); ragged lengths, so the row masks of the dv stores and
+    the partial chunks are hit."""
+    import torch
+    lens = [1, 63, 130, 64]
+    wl = datagen.small(variant + "_fwdbwd", "bf16", lens, H=2, d=128)
+    inp = datagen.make_inputs(wl, seed=204)
+    check(variant, inp, "bf16", device, out_dtype=torch.bfloat16, label="bf16 out")
 
 
 @pytest.mark.slow
