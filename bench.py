@@ -9,12 +9,16 @@ As in training, the forward saves what the backward needs (chunk states,
 clip masks, the U, UR, r blocks) in the workspace and the backward reads it
 instead of recomputing the forward.
 
-Prints ONE JSON line with the throughput (tokens/s, whole job), per-stage
-launch times (HIP events recorded on the launch stream around each kernel
-stage) with their algorithmic TFLOP/s and GB/s, the roofline of the dominant
-kernel (its binding resource: algorithmic bytes or flops per launch over its
-launch time), and the fp64 CPU oracle timed on a bounded sample of the same
-workload on this host.
+Prints ONE JSON line with the throughput (tokens/s, whole job) and the
+metric's second figure, the step's share of the dense bf16 MFMA peak (the
+chunked method's count model, ~1.52 Mflop per token-head, over the step
+time); per-stage launch times (HIP events recorded on the launch stream
+around each kernel stage) with their algorithmic TFLOP/s and GB/s (bytes:
+only the operator's own inputs and outputs each kernel touches); the roofline
+of the dominant kernel (HBM or MFMA by its algorithmic intensity against the
+ridge), with the design's bytes (intermediates included) and the counter
+traffic beside the algorithmic bytes; and the fp64 CPU oracle timed on the
+same workload on this host.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
                     [--copy-calibration-mib M] [--op fwdbwd|decode]
@@ -66,36 +70,75 @@ def measured_traffic(stage: str):
     return read + written if h.hexdigest()[:16] == digest else None
 
 
-def stage_model(stage: str, d: int, C: int = CHUNK) -> tuple:
-    """Algorithmic (flops, HBM bytes) of one (chunk, head) for each kernel
-    stage of the RDN fwd+bwd path with bf16 inputs, fp32 outputs, d_k = d_v = d.
-
-    Flops: each matrix product counted once as 2*m*n*k (no split-precision
-    repeats); products restricted to a triangle count only its C(C+1)/2 rows
-    x columns.  Bytes: every tensor the stage must read or write once
-    (inputs bf16, prep's matrices and the saved token blocks fp16, states and
-    outputs fp32)."""
+def kernel_flops(stage: str, d: int, C: int = CHUNK) -> float:
+    """Algorithmic flops of one (chunk, head) for each kernel of the RDN
+    fwd+bwd path, d_k = d_v = d: every matrix product the kernel's chunk
+    algebra needs, counted once as 2*m*n*k (split-precision repeats are not
+    counted), products restricted to a triangle over its C(C+1)/2 entries."""
     cd2, c2d, tri = 2.0 * C * d * d, 2.0 * C * C * d, float(C * (C + 1)) * d
-    tok_bf16, tok_h, tok_f32 = C * d * 2, C * d * 2, C * d * 4
-    state = d * d * 4
-    mats = 5 * C * C * 2
-    gates_in, gate_blk = 4 * C * 4, 256 * 4
     if stage == "prep":           # G = K K^T, P = Q K^T, two triangular inverses
-        return 2 * c2d + 2 * (C ** 3) / 3.0, 2 * tok_bf16 + gates_in + mats + gate_blk
-    if stage == "fwd_scan":       # KS QS KR QR, T^S Y MG U MP U T^R YR MR UR, S/R updates
-        flops = 6 * cd2 + 5 * c2d
-        # K Q V, matrices, gates; o, chunk-start S R, clip mask, U UR r
-        return flops, 3 * tok_bf16 + mats + gate_blk + tok_f32 + 2 * state + C * d + 3 * tok_h
-    if stage == "bwd_scan":       # K dS K dR, 5 transposed C x C products, dS/dR updates (4)
-        flops = 6 * cd2 + 5 * c2d
-        # K Q dO, matrices, gates, mask; dS dR at chunk ends, dX dY dYR, dv
-        return flops, 3 * tok_bf16 + mats + gate_blk + C * d + 2 * state + 3 * tok_h + tok_f32
-    if stage == "bwd_grad":       # 7 state products, W1..W5 G P (lower), dP K dP^T Q (dG+dG^T) K
-        flops = 7 * cd2 + 7 * tri + 3 * c2d
-        # K Q V dO, S0 R0 dS1 dR1, U UR r dX dY dYR, gates; dq dk, gate grads
-        return flops, (4 * tok_bf16 + 4 * state + 6 * tok_h + gate_blk + 2 * C * 4
-                       + 2 * tok_f32 + 4 * C * 4)
+        return 2 * c2d + 2 * (C ** 3) / 3.0
+    if stage == "fwd_scan":       # KS QS KR QR, S/R updates; T^S Y, MG U, MP U, T^R YR, MR UR
+        return 6 * cd2 + 5 * c2d
+    if stage == "bwd_scan":       # K dS, K dR, dS/dR updates (4); 5 transposed C x C products
+        return 6 * cd2 + 5 * c2d
+    if stage == "bwd_grad":       # 7 state products, W1..W5 G P (lower), dP K, dP^T Q, (dG+dG^T) K
+        return 7 * cd2 + 7 * tri + 3 * c2d
     raise KeyError(stage)
+
+
+def kernel_io_bytes(stage: str, d: int, C: int = CHUNK) -> int:
+    """Algorithmic HBM bytes of one (chunk, head): only the operator's own
+    inputs and outputs that the kernel must read or write (bf16 q, k, v, dO;
+    fp32 gates; fp32 o, dq, dk, dv and gate gradients as this benchmark
+    writes them).  Intermediates of the design (matrices, checkpoints, saved
+    blocks, masks) are not algorithmic and are not counted here."""
+    row_in, row_out, gate = d * 2, d * 4, 4
+    if stage == "prep":           # q, k, four gates
+        return C * (2 * row_in + 4 * gate)
+    if stage == "fwd_scan":       # q, k, v, four gates in; o out
+        return C * (3 * row_in + 4 * gate + row_out)
+    if stage == "bwd_scan":       # q, k, dO, four gates in; dv out
+        return C * (3 * row_in + 4 * gate + row_out)
+    if stage == "bwd_grad":       # q, k, v, dO, four gates in; dq, dk, four gate gradients out
+        return C * (4 * row_in + 4 * gate + 2 * row_out + 4 * gate)
+    raise KeyError(stage)
+
+
+def design_bytes(stage: str, d: int, C: int = CHUNK) -> int:
+    """HBM bytes of one (chunk, head) that the kernel moves by design,
+    intermediates included: the algorithmic bytes plus prep's five fp16 64x64
+    matrices and gate block, the fp16 chunk-start states S, R and chunk-end
+    gradient states dS, dR with their tile scales, the clip mask (one byte per
+    element) and the fp16 token blocks U, UR, r, dX, dY, dYR.  This is the
+    traffic the counters should read; the excess over kernel_io_bytes is the
+    price of the split into four kernels."""
+    tok_h = C * d * 2
+    mats, gate_blk = 5 * C * C * 2, 256 * 4
+    state = d * d * 2 + (d // 16) * (d // 32) * 4
+    if stage == "prep":
+        return kernel_io_bytes(stage, d, C) + mats + gate_blk
+    if stage == "fwd_scan":       # + matrices, gate block in; S R, mask, U UR r out
+        return kernel_io_bytes(stage, d, C) + mats + gate_blk + 2 * state + C * d + 3 * tok_h
+    if stage == "bwd_scan":       # + matrices, gate block, mask in; dS dR, dX dY dYR out
+        return kernel_io_bytes(stage, d, C) + mats + gate_blk + C * d + 2 * state + 3 * tok_h
+    if stage == "bwd_grad":       # + S0 R0 dS1 dR1, U UR r dX dY dYR, gate block in
+        return kernel_io_bytes(stage, d, C) + 4 * state + 6 * tok_h + gate_blk
+    raise KeyError(stage)
+
+
+def step_flops_per_token_head(d: int, C: int = CHUNK) -> float:
+    """The count model of the RDN chunked method per token-head: forward =
+    state-independent intra-chunk work 10Cd + 2C^2/3 (Gram, scores, UT
+    transform, W and U0 formation) + state-dependent intra-chunk work 8Cd +
+    state products 14d^2; forward + backward = 4x the forward (the backward
+    recomputes the forward and takes two gradient products per forward
+    product).  ~1.52 Mflop at C = 64, d = 128."""
+    fwd = 10.0 * C * d + 2.0 * C * C / 3.0 + 8.0 * C * d + 14.0 * d * d
+    return 4.0 * fwd
+
+
+RIDGE = PEAK_MFMA_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)   # flop per byte
 
 
 def main() -> int:
@@ -227,31 +270,48 @@ def run_fwdbwd(args) -> int:
         for i, name in enumerate(names):
             stage_ms[tag + name] = float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
     units = B * ((T + CHUNK - 1) // CHUNK) * H   # (chunk, head) pairs per launch
-    step_flops = sum(stage_model(st, d)[0] for st in fwd_stages + bwd_stages) * units
     stages = {}
     for key, ms in stage_ms.items():
-        fl, by = stage_model(key.split(".", 1)[1], d)
+        name = key.split(".", 1)[1]
+        fl, by, dby = kernel_flops(name, d), kernel_io_bytes(name, d), design_bytes(name, d)
         tf = fl * units / (ms * 1e-3) / 1e12
         gb = by * units / (ms * 1e-3) / 1e9
+        traffic = None if vnames else measured_traffic(name)
         stages[key] = {"ms": round(ms, 4), "tflops": round(tf, 2), "gbs": round(gb, 1),
                        "mfma_frac": round(tf / PEAK_MFMA_TFLOPS, 4),
                        "hbm_frac": round(gb / PEAK_HBM_GBS, 4),
-                       "traffic": None if vnames else measured_traffic(key.split(".", 1)[1])}
+                       "intensity": round(fl / by, 1),
+                       "design_bytes": dby * units,
+                       "traffic": traffic,
+                       "traffic_over_algorithmic": None if traffic is None else round(traffic / (by * units), 2)}
     dom = max(stage_ms, key=stage_ms.get)
     ds = stages[dom]
+    dname = dom.split(".", 1)[1]
     kernel_names = {"prep": "prep_kernel", "fwd_scan": "fwd_scan_kernel (saving)",
                     "bwd_scan": "bwd_scan_kernel", "bwd_grad": "bwd_grad_kernel"}
-    fl, by = stage_model(dom.split(".", 1)[1], d)
-    if ds["hbm_frac"] >= ds["mfma_frac"]:
+    fl, by = kernel_flops(dname, d), kernel_io_bytes(dname, d)
+    # the binding roof of the dominant kernel: HBM below the ridge intensity, MFMA above it
+    if fl / by < RIDGE:
         roofline = {"bound": "hbm", "achieved": ds["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
                     "frac": ds["hbm_frac"], "traffic": ds["traffic"],
-                    "bytes_per_launch": by * units}
+                    "bytes_per_launch": by * units, "flops_per_launch": fl * units,
+                    "mfma_frac": ds["mfma_frac"]}
     else:
         roofline = {"bound": "mfma", "achieved": ds["tflops"], "peak": PEAK_MFMA_TFLOPS,
                     "unit": "TFLOP/s", "frac": ds["mfma_frac"], "traffic": ds["traffic"],
-                    "flops_per_launch": fl * units}
-    roofline.update({"kernel": kernel_names[dom.split(".", 1)[1]], "stage": dom,
-                     "launch_ms": ds["ms"], "units_per_launch": units})
+                    "flops_per_launch": fl * units, "bytes_per_launch": by * units,
+                    "hbm_frac": ds["hbm_frac"]}
+    roofline.update({"kernel": kernel_names[dname], "stage": dom, "launch_ms": ds["ms"],
+                     "units_per_launch": units, "design_bytes_per_launch": ds["design_bytes"],
+                     "traffic_over_algorithmic": ds["traffic_over_algorithmic"]})
+    # the metric's own fraction: the count model's flops of the whole step over
+    # the step time, against the dense bf16 MFMA peak
+    step_flops = step_flops_per_token_head(d) * B * T * H
+    step_tflops = step_flops / (ms_per_step * 1e-3) / 1e12
+    step_roofline = {"bound": "mfma", "achieved": round(step_tflops, 2), "peak": PEAK_MFMA_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(step_tflops / PEAK_MFMA_TFLOPS, 4),
+                     "flops_per_step": step_flops,
+                     "flops_per_token_head": step_flops_per_token_head(d)}
 
     # ---- CPU baseline: the fp64 oracle on the same workload ----
     cpu = None
@@ -286,9 +346,9 @@ def run_fwdbwd(args) -> int:
         "config": dict({"workload": wl.name, "B": B, "T": T, "H": H, "d_k": d, "d_v": d,
                         "chunk": CHUNK, "clip": wl.clip, "outputs": "fp32",
                         "parallelism": "single GPU"}, **({"variants": vnames} if vnames else {})),
-        # algorithmic flops of the whole step (every stage's count model) over
-        # the step time, as a fraction of the dense bf16 MFMA peak
-        "step_mfma_frac": round(step_flops / (ms_per_step * 1e-3) / 1e12 / PEAK_MFMA_TFLOPS, 4),
+        # the metric's second figure: % of the dense bf16 MFMA peak of the whole step
+        "pct_bf16_mfma_peak": round(100.0 * step_roofline["frac"], 2),
+        "step_roofline": step_roofline,
         "stages": stages,
         "roofline": roofline,
         "cpu_baseline": cpu,

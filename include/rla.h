@@ -206,8 +206,10 @@ rla_status rdn_forward(const rla_problem *problem,
 
 /*
  * RDN backward: gradients of L = <dO, o> + <dS_final, S_T> + <dR_final, R_T>
- * with respect to every input of rdn_forward, recomputing the forward from the
- * inputs (nothing is saved between calls).  dS_final, dR_final, S0, R0 may be
+ * with respect to every input of rdn_forward.  By default the call recomputes
+ * the forward from the inputs; with RLA_FLAG_USE_SAVED it reads what a
+ * forward with RLA_FLAG_SAVE_FOR_BACKWARD left in the same workspace instead
+ * (see the save-for-backward flags above).  dS_final, dR_final, S0, R0 may be
  * NULL (zeros); dS0, dR0 may be NULL (not written).  dq, dk, dv are in
  * problem.out_dtype; gate gradients are fp32 and are with respect to the
  * gate values (not their logarithms).
@@ -250,8 +252,13 @@ rla_status rla_backward(const rla_problem *problem,
  *   S_out, R_out [B, H, d_k, d_v] fp32, required, 16-byte aligned; S_out may
  *     be the same pointer as S_in (in-place update), likewise R_out and R_in;
  *     any other overlap among the four state buffers is rejected.
- * No workspace.  problem.cu_seqlens must be NULL (RLA_ERR_UNSUPPORTED) and
- * problem.flags 0.  bf16 and fp32 inputs both support d_k, d_v in {64, 128};
+ * No workspace.  problem.cu_seqlens must be NULL (RLA_ERR_UNSUPPORTED).
+ * problem.flags may carry the variant flags (RLA_FLAG_RESIDUAL_TANH,
+ * RLA_FLAG_UNGATED_OUTPUT, RLA_FLAG_DECAYED_RESIDUAL) and the pre-processing
+ * flags (RLA_FLAG_QK_SILU_L2NORM, RLA_FLAG_GATE_PREACT), applied to each
+ * token as in the chunked entry points; RLA_FLAG_SAVE_FOR_BACKWARD and
+ * RLA_FLAG_USE_SAVED are rejected (RLA_ERR_VALUE).
+ * bf16 and fp32 inputs both support d_k, d_v in {64, 128};
  * all arithmetic is fp32 (bf16 inputs are widened exactly).  Decays are used
  * as given (no 2^-126 floor is needed here).  T = 0 copies S_in, R_in (or
  * zeros) to S_out, R_out.  Each (sequence, head) reads its states once and

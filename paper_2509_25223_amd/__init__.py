@@ -189,14 +189,54 @@ def _check(tensors, device):
             raise ValueError("%s must be contiguous" % name)
 
 
+def _expect(name, t, shape, dtype):
+    """t (if given) must have exactly this shape and dtype."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+
+
+def _check_operands(problem, q, k, v, gates, states):
+    """Shapes and dtypes of the operator's inputs against q: k like q, v with
+    q's leading dimensions, fp32 gates [.., H] and fp32 states [N, H, d_k, d_v].
+    The library trusts these shapes, so a mismatch must stop here."""
+    torch = _torch()
+    if v.dim() != q.dim() or tuple(v.shape[:-1]) != tuple(q.shape[:-1]):
+        raise ValueError("v must be %s + [d_v], got %s" % (tuple(q.shape[:-1]), tuple(v.shape)))
+    _expect("k", k, q.shape, q.dtype)
+    _expect("v", v, v.shape, q.dtype)
+    for name, t in gates.items():
+        if t is None:
+            raise ValueError("%s is required" % name)
+        _expect(name, t, q.shape[:-1], torch.float32)
+    for name, t in states.items():
+        _expect(name, t, _state_shape(problem), torch.float32)
+
+
+def _state_shape(problem):
+    N = problem.num_seqs if problem.cu_seqlens else problem.batch
+    return (N, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
+
+
 def _workspace(problem, op, device, workspace):
+    """(workspace tensor, its size in bytes): the caller's (checked for device,
+    contiguity and size) or a new uint8 tensor of rla_workspace_size bytes."""
     torch = _torch()
     need = rla_workspace_size(problem, op)
     if workspace is not None:
-        if workspace.numel() * workspace.element_size() < need:
+        if workspace.device != device:
+            raise ValueError("workspace must be on %s" % device)
+        if not workspace.is_contiguous():
+            raise ValueError("workspace must be contiguous")
+        have = workspace.numel() * workspace.element_size()
+        if have < need:
             raise ValueError("workspace too small: need %d bytes" % need)
-        return workspace, need
-    return torch.empty(max(need, 1), dtype=torch.uint8, device=device), need
+        return workspace, have
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=device)
+    return ws, ws.numel()
 
 
 _VARIANT_MASK = (RLA_FLAG_RESIDUAL_TANH | RLA_FLAG_UNGATED_OUTPUT | RLA_FLAG_DECAYED_RESIDUAL |
@@ -215,8 +255,8 @@ def _check_decay_param(variants, decay_param, H, device):
         if decay_param is None:
             raise ValueError("RLA_FLAG_GATE_PREACT needs decay_param [2, H] (a then b)")
         if decay_param.numel() != 2 * H or not decay_param.is_contiguous() or \
-                decay_param.device != device:
-            raise ValueError("decay_param must be a contiguous [2, H] tensor on %s" % device)
+                decay_param.device != device or decay_param.dtype != _torch().float32:
+            raise ValueError("decay_param must be a contiguous float32 [2, H] tensor on %s" % device)
     return decay_param
 
 
@@ -233,24 +273,21 @@ def _forward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S0, R0, cu_
         op = RLA_OP_RDN_BACKWARD if op == RLA_OP_RDN_FORWARD else RLA_OP_RLA_BACKWARD
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
-                S0=S0, R0=R0), dev)
-    for t in (alpha_s, beta, alpha_r, gamma, S0, R0):
-        if t is not None and t.dtype != torch.float32:
-            raise TypeError("gates and states must be float32")
-    N = problem.num_seqs if cu_seqlens is not None else problem.batch
+                S0=S0, R0=R0, out=out), dev)
+    _check_operands(problem, q, k, v, dict(alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma),
+                    dict(S0=S0, R0=R0))
     odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
     o = torch.empty(v.shape, dtype=odt, device=dev) if out is None else out
-    if o.dtype != odt or o.shape != v.shape:
-        raise ValueError("out must be %s with shape %s" % (odt, tuple(v.shape)))
+    _expect("out", o, v.shape, odt)
     Sf = Rf = None
     if return_states:
-        shape = (N, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
+        shape = _state_shape(problem)
         Sf = torch.empty(shape, dtype=torch.float32, device=dev)
         Rf = torch.empty(shape, dtype=torch.float32, device=dev)
-    ws, need = _workspace(problem, op, dev, workspace)
+    ws, ws_bytes = _workspace(problem, op, dev, workspace)
     st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
                             _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S0), _ptr(R0), _ptr(o),
-                            _ptr(Sf), _ptr(Rf), _ptr(ws), ws.numel(), _stream_handle(stream))
+                            _ptr(Sf), _ptr(Rf), _ptr(ws), ws_bytes, _stream_handle(stream))
     if st != RLA_OK:
         raise RLAError(st, name)
     return o, Sf, Rf
@@ -300,12 +337,14 @@ def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float 
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
                 S0=S0, R0=R0, dO=dO, dS_final=dS_final, dR_final=dR_final), dev)
-    if dO.dtype != q.dtype:
-        raise TypeError("dO must have the dtype of q, k, v")
+    _check_operands(problem, q, k, v, dict(alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma),
+                    dict(S0=S0, R0=R0, dS_final=dS_final, dR_final=dR_final))
+    if dO is None:
+        raise ValueError("dO is required")
+    _expect("dO", dO, v.shape, q.dtype)
     odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
-    N = problem.num_seqs if cu_seqlens is not None else problem.batch
+    shape = _state_shape(problem)
     if grads is None:
-        shape = (N, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
         grads = dict(dq=torch.empty(q.shape, dtype=odt, device=dev),
                      dk=torch.empty(k.shape, dtype=odt, device=dev),
                      dv=torch.empty(v.shape, dtype=odt, device=dev),
@@ -313,16 +352,30 @@ def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float 
                      dalpha_r=torch.empty_like(alpha_r), dgamma=torch.empty_like(gamma),
                      dS0=torch.empty(shape, dtype=torch.float32, device=dev),
                      dR0=torch.empty(shape, dtype=torch.float32, device=dev))
+    else:   # caller-supplied gradient buffers: every one is written by the library
+        for key in ("dq", "dk", "dv", "dalpha_s", "dbeta", "dalpha_r", "dgamma"):
+            if grads.get(key) is None:
+                raise ValueError("grads[%r] is required" % key)
+    _check({"grads[%s]" % key: t for key, t in grads.items()}, dev)
+    gshape = dict(dq=(q.shape, odt), dk=(q.shape, odt), dv=(v.shape, odt),
+                  dalpha_s=(q.shape[:-1], torch.float32), dbeta=(q.shape[:-1], torch.float32),
+                  dalpha_r=(q.shape[:-1], torch.float32), dgamma=(q.shape[:-1], torch.float32),
+                  dS0=(shape, torch.float32), dR0=(shape, torch.float32),
+                  ddecay_param=((2, q.shape[-2]), torch.float32))
+    for key, t in grads.items():
+        if key not in gshape:
+            raise ValueError("unknown gradient %r" % key)
+        _expect("grads[%s]" % key, t, *gshape[key])
     if ddp is not None:
         grads["ddecay_param"] = ddp
-    ws, need = _workspace(problem, op, dev, workspace)
+    ws, ws_bytes = _workspace(problem, op, dev, workspace)
     g = grads
     st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
                           _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S0), _ptr(R0), _ptr(dO),
                           _ptr(dS_final), _ptr(dR_final), _ptr(g["dq"]), _ptr(g["dk"]),
                           _ptr(g["dv"]), _ptr(g["dalpha_s"]), _ptr(g["dbeta"]),
                           _ptr(g["dalpha_r"]), _ptr(g["dgamma"]), _ptr(g.get("dS0")),
-                          _ptr(g.get("dR0")), _ptr(ws), ws.numel(), _stream_handle(stream))
+                          _ptr(g.get("dR0")), _ptr(ws), ws_bytes, _stream_handle(stream))
     if st != RLA_OK:
         raise RLAError(st, name)
     return g
@@ -360,22 +413,17 @@ def _decode(name, q, k, v, alpha_s, beta, alpha_r, gamma, clip, S_in, R_in, S_ou
                            _check_decay_param(variants, decay_param, q.shape[-2], q.device))
     dev = q.device
     _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
-                S_in=S_in, R_in=R_in, S_out=S_out, R_out=R_out), dev)
-    for t in (alpha_s, beta, alpha_r, gamma, S_in, R_in, S_out, R_out):
-        if t is not None and t.dtype != torch.float32:
-            raise TypeError("gates and states must be float32")
+                S_in=S_in, R_in=R_in, S_out=S_out, R_out=R_out, out=out), dev)
+    _check_operands(problem, q, k, v, dict(alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma),
+                    dict(S_in=S_in, R_in=R_in, S_out=S_out, R_out=R_out))
     shape = (problem.batch, problem.num_heads, problem.head_dim_k, problem.head_dim_v)
     if S_out is None:
         S_out = torch.empty(shape, dtype=torch.float32, device=dev)
     if R_out is None:
         R_out = torch.empty(shape, dtype=torch.float32, device=dev)
-    for nm, t in (("S_in", S_in), ("R_in", R_in), ("S_out", S_out), ("R_out", R_out)):
-        if t is not None and tuple(t.shape) != shape:
-            raise ValueError("%s must have shape %s" % (nm, shape))
     odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
     o = torch.empty(v.shape, dtype=odt, device=dev) if out is None else out
-    if o.dtype != odt or o.shape != v.shape:
-        raise ValueError("out must be %s with shape %s" % (odt, tuple(v.shape)))
+    _expect("out", o, v.shape, odt)
     st = getattr(lib, name)(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
                             _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S_in), _ptr(R_in),
                             _ptr(o), _ptr(S_out), _ptr(R_out), _stream_handle(stream))

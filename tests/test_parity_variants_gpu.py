@@ -10,7 +10,7 @@ import pytest
 import datagen
 import paper_2509_25223_amd as rla
 from tests.gpu_util import (GRAD_KEYS, TOL, gpu_backward, gpu_forward, nudge, oracle_backward,
-                            oracle_forward, rel_err, select)
+                            oracle_forward, rel_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -103,15 +103,17 @@ def test_decode(device, variant, flags):
 
 
 @pytest.mark.slow
-def test_full_training_workload_all_variants_sampled(device):
+@pytest.mark.timeout(900)
+def test_full_training_workload_all_variants(device):
     """The benchmarked training shape (B=4, T=4096, H=16, d=128, bf16) with all
-    three variants on: forward and backward on the GPU at full size, checked
-    on two sequences x two heads against the oracle."""
+    three variants on: forward and backward on the GPU at full size, every
+    element of every (sequence, head) pair against the oracle (the log-cosh
+    residual has no kink, so no input is moved)."""
     import torch
     from tests.gpu_util import dev, host
+    from tests.test_parity_full_gpu import check_all
     flags = TANH | UNG | DEC
     wl = datagen.WORKLOADS[datagen.TRAINING]
-    seqs, heads = [0, 3], [0, 11]
     inp = datagen.make_inputs(wl, seed=305)
     B, T, H, d = wl.B, wl.T, wl.H, wl.dk
     q, k, v, dO = (dev(inp[n], torch.bfloat16, device).view(B, T, H, d) for n in ("q", "k", "v", "dO"))
@@ -120,16 +122,15 @@ def test_full_training_workload_all_variants_sampled(device):
     o, Sf, Rf = rla.rdn_forward(q, k, v, *gates, variants=flags)
     g = rla.rdn_backward(q, k, v, *gates, dO, variants=flags)
     torch.cuda.synchronize()
-    sub = select(inp, seqs, heads)
-    ro, rS, rR = oracle_forward("rdn", sub, variants=flags)
-    ref = oracle_backward("rdn", sub, variants=flags)
-    idx = np.concatenate([np.arange(n * T, (n + 1) * T) for n in seqs])
-    errs = dict(o=rel_err(host(o).reshape(-1, H, d)[idx][:, heads], ro),
-                S=rel_err(host(Sf)[seqs][:, heads], rS), R=rel_err(host(Rf)[seqs][:, heads], rR))
+    got = dict(o=host(o).reshape(-1, H, d), S=host(Sf), R=host(Rf))
     for key in ("dq", "dk", "dv"):
-        errs[key] = rel_err(host(g[key]).reshape(-1, H, d)[idx][:, heads], ref[key])
+        got[key] = host(g[key]).reshape(-1, H, d)
     for key in ("dalpha_s", "dbeta", "dalpha_r", "dgamma"):
-        errs[key] = rel_err(host(g[key]).reshape(-1, H)[idx][:, heads], ref[key])
+        got[key] = host(g[key]).reshape(-1, H)
     for key in ("dS0", "dR0"):
-        errs[key] = rel_err(host(g[key])[seqs][:, heads], ref[key])
-    report("full training shape, all variants", errs, TOL["bf16"])
+        got[key] = host(g[key])
+    ro, rS, rR = oracle_forward("rdn", inp, variants=flags)
+    ref = oracle_backward("rdn", inp, variants=flags)
+    want = dict(o=ro, S=rS, R=rR, **{key: ref[key] for key in GRAD_KEYS})
+    check_all("full training shape, all variants", got, want, inp["cu_seqlens"], TOL["bf16"],
+              token_keys=("o", "dq", "dk", "dv", "dalpha_s", "dbeta", "dalpha_r", "dgamma"))
