@@ -63,6 +63,11 @@
  *   and the gates), so bf16 q and k are expected within fp16's range, as
  *   L2-normalised rows are.  States are carried in fp32.
  *   out_dtype may be fp32 (no output rounding) or bf16 (for bf16 inputs).
+ *   Backward, bf16 inputs: for each (sequence, head) the upstream gradients
+ *   dO, dS_final, dR_final are multiplied by one power of two that brings
+ *   their largest magnitude into [4, 8) and every gradient is multiplied back
+ *   when written (exact), so any loss scale is handled alike; fp16 operands
+ *   then resolve values down to about 2^-16 of that largest magnitude.
  */
 #ifndef RLA_MI355X_RLA_H
 #define RLA_MI355X_RLA_H
@@ -171,7 +176,9 @@ size_t rla_workspace_size(const rla_problem *problem, int op);
  * each later forward/backward call on this thread records events[0] on its
  * stream when its first kernel stage starts and events[i] after stage i,
  * up to num_events events.  Stages: forward = {prep, scan}; backward =
- * {prep, checkpointing forward scan, reverse scan, gradient kernel}.
+ * {prep, checkpointing forward scan (these two are skipped with
+ * RLA_FLAG_USE_SAVED), upstream-gradient maxima (bf16 inputs only), reverse
+ * scan, gradient kernel}.
  * The events are hipEvent_t handles owned by the caller.  NULL turns it off.
  */
 void rla_set_stage_events(void **events, int num_events);

@@ -43,6 +43,7 @@ struct Workspace {
   size_t ckS = 0, ckR = 0, mask = 0, dS = 0, dR = 0, fblk = 0, bblk = 0, total = 0;
   size_t ckS_sc = 0, ckR_sc = 0, dS_sc = 0, dR_sc = 0;
   size_t qh = 0, kh = 0, dqh = 0, dkh = 0, dpart = 0;   // pre-processing
+  size_t gmax = 0, gscale = 0;   // upstream-gradient maxima and scales (bf16 backward)
 };
 
 // recurrent: the decoding step, whose kernel has no fp32 d_k restriction
@@ -144,6 +145,10 @@ Workspace plan(const Problem& pr, int op) {
     const size_t bl = (pr.bf16 ? 2 : 4) * mc * H * kNumBlk * kChunk * (size_t)pr.DV;
     w.fblk = take(bl);
     w.bblk = take(bl);
+    if (pr.bf16) {
+      w.gmax = take(sizeof(uint32_t) * mc * H);
+      w.gscale = take(sizeof(float) * (size_t)pr.N * H);
+    }
   }
   w.total = off;
   return w;
@@ -334,6 +339,12 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
     if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
     if (e == hipSuccess) e = mark_stage(stream, false);
     if (e == hipSuccess) e = launch_fwd_scan(p, pr.bf16, /*write_o=*/false, /*ckpt=*/true, stream);
+    if (e == hipSuccess) e = mark_stage(stream, false);
+  }
+  if (pr.bf16) {   // one power-of-two scale of the upstream gradients per (sequence, head)
+    p.grad_absmax = reinterpret_cast<const uint32_t*>(ws + w.gmax);
+    p.grad_scale = reinterpret_cast<float*>(ws + w.gscale);
+    if (e == hipSuccess) e = launch_grad_absmax(p, reinterpret_cast<uint32_t*>(ws + w.gmax), stream);
     if (e == hipSuccess) e = mark_stage(stream, false);
   }
   if (e == hipSuccess) e = launch_bwd_scan(p, pr.bf16, stream);

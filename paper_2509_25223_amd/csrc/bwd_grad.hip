@@ -39,7 +39,10 @@
 // Precision (bf16 inputs): fp16 MFMA operands with fp32 accumulation.  The
 // scans store the states in fp16 scaled by a power of two per (16 rows, 32
 // columns); here each row is brought to one scale (its largest) when loaded,
-// and a contraction multiplies its result by that scale.
+// and a contraction multiplies its result by that scale.  The reverse scan's
+// blocks and gradient states carry the (sequence, head)'s upstream-gradient
+// scale 2^e (grad_scale); dO is multiplied by it here too, so everything is in
+// one scale, and every gradient written is multiplied by 2^-e.
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -170,6 +173,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   if (!chunk_info(p.st, c, ci)) return;
   const int H = p.H, len = ci.len;
   const int64_t tok = ci.tok;
+  // upstream-gradient scale of this (sequence, head) (a power of two) and its inverse
+  const float sig = p.grad_scale ? p.grad_scale[(int64_t)ci.seq * H + h] : 1.f;
+  const float isig = 1.f / sig;
 
   const IN* qg = reinterpret_cast<const IN*>(p.q);
   const IN* kg = reinterpret_cast<const IN*>(p.k);
@@ -271,14 +277,15 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     vrow[u] = *reinterpret_cast<const uint4*>(vg + ((tok + in_row(t)) * H + h) * (int64_t)DV + j);
     rrow[u] = *reinterpret_cast<const uint4*>(fb + blk_off(c, h, H, 2, DV) + t * DV + j);
   }
-  // K, Q, dO rows: converted to the operand type, stored swizzled
+  // K, Q, dO rows: converted to the operand type (dO multiplied by the
+  // upstream-gradient scale), stored swizzled
   {
-    auto conv = [&](uint4 x) -> uint4 {
+    auto conv = [&](uint4 x, float scale) -> uint4 {
       if constexpr (BF) {
         const u16x8 a = __builtin_bit_cast(u16x8, x);
         f16x8 o;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[e] = (f16)bf2f(a[e]);
+        for (int e = 0; e < 8; ++e) o[e] = (f16)(bf2f(a[e]) * scale);
         return __builtin_bit_cast(uint4, o);
       } else {
         return x;
@@ -287,13 +294,13 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
     for (int u = 0; u < kKV; ++u) {
       const int e = tid + u * NT, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
-      *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(keep_if(kv[u], t < len));
-      *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(keep_if(qv[u], t < len));
+      *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(keep_if(kv[u], t < len), 1.f);
+      *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(keep_if(qv[u], t < len), 1.f);
     }
 #pragma unroll
     for (int u = 0; u < kOV; ++u) {
       const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
-      *reinterpret_cast<uint4*>(tokblk(bDO) + TV::off(t, j)) = conv(keep_if(ov[u], t < len));
+      *reinterpret_cast<uint4*>(tokblk(bDO) + TV::off(t, j)) = conv(keep_if(ov[u], t < len), sig);
     }
   }
   if (tid < kChunk) {
@@ -650,12 +657,14 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       const float a = __shfl_down(ss, off, 64), b = __shfl_down(sr, off, 64);
       if (t + off < 64) { ss += a; sr += b; }
     }
+    ss *= isig;   // out of the upstream-gradient scale
+    sr *= isig;
     // ss, sr: gradients of log aS_t, log aR_t
     float pa = 0.f, pb = 0.f;   // this token's share of d/da_h, d/db_h (pre-activations)
     if (t < len) {
       const int64_t gi = (tok + t) * H + h;
-      const float db = esum[t] + total(sB, t) + total(sZB, t);
-      const float dgm = esum[kChunk + t] + total(sGM, t) + total(sZGM, t);
+      const float db = (esum[t] + total(sB, t) + total(sZB, t)) * isig;
+      const float dgm = (esum[kChunk + t] + total(sGM, t) + total(sZGM, t)) * isig;
       if (vf & kVarGatePreact) {
         // log a = -A softplus(z + Bb): d/dz = -A sigmoid(z + Bb), d/dA = -softplus(z + Bb);
         // beta = sigmoid(z): d/dz = beta (1 - beta), likewise gamma
@@ -721,8 +730,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
         const int t = 16 * tt + acc_row(r);
         if (t < len) {
           const int64_t gi = ((tok + t) * H + h) * (int64_t)DK + 16 * (w + NW * m) + acc_col();
-          dqg[gi] = from_f<OT>(dQ[m][tt][r]);
-          dkg[gi] = from_f<OT>(dK[m][tt][r]);
+          dqg[gi] = from_f<OT>(dQ[m][tt][r] * isig);
+          dkg[gi] = from_f<OT>(dK[m][tt][r] * isig);
         }
       }
 }

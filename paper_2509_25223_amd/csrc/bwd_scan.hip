@@ -22,9 +22,16 @@
 // log-cosh residual dX = (1 - (r / c)^2) gamma dYR, r read from the forward's
 // saved block instead of the clip mask.
 // Every column of dS, dR only sees its own value column, so value blocks are
-// independent here as in the forward.  Operand precision as in the forward
-// scan: K x (dS, dR) uses bf16 K with the gradient state split into bf16
-// hi + lo; all other products use fp16 operands (fp32 for fp32 inputs).
+// independent here as in the forward.  Operand precision (bf16 inputs): K x
+// (dS, dR) takes fp16 K times one fp16 copy of each gradient state scaled by
+// a power of two per chunk; all other products use fp16 operands (fp32 for
+// fp32 inputs).  The upstream gradients dO, dS_T, dR_T of each (sequence,
+// head) enter multiplied by the power of two 2^e that brings their largest
+// magnitude into [4, 8) (from the per-chunk maxima of grad_scale.hip), so the
+// fp16 operands derived from them keep fp16's range for any loss scale; dv,
+// dS0 and dR0 are multiplied by 2^-e when written, and 2^e is left in
+// grad_scale for the gradient kernel, which reads the scaled blocks and
+// checkpoints.
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -192,6 +199,25 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   const int j0 = vb * BV;
   const int64_t state_off = ((int64_t)n * H + h) * DK * DV;
 
+  // scale of the upstream gradients of this (sequence, head): the largest of
+  // the per-chunk maxima, brought into [4, 8) by sig = 2^e (1 if all are zero)
+  float sig = 1.f, isig = 1.f;
+  if (p.grad_absmax) {
+    uint32_t m = 0;
+    for (int c = tid; c < nch; c += kThreads)
+      m = max(m, p.grad_absmax[(int64_t)(si.chunk0 + c) * H + h]);
+    m = wave_absmax_bits(m);
+    smax[w] = m;   // every lane stores the wave-uniform value
+    barrier_lds();
+    m = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
+    barrier_lds();
+    const int be = (int)(m >> 23);
+    const int e = be == 0 ? 0 : min(max(129 - be, -126), 126);
+    sig = exp2_int(e);
+    isig = exp2_int(-e);
+    if (vb == 0 && tid == 0) p.grad_scale[(int64_t)n * H + h] = sig;
+  }
+
   floatx4 dS[IT][JT], dR[IT][JT];
 #pragma unroll
   for (int it = 0; it < IT; ++it)
@@ -200,8 +226,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
-        dS[it][jt][r] = p.dS_fin ? p.dS_fin[state_off + (int64_t)i * DV + j] : 0.f;
-        dR[it][jt][r] = p.dR_fin ? p.dR_fin[state_off + (int64_t)i * DV + j] : 0.f;
+        dS[it][jt][r] = p.dS_fin ? p.dS_fin[state_off + (int64_t)i * DV + j] * sig : 0.f;
+        dR[it][jt][r] = p.dR_fin ? p.dR_fin[state_off + (int64_t)i * DV + j] * sig : 0.f;
       }
   // Copies of the gradient states for the next chunk's K dS, K dR products.
   // bf16 inputs: fp16, scaled by 2^-e with e from the largest magnitude of
@@ -378,7 +404,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) val[jt][r] = __builtin_fmaf(b4[r], tail[jt][r], dx[jt][r]);
+        for (int r = 0; r < 4; ++r) val[jt][r] = __builtin_fmaf(b4[r], tail[jt][r], dx[jt][r]) * isig;
         val[jt] = quad_transpose(val[jt]);
       }
       const int tq = t0 + (lane & 3);
@@ -449,7 +475,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       XT* dbT = blk(bDB_DKS);
 #pragma unroll
       for (int u = 0; u < kOPerThread; ++u)   // lanes write consecutive tokens
-        *TT::ptr(dbT, w * kOPerThread + u, lane) = from_f<XT>(to_f<IN>(on[u]));
+        *TT::ptr(dbT, w * kOPerThread + u, lane) = from_f<XT>(to_f<IN>(on[u]) * sig);
       // gate vectors (lane = token), shared out over the four waves by a
       // wave-uniform index; the chunk-edge factors are stored by every lane
       // of their wave to one address
@@ -664,8 +690,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = w * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
-          if (p.dS0) p.dS0[state_off + (int64_t)i * DV + j] = dS[it][jt][r];
-          if (p.dR0) p.dR0[state_off + (int64_t)i * DV + j] = dR[it][jt][r];
+          if (p.dS0) p.dS0[state_off + (int64_t)i * DV + j] = dS[it][jt][r] * isig;
+          if (p.dR0) p.dR0[state_off + (int64_t)i * DV + j] = dR[it][jt][r] * isig;
         }
   }
 }

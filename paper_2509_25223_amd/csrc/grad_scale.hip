@@ -1,0 +1,71 @@
+// Largest magnitude of the backward's upstream gradients, per (chunk, head):
+// over the chunk's rows of dO and, for the first chunk of a sequence, over
+// that (sequence, head)'s final-state gradients dS_T and dR_T.
+//
+// The backward is linear in (dO, dS_T, dR_T) jointly, and its fp16 operands
+// (dO itself, the gate-weighted copies of it, the blocks dX, dY, dYR) inherit
+// the magnitude of the loss gradient, which in bf16 training without loss
+// scaling is often far below fp16's normal range.  The reverse scan therefore
+// reduces these maxima over each (sequence, head) and multiplies dO, dS_T and
+// dR_T by one power of two 2^e that brings their largest magnitude into
+// [4, 8) (the range of N(0, 1) data); every output of the backward is
+// multiplied by 2^-e when written.  Powers of two are exact, so the result is
+// the unscaled computation wherever no fp16 value underflows or overflows.
+#include "kernels.hpp"
+
+namespace rla {
+
+namespace {
+
+__device__ __forceinline__ uint32_t bf16_mag_bits(uint32_t two) {
+  // the two bf16 values of a 32-bit word as fp32 magnitude bit patterns
+  return max((two & 0x7FFFu) << 16, two & 0x7FFF0000u);
+}
+
+__global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint32_t* out) {
+  __shared__ uint32_t wmax[kWaves];
+  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
+  ChunkInfo ci;
+  if (!chunk_info(p.st, c, ci)) return;
+  const int H = p.H, DV = p.DV, DK = p.DK;
+  uint32_t m = 0;
+  {   // dO rows of the chunk, 16 bytes (8 bf16) per load
+    const int per_row = DV / 8;
+    const uint4* src = reinterpret_cast<const uint4*>(p.dO);
+    for (int e = tid; e < ci.len * per_row; e += kThreads) {
+      const int t = e / per_row, j = e % per_row;
+      const uint4 x = src[((ci.tok + t) * H + h) * (int64_t)per_row + j];
+      m = max(m, max(max(bf16_mag_bits(x.x), bf16_mag_bits(x.y)),
+                     max(bf16_mag_bits(x.z), bf16_mag_bits(x.w))));
+    }
+  }
+  const SeqInfo si = seq_info(p.st, ci.seq);
+  if (ci.tok == si.start) {   // first chunk: the final-state gradients of (sequence, head)
+    const int64_t off = ((int64_t)ci.seq * H + h) * DK * DV;
+    const float* st[2] = {p.dS_fin, p.dR_fin};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      if (!st[s]) continue;
+      const float4* src = reinterpret_cast<const float4*>(st[s] + off);
+      for (int e = tid; e < DK * DV / 4; e += kThreads) {
+        const float4 x = src[e];
+        m = max(m, max(max(__float_as_uint(x.x) & 0x7FFFFFFFu, __float_as_uint(x.y) & 0x7FFFFFFFu),
+                       max(__float_as_uint(x.z) & 0x7FFFFFFFu, __float_as_uint(x.w) & 0x7FFFFFFFu)));
+      }
+    }
+  }
+  m = wave_absmax_bits(m);
+  if ((tid & 63) == 0) wmax[w] = m;
+  __syncthreads();
+  if (tid == 0) out[(int64_t)c * H + h] = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+}
+
+}  // namespace
+
+hipError_t launch_grad_absmax(const OpParams& p, uint32_t* out, hipStream_t stream) {
+  if (p.max_chunks == 0) return hipSuccess;
+  hipLaunchKernelGGL(grad_absmax_kernel, dim3(p.max_chunks, p.H), dim3(kThreads), 0, stream, p, out);
+  return hipGetLastError();
+}
+
+}  // namespace rla

@@ -86,6 +86,13 @@ struct OpParams {
   float* dgamma = nullptr;
   float* dS0 = nullptr;
   float* dR0 = nullptr;
+  // bf16 inputs: per (chunk, head) largest magnitude of dO (and, for a
+  // sequence's first chunk, of dS_T and dR_T) as fp32 bits, [max_chunks][H];
+  // and the power-of-two scale of the upstream gradients of each (sequence,
+  // head), [nseq][H], written by the reverse scan, read by the gradient kernel
+  // (NULL: scale 1)
+  const uint32_t* grad_absmax = nullptr;
+  float* grad_scale = nullptr;
 };
 
 // Builds SeqInfo / ChunkInfo / order tables from device cu_seqlens.
@@ -101,6 +108,10 @@ hipError_t launch_prep(const OpParams& p, bool bf16, hipStream_t stream);
 // states, clip masks and the U, UR, r blocks for the backward.
 hipError_t launch_fwd_scan(const OpParams& p, bool bf16, bool write_o, bool ckpt,
                            hipStream_t stream);
+
+// Per (chunk, head) largest magnitude of the upstream gradients (dO; dS_T and
+// dR_T folded into a sequence's first chunk) into out[max_chunks][H].
+hipError_t launch_grad_absmax(const OpParams& p, uint32_t* out, hipStream_t stream);
 
 // Reverse state-gradient scan (RDN / RLA); also writes dv and the dX, dY,
 // dYR blocks.

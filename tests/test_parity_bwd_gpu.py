@@ -76,6 +76,31 @@ def test_varlen_edges(device, variant, dtype, d):
 
 
 @pytest.mark.parametrize("variant", ["rdn", "rla"])
+@pytest.mark.parametrize("scale", ["2^-30", "2^-20", "2^12", "chunkwise"])
+def test_upstream_gradient_scale(device, variant, scale):
+    """The upstream gradients dO, dS_T, dR_T multiplied by 2^-30, 2^-20, 2^12
+    (exact in bf16 and fp32; bf16 training without loss scaling sees the small
+    ones), or dO shrinking 4x per chunk along each sequence: every gradient
+    scales with them, so the relative bound applies unchanged.  Unscaled fp16
+    operands would flush the small cases to zero and overflow the large one."""
+    lens = [300, 70]
+    wl = datagen.small(variant + "_fwdbwd", "bf16", lens, H=2, d=128)
+    inp = datagen.make_inputs(wl, seed=205)
+    S0, R0 = datagen.random_states(12, len(lens), 2, 128, 128)
+    dSf, dRf = datagen.random_states(13, len(lens), 2, 128, 128, scale=1.0)
+    if scale == "chunkwise":
+        cu = inp["cu_seqlens"]
+        f = np.concatenate([4.0 ** -(np.arange(cu[n + 1] - cu[n]) // 64) for n in range(len(lens))])
+        inp["dO"] = (inp["dO"] * f[:, None, None]).astype(np.float32)
+        dSf = dRf = None
+    else:
+        f = 2.0 ** int(scale[2:])
+        inp["dO"] = (inp["dO"] * f).astype(np.float32)
+        dSf, dRf = (dSf * f).astype(np.float32), (dRf * f).astype(np.float32)
+    check(variant, inp, "bf16", device, S0=S0, R0=R0, dSf=dSf, dRf=dRf, label="dO x %s" % scale)
+
+
+@pytest.mark.parametrize("variant", ["rdn", "rla"])
 def test_bf16_outputs(device, variant):
     """dq, dk, dv returned in bf16 (out_dtype): the same gradients rounded once
     to bf16, compared with the bound after setting that rounding aside
