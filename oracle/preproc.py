@@ -9,9 +9,9 @@ its architecture figure) feeds the recurrences with
             the decays of S and R; pass the same pre-activations for both to
             tie the decays as the paper does);
   beta_t = sigmoid(z^beta_t),  gamma_t = sigmoid(z^gamma_t).
-With bf16 inputs the operator stores the normalised rows in bf16 once
-(``qk_round="bf16"``: round to nearest even), as the recurrences of the plain
-path read bf16 inputs; the gradient passes that rounding straight through.
+Every step is computed in fp64 exactly as defined, with no rounding of the
+normalised rows: whatever precision an implementation keeps them in is part
+of the error measured against this oracle.
 ``forward`` applies these steps to raw inputs and calls the recurrent oracle;
 ``backward`` calls the recurrent oracle's adjoint on the transformed inputs
 and applies the chain rule of each step, so it returns gradients with respect
@@ -38,14 +38,6 @@ def _softplus(x):
 
 
 NORM_EPS = 1e-12
-
-
-def _round_bf16(x):
-    """Round-to-nearest-even onto the bf16 grid (the upper 16 bits of fp32)."""
-    a = np.ascontiguousarray(np.asarray(x, np.float64).astype(np.float32))
-    u = a.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
 
 
 def qk_transform(x):
@@ -82,13 +74,10 @@ def decay_from_preact(z, a, b):
     return np.exp(-A * _softplus(z + Bb))
 
 
-def transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b, qk_norm=True, gate_preact=True,
-                     qk_round=None):
+def transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b, qk_norm=True, gate_preact=True):
     """The operator's inputs (q, k, alpha_s, beta, alpha_r, gamma) from raw ones."""
     if qk_norm:
         q, k = qk_transform(q), qk_transform(k)
-        if qk_round == "bf16":
-            q, k = _round_bf16(q), _round_bf16(k)
     if gate_preact:
         return (q, k, decay_from_preact(z_as, decay_a, decay_b), _sigmoid(np.asarray(z_b, np.float64)),
                 decay_from_preact(z_ar, decay_a, decay_b), _sigmoid(np.asarray(z_g, np.float64)))
@@ -96,23 +85,22 @@ def transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b, qk_norm=True,
 
 
 def forward(variant, q, k, v, z_as, z_b, z_ar, z_g, decay_a=None, decay_b=None, clip=1.0,
-            S0=None, R0=None, cu_seqlens=None, flags=0, qk_norm=True, gate_preact=True,
-            qk_round=None):
+            S0=None, R0=None, cu_seqlens=None, flags=0, qk_norm=True, gate_preact=True):
     """Forward from raw inputs: (o, S_final, R_final)."""
     qq, kk, aS, bb, aR, gg = transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b,
-                                             qk_norm, gate_preact, qk_round)
+                                             qk_norm, gate_preact)
     return oracle.forward(variant, qq, kk, v, aS, bb, aR, gg, clip=clip, S0=S0, R0=R0,
                           cu_seqlens=cu_seqlens, flags=flags)
 
 
 def backward(variant, q, k, v, z_as, z_b, z_ar, z_g, dO, decay_a=None, decay_b=None, clip=1.0,
              S0=None, R0=None, dS_final=None, dR_final=None, cu_seqlens=None, flags=0,
-             qk_norm=True, gate_preact=True, qk_round=None):
+             qk_norm=True, gate_preact=True):
     """Gradients w.r.t. the raw inputs: dq, dk (raw q, k), dv, dalpha_s, dbeta,
     dalpha_r, dgamma (pre-activations), dS0, dR0 and, with gate_preact,
     ddecay_a, ddecay_b [H] (summed over every token of both decays)."""
     qq, kk, aS, bb, aR, gg = transform_inputs(q, k, z_as, z_b, z_ar, z_g, decay_a, decay_b,
-                                             qk_norm, gate_preact, qk_round)
+                                             qk_norm, gate_preact)
     g = oracle.backward(variant, qq, kk, v, aS, bb, aR, gg, dO, clip=clip, S0=S0, R0=R0,
                         dS_final=dS_final, dR_final=dR_final, cu_seqlens=cu_seqlens, flags=flags)
     out = dict(g)

@@ -116,7 +116,7 @@ Workspace plan(const Problem& pr, int op) {
   }
   w.gates = take(sizeof(float) * mc * H * kGateBlock);
   const bool bwd = op == RLA_OP_RDN_BACKWARD || op == RLA_OP_RLA_BACKWARD;
-  if (pr.vflags & kVarQkNorm) {   // normalised q, k (input type); backward: their fp32 gradients
+  if (pr.vflags & kVarQkNorm) {   // normalised q, k (fp16 / fp32); backward: their fp32 gradients
     const size_t rows = (size_t)pr.ntok * H * (size_t)pr.DK;
     w.qh = take((pr.bf16 ? 2 : 4) * rows);
     w.kh = take((pr.bf16 ? 2 : 4) * rows);
@@ -259,6 +259,7 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
     e = launch_qk_norm_fwd(q, k, ws + w.qh, ws + w.kh, pr.ntok * pr.H, (int)pr.DK, pr.bf16, stream);
     p.q = ws + w.qh;
     p.k = ws + w.kh;
+    p.qk_f16 = pr.bf16 ? 1 : 0;
   }
   if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
   if (e == hipSuccess) e = mark_stage(stream, false);
@@ -320,6 +321,7 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
       e = launch_qk_norm_fwd(q, k, ws + w.qh, ws + w.kh, pr.ntok * pr.H, (int)pr.DK, pr.bf16, stream);
     p.q = ws + w.qh;
     p.k = ws + w.kh;
+    p.qk_f16 = pr.bf16 ? 1 : 0;
     // the gradient kernel writes d(normalised q, k) in fp32 into the workspace
     p.dq = ws + w.dqh;
     p.dk = ws + w.dkh;

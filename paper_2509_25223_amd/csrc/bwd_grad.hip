@@ -113,8 +113,8 @@ __device__ __forceinline__ void put_cols(float* dst, int s0, const float (&v)[4]
   dst[s0 + (threadIdx.x & 15)] = s;
 }
 
-// VAR: an instance that reads the variant flags (the default instance
-// compiles them away)
+// VAR: an instance that reads the variant flags and qk_f16 (the default
+// instance compiles them away)
 template <typename IN, int DK, int DV, bool RDN, typename OT, bool VAR>
 __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   typedef GradLayout<IN, DK, DV> L;
@@ -294,8 +294,13 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
     for (int u = 0; u < kKV; ++u) {
       const int e = tid + u * NT, t = e / (DK / kE), i = (e % (DK / kE)) * kE;
-      *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(keep_if(kv[u], t < len), 1.f);
-      *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(keep_if(qv[u], t < len), 1.f);
+      if (VAR && p.qk_f16) {   // the pre-processing's fp16 rows
+        *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = keep_if(kv[u], t < len);
+        *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = keep_if(qv[u], t < len);
+      } else {
+        *reinterpret_cast<uint4*>(Kl + TK::off(t, i)) = conv(keep_if(kv[u], t < len), 1.f);
+        *reinterpret_cast<uint4*>(Ql + TK::off(t, i)) = conv(keep_if(qv[u], t < len), 1.f);
+      }
     }
 #pragma unroll
     for (int u = 0; u < kOV; ++u) {
@@ -739,8 +744,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 template <typename IN, int DK, int DV, bool RDN, typename OT>
 hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
   typedef GradLayout<IN, DK, DV> L;
-  auto kern = (p.vflags & (kVarOperator | kVarGatePreact)) ? bwd_grad_kernel<IN, DK, DV, RDN, OT, true>
-                                                            : bwd_grad_kernel<IN, DK, DV, RDN, OT, false>;
+  auto kern = ((p.vflags & (kVarOperator | kVarGatePreact)) || p.qk_f16)
+                  ? bwd_grad_kernel<IN, DK, DV, RDN, OT, true>
+                  : bwd_grad_kernel<IN, DK, DV, RDN, OT, false>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;

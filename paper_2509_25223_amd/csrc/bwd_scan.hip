@@ -117,8 +117,8 @@ __device__ __forceinline__ void store_state_copy(T* dst, int r0, int c0, floatx4
   }
 }
 
-// VAR: an instance that reads the variant flags (the default instance
-// compiles them away)
+// VAR: an instance that reads the variant flags and qk_f16 (the default
+// instance compiles them away)
 template <typename IN, int DK, int BV, bool RDN, bool VAR>
 __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   typedef BwdScanLayout<IN, DK, BV, RDN, VAR> L;
@@ -457,10 +457,15 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
           const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
           const u16x8 qv = __builtin_bit_cast(u16x8, Qn[s2]);
           f16x8 kh, qh;
+          if (VAR && p.qk_f16) {   // the pre-processing's fp16 rows
+            kh = __builtin_bit_cast(f16x8, kv);
+            qh = __builtin_bit_cast(f16x8, qv);
+          } else {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            kh[e] = (f16)bf2f(kv[e]);
-            qh[e] = (f16)bf2f(qv[e]);
+            for (int e = 0; e < 8; ++e) {
+              kh[e] = (f16)bf2f(kv[e]);
+              qh[e] = (f16)bf2f(qv[e]);
+            }
           }
           const int i = s2 * 32 + (lane >> 4) * 8;
           Kf[s2] = kh;
@@ -713,8 +718,8 @@ hipError_t launch_bwd_scan_v(const OpParams& p, hipStream_t stream) {
 
 template <typename IN, int DK, int BV, bool RDN>
 hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
-  return (p.vflags & kVarOperator) ? launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream)
-                  : launch_bwd_scan_v<IN, DK, BV, RDN, false>(p, stream);
+  return ((p.vflags & kVarOperator) || p.qk_f16) ? launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream)
+                                                 : launch_bwd_scan_v<IN, DK, BV, RDN, false>(p, stream);
 }
 
 }  // namespace

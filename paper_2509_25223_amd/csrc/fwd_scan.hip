@@ -22,7 +22,10 @@
 // Operand precision (bf16 inputs; fp32 inputs use fp32 MFMA throughout):
 //   K, Q x state: bf16 K/Q fragments (exact inputs, loaded from HBM straight
 //     into registers) times the state split as bf16 hi + bf16 lo (~16-bit
-//     mantissa, fp32 range): two MFMAs per step.
+//     mantissa, fp32 range): two MFMAs per step.  When q, k are the fp16 rows
+//     of the in-operator normalisation (qk_f16, variant instance), each row
+//     is split as bf16 hi + bf16 lo too (exact: 11 = 8 + 3 bits) and a third
+//     MFMA adds lo x state-hi.
 //   everything else: fp16 operands (intermediates bounded by the data, clip
 //     and gates), fp32 accumulation.
 // With `CKPT` the chunk-start states, the clip mask |x| <= c and the blocks
@@ -106,8 +109,8 @@ __device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0,
   }
 }
 
-// VAR: an instance that reads the variant flags (the default instance
-// compiles them away, so the boxed operator keeps its register budget)
+// VAR: an instance that reads the variant flags and qk_f16 (the default
+// instance compiles them away, so the boxed operator keeps its register budget)
 template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT, bool VAR>
 __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
@@ -150,6 +153,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   float* gout = VAR ? edge + kChunk : ggm;
   // per-token factors of S0 in the residual's and the base read-out's terms
   const int vf = VAR ? p.vflags : 0;
+  const bool qk16 = VAR && BF && p.qk_f16;   // q, k rows are fp16
   const float* ekp = (vf & kVarDecayed) ? egs : egsp;
   const float* eqb = (vf & kVarUngated) ? egsp : egs;
   const bool tanh_resid = (vf & kVarTanh) != 0;
@@ -267,6 +271,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     // ---- commit: K, Q fragments from the prefetch registers, K^T (XT) and
     //      the gate-derived vectors into LDS ----
     typename MI::frag Kf[KS_STEPS], Qf[KS_STEPS];
+    typename MI::frag Klo[VAR ? KS_STEPS : 1], Qlo[VAR ? KS_STEPS : 1];   // fp16 rows: bf16 residuals
     {
       const int t = 16 * w + (lane & 15);
 #pragma unroll
@@ -276,8 +281,31 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         if constexpr (BF) {   // row t, 8 columns: one 16-byte store
           const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s2]);
           f16x8 kh;
+          if constexpr (VAR) {
+            if (qk16) {   // fp16 rows: K^T as is; hi + lo bf16 fragments for the state products
+              kh = __builtin_bit_cast(f16x8, kv);
+              const f16x8 qh = __builtin_bit_cast(f16x8, Qf[s2]);
+              u16x8 khi, klo, qhi, qlo;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
+              for (int e = 0; e < 8; ++e) {
+                const float kx = (float)kh[e], qx = (float)qh[e];
+                khi[e] = f2bf(kx);
+                klo[e] = f2bf(kx - bf2f(khi[e]));
+                qhi[e] = f2bf(qx);
+                qlo[e] = f2bf(qx - bf2f(qhi[e]));
+              }
+              Kf[s2] = __builtin_bit_cast(typename MI::frag, khi);
+              Klo[s2] = __builtin_bit_cast(typename MI::frag, klo);
+              Qf[s2] = __builtin_bit_cast(typename MI::frag, qhi);
+              Qlo[s2] = __builtin_bit_cast(typename MI::frag, qlo);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
+          }
           *reinterpret_cast<f16x8*>(TK::ptr(KT, t, s2 * 32 + (lane >> 4) * 8)) = kh;
         } else {
           *TT::ptr(KT, s2 * 4 + (lane >> 4), t) = Kf[s2];
@@ -322,6 +350,14 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
         mma_rega_tile<IN, DK, TSC>(QS[jt], Qf, Slo, jt * 16);
         mma_rega_tile<IN, DK, TSC>(KR[jt], Kf, Rlo, jt * 16);
         mma_rega_tile<IN, DK, TSC>(QR[jt], Qf, Rlo, jt * 16);
+        if constexpr (VAR) {
+          if (qk16) {
+            mma_rega_tile<IN, DK, TSC>(KS[jt], Klo, Shi, jt * 16);
+            mma_rega_tile<IN, DK, TSC>(QS[jt], Qlo, Shi, jt * 16);
+            mma_rega_tile<IN, DK, TSC>(KR[jt], Klo, Rhi, jt * 16);
+            mma_rega_tile<IN, DK, TSC>(QR[jt], Qlo, Rhi, jt * 16);
+          }
+        }
       }
     }
     float vloc[JT][4];
@@ -562,8 +598,9 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
 template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT>
 hipError_t launch_fwd_t(const OpParams& p, hipStream_t stream) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
-  auto kern = (p.vflags & kVarOperator) ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
-                       : fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, false>;
+  auto kern = ((p.vflags & kVarOperator) || p.qk_f16)
+                  ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
+                  : fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, false>;
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;

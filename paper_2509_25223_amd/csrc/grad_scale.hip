@@ -22,22 +22,32 @@ __device__ __forceinline__ uint32_t bf16_mag_bits(uint32_t two) {
   return max((two & 0x7FFFu) << 16, two & 0x7FFF0000u);
 }
 
+template <int DV>
 __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint32_t* out) {
   __shared__ uint32_t wmax[kWaves];
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
+  // heads vary fastest over consecutive workgroups, which then read one
+  // contiguous stretch of dO (the chunk's rows of every head)
+  const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
   ChunkInfo ci;
   if (!chunk_info(p.st, c, ci)) return;
-  const int H = p.H, DV = p.DV, DK = p.DK;
+  const int H = p.H, DK = p.DK;
   uint32_t m = 0;
-  {   // dO rows of the chunk, 16 bytes (8 bf16) per load
-    const int per_row = DV / 8;
+  {   // dO rows of the chunk, 16 bytes (8 bf16) per load, all issued at once;
+      // rows past the chunk's end re-read its last row (no effect on a maximum)
+    constexpr int kPerRow = DV / 8;
+    constexpr int kIter = kChunk * kPerRow / kThreads;
+    static_assert(kIter * kThreads == kChunk * kPerRow, "whole rows per step");
     const uint4* src = reinterpret_cast<const uint4*>(p.dO);
-    for (int e = tid; e < ci.len * per_row; e += kThreads) {
-      const int t = e / per_row, j = e % per_row;
-      const uint4 x = src[((ci.tok + t) * H + h) * (int64_t)per_row + j];
-      m = max(m, max(max(bf16_mag_bits(x.x), bf16_mag_bits(x.y)),
-                     max(bf16_mag_bits(x.z), bf16_mag_bits(x.w))));
+    uint4 x[kIter];
+#pragma unroll
+    for (int u = 0; u < kIter; ++u) {
+      const int e = tid + u * kThreads, t = min(e / kPerRow, ci.len - 1), j = e % kPerRow;
+      x[u] = src[((ci.tok + t) * H + h) * (int64_t)kPerRow + j];
     }
+#pragma unroll
+    for (int u = 0; u < kIter; ++u)
+      m = max(m, max(max(bf16_mag_bits(x[u].x), bf16_mag_bits(x[u].y)),
+                     max(bf16_mag_bits(x[u].z), bf16_mag_bits(x[u].w))));
   }
   const SeqInfo si = seq_info(p.st, ci.seq);
   if (ci.tok == si.start) {   // first chunk: the final-state gradients of (sequence, head)
@@ -47,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint3
     for (int s = 0; s < 2; ++s) {
       if (!st[s]) continue;
       const float4* src = reinterpret_cast<const float4*>(st[s] + off);
-      for (int e = tid; e < DK * DV / 4; e += kThreads) {
+      for (int e = tid; e < DK * (DV / 4); e += kThreads) {
         const float4 x = src[e];
         m = max(m, max(max(__float_as_uint(x.x) & 0x7FFFFFFFu, __float_as_uint(x.y) & 0x7FFFFFFFu),
                        max(__float_as_uint(x.z) & 0x7FFFFFFFu, __float_as_uint(x.w) & 0x7FFFFFFFu)));
@@ -64,7 +74,8 @@ __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint3
 
 hipError_t launch_grad_absmax(const OpParams& p, uint32_t* out, hipStream_t stream) {
   if (p.max_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(grad_absmax_kernel, dim3(p.max_chunks, p.H), dim3(kThreads), 0, stream, p, out);
+  auto kern = p.DV == 128 ? grad_absmax_kernel<128> : grad_absmax_kernel<64>;
+  hipLaunchKernelGGL(kern, dim3(p.H, p.max_chunks), dim3(kThreads), 0, stream, p, out);
   return hipGetLastError();
 }
 

@@ -35,6 +35,7 @@ struct OpParams {
   int32_t vflags = 0;           // kVar* bits
   int32_t out_bf16 = 0;         // o, dq, dk, dv in bf16 (else fp32)
   int32_t max_chunks = 0;       // upper bound on chunks (grid size of chunk-parallel kernels)
+  int32_t qk_f16 = 0;           // bf16 inputs: q, k are fp16 rows (the pre-processing's output)
   SeqTable st{};
 
   const void* q = nullptr;

@@ -5,7 +5,8 @@
 // chunk form; padding rows beyond the chunk's length carry k = q = 0,
 // beta = gamma = 0 and decay 1, which makes them exact no-ops):
 //   g_t = sum_{j<=t} log aS_j,  h_t = sum_{j<=t} log aR_j
-//   Gram G = K K^T and scores P = Q K^T on bf16 (or fp32) MFMA
+//   Gram G = K K^T and scores P = Q K^T on bf16 (or fp32) MFMA; fp16 MFMA
+//   for the fp16 rows of the in-operator q, k normalisation
 //   MG[t][s] = e^{g_{t-1}-g_s} G[t][s]  (s < t)   -> S_{t-1} k_t read-out
 //   MP[t][s] = e^{g_t - g_s}   P[t][s]  (s < t)   -> aS_t S_{t-1} q_t read-out
 //   MR[t][s] = e^{h_t - h_s}   P[t][s]  (s <= t)  -> R_t q_t read-out
@@ -207,15 +208,23 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
     gate_out[192 + tid] = gm[tid];
   }
 
-  // ---- G = K K^T and P = Q K^T: wave w owns rows 16w..16w+15 ----
+  // ---- G = K K^T and P = Q K^T: wave w owns rows 16w..16w+15 (fp16 MFMA
+  //      when q, k are the pre-processing's fp16 rows) ----
   const int w = tid >> 6;
   floatx4 G[4], P[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) {
     G[ct] = zero4();
     P[ct] = zero4();
-    mma_tile<T, DK, true, true>(G[ct], Kc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
-    mma_tile<T, DK, true, true>(P[ct], Qc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
+    if (sizeof(T) == 2 && p.qk_f16) {
+      const f16* Kh = reinterpret_cast<const f16*>(Kc);
+      const f16* Qh = reinterpret_cast<const f16*>(Qc);
+      mma_tile<f16, DK, true, true>(G[ct], Kh + 16 * w * L::kLdK, L::kLdK, Kh + 16 * ct * L::kLdK, L::kLdK);
+      mma_tile<f16, DK, true, true>(P[ct], Qh + 16 * w * L::kLdK, L::kLdK, Kh + 16 * ct * L::kLdK, L::kLdK);
+    } else {
+      mma_tile<T, DK, true, true>(G[ct], Kc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
+      mma_tile<T, DK, true, true>(P[ct], Qc + 16 * w * L::kLdK, L::kLdK, Kc + 16 * ct * L::kLdK, L::kLdK);
+    }
   }
   __syncthreads();   // Kc/Qc dead: region 0 becomes As/Ar
 

@@ -3,14 +3,18 @@
 // decay re-parameterisation's per-head gradients.
 //
 // qk_norm_fwd: one wave per token-head row, y = SiLU(x) = x sigmoid(x),
-//   x_hat = y / max(||y||, 1e-12), stored in the input type (the chunked
-//   kernels then read x_hat as they would read normalised inputs).
+//   x_hat = y / max(||y||, 1e-12), stored as fp32 for fp32 inputs and as fp16
+//   for bf16 inputs (|x_hat| <= 1, so fp16's 11 significant bits lose
+//   nothing to range; bf16's 8 would cost about 2e-2 of max|error|/RMS on o
+//   by themselves); the chunked kernels read these rows in place of q, k.
 // qk_norm_bwd: dx = SiLU'(x) (dx_hat - x_hat (x_hat . dx_hat)) / ||y||, with
 //   SiLU'(x) = s (1 + x (1 - s)), s = sigmoid(x); below the 1e-12 floor the
 //   normalisation is the fixed scale 1e12 and dy = dx_hat 1e12.  x_hat is
 //   recomputed in fp32 from the raw row.
 // decay_grad_reduce: one workgroup per head sums the per-chunk partials in a
 //   fixed order (deterministic).
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace rla {
@@ -30,17 +34,17 @@ __device__ __forceinline__ float wave_allsum(float v) {
   return v;
 }
 
-template <typename IN, int DK>
+template <typename IN, typename NT, int DK>
 __global__ __launch_bounds__(kThreads) void qk_norm_fwd_kernel(const IN* __restrict__ q,
                                                                const IN* __restrict__ k,
-                                                               IN* __restrict__ qh, IN* __restrict__ kh,
+                                                               NT* __restrict__ qh, NT* __restrict__ kh,
                                                                int64_t rows) {
   constexpr int PL = DK / 64;   // values per lane
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * kWaves + w;
   if (row >= rows) return;
   const IN* src = (blockIdx.y == 0 ? q : k) + row * DK + lane * PL;
-  IN* dst = (blockIdx.y == 0 ? qh : kh) + row * DK + lane * PL;
+  NT* dst = (blockIdx.y == 0 ? qh : kh) + row * DK + lane * PL;
   float y[PL], ss = 0.f;
 #pragma unroll
   for (int e = 0; e < PL; ++e) {
@@ -50,7 +54,7 @@ __global__ __launch_bounds__(kThreads) void qk_norm_fwd_kernel(const IN* __restr
   }
   const float inv = 1.f / fmaxf(sqrtf(wave_allsum(ss)), kNormEps);
 #pragma unroll
-  for (int e = 0; e < PL; ++e) dst[e] = from_f<IN>(y[e] * inv);
+  for (int e = 0; e < PL; ++e) dst[e] = from_f<NT>(y[e] * inv);
 }
 
 template <typename IN, typename OT, int DK>
@@ -118,10 +122,11 @@ __global__ __launch_bounds__(kThreads) void decay_grad_reduce_kernel(const float
 
 template <typename IN, int DK>
 hipError_t qk_fwd_t(const void* q, const void* k, void* qh, void* kh, int64_t rows, hipStream_t s) {
+  typedef typename std::conditional<sizeof(IN) == 2, f16, float>::type NT;
   const dim3 grid((unsigned)((rows + kWaves - 1) / kWaves), 2);
-  hipLaunchKernelGGL((qk_norm_fwd_kernel<IN, DK>), grid, dim3(kThreads), 0, s,
+  hipLaunchKernelGGL((qk_norm_fwd_kernel<IN, NT, DK>), grid, dim3(kThreads), 0, s,
                      reinterpret_cast<const IN*>(q), reinterpret_cast<const IN*>(k),
-                     reinterpret_cast<IN*>(qh), reinterpret_cast<IN*>(kh), rows);
+                     reinterpret_cast<NT*>(qh), reinterpret_cast<NT*>(kh), rows);
   return hipGetLastError();
 }
 

@@ -1,7 +1,8 @@
 """GPU parity of the in-operator input pre-processing (SiLU + L2 norm of q, k;
 gates from pre-activations with per-head Mamba-2 decay parameters) against
-the fp64 oracle's pre-processing (oracle/preproc.py): forward, backward
-(recomputing and saved), the (a, b) gradients, and decoding."""
+the fp64 oracle's pre-processing (oracle/preproc.py), the same oracle for
+every entry point: forward, backward (recomputing and saved), the (a, b)
+gradients, and decoding."""
 import math
 
 import numpy as np
@@ -42,9 +43,11 @@ def raw_inputs(seed, lens, H, d, dtype, flags, grads=False):
     return inp, dp
 
 
-def oracle_args(inp, dp, flags, dtype="bf16"):
+def oracle_args(inp, dp, flags):
+    """The one fp64 pre-processing oracle (no rounding of the normalised rows)
+    for every entry point: chunked forward, backward and decoding alike."""
     return dict(decay_a=dp[0], decay_b=dp[1], qk_norm=bool(flags & QKN), gate_preact=bool(flags & PRE),
-                flags=oracle_flags(flags), qk_round="bf16" if dtype == "bf16" else None)
+                flags=oracle_flags(flags))
 
 
 def nudged(variant, inp, dp, flags, dtype, S0=None, R0=None):
@@ -53,8 +56,7 @@ def nudged(variant, inp, dp, flags, dtype, S0=None, R0=None):
         return inp
     qq, kk, aS, bb, aR, gg = preproc.transform_inputs(inp["q"], inp["k"], inp["alpha_s"], inp["beta"],
                                                        inp["alpha_r"], inp["gamma"], dp[0], dp[1],
-                                                       bool(flags & QKN), bool(flags & PRE),
-                                                       "bf16" if dtype == "bf16" else None)
+                                                       bool(flags & QKN), bool(flags & PRE))
     v, _ = oracle.nudge_margin(variant, qq, kk, inp["v"], aS, bb, aR, gg, clip=1.0, S0=S0, R0=R0,
                                cu_seqlens=inp["cu_seqlens"], margin=2e-2 if dtype == "bf16" else 1e-4,
                                grid="bf16" if dtype == "bf16" else "f32", flags=oracle_flags(flags))
@@ -94,7 +96,7 @@ def test_forward(device, variant, dtype, d, flags):
     torch.cuda.synchronize()
     ro, rS, rR = preproc.forward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
                                  inp["alpha_r"], inp["gamma"], S0=S0, R0=R0,
-                                 cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags, dtype))
+                                 cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags))
     report("fwd %s %s %s" % (variant, dtype, NAMES[flags]),
            dict(o=rel_err(host(o), ro), S=rel_err(host(Sf), rS), R=rel_err(host(Rf), rR)), TOL[dtype])
 
@@ -116,7 +118,7 @@ def test_backward(device, variant, dtype, d, flags):
     torch.cuda.synchronize()
     ref = preproc.backward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
                            inp["alpha_r"], inp["gamma"], inp["dO"], S0=S0, R0=R0,
-                           cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags, dtype))
+                           cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags))
     errs = {}
     for key in GRAD_KEYS:
         a = host(g[key])
@@ -169,7 +171,6 @@ def test_decode(device, variant):
     torch.cuda.synchronize()
     ro, rS, rR = preproc.forward(variant, inp["q"], inp["k"], inp["v"], inp["alpha_s"], inp["beta"],
                                  inp["alpha_r"], inp["gamma"], S0=S0, R0=R0,
-                                 cu_seqlens=inp["cu_seqlens"],
-                                 **oracle_args(inp, dp, flags, "fp32 rows"))   # decoding keeps the rows in fp32
+                                 cu_seqlens=inp["cu_seqlens"], **oracle_args(inp, dp, flags))
     report("decode %s both" % variant, dict(o=rel_err(host(o).reshape(-1, H, d), ro),
                                             S=rel_err(host(Sd), rS), R=rel_err(host(Rd), rR)), TOL["bf16"])
