@@ -96,6 +96,10 @@ struct OpParams {
   float* grad_scale = nullptr;
 };
 
+// Zeroes `bytes` (a multiple of 4) at dst with a kernel rather than a memset
+// node, so that a caller may capture the call in a HIP graph.
+hipError_t launch_zero_fill(void* dst, size_t bytes, hipStream_t stream);
+
 // Builds SeqInfo / ChunkInfo / order tables from device cu_seqlens.
 hipError_t launch_seq_table(const int32_t* cu, int32_t nseq, int64_t ntok, int32_t max_chunks,
                             SeqInfo* seqs, ChunkInfo* chunks, int32_t* nchunks, int32_t* order,

@@ -109,7 +109,29 @@ __global__ __launch_bounds__(kThreads) void chunk_table_kernel(const SeqInfo* se
   chunks[c] = ChunkInfo{si.start + (int64_t)j * kChunk, rem < kChunk ? rem : kChunk, lo};
 }
 
+// dst[0 .. n) = 0 for n 4-byte words (16-byte words when aligned).
+template <typename W>
+__global__ __launch_bounds__(kThreads) void zero_fill_kernel(W* dst, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) dst[i] = W{};
+}
+
 }  // namespace
+
+hipError_t launch_zero_fill(void* dst, size_t bytes, hipStream_t stream) {
+  if (bytes == 0) return hipSuccess;
+  const bool wide = ((uintptr_t)dst % 16 == 0) && (bytes % 16 == 0);
+  const int64_t n = (int64_t)(bytes / (wide ? 16 : 4));
+  const int64_t blocks = (n + kThreads - 1) / kThreads;
+  const unsigned grid = (unsigned)(blocks < 4096 ? blocks : 4096);
+  if (wide)
+    hipLaunchKernelGGL(zero_fill_kernel<uint4>, dim3(grid), dim3(kThreads), 0, stream,
+                       reinterpret_cast<uint4*>(dst), n);
+  else
+    hipLaunchKernelGGL(zero_fill_kernel<uint32_t>, dim3(grid), dim3(kThreads), 0, stream,
+                       reinterpret_cast<uint32_t*>(dst), n);
+  return hipGetLastError();
+}
 
 hipError_t launch_seq_table(const int32_t* cu, int32_t nseq, int64_t ntok, int32_t max_chunks,
                             SeqInfo* seqs, ChunkInfo* chunks, int32_t* nchunks, int32_t* order,
