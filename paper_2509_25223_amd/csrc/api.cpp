@@ -252,7 +252,7 @@ rla_status forward(bool rdn, const rla_problem* problem, const void* q, const vo
 
   hipError_t e = hipSuccess;
   if (pr.varlen && pr.ntok > 0)   // tokens outside every sequence read as zero
-    e = hipMemsetAsync(o, 0, (size_t)pr.ntok * pr.H * pr.DV * (pr.out_bf16 ? 2 : 4), stream);
+    e = launch_zero_fill(o, (size_t)pr.ntok * pr.H * pr.DV * (pr.out_bf16 ? 2 : 4), stream);
   if (e == hipSuccess) e = build_tables(pr, w, ws, stream);
   if (e == hipSuccess) e = mark_stage(stream, true);
   if (e == hipSuccess && (pr.vflags & kVarQkNorm)) {   // q, k -> SiLU + L2 norm rows
@@ -305,13 +305,13 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
   hipError_t e = hipSuccess;
   if (pr.varlen && pr.ntok > 0) {   // tokens outside every sequence get zero gradients
     const size_t el = pr.out_bf16 ? 2 : 4, tok = (size_t)pr.ntok * pr.H;
-    e = hipMemsetAsync(dq, 0, tok * pr.DK * el, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dk, 0, tok * pr.DK * el, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dv, 0, tok * pr.DV * el, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dalpha_s, 0, tok * 4, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dbeta, 0, tok * 4, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dalpha_r, 0, tok * 4, stream);
-    if (e == hipSuccess) e = hipMemsetAsync(dgamma, 0, tok * 4, stream);
+    e = launch_zero_fill(dq, tok * pr.DK * el, stream);
+    if (e == hipSuccess) e = launch_zero_fill(dk, tok * pr.DK * el, stream);
+    if (e == hipSuccess) e = launch_zero_fill(dv, tok * pr.DV * el, stream);
+    if (e == hipSuccess) e = launch_zero_fill(dalpha_s, tok * 4, stream);
+    if (e == hipSuccess) e = launch_zero_fill(dbeta, tok * 4, stream);
+    if (e == hipSuccess) e = launch_zero_fill(dalpha_r, tok * 4, stream);
+    if (e == hipSuccess) e = launch_zero_fill(dgamma, tok * 4, stream);
   }
   if (e == hipSuccess && !pr.use_saved) e = build_tables(pr, w, ws, stream);
   if (e == hipSuccess) e = mark_stage(stream, true);
@@ -327,15 +327,15 @@ rla_status backward(bool rdn, const rla_problem* problem, const void* q, const v
     p.dk = ws + w.dkh;
     if (e == hipSuccess && pr.varlen) {   // rows outside every sequence stay zero
       const size_t bytes = (size_t)pr.ntok * pr.H * pr.DK * 4;
-      e = hipMemsetAsync(ws + w.dqh, 0, bytes, stream);
-      if (e == hipSuccess) e = hipMemsetAsync(ws + w.dkh, 0, bytes, stream);
+      e = launch_zero_fill(ws + w.dqh, bytes, stream);
+      if (e == hipSuccess) e = launch_zero_fill(ws + w.dkh, bytes, stream);
     }
   }
   const bool pre = (pr.vflags & kVarGatePreact) != 0;
   if (pre) {
     p.decay_partials = reinterpret_cast<float*>(ws + w.dpart);
     if (e == hipSuccess)
-      e = hipMemsetAsync(ws + w.dpart, 0, sizeof(float) * (size_t)pr.max_chunks * pr.H * 2, stream);
+      e = launch_zero_fill(ws + w.dpart, sizeof(float) * (size_t)pr.max_chunks * pr.H * 2, stream);
   }
   if (!pr.use_saved) {
     if (e == hipSuccess) e = launch_prep(p, pr.bf16, stream);
