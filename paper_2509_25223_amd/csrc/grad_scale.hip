@@ -22,26 +22,26 @@ __device__ __forceinline__ uint32_t bf16_mag_bits(uint32_t two) {
   return max((two & 0x7FFFu) << 16, two & 0x7FFF0000u);
 }
 
+// One wave per (chunk, head), four chunks of one head per workgroup; heads
+// vary fastest over consecutive workgroups, which then read contiguous
+// stretches of dO.  Every load of a wave is issued before any is used.
 template <int DV>
 __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint32_t* out) {
-  __shared__ uint32_t wmax[kWaves];
-  // heads vary fastest over consecutive workgroups, which then read one
-  // contiguous stretch of dO (the chunk's rows of every head)
-  const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6;
+  const int h = blockIdx.x, w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c = blockIdx.y * kWaves + w;
   ChunkInfo ci;
-  if (!chunk_info(p.st, c, ci)) return;
+  if (c >= p.max_chunks || !chunk_info(p.st, c, ci)) return;
   const int H = p.H, DK = p.DK;
   uint32_t m = 0;
-  {   // dO rows of the chunk, 16 bytes (8 bf16) per load, all issued at once;
-      // rows past the chunk's end re-read its last row (no effect on a maximum)
+  {   // the chunk's dO rows, 16 bytes (8 bf16) per load; rows past the
+      // chunk's end re-read its last row (no effect on a maximum)
     constexpr int kPerRow = DV / 8;
-    constexpr int kIter = kChunk * kPerRow / kThreads;
-    static_assert(kIter * kThreads == kChunk * kPerRow, "whole rows per step");
+    constexpr int kIter = kChunk * kPerRow / 64;
     const uint4* src = reinterpret_cast<const uint4*>(p.dO);
     uint4 x[kIter];
 #pragma unroll
     for (int u = 0; u < kIter; ++u) {
-      const int e = tid + u * kThreads, t = min(e / kPerRow, ci.len - 1), j = e % kPerRow;
+      const int e = lane + u * 64, t = min(e / kPerRow, ci.len - 1), j = e % kPerRow;
       x[u] = src[((ci.tok + t) * H + h) * (int64_t)kPerRow + j];
     }
 #pragma unroll
@@ -57,7 +57,7 @@ __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint3
     for (int s = 0; s < 2; ++s) {
       if (!st[s]) continue;
       const float4* src = reinterpret_cast<const float4*>(st[s] + off);
-      for (int e = tid; e < DK * (DV / 4); e += kThreads) {
+      for (int e = lane; e < DK * (DV / 4); e += 64) {
         const float4 x = src[e];
         m = max(m, max(max(__float_as_uint(x.x) & 0x7FFFFFFFu, __float_as_uint(x.y) & 0x7FFFFFFFu),
                        max(__float_as_uint(x.z) & 0x7FFFFFFFu, __float_as_uint(x.w) & 0x7FFFFFFFu)));
@@ -65,9 +65,7 @@ __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint3
     }
   }
   m = wave_absmax_bits(m);
-  if ((tid & 63) == 0) wmax[w] = m;
-  __syncthreads();
-  if (tid == 0) out[(int64_t)c * H + h] = max(max(wmax[0], wmax[1]), max(wmax[2], wmax[3]));
+  if (lane == 0) out[(int64_t)c * H + h] = m;
 }
 
 }  // namespace
@@ -75,7 +73,8 @@ __global__ __launch_bounds__(kThreads) void grad_absmax_kernel(OpParams p, uint3
 hipError_t launch_grad_absmax(const OpParams& p, uint32_t* out, hipStream_t stream) {
   if (p.max_chunks == 0) return hipSuccess;
   auto kern = p.DV == 128 ? grad_absmax_kernel<128> : grad_absmax_kernel<64>;
-  hipLaunchKernelGGL(kern, dim3(p.H, p.max_chunks), dim3(kThreads), 0, stream, p, out);
+  hipLaunchKernelGGL(kern, dim3(p.H, (p.max_chunks + kWaves - 1) / kWaves), dim3(kThreads), 0,
+                     stream, p, out);
   return hipGetLastError();
 }
 
