@@ -87,7 +87,9 @@ typedef enum {
   RLA_ERR_UNSUPPORTED = 4, /* valid request this build does not implement */
   RLA_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than required */
   RLA_ERR_VALUE = 6,       /* bad scalar (clip < 0 or NaN) or misaligned pointer */
-  RLA_ERR_HIP = 7          /* a HIP runtime call or kernel launch failed */
+  RLA_ERR_HIP = 7,         /* a HIP runtime call or kernel launch failed */
+  RLA_ERR_SCRATCH = 8      /* rdn_forward_noalloc: the problem needs more workspace
+                              than RLA_NOALLOC_SCRATCH_BYTES */
 } rla_status;
 
 typedef enum { RLA_F32 = 0, RLA_BF16 = 1 } rla_dtype;
@@ -210,6 +212,32 @@ rla_status rdn_forward(const rla_problem *problem,
                        const float *S0, const float *R0,
                        void *o, float *S_final, float *R_final,
                        void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Allocation-free RDN forward, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): rdn_forward with the workspace taken from a static device array
+ * of RLA_NOALLOC_SCRATCH_BYTES (128 MiB) inside the library instead of an
+ * argument.  Each GPU the library runs on holds its own array from the first
+ * call on it until the process ends; the call uses the array of the calling
+ * thread's current device, so `stream` must belong to that device.  The call
+ * allocates nothing and launches only the kernels rdn_forward launches (no
+ * memset nodes).  Problems whose rla_workspace_size(problem,
+ * RLA_OP_RDN_FORWARD) exceeds the array return RLA_ERR_SCRATCH before any HIP
+ * call (bf16, H = 16, d = 128, one sequence: up to 12,736 tokens);
+ * RLA_FLAG_SAVE_FOR_BACKWARD and RLA_FLAG_USE_SAVED are rejected
+ * (RLA_ERR_VALUE).  The array keeps the last call's contents; nothing in it
+ * needs to start at zero.  All calls on one GPU share its array: calls that
+ * overlap in time on one GPU (other streams, other threads) race and must be
+ * serialised by the caller.  Other arguments and results as rdn_forward.
+ */
+#define RLA_NOALLOC_SCRATCH_BYTES (128u << 20)
+rla_status rdn_forward_noalloc(const rla_problem *problem,
+                               const void *q, const void *k, const void *v,
+                               const float *alpha_s, const float *beta,
+                               const float *alpha_r, const float *gamma,
+                               const float *S0, const float *R0,
+                               void *o, float *S_final, float *R_final, void *stream);
 
 /*
  * RDN backward: gradients of L = <dO, o> + <dS_final, S_T> + <dR_final, R_T>

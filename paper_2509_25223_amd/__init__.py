@@ -33,7 +33,10 @@ RLA_F32, RLA_BF16 = 0, 1
 RLA_OP_RLA_FORWARD, RLA_OP_RDN_FORWARD, RLA_OP_RDN_BACKWARD, RLA_OP_RLA_BACKWARD = 0, 1, 2, 3
 
 SYMBOLS = ("rla_workspace_size", "rla_status_string", "rla_forward", "rdn_forward",
-           "rla_backward", "rdn_backward", "rla_set_stage_events", "rla_decode", "rdn_decode")
+           "rla_backward", "rdn_backward", "rla_set_stage_events", "rla_decode", "rdn_decode",
+           "rdn_forward_noalloc")
+RLA_ERR_SCRATCH = 8
+RLA_NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
 class rla_problem(ctypes.Structure):
@@ -75,7 +78,7 @@ def load_library():
         f = getattr(lib, name)
         f.argtypes = fwd_args
         f.restype = ctypes.c_int
-    for name in ("rla_decode", "rdn_decode"):
+    for name in ("rla_decode", "rdn_decode", "rdn_forward_noalloc"):
         f = getattr(lib, name)
         f.argtypes = [pp] + [vp] * 3 + [vp] * 4 + [vp] * 2 + [vp] * 3 + [vp]
         f.restype = ctypes.c_int
@@ -315,6 +318,37 @@ def rdn_forward(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=No
     return _forward("rdn_forward", RLA_OP_RDN_FORWARD, q, k, v, alpha_s, beta, alpha_r, gamma,
                     clip, S0, R0, cu_seqlens, out, workspace, stream, return_states, out_dtype,
                     save_for_backward, variants, decay_param)
+
+
+def rdn_forward_noalloc(q, k, v, alpha_s, beta, alpha_r, gamma, clip: float = 1.0, S0=None,
+                        R0=None, cu_seqlens=None, out=None, S_final=None, R_final=None,
+                        stream=None, out_dtype=None, variants=0, decay_param=None):
+    """RDN forward whose workspace is the library's static per-device scratch
+    array (no allocation inside the call; see include/rla.h).  The outputs
+    out, S_final, R_final are the caller's (allocated here only when not
+    given: pass them to keep the call allocation-free).  Returns (o, S_final,
+    R_final)."""
+    torch = _torch()
+    lib = load_library()
+    problem = make_problem(q, v, cu_seqlens, clip, out_dtype, _variant_bits(variants),
+                           _check_decay_param(variants, decay_param, q.shape[-2], q.device))
+    dev = q.device
+    _check(dict(q=q, k=k, v=v, alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma,
+                S0=S0, R0=R0, out=out, S_final=S_final, R_final=R_final), dev)
+    _check_operands(problem, q, k, v, dict(alpha_s=alpha_s, beta=beta, alpha_r=alpha_r, gamma=gamma),
+                    dict(S0=S0, R0=R0, S_final=S_final, R_final=R_final))
+    odt = torch.float32 if problem.out_dtype == RLA_F32 else torch.bfloat16
+    o = torch.empty(v.shape, dtype=odt, device=dev) if out is None else out
+    _expect("out", o, v.shape, odt)
+    shape = _state_shape(problem)
+    Sf = torch.empty(shape, dtype=torch.float32, device=dev) if S_final is None else S_final
+    Rf = torch.empty(shape, dtype=torch.float32, device=dev) if R_final is None else R_final
+    st = lib.rdn_forward_noalloc(ctypes.byref(problem), _ptr(q), _ptr(k), _ptr(v), _ptr(alpha_s),
+                                 _ptr(beta), _ptr(alpha_r), _ptr(gamma), _ptr(S0), _ptr(R0),
+                                 _ptr(o), _ptr(Sf), _ptr(Rf), _stream_handle(stream))
+    if st != RLA_OK:
+        raise RLAError(st, "rdn_forward_noalloc")
+    return o, Sf, Rf
 
 
 def _backward(name, op, q, k, v, alpha_s, beta, alpha_r, gamma, dO, clip: float = 1.0, S0=None,

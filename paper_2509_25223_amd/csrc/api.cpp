@@ -4,6 +4,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
@@ -425,6 +427,32 @@ rla_status decode(bool rdn, const rla_problem* problem, const void* q, const voi
   return to_status(e);
 }
 
+// ---- allocation-free forward: the workspace is a static device array ----
+// Each GPU the library runs on holds its own copy from the first use until the
+// process ends.  Host code must not use the array's name as a device address:
+// the address is taken once per device with hipGetSymbolAddress (with that
+// device current) and kept in scratch_ptr.
+constexpr size_t kScratchBytes = size_t(RLA_NOALLOC_SCRATCH_BYTES);
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 256;
+std::mutex scratch_mutex;
+void* scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array (taken on its first use).
+rla_status current_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return RLA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return RLA_ERR_HIP;
+    scratch_ptr[dev] = ptr;
+  }
+  *out = scratch_ptr[dev];
+  return RLA_OK;
+}
+
 }  // namespace
 }  // namespace rla
 
@@ -455,6 +483,7 @@ const char* rla_status_string(rla_status s) {
     case RLA_ERR_WORKSPACE: return "workspace missing or too small";
     case RLA_ERR_VALUE: return "bad scalar argument or misaligned pointer";
     case RLA_ERR_HIP: return "HIP runtime error";
+    case RLA_ERR_SCRATCH: return "problem needs more workspace than the static scratch holds";
   }
   return "unknown status";
 }
@@ -475,6 +504,25 @@ rla_status rdn_forward(const rla_problem* problem, const void* q, const void* k,
                        void* stream) {
   return forward(true, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, o, S_final,
                  R_final, workspace, workspace_bytes, stream);
+}
+
+rla_status rdn_forward_noalloc(const rla_problem* problem, const void* q, const void* k,
+                               const void* v, const float* alpha_s, const float* beta,
+                               const float* alpha_r, const float* gamma, const float* S0,
+                               const float* R0, void* o, float* S_final, float* R_final,
+                               void* stream) {
+  Problem pr;
+  rla_status st = check_problem(problem, pr);
+  if (st != RLA_OK) return st;
+  if (pr.save || pr.use_saved) return RLA_ERR_VALUE;
+  if (plan(pr, RLA_OP_RDN_FORWARD).total > kScratchBytes) return RLA_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (pr.N > 0) {
+    st = current_scratch(&ws);
+    if (st != RLA_OK) return st;
+  }
+  return forward(true, problem, q, k, v, alpha_s, beta, alpha_r, gamma, S0, R0, o, S_final,
+                 R_final, ws, kScratchBytes, stream);
 }
 
 rla_status rla_backward(const rla_problem* problem, const void* q, const void* k, const void* v,

@@ -120,9 +120,34 @@ def test_saving_forward_shares_the_backward_limits(lib):
 
 
 def test_status_strings(lib):
-    for s in range(8):
+    for s in range(9):
         assert rla.status_string(s)
     assert "workspace" in rla.status_string(5)
+    assert "scratch" in rla.status_string(rla.RLA_ERR_SCRATCH)
+
+
+def call_noalloc(lib, p):
+    return lib.rdn_forward_noalloc(ctypes.byref(p) if p is not None else None, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, None)
+
+
+def test_noalloc_forward_limits(lib):
+    """The allocation-free forward rejects, before any HIP call, problems whose
+    workspace exceeds its static scratch array (bf16, H=16, d=128: 12,736
+    tokens fit, 12,800 do not) and the save / use-saved flags; other errors
+    are those of rdn_forward."""
+    fits = prob(B=1, T=12736, H=16)
+    assert rla.rla_workspace_size(fits, rla.RLA_OP_RDN_FORWARD) <= rla.RLA_NOALLOC_SCRATCH_BYTES
+    too_big = prob(B=1, T=12800, H=16)
+    assert rla.rla_workspace_size(too_big, rla.RLA_OP_RDN_FORWARD) > rla.RLA_NOALLOC_SCRATCH_BYTES
+    assert call_noalloc(lib, too_big) == rla.RLA_ERR_SCRATCH
+    assert call_noalloc(lib, prob(B=64, T=4096, H=16)) == rla.RLA_ERR_SCRATCH
+    for flag in (rla.RLA_FLAG_SAVE_FOR_BACKWARD, rla.RLA_FLAG_USE_SAVED):
+        p = prob(B=1, T=100, H=2)
+        p.flags = flag
+        assert call_noalloc(lib, p) == 6
+    assert call_noalloc(lib, None) == 1
+    assert call_noalloc(lib, prob(dk=96)) == 2
 
 
 def call_dec(lib, p, name="rdn_decode", **kw):
