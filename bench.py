@@ -49,10 +49,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "bwd_grad": ("42f020ac9c630148", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1249546473, 320918645),
-    "bwd_scan": ("d3c2963a85b9f99e", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407162643, 613416960),
-    "fwd_scan": ("25689f8b571ffdbe", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373572263, 638583296),
-    "prep": ("72bae810063c3ecd", ('prep.hip', 'common.hpp', 'kernels.hpp'), 149294713, 171970410),
+    "prep": ("7073f2c8a5029e13", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168044166, 171984085),
+    "grad_absmax": ("64f05d1d7a9bf2ed", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67195818, 131093),
+    "bwd_scan": ("b5a69d14349110aa", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407287120, 613419018),
+    "bwd_grad": ("57ad33f971204c55", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232586892, 305333856),
+    "fwd_scan": ("3effebc26a1a0648", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373579852, 638587430),
     "decode": ("093edbbe40eefd13", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746642, 539571891),
 }
 

@@ -160,7 +160,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   float* esum = reinterpret_cast<float*>(smem + L::kElem);   // [2][64]: dY.V, dYR.r
   float* red = reinterpret_cast<float*>(smem + L::kRed);
 
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  // heads vary fastest over consecutive workgroups, which then read one
+  // contiguous stretch of the token rows (every head of the chunk)
+  const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   float* wsum = sums + w * kNumSums * kChunk;   // this wave's sums
   auto sum_row = [&](int q) { return wsum + q * kChunk; };
   auto total = [&](int q, int t) {               // over the waves
@@ -751,7 +753,7 @@ hipError_t launch_grad_t(const OpParams& p, hipStream_t stream) {
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;
   if (p.max_chunks == 0) return hipSuccess;
-  hipLaunchKernelGGL(kern, dim3(p.max_chunks, p.H), dim3(L::kNT), L::kBytes, stream, p);
+  hipLaunchKernelGGL(kern, dim3(p.H, p.max_chunks), dim3(L::kNT), L::kBytes, stream, p);
   return hipGetLastError();
 }
 

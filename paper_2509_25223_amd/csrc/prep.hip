@@ -136,7 +136,9 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   float* gm = bt + kChunk;
   float* gsp = gm + kChunk;   // g_{t-1}
 
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  // heads vary fastest over consecutive workgroups, which then read one
+  // contiguous stretch of the token rows (every head of the chunk)
+  const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x;
   ChunkInfo ci;
   if (!chunk_info(p.st, c, ci)) return;
   const int H = p.H;
@@ -337,7 +339,7 @@ hipError_t launch_prep_t(const OpParams& p, hipStream_t stream) {
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
   if (err != hipSuccess) return err;
-  hipLaunchKernelGGL(kern, dim3(p.max_chunks, p.H), dim3(kThreads), L::kBytes, stream, p);
+  hipLaunchKernelGGL(kern, dim3(p.H, p.max_chunks), dim3(kThreads), L::kBytes, stream, p);
   return hipGetLastError();
 }
 
