@@ -29,6 +29,11 @@ FLAGS = [
     # that every template instantiation of a kernel rounds alike (the default,
     # fast contraction, lets the backend fuse differently per instantiation)
     "-ffp-contract=on",
+    # MFMA results in ordinary vector registers: with the accumulator
+    # registers the backend copies every product out (v_accvgpr_read) before
+    # the elementwise work that follows it (about 10% of the scans' vector
+    # instructions)
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
 
