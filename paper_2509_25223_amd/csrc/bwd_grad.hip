@@ -81,7 +81,12 @@ struct GradLayout {
   static constexpr int kQT = kKT + DK * kLdP * (int)sizeof(XT);
   static constexpr int kOvlEnd = kQT + DK * kLdP * (int)sizeof(XT);
   static constexpr int kBlkEnd = kBlk + kNumTokBlk * kBlkBytes;
+  // the per-token sums totalled over the waves ([kNumSums][64]), written
+  // when the token blocks are dead: in place of K^T (16-bit operands, which
+  // read K, Q transposed instead) or past the overlay
+  static constexpr int kTot = kBF ? kKT : kOvlEnd;
   static constexpr int kGates = kBlkEnd > kOvlEnd ? kBlkEnd : kOvlEnd;
+  static_assert(kTot + kNumSums * kChunk * 4 <= kGates, "totals inside the dead token blocks");
   static constexpr int kNumGateArrays = 11;
   static constexpr int kSums = kGates + kNumGateArrays * kChunk * 4;
   static constexpr int kElem = kSums + kNW * kNumSums * kChunk * 4;  // per-wave sums
@@ -165,12 +170,6 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   float* wsum = sums + w * kNumSums * kChunk;   // this wave's sums
   auto sum_row = [&](int q) { return wsum + q * kChunk; };
-  auto total = [&](int q, int t) {               // over the waves
-    float x = 0.f;
-#pragma unroll
-    for (int v = 0; v < NW; ++v) x += sums[(v * kNumSums + q) * kChunk + t];
-    return x;
-  };
   ChunkInfo ci;
   if (!chunk_info(p.st, c, ci)) return;
   const int H = p.H, len = ci.len;
@@ -258,6 +257,14 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   for (int u = 0; u < kOV; ++u) {
     const int e = tid + u * NT, t = in_row(e / (DV / kE)), j = (e % (DV / kE)) * kE;
     ov[u] = *reinterpret_cast<const uint4*>(dog + ((tok + t) * H + h) * (int64_t)DV + j);
+  }
+  // this token's decay inputs for the gate gradients of wave 0 (lane = token),
+  // loaded now so that their latency is not left to the kernel's end
+  float a_s = 0.f, a_r = 0.f;
+  if (w == 0) {
+    const int64_t gi = (tok + in_row(lane)) * H + h;
+    a_s = p.alpha_s[gi];
+    a_r = p.alpha_r[gi];
   }
   // the gate block (every wave reads it; wave 0 stores the derived arrays)
   const float* gb = p.gate_ws + ((int64_t)c * H + h) * kGateBlock;
@@ -629,6 +636,17 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       if constexpr (!BF) dPTm[s * ldp + t] = from_f<XT>(0.f);
     }
   }
+  // the per-token sums over the waves, shared out over all threads (in the
+  // order of the waves, so every total is rounded alike)
+  {
+    float* tot = reinterpret_cast<float*>(smem + L::kTot);
+    for (int e = tid; e < kNumSums * kChunk; e += NT) {
+      float x = 0.f;
+#pragma unroll
+      for (int v = 0; v < NW; ++v) x += sums[v * kNumSums * kChunk + e];
+      tot[e] = x;
+    }
+  }
   // K^T, Q^T for the final products (fp32; 16-bit operands read K, Q and
   // dP transposed with transpose reads)
   if constexpr (!BF)
@@ -648,14 +666,16 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 
   // ---------------- phase 3: gate gradients; dQ += dP K, dK += dP^T Q + (dG + dG^T) K ----------------
   if (tid < kChunk) {
+    const float* tot = reinterpret_cast<const float*>(smem + L::kTot);
+    auto tot_at = [&](int q, int t) { return tot[q * kChunk + t]; };
     const int t = tid;
     float gsC_all = 0.f, grC_all = 0.f;
 #pragma unroll
     for (int v = 0; v < NW; ++v) { gsC_all += red[v]; grC_all += red[NW + v]; }
-    const float dgs = total(sGS, t) + total(sZRS, t) - total(sZCS, t) - total(sZCP, t) +
-                      (t + 1 < kChunk ? total(sGSP, t + 1) + total(sZRP, t + 1) : 0.f) +
+    const float dgs = tot_at(sGS, t) + tot_at(sZRS, t) - tot_at(sZCS, t) - tot_at(sZCP, t) +
+                      (t + 1 < kChunk ? tot_at(sGSP, t + 1) + tot_at(sZRP, t + 1) : 0.f) +
                       (t == kChunk - 1 ? gsC_all : 0.f);
-    const float dgr = total(sGR, t) + total(sZRR, t) - total(sZCR, t) +
+    const float dgr = tot_at(sGR, t) + tot_at(sZRR, t) - tot_at(sZCR, t) +
                       (t == kChunk - 1 ? grC_all : 0.f);
     // suffix sums over the chunk: d log a_j = sum_{t >= j} d g_t
     float ss = dgs, sr = dgr;
@@ -670,13 +690,13 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     float pa = 0.f, pb = 0.f;   // this token's share of d/da_h, d/db_h (pre-activations)
     if (t < len) {
       const int64_t gi = (tok + t) * H + h;
-      const float db = (esum[t] + total(sB, t) + total(sZB, t)) * isig;
-      const float dgm = (esum[kChunk + t] + total(sGM, t) + total(sZGM, t)) * isig;
+      const float db = (esum[t] + tot_at(sB, t) + tot_at(sZB, t)) * isig;
+      const float dgm = (esum[kChunk + t] + tot_at(sGM, t) + tot_at(sZGM, t)) * isig;
       if (vf & kVarGatePreact) {
         // log a = -A softplus(z + Bb): d/dz = -A sigmoid(z + Bb), d/dA = -softplus(z + Bb);
         // beta = sigmoid(z): d/dz = beta (1 - beta), likewise gamma
         const float A = p.decay_param[h], Bb = p.decay_param[H + h];
-        const float zs = p.alpha_s[gi] + Bb, zr = p.alpha_r[gi] + Bb;
+        const float zs = a_s + Bb, zr = a_r + Bb;
         const float dzs = ss * (-A * sigmoid_f(zs)), dzr = sr * (-A * sigmoid_f(zr));
         p.dalpha_s[gi] = dzs;
         p.dalpha_r[gi] = dzr;
@@ -685,9 +705,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
         p.dbeta[gi] = db * gbt[t] * (1.f - gbt[t]);
         p.dgamma[gi] = dgm * ggm[t] * (1.f - ggm[t]);
       } else {
-        const float as = p.alpha_s[gi], ar = p.alpha_r[gi];
-        p.dalpha_s[gi] = as >= 1.17549435e-38f ? ss / as : 0.f;
-        p.dalpha_r[gi] = ar >= 1.17549435e-38f ? sr / ar : 0.f;
+        p.dalpha_s[gi] = a_s >= 1.17549435e-38f ? ss / a_s : 0.f;
+        p.dalpha_r[gi] = a_r >= 1.17549435e-38f ? sr / a_r : 0.f;
         p.dbeta[gi] = db;
         p.dgamma[gi] = dgm;
       }
