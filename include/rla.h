@@ -224,7 +224,7 @@ rla_status rdn_forward(const rla_problem *problem,
  * allocates nothing and launches only the kernels rdn_forward launches (no
  * memset nodes).  Problems whose rla_workspace_size(problem,
  * RLA_OP_RDN_FORWARD) exceeds the array return RLA_ERR_SCRATCH before any HIP
- * call (bf16, H = 16, d = 128, one sequence: up to 12,736 tokens);
+ * call (bf16, H = 16, d = 128, one sequence: up to 19,648 tokens);
  * RLA_FLAG_SAVE_FOR_BACKWARD and RLA_FLAG_USE_SAVED are rejected
  * (RLA_ERR_VALUE).  The array keeps the last call's contents; nothing in it
  * needs to start at zero.  All calls on one GPU share its array: calls that

@@ -296,6 +296,7 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   auto mat_src = [&](int c, int m) {
     return matg + ((int64_t)(si.chunk0 + c) * H + h) * kNumMats * kMatElems + m * kMatElems;
   };
+  const MatDma<XT> mdo;   // this lane's matrix DMA offsets
   auto issue_regs = [&](int c) {
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
@@ -342,33 +343,33 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   };
   auto issue_early = [&](int c) {   // after P1
     issue_gates(c);
-    if constexpr (L::kDB) dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
+    if constexpr (L::kDB) dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo);
   };
   auto issue_mid = [&](int c) {     // after P3
     if constexpr (L::kDB) {
       issue_mask(c);
-      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0), mdo);
     }
   };
   auto issue_late = [&](int c) {    // after P4
     if constexpr (L::kDB) {
-      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
-      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
+      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0), mdo);
+      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0), mdo);
     }
   };
   auto issue_after5 = [&](int c) {  // after P5 (RDN)
-    if constexpr (L::kDB && RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
+    if constexpr (L::kDB && RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo);
   };
   auto issue_all_single = [&](int c) {   // fp32: everything after the last barrier
     if constexpr (!L::kDB) {
       issue_mask(c);
       if constexpr (RDN) {
-        dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
-        dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+        dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo);
+        dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0), mdo);
       }
-      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
-      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
-      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0));
+      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0), mdo);
+      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0), mdo);
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0), mdo);
     }
   };
   if (nch > 0) {
@@ -377,12 +378,12 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     issue_gates(c);
     issue_mask(c);
     if constexpr (RDN) {
-      dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
-      dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
+      dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo);
+      dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0), mdo);
     }
-    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
-    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
-    dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
+    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0), mdo);
+    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0), mdo);
+    dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo);
     wait_vmem();
   }
   barrier_lds();

@@ -267,6 +267,18 @@ template <typename T, int COLS> struct Tile {
 };
 template <typename T> using Swz = Tile<T, kChunk>;   // 64 x 64 matrices
 
+// The chunk matrices are lower block-triangular in 16 x 16 blocks.  Only the
+// 10 blocks on and below the diagonal are stored, each row-major, block
+// (bi, bj), bj <= bi, at index bi (bi + 1) / 2 + bj; the blocks above the
+// diagonal are zero.  Each stored matrix is followed by 64 zero elements,
+// the source of the LDS-DMA lanes that fill the blocks above the diagonal.
+constexpr int kMatBlocks = 10;
+constexpr int kMatPacked = kMatBlocks * 256;   // elements of the stored blocks
+constexpr int kMatElems = kMatPacked + 64;     // per matrix, with the zero pad
+__host__ __device__ constexpr int tri_off(int t, int s) {
+  return (((t >> 4) * ((t >> 4) + 1)) / 2 + (s >> 4)) * 256 + (t & 15) * 16 + (s & 15);
+}
+
 // LDS transpose read of 16-bit elements (gfx950 ds_read_b64_tr_b16).  In each
 // 16-lane group, the 8-byte pieces the lanes address form a 16 x 4 array D
 // (row j: the group's lane j); lane i of the group receives D[i / 4 + 4 e][i % 4]
@@ -402,11 +414,40 @@ __device__ __forceinline__ void dma_tile64(const void* gsrc, void* lds) {
   }
 }
 
-// DMA of one row-major 64 x 64 matrix (global) into a swizzled LDS tile by
-// the NW waves of the workgroup.
+// This lane's source offsets (bytes, from the start of a stored matrix) for
+// the LDS-DMA of a packed matrix into a swizzled 64 x 64 tile by NW waves:
+// the element of tri_off at the lane's 16-byte chunk, or the zero pad for
+// the chunks above the diagonal blocks.  The same for every matrix and
+// chunk, so computed once.
 template <typename T, int NW = kWaves>
-__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds) {
-  dma_tile64<Swz<T>, NW>(gsrc, lds);
+struct MatDma {
+  static constexpr int kInst = kChunk * Swz<T>::kRowB / 1024;
+  static constexpr int kPerWave = kInst / NW;
+  static_assert(kInst % NW == 0, "equal DMA share per wave");
+  int off[kPerWave];
+  __device__ __forceinline__ MatDma() {
+    typedef Swz<T> TL;
+    constexpr int kEpc = 16 / (int)sizeof(T);   // elements per 16-byte chunk
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int m = 0; m < kPerWave; ++m) {
+      const int P = (w * kPerWave + m) * 64 + lane;   // physical 16-byte chunk
+      const int r = P / TL::kCpr, col = ((P % TL::kCpr) ^ TL::sw(r)) * kEpc;   // its logical position
+      off[m] = ((col >> 4) <= (r >> 4) ? tri_off(r, col) : kMatPacked) * (int)sizeof(T);
+    }
+  }
+};
+
+// DMA of one packed lower block-triangular 64 x 64 matrix (global, tri_off
+// layout, followed by its zero pad) into a swizzled LDS tile by the NW waves
+// of the workgroup: no lane is masked and no branch is taken.
+template <typename T, int NW = kWaves>
+__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds, const MatDma<T, NW>& md) {
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int m = 0; m < MatDma<T, NW>::kPerWave; ++m)
+    dma16(reinterpret_cast<const char*>(gsrc) + md.off[m],
+          reinterpret_cast<char*>(lds) + (w * MatDma<T, NW>::kPerWave + m) * 1024);
 }
 
 // DMA of `bytes` contiguous bytes (a multiple of 1 KiB) by wave `wave` only.
@@ -937,7 +978,8 @@ __device__ __forceinline__ float wave_inclusive_scan(float x) {
 constexpr int kGateBlock = 4 * kChunk;
 
 // Matrices of one (chunk, head), as written by the prep kernel, each 64 x 64
-// row-major (row = query token t, column = key token s):
+// (row = query token t, column = key token s) and lower block-triangular in
+// 16 x 16 blocks, stored packed (tri_off):
 enum : int {
   kMatTS = 0,   // T^S = (I + A^S)^{-1}                     (RDN only)
   kMatMG = 1,   // e^{g_{t-1} - g_s} (k_t . k_s)       s < t
@@ -946,6 +988,5 @@ enum : int {
   kMatMR = 4,   // e^{h_t - h_s}     (q_t . k_s)       s <= t
   kNumMats = 5
 };
-constexpr int kMatElems = kChunk * kChunk;
 
 }  // namespace rla

@@ -216,6 +216,7 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   auto mat_src = [&](int c, int m) {
     return matg + ((int64_t)(si.chunk0 + c) * H + h) * kNumMats * kMatElems + m * kMatElems;
   };
+  const MatDma<XT> mdo;   // this lane's matrix DMA offsets
   auto issue_regs = [&](int c) {
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int t = 16 * w + (lane & 15);
@@ -238,19 +239,19 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
       dma_linear_wave(p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock, graw,
                       kGateBlock * 4);
     if constexpr (L::kDB) {
-      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, c & 1));
-      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1));
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, c & 1), mdo);
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo);
     }
   };
   auto issue_late = [&](int c) {    // T^S, MG, MP
-    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0));
-    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0));
-    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0));
+    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo);
+    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0), mdo);
+    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0), mdo);
   };
   auto issue_tail = [&](int c) {    // T^R, MR when single-buffered
     if constexpr (!L::kDB) {
-      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0));
-      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0));
+      if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0), mdo);
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, 0), mdo);
     }
   };
   if (nch > 0) {

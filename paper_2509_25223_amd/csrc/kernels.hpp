@@ -56,7 +56,7 @@ struct OpParams {
 
   // workspace regions
   float* gate_ws = nullptr;     // [max_chunks][H][kGateBlock]
-  void* mat_ws = nullptr;       // [max_chunks][H][kNumMats][64][64]  (mm type)
+  void* mat_ws = nullptr;       // [max_chunks][H][kNumMats][kMatElems]: packed lower blocks (mm type)
   // chunk states saved for the gradient kernel, [max_chunks][H][DK][DV]: fp32
   // for fp32 inputs; fp16 for bf16 inputs, each (row, 32 columns) scaled by a
   // power of two held in the matching *_sc array [max_chunks][H][DK][DV / 32]

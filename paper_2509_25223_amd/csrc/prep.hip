@@ -231,6 +231,8 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   __syncthreads();   // Kc/Qc dead: region 0 becomes As/Ar
 
   XT* mats = reinterpret_cast<XT*>(p.mat_ws) + ((int64_t)c * H + h) * kNumMats * kMatElems;
+  if (tid < kNumMats)   // each matrix's zero pad (the scans' DMA source above the diagonal)
+    *reinterpret_cast<uint4*>(mats + tid * kMatElems + kMatPacked) = make_uint4(0, 0, 0, 0);
   floatx4 mg[4], mp[4], mr[4];   // this wave's 16-row strips of MG, MP, MR
   // the gate values of this lane's rows and columns, read once up front (a
   // read needed only under a condition would become a branch with its own
@@ -274,6 +276,8 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
       }
     }
   }
+  // the blocks on and below the diagonal, packed (tri_off): wave w holds
+  // block row w
   if constexpr (sizeof(XT) == 2) {   // fp16 rows leave in 16-byte stores (two strips of 32 columns)
 #pragma unroll
     for (int m = 0; m < 3; ++m) {
@@ -281,28 +285,33 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
       XT* base = mats + (m == 0 ? kMatMG : m == 1 ? kMatMP : kMatMR) * kMatElems;
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
+        if (2 * half > w) continue;   // both blocks of the strip pair above the diagonal
         int row, col;
         const uint4 v = pack_strip_f16(x[2 * half], x[2 * half + 1], 1.f, row, col);
-        *reinterpret_cast<uint4*>(base + (16 * w + row) * kChunk + 32 * half + col) = v;
+        const int s0 = 32 * half + col;
+        if ((s0 >> 4) <= w) *reinterpret_cast<uint4*>(base + tri_off(16 * w + row, s0)) = v;
       }
     }
   } else {
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
+    for (int ct = 0; ct < 4; ++ct) {
+      if (ct > w) continue;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * w + acc_row(r), s = 16 * ct + acc_col();
-        mats[kMatMG * kMatElems + t * kChunk + s] = mg[ct][r];
-        mats[kMatMP * kMatElems + t * kChunk + s] = mp[ct][r];
-        mats[kMatMR * kMatElems + t * kChunk + s] = mr[ct][r];
+        mats[kMatMG * kMatElems + tri_off(t, s)] = mg[ct][r];
+        mats[kMatMP * kMatElems + tri_off(t, s)] = mp[ct][r];
+        mats[kMatMR * kMatElems + tri_off(t, s)] = mr[ct][r];
       }
+    }
   }
   if constexpr (RDN) {
     __syncthreads();
     invert_unit_lower_pair(As, Ar, W);
     __syncthreads();
-    // 8 consecutive elements per thread and step (16-byte fp16 stores)
-    for (int e = 8 * tid; e < kMatElems; e += 8 * kThreads) {
+    // 8 consecutive elements per thread and step (16-byte fp16 stores), the
+    // blocks on and below the diagonal packed (tri_off)
+    for (int e = 8 * tid; e < kChunk * kChunk; e += 8 * kThreads) {
       const int t = e / kChunk, s = e % kChunk;
       const bool upper = (s >> 4) > (t >> 4);   // blocks above the diagonal are zero
 #pragma unroll
@@ -320,7 +329,8 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
           vals[k] = from_f<XT>(f0[k]);
           vals[4 + k] = from_f<XT>(f1[k]);
         }
-        XT* dst = mats + (m ? kMatTR : kMatTS) * kMatElems + e;
+        XT* dst = mats + (m ? kMatTR : kMatTS) * kMatElems + tri_off(t, s);
+        if (upper) continue;
         if constexpr (sizeof(XT) == 2) {
           *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(vals);
         } else {

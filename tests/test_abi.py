@@ -133,12 +133,12 @@ def call_noalloc(lib, p):
 
 def test_noalloc_forward_limits(lib):
     """The allocation-free forward rejects, before any HIP call, problems whose
-    workspace exceeds its static scratch array (bf16, H=16, d=128: 12,736
-    tokens fit, 12,800 do not) and the save / use-saved flags; other errors
+    workspace exceeds its static scratch array (bf16, H=16, d=128: 19,648
+    tokens fit, 19,712 do not) and the save / use-saved flags; other errors
     are those of rdn_forward."""
-    fits = prob(B=1, T=12736, H=16)
+    fits = prob(B=1, T=19648, H=16)
     assert rla.rla_workspace_size(fits, rla.RLA_OP_RDN_FORWARD) <= rla.RLA_NOALLOC_SCRATCH_BYTES
-    too_big = prob(B=1, T=12800, H=16)
+    too_big = prob(B=1, T=19712, H=16)
     assert rla.rla_workspace_size(too_big, rla.RLA_OP_RDN_FORWARD) > rla.RLA_NOALLOC_SCRATCH_BYTES
     assert call_noalloc(lib, too_big) == rla.RLA_ERR_SCRATCH
     assert call_noalloc(lib, prob(B=64, T=4096, H=16)) == rla.RLA_ERR_SCRATCH

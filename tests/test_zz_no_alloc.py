@@ -61,8 +61,8 @@ def test_noalloc_forward_matches_rdn_forward(device):
 
 def test_noalloc_forward_rejects_oversized_problem(device):
     import torch
-    q = torch.zeros(1, 12800, 16, 128, dtype=torch.bfloat16, device=device)
-    g = torch.zeros(1, 12800, 16, dtype=torch.float32, device=device)
+    q = torch.zeros(1, 19712, 16, 128, dtype=torch.bfloat16, device=device)
+    g = torch.zeros(1, 19712, 16, dtype=torch.float32, device=device)
     with pytest.raises(rla.RLAError) as err:
         rla.rdn_forward_noalloc(q, q, q, g, g, g, g)
     assert err.value.status == rla.RLA_ERR_SCRATCH
