@@ -589,6 +589,35 @@ __device__ __forceinline__ MatFrags<T> swz_cols_frags_sync(const T* M, int t0) {
   }
   return a;
 }
+// frag_tr for N fragments (tile-transpose rows r0[n], k = k0[n] ..) issued
+// as inline assembly, so that the compiler does not drain the wave's
+// in-flight LDS-DMA and stores before them; the function waits for its own
+// reads (lgkmcnt(0)) and ties the results to that wait.
+template <class TL, typename T, int N>
+__device__ __forceinline__ void frags_tr_sync(const void* base, const int (&r0)[N], const int (&k0)[N],
+                                              typename Mfma<T>::frag (&f)[N]) {
+  static_assert(sizeof(T) == 2 && Mfma<T>::kStep == 32, "16-bit k-steps of 32");
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const char* b = reinterpret_cast<const char*>(base);
+  u16x4 x[N], y[N];
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    const int row = k0[n] + 8 * (lane >> 4) + (jj >> 2), col = r0[n] + 4 * (jj & 3);
+    const uint32_t a0 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(row, col));
+    const uint32_t a1 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(row + 4, col));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(x[n]) : "v"(a0));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(y[n]) : "v"(a1));
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+  for (int n = 0; n < N; ++n) {
+    asm volatile("" : "+v"(x[n]), "+v"(y[n]));
+    const u16x8 v = {x[n][0], x[n][1], x[n][2], x[n][3], y[n][0], y[n][1], y[n][2], y[n][3]};
+    f[n] = __builtin_bit_cast(typename Mfma<T>::frag, v);
+  }
+}
+
 // acc += A * B with A from MatFrags and B^T rows b0.. of a 64-token tile
 template <typename T, class TB = Swz<T>>
 __device__ __forceinline__ void mma_frags(floatx4& acc, const MatFrags<T>& a, const void* B, int b0) {

@@ -508,23 +508,50 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
     }
 
     // ---- state update: S <- e^{g_C} S + K^T DU, R <- e^{h_C} R + K^T DUR ----
-    // (the compiler drains the wave's outstanding memory operations before
-    // the first transpose read: the prefetch has landed by now)
+    // (bf16 inputs: the K^T fragments from transpose reads issued as inline
+    // assembly, which leaves the next chunk's DMA and the checkpoint stores
+    // in flight; the builtin would drain them first)
     const float eS = edge[0], eR = edge[1];
+    if constexpr (BF) {
+      typedef Mfma<XT> MX;
+      constexpr int NF = IT * (kChunk / MX::kStep);
+      int fr0[NF], fk0[NF];
 #pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int i0 = w * (DK / 4) + it * 16;
+      for (int n = 0; n < NF; ++n) {
+        fr0[n] = w * (DK / 4) + (n / (kChunk / MX::kStep)) * 16;
+        fk0[n] = (n % (kChunk / MX::kStep)) * MX::kStep;
+      }
+      typename MX::frag kt[NF];
+      frags_tr_sync<TK, XT, NF>(KT, fr0, fk0, kt);
 #pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-        Sacc[it][jt] *= eS;
-        Racc[it][jt] *= eR;
-        mma_tiles<XT, kChunk, TK, TT>(Sacc[it][jt], KT, i0, DUt, jt * 16);
-        mma_tiles<XT, kChunk, TK, TT>(Racc[it][jt], KT, i0, DURt, jt * 16);
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          Sacc[it][jt] *= eS;
+          Racc[it][jt] *= eR;
+#pragma unroll
+          for (int ks = 0; ks < kChunk / MX::kStep; ++ks) {
+            const int n = it * (kChunk / MX::kStep) + ks;
+            Sacc[it][jt] = MX::mma(kt[n], TT::template frag<MX>(DUt, jt * 16, ks * MX::kStep), Sacc[it][jt]);
+            Racc[it][jt] = MX::mma(kt[n], TT::template frag<MX>(DURt, jt * 16, ks * MX::kStep), Racc[it][jt]);
+          }
+        }
+    } else {
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int i0 = w * (DK / 4) + it * 16;
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          Sacc[it][jt] *= eS;
+          Racc[it][jt] *= eR;
+          mma_tiles<XT, kChunk, TK, TT>(Sacc[it][jt], KT, i0, DUt, jt * 16);
+          mma_tiles<XT, kChunk, TK, TT>(Racc[it][jt], KT, i0, DURt, jt * 16);
+        }
       }
     }
-    // the next chunk's DMA data must have landed before anyone reads it (with
-    // fp32 inputs the checkpoint stores, issued last, may still be in flight;
-    // with bf16 inputs the update's transpose reads have drained them)
+    // the next chunk's DMA data must have landed before anyone reads it; the
+    // checkpoint stores, issued after the chunk's last DMA, may still be in
+    // flight
     wait_vmem_but<CKPT ? kCkptStores : 0>();
     barrier_lds();
     if (c + 1 < nch) issue_tail(c + 1);   // single-buffered T^R / MR: waited at P3
