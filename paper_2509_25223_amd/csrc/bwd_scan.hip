@@ -638,18 +638,52 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
     }
 
     // ---- P6: state gradients at the chunk start ----
+    // (bf16 inputs: the Q^T, K^T fragments from transpose reads issued as
+    // inline assembly, which leaves the DMA issued after P5 and the dv and
+    // checkpoint stores in flight; the builtin would drain them first)
     const float eS = edge[0], eR = edge[1];
+    if constexpr (BF) {
+      typedef Mfma<XT> MX;
+      constexpr int KS2 = kChunk / MX::kStep;
+      constexpr int NF = IT * KS2;
+      int fr0[NF], fk0[NF];
 #pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int i0 = w * (DK / 4) + it * 16;
+      for (int n = 0; n < NF; ++n) {
+        fr0[n] = w * (DK / 4) + (n / KS2) * 16;
+        fk0[n] = (n % KS2) * MX::kStep;
+      }
+      typename MX::frag qf[NF], kf[NF];
+      frags_tr_sync<TKQ, XT, NF>(QT, fr0, fk0, qf);
+      frags_tr_sync<TKQ, XT, NF>(KT, fr0, fk0, kf);
+      auto acc = [&](floatx4& d, const typename MX::frag* a, const XT* b, int it, int jt) {
 #pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-        dS[it][jt] *= eS;
-        dR[it][jt] *= eR;
-        mma_tiles<XT, kChunk, TKQ, TT>(dS[it][jt], QT, i0, blk(bQDB), jt * 16);
-        mma_tiles<XT, kChunk, TKQ, TT>(dS[it][jt], KT, i0, blk(RDN ? bDB_DKS : bDKR), jt * 16);
-        mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], QT, i0, blk(bQDC), jt * 16);
-        if constexpr (RDN) mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], KT, i0, blk(bDKR), jt * 16);
+        for (int ks = 0; ks < KS2; ++ks)
+          d = MX::mma(a[it * KS2 + ks], TT::template frag<MX>(b, jt * 16, ks * MX::kStep), d);
+      };
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          dS[it][jt] *= eS;
+          dR[it][jt] *= eR;
+          acc(dS[it][jt], qf, blk(bQDB), it, jt);
+          acc(dS[it][jt], kf, blk(RDN ? bDB_DKS : bDKR), it, jt);
+          acc(dR[it][jt], qf, blk(bQDC), it, jt);
+          if constexpr (RDN) acc(dR[it][jt], kf, blk(bDKR), it, jt);
+        }
+    } else {
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int i0 = w * (DK / 4) + it * 16;
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          dS[it][jt] *= eS;
+          dR[it][jt] *= eR;
+          mma_tiles<XT, kChunk, TKQ, TT>(dS[it][jt], QT, i0, blk(bQDB), jt * 16);
+          mma_tiles<XT, kChunk, TKQ, TT>(dS[it][jt], KT, i0, blk(RDN ? bDB_DKS : bDKR), jt * 16);
+          mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], QT, i0, blk(bQDC), jt * 16);
+          if constexpr (RDN) mma_tiles<XT, kChunk, TKQ, TT>(dR[it][jt], KT, i0, blk(bDKR), jt * 16);
+        }
       }
     }
     publish_state_max();
@@ -658,9 +692,8 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
       if (c > 0) issue_all_single(c - 1);
     }
     // the next chunk's DMA data must have landed before anyone reads it (bf16
-    // inputs: the update's transpose reads have drained every operation of
-    // the wave; single-buffered fp32 issues its DMAs after the checkpoint
-    // stores)
+    // inputs: the checkpoint stores, issued after the chunk's last DMA, may
+    // still be in flight; single-buffered fp32 issues its DMAs after them)
     wait_vmem_but<L::kDB ? kCkptStores : 0>();
     barrier_lds();
     {   // this chunk's dX, dY, dYR (value-major in LDS) as token-major rows in
