@@ -49,11 +49,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("7073f2c8a5029e13", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168044166, 171984085),
-    "grad_absmax": ("64f05d1d7a9bf2ed", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67195818, 131093),
-    "bwd_scan": ("b5a69d14349110aa", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 407287120, 613419018),
-    "bwd_grad": ("57ad33f971204c55", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232586892, 305333856),
-    "fwd_scan": ("3effebc26a1a0648", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 373579852, 638587430),
+    "prep": ("58be47277bb005b2", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168042589, 109707264),
+    "grad_absmax": ("58aebcb3891a399f", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196002, 131178),
+    "bwd_scan": ("a715cec40acbb23c", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 346969119, 613419008),
+    "bwd_grad": ("f3b7657e103f78f1", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232663241, 302373232),
+    "fwd_scan": ("f561cad3aa9097b4", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 313238770, 638582918),
     "decode": ("093edbbe40eefd13", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746642, 539571891),
 }
 
