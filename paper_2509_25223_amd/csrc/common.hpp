@@ -307,6 +307,60 @@ __device__ __forceinline__ uint4 tile_token_vec8(const void* base, int j0) {
                c[0] | ((uint32_t)c[1] << 16), c[2] | ((uint32_t)c[3] << 16)};
 }
 
+// tile_token_vec8 with its two transpose reads issued as inline assembly, so
+// that the compiler does not drain the wave's in-flight LDS-DMA before them;
+// the function waits for its own reads (lgkmcnt(0), tied to their registers).
+template <class TL>
+__device__ __forceinline__ uint4 tile_token_vec8_sync(const void* base, int j0) {
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const int t = 16 * (lane >> 4) + 4 * (jj & 3), j = j0 + (jj >> 2);
+  const char* b = reinterpret_cast<const char*>(base);
+  const uint32_t a0 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(j, t));
+  const uint32_t a1 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(j + 4, t));
+  u16x4 a, c;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(a) : "v"(a0));
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(c) : "v"(a1));
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(c));
+  return uint4{a[0] | ((uint32_t)a[1] << 16), a[2] | ((uint32_t)a[3] << 16),
+               c[0] | ((uint32_t)c[1] << 16), c[2] | ((uint32_t)c[3] << 16)};
+}
+
+// Token-major 16 bytes of a value-major tile of 16-bit elements (tile rows =
+// values, columns = 64 tokens), 16 tokens per instruction: lane (g, i) (g =
+// lane / 16, i = lane % 16) receives rows 8 g .. 8 g + 7 of column t0 + i, so
+// the four lanes of a token hold 32 consecutive values (a 64-byte store
+// segment).  Two transpose reads as inline assembly (no drain of in-flight
+// LDS-DMA), waited for by the function.
+template <class TL>
+__device__ __forceinline__ uint4 tile_token_rows16_sync(const void* base, int t0) {
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  const int lane = threadIdx.x & 63, jj = lane & 15;
+  const int t = t0 + 4 * (jj & 3), j = 8 * (lane >> 4) + (jj >> 2);
+  const char* b = reinterpret_cast<const char*>(base);
+  const uint32_t a0 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(j, t));
+  const uint32_t a1 = (uint32_t)(uintptr_t)(lds_ptr)(b + TL::off(j + 4, t));
+  u16x4 a, c;
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(a) : "v"(a0));
+  asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(c) : "v"(a1));
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(a), "+v"(c));
+  return uint4{a[0] | ((uint32_t)a[1] << 16), a[2] | ((uint32_t)a[3] << 16),
+               c[0] | ((uint32_t)c[1] << 16), c[2] | ((uint32_t)c[3] << 16)};
+}
+
+// 16 bytes from LDS, issued as inline assembly so that the compiler does not
+// drain the wave's in-flight LDS-DMA before it (it cannot always prove the
+// addresses disjoint); waits for its own read.
+__device__ __forceinline__ uint4 lds_read16_sync(const void* p) {
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)(reinterpret_cast<const char*>(p));
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v));
+  return uint4{v[0], v[1], v[2], v[3]};
+}
+
 // A 64-row tile of 16-bit elements stored row-major (COLS per row, written
 // in 16-byte pieces) and read back as MFMA fragments of its transpose:
 // frag(base, r0, k0) holds rows r0 .. r0+15 of the transpose (tile columns)
@@ -425,10 +479,12 @@ struct MatDma {
   static constexpr int kPerWave = kInst / NW;
   static_assert(kInst % NW == 0, "equal DMA share per wave");
   int off[kPerWave];
-  __device__ __forceinline__ MatDma() {
+  __device__ __forceinline__ MatDma() : MatDma(threadIdx.x >> 6) {}
+  // w: this wave's index among the NW waves that issue the copy
+  __device__ __forceinline__ explicit MatDma(int w) {
     typedef Swz<T> TL;
     constexpr int kEpc = 16 / (int)sizeof(T);   // elements per 16-byte chunk
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int m = 0; m < kPerWave; ++m) {
       const int P = (w * kPerWave + m) * 64 + lane;   // physical 16-byte chunk
@@ -442,12 +498,16 @@ struct MatDma {
 // layout, followed by its zero pad) into a swizzled LDS tile by the NW waves
 // of the workgroup: no lane is masked and no branch is taken.
 template <typename T, int NW = kWaves>
-__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds, const MatDma<T, NW>& md) {
-  const int w = threadIdx.x >> 6;
+__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds, const MatDma<T, NW>& md, int w) {
 #pragma unroll
   for (int m = 0; m < MatDma<T, NW>::kPerWave; ++m)
     dma16(reinterpret_cast<const char*>(gsrc) + md.off[m],
           reinterpret_cast<char*>(lds) + (w * MatDma<T, NW>::kPerWave + m) * 1024);
+}
+
+template <typename T, int NW = kWaves>
+__device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds, const MatDma<T, NW>& md) {
+  dma_mat64<T, NW>(gsrc, lds, md, threadIdx.x >> 6);
 }
 
 // DMA of `bytes` contiguous bytes (a multiple of 1 KiB) by wave `wave` only.

@@ -623,20 +623,603 @@ __global__ __launch_bounds__(kThreads) void fwd_scan_kernel(OpParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wave-specialised forward scan: bf16 inputs, d_k = 128, 32 value columns,
+// the boxed operator (no variant flags).  Eight waves per workgroup in two
+// groups of four that pass the same barriers in the same order:
+//   chain waves (0-3): hold S and R (rows 32 w' .. 32 w' + 31) in their
+//     accumulators and do every product of the chunk (the algebra of
+//     fwd_scan_kernel), loading only their own K and Q rows and storing
+//     nothing to HBM: o goes to LDS;
+//   side waves (4-7): all other HBM traffic — the chunk-start checkpoints
+//     (formed from the LDS state copies), the U, U^R, r blocks, the clip
+//     mask and o, and the staging of the next chunk (LDS-DMA of V and the
+//     matrices, the gate values) — so it overlaps the chain instead of
+//     stalling it.
+// Per chunk (phase: chain waves | side waves):
+//   1: K^T commit; KS, KR, QS, QR;               | the previous chunk's o rows;
+//      Y = diag(b)(V - e^g KS)                     DMA of the next chunk's V, MG,
+//                                                   MP, T^R, MR; its gate values;
+//                                                   S checkpoint
+//   2: U = T^S Y; next K, Q rows                  | DMA of the next T^S
+//   3: p, r = clip(V - p), mask, Y^R;             | R checkpoint; U rows
+//      base = e^g QS + MP U
+//   4: U^R = T^R Y^R                              | r rows, mask
+//   5: S, R update; o = base + diag(gamma) c      | wait for the DMA; next gate
+//      into free LDS; state copies                  vectors; U^R rows
+// V, MG, MP, T^R and MR are double-buffered; T^S (read into registers
+// before the first barrier) is refilled from phase 2.  The precision scheme
+// and the arithmetic are those of fwd_scan_kernel, except that the split-
+// state products sum the hi and lo terms per k-step and the checkpoints are
+// formed from the bf16 hi + lo state copies (the fp32 state to ~16 bits)
+// instead of the accumulators.
+// ---------------------------------------------------------------------------
+template <typename IN, int DK, int BV, bool RDN>
+struct FwdWsLayout {
+  typedef f16 XT;
+  typedef Tile<XT, kChunk> TT;
+  typedef TrTile<XT, DK> TK;
+  typedef Tile<IN, DK> TSC;
+  static constexpr int kNumSlots = RDN ? 9 : 6;
+  static constexpr int kKT = 0;
+  static constexpr int kCopies = kKT + kChunk * TK::kRowB;
+  static constexpr int kCopyBytes = BV * TSC::kRowB;
+  static constexpr int kMats = kCopies + 4 * kCopyBytes;
+  static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
+  static constexpr int kBufBytes = BV * TT::kRowB;
+  static constexpr int kVBytes = kChunk * BV * (int)sizeof(IN);
+  static constexpr int kVc = kBufs + 5 * kBufBytes;   // two V blocks (chunk parity)
+  static constexpr int kGateVec = 8 * kChunk;         // floats per chunk's gate vectors
+  static constexpr int kGates = kVc + 2 * kVBytes;    // two sets (chunk parity)
+  static constexpr int kRst = kGates + 2 * kGateVec * 4;
+  static constexpr int kMst = kRst + kBufBytes;
+  static constexpr int kBytes = kMst + kChunk * BV;
+  static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
+  static_assert(kVBytes == 4 * 1024, "V block = one DMA instruction per side wave");
+  static_assert(kBytes <= 160 * 1024, "forward scan LDS");
+  // RDN: T^S, then MG, MP, T^R, MR each double-buffered; RLA: MG, MP, MR
+  __device__ static constexpr int slot(int mat, int buf) {
+    if (RDN) {
+      if (mat == kMatTS) return 0;
+      if (mat == kMatMG) return 1 + buf;
+      if (mat == kMatMP) return 3 + buf;
+      if (mat == kMatTR) return 5 + buf;
+      return 7 + buf;
+    }
+    if (mat == kMatMG) return buf;
+    if (mat == kMatMP) return 2 + buf;
+    return 4 + buf;
+  }
+};
+
+template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT>
+__global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
+  typedef FwdWsLayout<IN, DK, BV, RDN> L;
+  typedef typename L::XT XT;
+  typedef Mfma<IN> MI;
+  typedef typename L::TT TT;
+  typedef typename L::TK TK;
+  typedef typename L::TSC TSC;
+  constexpr int JT = BV / 16;          // value tiles per block
+  constexpr int IT = DK / 64;          // state row tiles per wave
+  constexpr int KS_STEPS = DK / MI::kStep;
+  extern __shared__ __align__(16) unsigned char smem[];
+  XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
+  IN* Shi = reinterpret_cast<IN*>(smem + L::kCopies);
+  IN* Rhi = reinterpret_cast<IN*>(smem + L::kCopies + 1 * L::kCopyBytes);
+  IN* Slo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);
+  IN* Rlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);
+  auto mat = [&](int m, int buf) {
+    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
+  };
+  XT* Yt = reinterpret_cast<XT*>(smem + L::kBufs);               // Y, later YR
+  XT* Ut = reinterpret_cast<XT*>(smem + L::kBufs + 1 * L::kBufBytes);
+  XT* URt = reinterpret_cast<XT*>(smem + L::kBufs + 2 * L::kBufBytes);
+  XT* DUt = reinterpret_cast<XT*>(smem + L::kBufs + 3 * L::kBufBytes);
+  XT* DURt = reinterpret_cast<XT*>(smem + L::kBufs + 4 * L::kBufBytes);
+  auto vblk = [&](int c) { return reinterpret_cast<IN*>(smem + L::kVc + (c & 1) * L::kVBytes); };
+  float* gates = reinterpret_cast<float*>(smem + L::kGates);
+  XT* Rst = reinterpret_cast<XT*>(smem + L::kRst);            // r (saving mode)
+  uint8_t* Mst = reinterpret_cast<uint8_t*>(smem + L::kMst);  // clip mask (saving mode)
+
+  const int H = p.H, DV = p.DV, tid = threadIdx.x, lane = tid & 63;
+  const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool chain = wu < kWaves;      // wave-uniform role
+  const int ww = wu & (kWaves - 1);    // index within the role's four waves
+  // XCD-aware block mapping (as fwd_scan_kernel)
+  const int nvb = DV / BV;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int pair = (slot / nvb) * 8 + xcd, vb = slot % nvb;
+  if (pair >= p.st.nseq * H) return;
+  const int n = seq_order(p.st, pair / H), h = pair % H;
+  const SeqInfo si = seq_info(p.st, n);
+  const int nch = (si.len + kChunk - 1) / kChunk;
+  const int j0 = vb * BV;
+  const float clip = p.clip;
+  const int64_t state_off = ((int64_t)n * H + h) * DK * DV;
+
+  const IN* qg = reinterpret_cast<const IN*>(p.q);
+  const IN* kg = reinterpret_cast<const IN*>(p.k);
+  const IN* vg = reinterpret_cast<const IN*>(p.v);
+  OT* og = reinterpret_cast<OT*>(p.o);
+  const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
+  XT* fblk = reinterpret_cast<XT*>(p.fwd_blk);   // CKPT: U, UR, r blocks
+  auto chunk_len = [&](int c) { return min(kChunk, si.len - c * kChunk); };
+  auto mat_src = [&](int c, int m) {
+    return matg + ((int64_t)(si.chunk0 + c) * H + h) * kNumMats * kMatElems + m * kMatElems;
+  };
+  // gate vectors of chunk c: beta, gamma, e^{g_t}, e^{g_{t-1}}, e^{h_t},
+  // e^{g_C - g_t}, e^{h_C - h_t}, then [e^{g_C}, e^{h_C}]
+  auto gvec = [&](int c, int k) { return gates + (c & 1) * L::kGateVec + k * kChunk; };
+
+  // One loop body, instantiated once per role (std::true_type: chain
+  // waves): both roles pass the same barriers in the same order by
+  // construction, and each instance gets its own registers.
+  auto run = [&](auto role) {
+  constexpr bool CH = decltype(role)::value;
+  floatx4 Sacc[IT][JT], Racc[IT][JT];  // chain: the states
+  typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];   // chain: next chunk's K, Q rows 16 ww + (lane & 15)
+  float graw0 = 0.f, graw1 = 0.f;      // side: next chunk's gate-block values
+  if constexpr (CH) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = ww * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+          Sacc[it][jt][r] = p.S0 ? p.S0[state_off + (int64_t)i * DV + j] : 0.f;
+          Racc[it][jt][r] = p.R0 ? p.R0[state_off + (int64_t)i * DV + j] : 0.f;
+        }
+  }
+  auto write_state_copies = [&]() {
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        store_state_copy<TSC>(Shi, Slo, jt * 16, ww * (DK / 4) + it * 16, Sacc[it][jt]);
+        store_state_copy<TSC>(Rhi, Rlo, jt * 16, ww * (DK / 4) + it * 16, Racc[it][jt]);
+      }
+  };
+  auto issue_rows = [&](typename MI::frag (&dst)[KS_STEPS], const IN* src, int c) {
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int t = 16 * ww + (lane & 15);
+    const bool ok = t < chunk_len(c);
+    load_rowfrags<IN, DK>(dst, ok ? src + ((tok + t) * H + h) * (int64_t)DK : nullptr);
+  };
+  // side wave ww loads the two gate-block values its gate vectors need:
+  // 0: g_t, g_{t-1}; 1: h_t, h_C; 2: g_t, g_C; 3: beta_t, gamma_t
+  auto issue_gates = [&](int c) {
+    const float* gb = p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock;
+    const int t = lane;
+    const int o0 = ww == 1 ? 64 + t : ww == 3 ? 128 + t : t;
+    const int o1 = ww == 0 ? max(t - 1, 0) : ww == 1 ? 64 + kChunk - 1 : ww == 2 ? kChunk - 1 : 192 + t;
+    graw0 = gb[o0];
+    graw1 = gb[o1];
+  };
+  auto write_gates = [&](int c) {
+    const int t = lane;
+    if (ww == 0) {
+      gvec(c, 2)[t] = __expf(graw0);
+      gvec(c, 3)[t] = t > 0 ? __expf(graw1) : 1.f;
+    } else if (ww == 1) {
+      gvec(c, 4)[t] = __expf(graw0);
+      gvec(c, 6)[t] = __expf(graw1 - graw0);
+      gvec(c, 7)[1] = __expf(graw1);
+    } else if (ww == 2) {
+      gvec(c, 5)[t] = __expf(graw1 - graw0);
+      gvec(c, 7)[0] = __expf(graw1);
+    } else {
+      gvec(c, 0)[t] = graw0;
+      gvec(c, 1)[t] = graw1;
+    }
+  };
+  const MatDma<XT> mdo(ww);   // side waves: this lane's matrix DMA offsets
+  auto issue_early = [&](int c) {   // V, MG, MP, T^R, MR of chunk c (double-buffered)
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    constexpr int kChunksPerRow = BV * (int)sizeof(IN) / 16;
+    const int P = ww * 64 + lane, t = P / kChunksPerRow, cc = P % kChunksPerRow;
+    const int ts = t < len ? t : len - 1;   // padding rows: any valid row (multiplied by 0)
+    dma16(vg + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * (16 / (int)sizeof(IN)),
+          reinterpret_cast<char*>(vblk(c)) + ww * 1024);
+    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, c & 1), mdo, ww);
+    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, c & 1), mdo, ww);
+    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, c & 1), mdo, ww);
+    dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo, ww);
+  };
+  auto issue_ts = [&](int c) {   // T^S (single-buffered)
+    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo, ww);
+  };
+  // side waves: tokens 16 ww .. 16 ww + 15 of a token-major block, one
+  // 64-byte segment per token (lane (g, i): token 16 ww + i, values 8 g ..
+  // 8 g + 7); rows past the end are zero
+  auto store_block = [&](int c, int b, const XT* src) {
+    static_assert(BV == 32 && sizeof(XT) == 2, "four lanes per 32-value token row");
+    const int64_t gc = si.chunk0 + c;
+    const int t = 16 * ww + (lane & 15);
+    const uint4 x = keep_if(tile_token_rows16_sync<TT>(src, 16 * ww), t < chunk_len(c));
+    *reinterpret_cast<uint4*>(fblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
+  };
+  // side waves: chunk-start state X from its copies (hi + lo), rows
+  // 32 ww .. 32 ww + 31, fp16 blocked [DV / 32][DK][32] with one power-of-two
+  // scale per 16-row tile; the wave's two tile scales leave in one store
+  // (lane l writes tile l & 1's)
+  auto load_ckpt = [&](int st, floatx4 (&xv)[IT][JT]) {   // st: 0 = S, 1 = R
+    const IN* hi = st ? Rhi : Shi;
+    const IN* lo = st ? Rlo : Slo;
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        const int c0 = ww * (DK / 4) + it * 16;
+        xv[it][jt] = load_acc_tile<TSC>(hi, jt * 16, c0) + load_acc_tile<TSC>(lo, jt * 16, c0);
+      }
+  };
+  auto store_ckpt = [&](int c, int st, const floatx4 (&xv)[IT][JT]) {
+    const int64_t gc = si.chunk0 + c;
+    uint32_t mt[IT];
+    state_tile_absmax<IT>(xv, mt);
+    f16* dst = reinterpret_cast<f16*>(st ? p.ck_R : p.ck_S) + ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
+    float sc[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int e = pow2_scale_exp(mt[it]);
+      int row, col;
+      const uint4 v = pack_strip_f16(xv[it][0], xv[it][1], exp2_int(-e), row, col);
+      *reinterpret_cast<uint4*>(dst + (int64_t)(ww * (DK / 4) + 16 * it + row) * 32 + col) = v;
+      sc[it] = exp2_int(e);
+    }
+    static_assert(IT == 2, "two tiles per wave");
+    const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
+    if (lane < IT)   // one lane per tile scale
+      (st ? p.ck_R_sc : p.ck_S_sc)[so + (int64_t)(ww * IT + lane) * (DV / 32)] = lane ? sc[1] : sc[0];
+  };
+
+  // KS, KR, QS, QR for this wave's 16 token rows (K, Q as A fragments)
+  // from the state copies: each B fragment read once serves the K and the Q
+  // product; eight independent MFMA chains (value tile x state x K/Q), each
+  // adding the hi and the lo product of every k-step
+  auto split_products = [&](const typename MI::frag (&kf)[KS_STEPS], const typename MI::frag (&qf)[KS_STEPS],
+                            floatx4 (&ks)[JT], floatx4 (&kr)[JT], floatx4 (&qs)[JT], floatx4 (&qr)[JT]) {
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) ks[jt] = kr[jt] = qs[jt] = qr[jt] = zero4();
+#pragma unroll
+    for (int s2 = 0; s2 < KS_STEPS; ++s2)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        const int k0 = s2 * MI::kStep;
+        const typename MI::frag sh = TSC::template frag<MI>(Shi, jt * 16, k0);
+        const typename MI::frag rh = TSC::template frag<MI>(Rhi, jt * 16, k0);
+        const typename MI::frag sl = TSC::template frag<MI>(Slo, jt * 16, k0);
+        const typename MI::frag rl = TSC::template frag<MI>(Rlo, jt * 16, k0);
+        ks[jt] = MI::mma(kf[s2], sh, ks[jt]);
+        qs[jt] = MI::mma(qf[s2], sh, qs[jt]);
+        kr[jt] = MI::mma(kf[s2], rh, kr[jt]);
+        qr[jt] = MI::mma(qf[s2], rh, qr[jt]);
+        ks[jt] = MI::mma(kf[s2], sl, ks[jt]);
+        qs[jt] = MI::mma(qf[s2], sl, qs[jt]);
+        kr[jt] = MI::mma(kf[s2], rl, kr[jt]);
+        qr[jt] = MI::mma(qf[s2], rl, qr[jt]);
+      }
+  };
+
+  // o leaves through LDS regions that are free from phase 5 until the side
+  // waves read them in the next chunk's phase 1: value tile 0 in chunk c's
+  // V block, tile 1 in the r block; wave ww's 16 rows as 1 KiB at ww KiB,
+  // row-major [16][16] in OT.  The side wave reads its slice of the V block
+  // before its own DMA refills that slice.
+  auto ostage = [&](int c, int jt) {
+    return reinterpret_cast<char*>(jt ? reinterpret_cast<char*>(Rst) : reinterpret_cast<char*>(vblk(c))) + ww * 1024;
+  };
+  auto store_o = [&](int c) {   // side waves: chunk c's o rows 16 ww .. 16 ww + 15
+    constexpr int kVE = 16 / (int)sizeof(OT);   // elements per 16 bytes
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    const int t = 16 * ww + lane / (16 / kVE), col = (lane % (16 / kVE)) * kVE;
+#pragma unroll
+    for (int jt = 0; jt < JT; ++jt) {
+      const uint4 v = lds_read16_sync(ostage(c, jt) + (lane % (16 * 16 / kVE)) * 16);
+      if (lane < 16 * 16 / kVE && t < len)
+        *reinterpret_cast<uint4*>(og + (tok + t) * H * (int64_t)DV + h * (int64_t)DV + j0 + jt * 16 + col) = v;
+    }
+  };
+
+  // ---- prologue: chunk 0's staging and the initial state copies ----
+  if (nch > 0) {
+    if constexpr (CH) {
+      issue_rows(Kn, kg, 0);
+      issue_rows(Qn, qg, 0);
+    } else {
+      issue_gates(0);
+      issue_early(0);
+      issue_ts(0);
+      wait_vmem();
+      write_gates(0);
+    }
+  }
+  if constexpr (CH) write_state_copies();
+  barrier_lds();
+
+  floatx4 KS[JT], KR[JT], QS[JT], QR[JT], base[JT];
+  float vloc[JT][4];
+  MatFrags<XT> aTS, aMG, aMP, aTR, aMR;
+  for (int c = 0; c < nch; ++c) {
+    const int len = chunk_len(c);
+    const int buf = c & 1;
+    const bool more = c + 1 < nch;
+    const float* gbt = gvec(c, 0);
+    const float* ggm = gvec(c, 1);
+    const float* egs = gvec(c, 2);
+    const float* egsp = gvec(c, 3);
+    const float* egr = gvec(c, 4);
+    const float* dls = gvec(c, 5);
+    const float* dlr = gvec(c, 6);
+    const float* edge = gvec(c, 7);
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+
+    // ======== phase 1 ========
+    if constexpr (CH) {
+      typename MI::frag Kf[KS_STEPS], Qf[KS_STEPS];
+      const int t = 16 * ww + (lane & 15);
+#pragma unroll
+      for (int s2 = 0; s2 < KS_STEPS; ++s2) {   // K^T commit: row t, 8 columns per store
+        Kf[s2] = Kn[s2];
+        Qf[s2] = Qn[s2];
+        const u16x8 kv = __builtin_bit_cast(u16x8, Kf[s2]);
+        f16x8 kh;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
+        *reinterpret_cast<f16x8*>(TK::ptr(KT, t, s2 * 32 + (lane >> 4) * 8)) = kh;
+      }
+      split_products(Kf, Qf, KS, KR, QS, QR);
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        const u16x4 v4 = acc_tile_tr<PadRows<IN, BV, 0>>(vblk(c), 16 * ww, jt * 16);
+        floatx4 y;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int tr = 16 * ww + acc_row(r);
+          vloc[jt][r] = bf2f(v4[r]);
+          y[r] = RDN ? gbt[tr] * __builtin_fmaf(-egs[tr], KS[jt][r], vloc[jt][r]) : gbt[tr] * vloc[jt][r];
+        }
+        if constexpr (RDN) {
+          store_acc_tile<TT>(Yt, jt * 16, 16 * ww, y);
+        } else {
+          floatx4 du;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) du[r] = dls[16 * ww + acc_row(r)] * y[r];
+          store_acc_tile<TT>(Ut, jt * 16, 16 * ww, y);
+          store_acc_tile<TT>(DUt, jt * 16, 16 * ww, du);
+        }
+      }
+      if constexpr (RDN) aTS = swz_rows_frags<XT>(mat(kMatTS, 0), 16 * ww);
+      else aMG = swz_rows_frags<XT>(mat(kMatMG, buf), 16 * ww);
+    } else {
+      if constexpr (WRITE_O) {
+        if (c > 0) store_o(c - 1);   // before the DMA below refills chunk c - 1's V block
+      }
+      if (more) {
+        issue_early(c + 1);
+        issue_gates(c + 1);
+      }
+      if constexpr (CKPT) {   // chunk-start S
+        floatx4 xs[IT][JT];
+        load_ckpt(0, xs);
+        store_ckpt(c, 0, xs);
+      }
+    }
+    barrier_lds();
+
+    // ======== phase 2 ========
+    if constexpr (CH) {
+      if constexpr (RDN) {   // U = T^S Y
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          floatx4 u = zero4();
+          mma_frags<XT>(u, aTS, Yt, jt * 16);
+          floatx4 du;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) du[r] = dls[16 * ww + acc_row(r)] * u[r];
+          store_acc_tile<TT>(Ut, jt * 16, 16 * ww, u);
+          store_acc_tile<TT>(DUt, jt * 16, 16 * ww, du);
+        }
+        aMG = swz_rows_frags<XT>(mat(kMatMG, buf), 16 * ww);
+      }
+      if constexpr (WRITE_O) aMP = swz_rows_frags<XT>(mat(kMatMP, buf), 16 * ww);
+      if (more) {   // the next K, Q rows, while the side waves issue little
+        issue_rows(Kn, kg, c + 1);
+        issue_rows(Qn, qg, c + 1);
+      }
+    } else {
+      if (more) issue_ts(c + 1);   // T^S was read into registers before the first barrier
+    }
+    barrier_lds();
+
+    // ======== phase 3 ========
+    if constexpr (CH) {   // residual, clip, Y^R (explicit fmas as fwd_scan_kernel)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        floatx4 mgu = zero4();
+        mma_frags<XT>(mgu, aMG, Ut, jt * 16);
+        floatx4 y, rv;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * ww + acc_row(r);
+          const float x = __builtin_fmaf(-egsp[t], KS[jt][r], vloc[jt][r]) - mgu[r];
+          const float rr = clip < 0.f ? x : fminf(fmaxf(x, -clip), clip);
+          rv[r] = rr;
+          if constexpr (CKPT) Mst[t * BV + jt * 16 + acc_col()] = (clip < 0.f || fabsf(x) <= clip) ? 1 : 0;
+          y[r] = RDN ? ggm[t] * __builtin_fmaf(-egr[t], KR[jt][r], rr) : ggm[t] * rr;
+        }
+        if constexpr (RDN) {
+          store_acc_tile<TT>(Yt, jt * 16, 16 * ww, y);
+        } else {
+          floatx4 du;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) du[r] = dlr[16 * ww + acc_row(r)] * y[r];
+          store_acc_tile<TT>(URt, jt * 16, 16 * ww, y);
+          store_acc_tile<TT>(DURt, jt * 16, 16 * ww, du);
+        }
+        if constexpr (CKPT) store_acc_tile<TT>(Rst, jt * 16, 16 * ww, rv);
+      }
+      if constexpr (WRITE_O) {   // base = e^g QS + MP U
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          floatx4 mpu = zero4();
+          mma_frags<XT>(mpu, aMP, Ut, jt * 16);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) base[jt][r] = __builtin_fmaf(egs[16 * ww + acc_row(r)], QS[jt][r], mpu[r]);
+        }
+      }
+      if constexpr (RDN) aTR = swz_rows_frags<XT>(mat(kMatTR, buf), 16 * ww);
+    } else {
+      if constexpr (CKPT) {   // chunk-start R
+        floatx4 xr[IT][JT];
+        load_ckpt(1, xr);
+        store_ckpt(c, 1, xr);
+      }
+      if constexpr (CKPT) store_block(c, 0, Ut);
+    }
+    barrier_lds();
+
+    // ======== phase 4 ========
+    if constexpr (CH) {
+      if constexpr (RDN) {   // U^R = T^R Y^R
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          floatx4 u = zero4();
+          mma_frags<XT>(u, aTR, Yt, jt * 16);
+          floatx4 du;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) du[r] = dlr[16 * ww + acc_row(r)] * u[r];
+          store_acc_tile<TT>(URt, jt * 16, 16 * ww, u);
+          store_acc_tile<TT>(DURt, jt * 16, 16 * ww, du);
+        }
+      }
+      if constexpr (WRITE_O) aMR = swz_rows_frags<XT>(mat(kMatMR, buf), 16 * ww);
+    } else {
+      if constexpr (CKPT) {
+        store_block(c, 2, Rst);
+        {   // clip mask rows (side waves 0 and 1, one 16-byte piece per lane);
+            // past the end, a lane rewrites the last row's own bytes, so the
+            // store needs no lane condition
+          constexpr int kVPR = BV / 16;
+          const int e = (ww & 1) * 64 + lane, t = min(e / kVPR, len - 1), v = e % kVPR;
+          if (ww < 2)
+            *reinterpret_cast<uint4*>(p.ck_mask + ((tok + t) * H + h) * (int64_t)DV + j0 + v * 16) =
+                lds_read16_sync(Mst + t * BV + v * 16);
+        }
+      }
+    }
+    barrier_lds();
+
+    // ======== phase 5 ========
+    if constexpr (CH) {   // S <- e^{g_C} S + K^T DU, R <- e^{h_C} R + K^T DUR
+      const float eS = edge[0], eR = edge[1];
+      typedef Mfma<XT> MX;
+      constexpr int NF = IT * (kChunk / MX::kStep);
+      int fr0[NF], fk0[NF];
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        fr0[f] = ww * (DK / 4) + (f / (kChunk / MX::kStep)) * 16;
+        fk0[f] = (f % (kChunk / MX::kStep)) * MX::kStep;
+      }
+      typename MX::frag kt[NF];
+      frags_tr_sync<TK, XT, NF>(KT, fr0, fk0, kt);
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          Sacc[it][jt] *= eS;
+          Racc[it][jt] *= eR;
+#pragma unroll
+          for (int ks = 0; ks < kChunk / MX::kStep; ++ks) {
+            const int f = it * (kChunk / MX::kStep) + ks;
+            Sacc[it][jt] = MX::mma(kt[f], TT::template frag<MX>(DUt, jt * 16, ks * MX::kStep), Sacc[it][jt]);
+            Racc[it][jt] = MX::mma(kt[f], TT::template frag<MX>(DURt, jt * 16, ks * MX::kStep), Racc[it][jt]);
+          }
+        }
+      if constexpr (WRITE_O) {   // o = base + diag(gamma) (e^h QR + MR UR), this wave's rows
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          floatx4 mru = zero4(), ov;
+          mma_frags<XT>(mru, aMR, URt, jt * 16);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = 16 * ww + acc_row(r);
+            ov[r] = __builtin_fmaf(ggm[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
+          }
+          // quad transpose: this lane's row 4 (lane / 16) + lane % 4, columns
+          // 4 ((lane % 16) / 4) .. + 3 of the wave's 16 x 16 tile
+          const floatx4 x = quad_transpose(ov);
+          const int row = 4 * (lane >> 4) + (lane & 3), col = 4 * ((lane & 15) >> 2);
+          char* dst = ostage(c, jt) + (row * 16 + col) * (int)sizeof(OT);
+          if constexpr (sizeof(OT) == 4) {
+            *reinterpret_cast<floatx4*>(dst) = x;
+          } else {
+            u16x4 b;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) b[k] = f2bf(x[k]);
+            *reinterpret_cast<u16x4*>(dst) = b;
+          }
+        }
+      }
+      write_state_copies();
+    } else {
+      // the next chunk's DMA (and this wave's earlier stores) complete; the
+      // barrier below publishes the DMA data
+      wait_vmem();
+      if (more) write_gates(c + 1);
+      if constexpr (CKPT) store_block(c, 1, URt);
+    }
+    barrier_lds();
+  }
+
+  if constexpr (!CH && WRITE_O) {
+    if (nch > 0) store_o(nch - 1);
+  }
+  if constexpr (CH) {
+    if (p.S_fin || p.R_fin) {
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ww * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+            if (p.S_fin) p.S_fin[state_off + (int64_t)i * DV + j] = Sacc[it][jt][r];
+            if (p.R_fin) p.R_fin[state_off + (int64_t)i * DV + j] = Racc[it][jt][r];
+          }
+    }
+  }
+  };
+  if (chain) run(std::true_type{});
+  else run(std::false_type{});
+}
+
 template <typename IN, int DK, int BV, bool RDN, bool WRITE_O, bool CKPT, typename OT>
 hipError_t launch_fwd_t(const OpParams& p, hipStream_t stream) {
   typedef FwdLayout<IN, DK, BV, RDN> L;
-  auto kern = ((p.vflags & kVarOperator) || p.qk_f16)
-                  ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
+  const bool var = (p.vflags & kVarOperator) || p.qk_f16;
+  auto kern = var ? fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, true>
                   : fwd_scan_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT, false>;
+  int threads = kThreads, lds = L::kBytes;
+  if constexpr (sizeof(IN) == 2 && DK == 128 && BV == 32) {
+    if (!var) {   // the boxed operator: the wave-specialised scan
+      kern = fwd_scan_ws_kernel<IN, DK, BV, RDN, WRITE_O, CKPT, OT>;
+      threads = 2 * kThreads;
+      lds = FwdWsLayout<IN, DK, BV, RDN>::kBytes;
+    }
+  }
   hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (err != hipSuccess) return err;
   const int nvb = p.DV / BV;
   const int npairs = p.st.nseq * p.H;
   const int grid = ((npairs + 7) / 8) * 8 * nvb;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreads), L::kBytes, stream, p);
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(threads), lds, stream, p);
   return hipGetLastError();
 }
 
