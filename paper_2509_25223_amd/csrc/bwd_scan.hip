@@ -735,6 +735,547 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Wave-specialised reverse scan: bf16 inputs, d_k = 128, 32 value columns,
+// the boxed operator (no variant flags).  Eight waves per workgroup in two
+// groups of four that pass the same seven barriers per chunk in the same
+// order:
+//   chain waves (0-3): hold dS and dR (rows 32 w' .. 32 w' + 31) and do every
+//     product of the chunk (the algebra of bwd_scan_kernel), load their K, Q
+//     and dO rows and store the chunk-end checkpoints; dv goes to LDS (fp32);
+//   side waves (4-7): the dX, dY, dYR blocks and dv, the gate vectors of the
+//     next (earlier) chunk and the LDS-DMA of its matrices and clip mask, so
+//     that these memory operations overlap the chain.
+// Per chunk (phase: chain waves | side waves), walking backwards:
+//   0: state copies; K^T, Q^T, dO^T commit        | the later chunk's blocks and dv
+//   1: K dS, K dR; dc, e^g db, e^h dc             | the next chunk's gate values;
+//                                                   DMA of its MR (double-buffered)
+//   2: next K, Q, dO rows; dUR                    |
+//   3: dYR, dX, dKR                               | DMA of the next T^R
+//   4: dU                                         | DMA of the next mask, MG, MP
+//   5: dY, dKS; dv into LDS; checkpoints          | DMA of the next T^S
+//   6: dS, dR at the chunk start; their maxima    | wait for the DMA; next gate vectors
+// Each matrix is refilled once the chain has read it into registers (T^R,
+// MG, MP, T^S) or, for MR, into the other buffer.
+// ---------------------------------------------------------------------------
+template <typename IN, int DK, int BV, bool RDN>
+struct BwdWsLayout {
+  typedef BwdScanLayout<IN, DK, BV, RDN, false> B;
+  typedef typename B::XT XT;
+  typedef typename B::TT TT;
+  typedef typename B::TKQ TKQ;
+  typedef typename B::TSC TSC;
+  static constexpr int kKT = B::kKT, kQT = B::kQT, kCopies = B::kCopies, kCopyBytes = B::kCopyBytes;
+  static constexpr int kMats = B::kMats, kBufs = B::kBufs, kBufBytes = B::kBufBytes, kMask = B::kMask;
+  static constexpr int kGateVec = 8 * kChunk;   // floats per chunk's gate vectors
+  static constexpr int kGates = B::kMask + B::kMaskBytes;   // two sets (chunk parity)
+  static constexpr int kYst = kGates + 2 * kGateVec * 4;    // dYR (token tile)
+  static constexpr int kRed = kYst + kBufBytes;             // per-wave maxima [8]
+  static constexpr int kDv = kRed + 8 * 4;                  // dv, fp32 [64][BV]
+  static constexpr int kBytes = kDv + kChunk * BV * 4;
+  static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
+  static_assert(kBytes <= 160 * 1024, "backward scan LDS");
+  __device__ static constexpr int slot(int mat, int buf) { return B::slot(mat, buf); }
+};
+
+template <typename IN, int DK, int BV, bool RDN>
+__global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
+  typedef BwdWsLayout<IN, DK, BV, RDN> L;
+  typedef typename L::XT XT;
+  typedef typename L::TT TT;
+  typedef typename L::TKQ TKQ;
+  typedef typename L::TSC TSC;
+  typedef Mfma<IN> MI;
+  constexpr int JT = BV / 16;
+  constexpr int IT = DK / 64;
+  constexpr int KS_STEPS = DK / MI::kStep;
+  extern __shared__ __align__(16) unsigned char smem_[];
+  unsigned char* smem = smem_;
+  XT* KT = reinterpret_cast<XT*>(smem + L::kKT);
+  XT* QT = reinterpret_cast<XT*>(smem + L::kQT);
+  XT* dSc = reinterpret_cast<XT*>(smem + L::kCopies);
+  XT* dRc = reinterpret_cast<XT*>(smem + L::kCopies + L::kCopyBytes);
+  uint32_t* smax = reinterpret_cast<uint32_t*>(smem + L::kRed);
+  uint8_t* mask = reinterpret_cast<uint8_t*>(smem + L::kMask);
+  float* gates = reinterpret_cast<float*>(smem + L::kGates);
+  XT* Yst = reinterpret_cast<XT*>(smem + L::kYst);
+  float* dvst = reinterpret_cast<float*>(smem + L::kDv);
+  auto mat = [&](int m, int buf) {
+    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
+  };
+  auto blk = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBufs + b * L::kBufBytes); };
+  // gate vectors of chunk c: beta, gamma, e^{g_t}, e^{g_{t-1}}, e^{h_t},
+  // e^{g_C - g_t}, e^{h_C - h_t}, then [e^{g_C}, e^{h_C}]
+  auto gvec = [&](int c, int k) { return gates + (c & 1) * L::kGateVec + k * kChunk; };
+
+  const int H = p.H, DV = p.DV, tid = threadIdx.x, lane = tid & 63;
+  const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool chain = wu < kWaves;      // wave-uniform role
+  const int ww = wu & (kWaves - 1);    // index within the role's four waves
+  const int nvb = DV / BV;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int pair = (slot / nvb) * 8 + xcd, vb = slot % nvb;
+  if (pair >= p.st.nseq * H) return;
+  const int n = seq_order(p.st, pair / H), h = pair % H;
+  const SeqInfo si = seq_info(p.st, n);
+  const int nch = (si.len + kChunk - 1) / kChunk;
+  const int j0 = vb * BV;
+  const int64_t state_off = ((int64_t)n * H + h) * DK * DV;
+
+  // scale of the upstream gradients of this (sequence, head), as
+  // bwd_scan_kernel (over all eight waves)
+  float sig = 1.f, isig = 1.f;
+  if (p.grad_absmax) {
+    uint32_t m = 0;
+    for (int c = tid; c < nch; c += 2 * kThreads)
+      m = max(m, p.grad_absmax[(int64_t)(si.chunk0 + c) * H + h]);
+    m = wave_absmax_bits(m);
+    smax[wu] = m;   // every lane stores the wave-uniform value
+    barrier_lds();
+    m = 0;
+#pragma unroll
+    for (int k = 0; k < 2 * kWaves; ++k) m = max(m, smax[k]);
+    barrier_lds();
+    const int be = (int)(m >> 23);
+    const int e = be == 0 ? 0 : min(max(129 - be, -126), 126);
+    sig = exp2_int(e);
+    isig = exp2_int(-e);
+    if (vb == 0 && tid == 0) p.grad_scale[(int64_t)n * H + h] = sig;
+  }
+
+  const IN* qg = reinterpret_cast<const IN*>(p.q);
+  const IN* kg = reinterpret_cast<const IN*>(p.k);
+  const IN* dog = reinterpret_cast<const IN*>(p.dO);
+  const XT* matg = reinterpret_cast<const XT*>(p.mat_ws);
+  XT* bblk = reinterpret_cast<XT*>(p.bwd_blk);
+  auto chunk_len = [&](int c) { return min(kChunk, si.len - c * kChunk); };
+  auto mat_src = [&](int c, int m) {
+    return matg + ((int64_t)(si.chunk0 + c) * H + h) * kNumMats * kMatElems + m * kMatElems;
+  };
+  constexpr int kOPerThread = 16 / (int)sizeof(IN);
+  static_assert(kChunk * BV == kThreads * kOPerThread, "one dO vector per chain thread");
+
+  // One loop body, instantiated once per role (std::true_type: chain
+  // waves): both roles pass the same barriers in the same order by
+  // construction, and each instance gets its own registers.
+  auto run = [&](auto role) {
+  constexpr bool CH = decltype(role)::value;
+  floatx4 dS[IT][JT], dR[IT][JT];      // chain: the gradient states
+  typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];
+  IN on[kOPerThread];
+  float scS = 1.f, scR = 1.f;
+  uint32_t tmS[IT], tmR[IT];
+  float graw0 = 0.f, graw1 = 0.f;      // side: the next chunk's gate-block values
+  auto publish_state_max = [&]() {   // chain
+    state_tile_absmax<IT>(dS, tmS);
+    state_tile_absmax<IT>(dR, tmR);
+    uint32_t ms = tmS[0], mr = tmR[0];
+#pragma unroll
+    for (int it = 1; it < IT; ++it) {
+      ms = max(ms, tmS[it]);
+      mr = max(mr, tmR[it]);
+    }
+    smax[ww] = ms;   // every lane stores the wave-uniform value
+    smax[4 + ww] = mr;
+  };
+  auto write_copies = [&]() {   // chain, after a barrier that follows publish_state_max
+    const uint32_t ms = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
+    const uint32_t mr = max(max(smax[4], smax[5]), max(smax[6], smax[7]));
+    const int es = pow2_scale_exp(ms), er = pow2_scale_exp(mr);
+    scS = exp2_int(es);
+    scR = exp2_int(er);
+    const float iS = exp2_int(-es), iR = exp2_int(-er);
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        store_state_copy<TSC>(dSc, jt * 16, ww * (DK / 4) + it * 16, dS[it][jt] * iS);
+        store_state_copy<TSC>(dRc, jt * 16, ww * (DK / 4) + it * 16, dR[it][jt] * iR);
+      }
+  };
+  auto issue_regs = [&](int c) {   // chain: K, Q rows and this thread's dO vector of chunk c
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    const int t = 16 * ww + (lane & 15);
+    const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
+    load_rowfrags<IN, DK>(Kn, t < len ? kg + roff : nullptr);
+    load_rowfrags<IN, DK>(Qn, t < len ? qg + roff : nullptr);
+    typedef IN INV __attribute__((ext_vector_type(kOPerThread)));
+    const int tt = lane, j = ww * kOPerThread;
+    INV v = {};
+    if (tt < len) v = *reinterpret_cast<const INV*>(dog + ((tok + tt) * H + h) * (int64_t)DV + j0 + j);
+#pragma unroll
+    for (int u = 0; u < kOPerThread; ++u) on[u] = v[u];
+  };
+  // side wave ww loads the two gate-block values its gate vectors need:
+  // 0: g_t, g_{t-1}; 1: h_t, h_C; 2: g_t, g_C; 3: beta_t, gamma_t
+  auto issue_gates = [&](int c) {
+    const float* gb = p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock;
+    const int t = lane;
+    const int o0 = ww == 1 ? 64 + t : ww == 3 ? 128 + t : t;
+    const int o1 = ww == 0 ? max(t - 1, 0) : ww == 1 ? 64 + kChunk - 1 : ww == 2 ? kChunk - 1 : 192 + t;
+    graw0 = gb[o0];
+    graw1 = gb[o1];
+  };
+  auto write_gates = [&](int c) {
+    const int t = lane;
+    if (ww == 0) {
+      gvec(c, 2)[t] = __expf(graw0);
+      gvec(c, 3)[t] = t > 0 ? __expf(graw1) : 1.f;
+    } else if (ww == 1) {
+      gvec(c, 4)[t] = __expf(graw0);
+      gvec(c, 6)[t] = __expf(graw1 - graw0);
+      gvec(c, 7)[1] = __expf(graw1);
+    } else if (ww == 2) {
+      gvec(c, 5)[t] = __expf(graw1 - graw0);
+      gvec(c, 7)[0] = __expf(graw1);
+    } else {
+      gvec(c, 0)[t] = graw0;
+      gvec(c, 1)[t] = graw1;
+    }
+  };
+  const MatDma<XT> mdo(ww);   // side waves: this lane's matrix DMA offsets
+  auto issue_mask = [&](int c) {   // side: rows of BV bytes; padding rows read row 0 (masked by 0 gradients)
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    constexpr int kPerRow = BV / 16;
+    constexpr int kInst = kChunk * BV / 1024;
+    static_assert(kInst <= kWaves, "one mask DMA instruction per side wave at most");
+    if (ww < kInst) {
+      const int P = ww * 64 + lane, t = P / kPerRow, cc = P % kPerRow;
+      const int ts = t < len ? t : 0;
+      dma16(p.ck_mask + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * 16, mask + ww * 1024);
+    }
+  };
+  // side: this chunk's dX, dY, dYR blocks (tokens 16 ww .. 16 ww + 15, one
+  // 64-byte segment per token; rows past the end are zero) and dv rows
+  auto store_outputs = [&](int c) {
+    static_assert(sizeof(XT) == 2, "four lanes per 32-value token row");
+    const int64_t gc = si.chunk0 + c;
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const int len = chunk_len(c);
+    {
+      const int t = 16 * ww + (lane & 15);
+#pragma unroll
+      for (int b = 0; b < 3; ++b) {
+        const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
+        const uint4 x = keep_if(tile_token_rows16_sync<TT>(srcb, 16 * ww), t < len);
+        *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {   // dv rows 16 ww + 8 u + lane / 8, columns 4 (lane % 8) ..
+      const int t = 16 * ww + 8 * u + (lane >> 3), col = 4 * (lane & 7);
+      const uint4 x = lds_read16_sync(dvst + t * BV + col);
+      if (t < len) {
+        const int64_t o = ((tok + t) * H + h) * (int64_t)DV + j0 + col;
+        if (p.out_bf16) {
+          const floatx4 f = {__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
+          u16x4 b;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) b[e] = f2bf(f[e]);
+          *reinterpret_cast<u16x4*>(reinterpret_cast<u16*>(p.dv) + o) = b;
+        } else {
+          *reinterpret_cast<uint4*>(reinterpret_cast<float*>(p.dv) + o) = x;
+        }
+      }
+    }
+  };
+
+  // ---- prologue: the last chunk's staging; the end-state maxima ----
+  if constexpr (CH) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = ww * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+          dS[it][jt][r] = p.dS_fin ? p.dS_fin[state_off + (int64_t)i * DV + j] * sig : 0.f;
+          dR[it][jt][r] = p.dR_fin ? p.dR_fin[state_off + (int64_t)i * DV + j] * sig : 0.f;
+        }
+    if (nch > 0) issue_regs(nch - 1);
+    publish_state_max();
+  } else {
+    if (nch > 0) {
+      const int c = nch - 1;
+      issue_gates(c);
+      issue_mask(c);
+      if constexpr (RDN) {
+        dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo, ww);
+        dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0), mdo, ww);
+      }
+      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0), mdo, ww);
+      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0), mdo, ww);
+      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo, ww);
+      wait_vmem();
+      write_gates(c);
+    }
+  }
+  barrier_lds();
+
+  floatx4 KdS[JT], KdR[JT], dUR[JT], dX[JT];
+  MatFrags<XT> aMR, aTR, aMP, aMG, aTS;
+  for (int c = nch - 1; c >= 0; --c) {
+    const int gc = si.chunk0 + c;
+    const int buf = c & 1;
+    const int len = chunk_len(c);
+    const int64_t tok = si.start + (int64_t)c * kChunk;
+    const float* gbt = gvec(c, 0);
+    const float* ggm = gvec(c, 1);
+    const float* egs = gvec(c, 2);
+    const float* egsp = gvec(c, 3);
+    const float* egr = gvec(c, 4);
+    const float* dls = gvec(c, 5);
+    const float* dlr = gvec(c, 6);
+    const float* edge = gvec(c, 7);
+
+    // ======== phase 0: copies and commit | the later chunk's outputs ========
+    if constexpr (CH) {
+      write_copies();
+      const int t = 16 * ww + (lane & 15);
+#pragma unroll
+      for (int s2 = 0; s2 < KS_STEPS; ++s2) {   // row t, 8 columns: one 16-byte store each
+        const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
+        const u16x8 qv = __builtin_bit_cast(u16x8, Qn[s2]);
+        f16x8 kh, qh;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          kh[e] = (f16)bf2f(kv[e]);
+          qh[e] = (f16)bf2f(qv[e]);
+        }
+        const int i = s2 * 32 + (lane >> 4) * 8;
+        *reinterpret_cast<f16x8*>(TKQ::ptr(KT, t, i)) = kh;
+        *reinterpret_cast<f16x8*>(TKQ::ptr(QT, t, i)) = qh;
+      }
+      XT* dbT = blk(bDB_DKS);
+#pragma unroll
+      for (int u = 0; u < kOPerThread; ++u)   // lanes write consecutive tokens
+        *TT::ptr(dbT, ww * kOPerThread + u, lane) = from_f<XT>(to_f<IN>(on[u]) * sig);
+    } else {
+      if (c + 1 < nch) store_outputs(c + 1);
+    }
+    barrier_lds();
+
+    // ======== phase 1: K dS_end, K dR_end; dc, e^g db, e^h dc ========
+    if constexpr (CH) {
+      typename Mfma<XT>::frag Kf[KS_STEPS];
+#pragma unroll
+      for (int s2 = 0; s2 < KS_STEPS; ++s2) {
+        const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
+        f16x8 kh;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
+        Kf[s2] = kh;
+      }
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        KdS[jt] = zero4();
+        KdR[jt] = zero4();
+        mma_rega_tile<XT, DK, TSC>(KdS[jt], Kf, dSc, jt * 16);
+        mma_rega_tile<XT, DK, TSC>(KdR[jt], Kf, dRc, jt * 16);
+        KdS[jt] *= scS;   // undo the copies' scales (powers of two: exact)
+        KdR[jt] *= scR;
+        floatx4 dc, qdb, qdc;
+        const floatx4 o4 = load_acc_tile<TT>(blk(bDB_DKS), jt * 16, 16 * ww);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * ww + acc_row(r);
+          dc[r] = ggm[t] * o4[r];
+          qdb[r] = egs[t] * o4[r];
+          qdc[r] = egr[t] * dc[r];
+        }
+        store_acc_tile<TT>(blk(bDC_DX), jt * 16, 16 * ww, dc);
+        store_acc_tile<TT>(blk(bQDB), jt * 16, 16 * ww, qdb);
+        store_acc_tile<TT>(blk(bQDC), jt * 16, 16 * ww, qdc);
+      }
+      aMR = swz_cols_frags_sync<XT>(mat(kMatMR, buf), 16 * ww);
+    } else {
+      if (c > 0) {
+        issue_gates(c - 1);
+        dma_mat64<XT>(mat_src(c - 1, kMatMR), mat(kMatMR, (c - 1) & 1), mdo, ww);
+      }
+    }
+    barrier_lds();
+
+    // ======== phase 2: dUR = diag(e^{h_C-h}) K dR_end + MR^T dc ========
+    if constexpr (CH) {
+      if (c > 0) issue_regs(c - 1);
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        floatx4 a = zero4();
+        mma_frags<XT, TT>(a, aMR, blk(bDC_DX), jt * 16);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dUR[jt][r] = dlr[16 * ww + acc_row(r)] * KdR[jt][r] + a[r];
+        if constexpr (RDN) store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * ww, dUR[jt]);
+      }
+      if constexpr (RDN) aTR = swz_cols_frags_sync<XT>(mat(kMatTR, 0), 16 * ww);
+    }
+    barrier_lds();
+
+    // ======== phase 3: dYR, dX, dKR (RLA: dKS) ========
+    if constexpr (CH) {
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        floatx4 dYR = dUR[jt];
+        if constexpr (RDN) {
+          dYR = zero4();
+          mma_frags<XT, TT>(dYR, aTR, blk(bDUR_DU), jt * 16);
+        }
+        floatx4 dkr, dks;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int t = 16 * ww + acc_row(r), j = jt * 16 + acc_col();
+          dX[jt][r] = mask[t * BV + j] ? ggm[t] * dYR[r] : 0.f;
+          dkr[r] = -ggm[t] * egr[t] * dYR[r];
+          dks[r] = -egsp[t] * dX[jt][r];
+        }
+        store_acc_tile<TT>(blk(bDC_DX), jt * 16, 16 * ww, dX[jt]);
+        store_acc_tile<TT>(blk(bDKR), jt * 16, 16 * ww, RDN ? dkr : dks);
+        store_acc_tile<TT>(Yst, jt * 16, 16 * ww, dYR);
+      }
+      aMP = swz_cols_frags_sync<XT>(mat(kMatMP, 0), 16 * ww);
+      aMG = swz_cols_frags_sync<XT>(mat(kMatMG, 0), 16 * ww);
+    } else {
+      if constexpr (RDN) {   // T^R was read into registers before the previous barrier
+        if (c > 0) dma_mat64<XT>(mat_src(c - 1, kMatTR), mat(kMatTR, 0), mdo, ww);
+      }
+    }
+    barrier_lds();
+
+    // ======== phase 4: dU = diag(e^{g_C-g}) K dS_end + MP^T db - MG^T dX ========
+    floatx4 dU[JT];   // RLA: U = diag(b) V, so dV gets b dU
+    if constexpr (CH) {
+#pragma unroll
+      for (int jt = 0; jt < JT; ++jt) {
+        floatx4 a = zero4(), b = zero4();
+        mma_frags<XT, TT>(a, aMP, blk(bDB_DKS), jt * 16);
+        mma_frags<XT, TT>(b, aMG, blk(bDC_DX), jt * 16);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dU[jt][r] = dls[16 * ww + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
+        store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * ww, dU[jt]);
+      }
+      if constexpr (RDN) aTS = swz_cols_frags_sync<XT>(mat(kMatTS, 0), 16 * ww);
+    } else {
+      if (c > 0) {   // the mask (read in phase 3) and MG, MP (read into registers)
+        issue_mask(c - 1);
+        dma_mat64<XT>(mat_src(c - 1, kMatMG), mat(kMatMG, 0), mdo, ww);
+        dma_mat64<XT>(mat_src(c - 1, kMatMP), mat(kMatMP, 0), mdo, ww);
+      }
+    }
+    barrier_lds();
+
+    // ======== phase 5: dY = T^S^T dU, dKS; dv; checkpoints ========
+    if constexpr (CH) {
+      floatx4 tail[JT];   // RDN: dY; RLA: dU
+      if constexpr (RDN) {
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          floatx4 dks;
+          tail[jt] = zero4();
+          mma_frags<XT, TT>(tail[jt], aTS, blk(bDUR_DU), jt * 16);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int t = 16 * ww + acc_row(r);
+            dks[r] = -egsp[t] * dX[jt][r] - gbt[t] * egs[t] * tail[jt][r];
+          }
+          store_acc_tile<TT>(blk(bDB_DKS), jt * 16, 16 * ww, dks);
+        }
+      } else {
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) tail[jt] = dU[jt];
+      }
+      {   // dv = dX + diag(b) tail into LDS: a quad transpose gives lane 4g + i
+          // token t0 + i at columns 4 g .. 4 g + 3 of each 16-column tile
+        const int t0 = 16 * ww + acc_row(0);
+        const floatx4 b4 = *reinterpret_cast<const floatx4*>(gbt + t0);
+        const int tq = t0 + (lane & 3), cq = 4 * ((lane & 15) >> 2);
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          floatx4 val;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) val[r] = __builtin_fmaf(b4[r], tail[jt][r], dX[jt][r]) * isig;
+          *reinterpret_cast<floatx4*>(dvst + tq * BV + jt * 16 + cq) = quad_transpose(val);
+        }
+      }
+      {   // gradient w.r.t. this chunk's end states (tile maxima from
+          // publish_state_max: dS, dR are unchanged since)
+        const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
+        const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
+        save_state_f16_max<IT>(dS, tmS, reinterpret_cast<f16*>(p.dS_ws) + ob, 32, p.dS_sc + so, DV / 32, ww * (DK / 4));
+        save_state_f16_max<IT>(dR, tmR, reinterpret_cast<f16*>(p.dR_ws) + ob, 32, p.dR_sc + so, DV / 32, ww * (DK / 4));
+      }
+      if constexpr (RDN) {   // dU is dead: its slot keeps dY for the block store
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * ww, tail[jt]);
+      }
+    } else {
+      if constexpr (RDN) {   // T^S was read into registers before the previous barrier
+        if (c > 0) dma_mat64<XT>(mat_src(c - 1, kMatTS), mat(kMatTS, 0), mdo, ww);
+      }
+    }
+    barrier_lds();
+
+    // ======== phase 6: state gradients at the chunk start ========
+    if constexpr (CH) {
+      typedef Mfma<XT> MX;
+      const float eS = edge[0], eR = edge[1];
+      constexpr int KS2 = kChunk / MX::kStep;
+      constexpr int NF = IT * KS2;
+      int fr0[NF], fk0[NF];
+#pragma unroll
+      for (int f = 0; f < NF; ++f) {
+        fr0[f] = ww * (DK / 4) + (f / KS2) * 16;
+        fk0[f] = (f % KS2) * MX::kStep;
+      }
+      typename MX::frag qf[NF], kf[NF];
+      frags_tr_sync<TKQ, XT, NF>(QT, fr0, fk0, qf);
+      frags_tr_sync<TKQ, XT, NF>(KT, fr0, fk0, kf);
+      auto acc = [&](floatx4& d, const typename MX::frag* a, const XT* b, int it, int jt) {
+#pragma unroll
+        for (int ks = 0; ks < KS2; ++ks)
+          d = MX::mma(a[it * KS2 + ks], TT::template frag<MX>(b, jt * 16, ks * MX::kStep), d);
+      };
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt) {
+          dS[it][jt] *= eS;
+          dR[it][jt] *= eR;
+          acc(dS[it][jt], qf, blk(bQDB), it, jt);
+          acc(dS[it][jt], kf, blk(RDN ? bDB_DKS : bDKR), it, jt);
+          acc(dR[it][jt], qf, blk(bQDC), it, jt);
+          if constexpr (RDN) acc(dR[it][jt], kf, blk(bDKR), it, jt);
+        }
+      publish_state_max();
+    } else {
+      wait_vmem();   // the next chunk's DMA; the barrier below publishes it
+      if (c > 0) write_gates(c - 1);
+    }
+    barrier_lds();
+  }
+
+  if constexpr (CH) {
+    if (p.dS0 || p.dR0) {
+#pragma unroll
+      for (int it = 0; it < IT; ++it)
+#pragma unroll
+        for (int jt = 0; jt < JT; ++jt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int i = ww * (DK / 4) + it * 16 + acc_row(r), j = j0 + jt * 16 + acc_col();
+            if (p.dS0) p.dS0[state_off + (int64_t)i * DV + j] = dS[it][jt][r] * isig;
+            if (p.dR0) p.dR0[state_off + (int64_t)i * DV + j] = dR[it][jt][r] * isig;
+          }
+    }
+  } else {
+    if (nch > 0) store_outputs(0);
+  }
+  };
+  if (chain) run(std::true_type{});
+  else run(std::false_type{});
+}
+
 template <typename IN, int DK, int BV, bool RDN, bool VAR>
 hipError_t launch_bwd_scan_v(const OpParams& p, hipStream_t stream) {
   typedef BwdScanLayout<IN, DK, BV, RDN, VAR> L;
@@ -751,9 +1292,27 @@ hipError_t launch_bwd_scan_v(const OpParams& p, hipStream_t stream) {
 }
 
 template <typename IN, int DK, int BV, bool RDN>
+hipError_t launch_bwd_scan_ws(const OpParams& p, hipStream_t stream) {
+  typedef BwdWsLayout<IN, DK, BV, RDN> L;
+  auto kern = bwd_scan_ws_kernel<IN, DK, BV, RDN>;
+  hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, L::kBytes);
+  if (err != hipSuccess) return err;
+  const int nvb = p.DV / BV;
+  const int npairs = p.st.nseq * p.H;
+  const int grid = ((npairs + 7) / 8) * 8 * nvb;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(2 * kThreads), L::kBytes, stream, p);
+  return hipGetLastError();
+}
+
+template <typename IN, int DK, int BV, bool RDN>
 hipError_t launch_bwd_scan_t(const OpParams& p, hipStream_t stream) {
-  return ((p.vflags & kVarOperator) || p.qk_f16) ? launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream)
-                                                 : launch_bwd_scan_v<IN, DK, BV, RDN, false>(p, stream);
+  if ((p.vflags & kVarOperator) || p.qk_f16) return launch_bwd_scan_v<IN, DK, BV, RDN, true>(p, stream);
+  if constexpr (sizeof(IN) == 2 && DK == 128 && BV == 32) {
+    return launch_bwd_scan_ws<IN, DK, BV, RDN>(p, stream);   // the boxed operator: wave-specialised
+  }
+  return launch_bwd_scan_v<IN, DK, BV, RDN, false>(p, stream);
 }
 
 }  // namespace
