@@ -741,19 +741,24 @@ __global__ __launch_bounds__(kThreads) void bwd_scan_kernel(OpParams p) {
 // groups of four that pass the same seven barriers per chunk in the same
 // order:
 //   chain waves (0-3): hold dS and dR (rows 32 w' .. 32 w' + 31) and do every
-//     product of the chunk (the algebra of bwd_scan_kernel), load their K, Q
-//     and dO rows and store the chunk-end checkpoints; dv goes to LDS (fp32);
-//   side waves (4-7): the dX, dY, dYR blocks and dv, the gate vectors of the
-//     next (earlier) chunk and the LDS-DMA of its matrices and clip mask, so
-//     that these memory operations overlap the chain.
+//     product of the chunk (the algebra of bwd_scan_kernel) with no global
+//     memory access: K comes from the K^T tile, dv and the packed chunk-end
+//     checkpoints go to LDS;
+//   side waves (4-7): all global memory traffic — the next (earlier)
+//     chunk's K, Q, dO rows and their commit into LDS, its gate vectors, the
+//     LDS-DMA of its matrices and clip mask, and the stores of the later
+//     chunk's dX, dY, dYR blocks, dv and checkpoints — overlapping the chain.
 // Per chunk (phase: chain waves | side waves), walking backwards:
-//   0: state copies; K^T, Q^T, dO^T commit        | the later chunk's blocks and dv
-//   1: K dS, K dR; dc, e^g db, e^h dc             | the next chunk's gate values;
-//                                                   DMA of its MR (double-buffered)
-//   2: next K, Q, dO rows; dUR                    |
-//   3: dYR, dX, dKR                               | DMA of the next T^R
+//   0: state copies                               | commit K^T, dO^T; the later
+//                                                   chunk's dX block
+//   1: K dS, K dR; dc, e^g db, e^h dc             | its dY, dYR blocks and
+//                                                   checkpoints; the next gate
+//                                                   values; DMA of the next MR
+//   2: dUR                                        | its dv
+//   3: dYR, dX, dKR                               | commit Q^T; the next K, Q, dO
+//                                                   rows; DMA of the next T^R
 //   4: dU                                         | DMA of the next mask, MG, MP
-//   5: dY, dKS; dv into LDS; checkpoints          | DMA of the next T^S
+//   5: dY, dKS; dv and checkpoints into LDS       | DMA of the next T^S
 //   6: dS, dR at the chunk start; their maxima    | wait for the DMA; next gate vectors
 // Each matrix is refilled once the chain has read it into registers (T^R,
 // MG, MP, T^S) or, for MR, into the other buffer.
@@ -772,7 +777,11 @@ struct BwdWsLayout {
   static constexpr int kYst = kGates + 2 * kGateVec * 4;    // dYR (token tile)
   static constexpr int kRed = kYst + kBufBytes;             // per-wave maxima [8]
   static constexpr int kDv = kRed + 8 * 4;                  // dv, fp32 [64][BV]
-  static constexpr int kBytes = kDv + kChunk * BV * 4;
+  // chunk-end checkpoints of dS, dR as stored: fp16 [DK][BV] each, then the
+  // tile scales [2][DK / 16]
+  static constexpr int kCk = kDv + kChunk * BV * 4;
+  static constexpr int kCkSc = kCk + 2 * DK * BV * 2;
+  static constexpr int kBytes = kCkSc + 2 * (DK / 16) * 4;
   static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
   __device__ static constexpr int slot(int mat, int buf) { return B::slot(mat, buf); }
@@ -800,6 +809,8 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
   float* gates = reinterpret_cast<float*>(smem + L::kGates);
   XT* Yst = reinterpret_cast<XT*>(smem + L::kYst);
   float* dvst = reinterpret_cast<float*>(smem + L::kDv);
+  f16* ckst = reinterpret_cast<f16*>(smem + L::kCk);
+  float* ckscl = reinterpret_cast<float*>(smem + L::kCkSc);
   auto mat = [&](int m, int buf) {
     return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
   };
@@ -861,8 +872,8 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
   auto run = [&](auto role) {
   constexpr bool CH = decltype(role)::value;
   floatx4 dS[IT][JT], dR[IT][JT];      // chain: the gradient states
-  typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];
-  IN on[kOPerThread];
+  typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];   // side: the next chunk's K, Q rows 16 ww + (lane & 15)
+  IN on[kOPerThread];                              // side: its dO vector
   float scS = 1.f, scR = 1.f;
   uint32_t tmS[IT], tmR[IT];
   float graw0 = 0.f, graw1 = 0.f;      // side: the next chunk's gate-block values
@@ -893,7 +904,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         store_state_copy<TSC>(dRc, jt * 16, ww * (DK / 4) + it * 16, dR[it][jt] * iR);
       }
   };
-  auto issue_regs = [&](int c) {   // chain: K, Q rows and this thread's dO vector of chunk c
+  auto issue_regs = [&](int c) {   // side: K, Q rows and this thread's dO vector of chunk c
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
     const int t = 16 * ww + (lane & 15);
@@ -947,24 +958,21 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       dma16(p.ck_mask + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * 16, mask + ww * 1024);
     }
   };
-  // side: this chunk's dX, dY, dYR blocks (tokens 16 ww .. 16 ww + 15, one
-  // 64-byte segment per token; rows past the end are zero) and dv rows
-  auto store_outputs = [&](int c) {
+  // side: block b (0 dX, 1 dY, 2 dYR) of chunk c, tokens 16 ww .. 16 ww + 15,
+  // one 64-byte segment per token; rows past the end are zero
+  auto store_block = [&](int c, int b) {
     static_assert(sizeof(XT) == 2, "four lanes per 32-value token row");
     const int64_t gc = si.chunk0 + c;
+    const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
+    const int t = 16 * ww + (lane & 15);
+    const uint4 x = keep_if(tile_token_rows16_sync<TT>(srcb, 16 * ww), t < chunk_len(c));
+    *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
+  };
+  auto store_dv = [&](int c) {   // side: dv rows 16 ww + 8 u + lane / 8, columns 4 (lane % 8) ..
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
-    {
-      const int t = 16 * ww + (lane & 15);
 #pragma unroll
-      for (int b = 0; b < 3; ++b) {
-        const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
-        const uint4 x = keep_if(tile_token_rows16_sync<TT>(srcb, 16 * ww), t < len);
-        *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {   // dv rows 16 ww + 8 u + lane / 8, columns 4 (lane % 8) ..
+    for (int u = 0; u < 2; ++u) {
       const int t = 16 * ww + 8 * u + (lane >> 3), col = 4 * (lane & 7);
       const uint4 x = lds_read16_sync(dvst + t * BV + col);
       if (t < len) {
@@ -981,6 +989,42 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       }
     }
   };
+  // side: chunk c's end-state checkpoints from LDS, rows 32 ww .. 32 ww + 31
+  // of each (2 KiB contiguous: two 1 KiB stores), and their tile scales
+  auto store_ckpt = [&](int c) {
+    const int64_t gc = si.chunk0 + c;
+    const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
+    const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      f16* dst = reinterpret_cast<f16*>(st ? p.dR_ws : p.dS_ws) + ob + ww * (DK / 4) * BV;
+      const f16* src = ckst + st * DK * BV + ww * (DK / 4) * BV;
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        *reinterpret_cast<uint4*>(dst + (u * 64 + lane) * 8) = lds_read16_sync(src + (u * 64 + lane) * 8);
+      if (lane < IT)   // one lane per tile scale
+        (st ? p.dR_sc : p.dS_sc)[so + (int64_t)(ww * IT + lane) * (DV / 32)] = ckscl[st * (DK / 16) + ww * IT + lane];
+    }
+  };
+  // side: rows 16 ww + (lane & 15) of a K^T or Q^T tile (fp16) from the
+  // prefetched bf16 rows, one 16-byte store per k-step
+  auto commit_rows = [&](XT* dst, const typename MI::frag (&src)[KS_STEPS]) {
+    const int t = 16 * ww + (lane & 15);
+#pragma unroll
+    for (int s2 = 0; s2 < KS_STEPS; ++s2) {
+      const u16x8 v = __builtin_bit_cast(u16x8, src[s2]);
+      f16x8 x;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = (f16)bf2f(v[e]);
+      *reinterpret_cast<f16x8*>(TKQ::ptr(dst, t, s2 * 32 + (lane >> 4) * 8)) = x;
+    }
+  };
+  auto commit_do = [&]() {   // side: dO^T (scaled) of the chunk whose vector on holds
+    XT* dbT = blk(bDB_DKS);
+#pragma unroll
+    for (int u = 0; u < kOPerThread; ++u)   // lanes write consecutive tokens
+      *TT::ptr(dbT, ww * kOPerThread + u, lane) = from_f<XT>(to_f<IN>(on[u]) * sig);
+  };
 
   // ---- prologue: the last chunk's staging; the end-state maxima ----
   if constexpr (CH) {
@@ -994,11 +1038,11 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
           dS[it][jt][r] = p.dS_fin ? p.dS_fin[state_off + (int64_t)i * DV + j] * sig : 0.f;
           dR[it][jt][r] = p.dR_fin ? p.dR_fin[state_off + (int64_t)i * DV + j] * sig : 0.f;
         }
-    if (nch > 0) issue_regs(nch - 1);
     publish_state_max();
   } else {
     if (nch > 0) {
       const int c = nch - 1;
+      issue_regs(c);
       issue_gates(c);
       issue_mask(c);
       if constexpr (RDN) {
@@ -1033,41 +1077,20 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
     // ======== phase 0: copies and commit | the later chunk's outputs ========
     if constexpr (CH) {
       write_copies();
-      const int t = 16 * ww + (lane & 15);
-#pragma unroll
-      for (int s2 = 0; s2 < KS_STEPS; ++s2) {   // row t, 8 columns: one 16-byte store each
-        const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
-        const u16x8 qv = __builtin_bit_cast(u16x8, Qn[s2]);
-        f16x8 kh, qh;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          kh[e] = (f16)bf2f(kv[e]);
-          qh[e] = (f16)bf2f(qv[e]);
-        }
-        const int i = s2 * 32 + (lane >> 4) * 8;
-        *reinterpret_cast<f16x8*>(TKQ::ptr(KT, t, i)) = kh;
-        *reinterpret_cast<f16x8*>(TKQ::ptr(QT, t, i)) = qh;
-      }
-      XT* dbT = blk(bDB_DKS);
-#pragma unroll
-      for (int u = 0; u < kOPerThread; ++u)   // lanes write consecutive tokens
-        *TT::ptr(dbT, ww * kOPerThread + u, lane) = from_f<XT>(to_f<IN>(on[u]) * sig);
     } else {
-      if (c + 1 < nch) store_outputs(c + 1);
+      commit_rows(KT, Kn);   // read by phase 1 (Q^T, read in phase 6 only, in phase 3)
+      commit_do();
+      if (c + 1 < nch) store_block(c + 1, 0);   // dX: its slot takes dc in phase 1
     }
     barrier_lds();
 
     // ======== phase 1: K dS_end, K dR_end; dc, e^g db, e^h dc ========
     if constexpr (CH) {
-      typename Mfma<XT>::frag Kf[KS_STEPS];
+      typename Mfma<XT>::frag Kf[KS_STEPS];   // rows 16 ww + (lane & 15) of the K^T tile
 #pragma unroll
-      for (int s2 = 0; s2 < KS_STEPS; ++s2) {
-        const u16x8 kv = __builtin_bit_cast(u16x8, Kn[s2]);
-        f16x8 kh;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kh[e] = (f16)bf2f(kv[e]);
-        Kf[s2] = kh;
-      }
+      for (int s2 = 0; s2 < KS_STEPS; ++s2)
+        Kf[s2] = *reinterpret_cast<const typename Mfma<XT>::frag*>(
+            TKQ::ptr(KT, 16 * ww + (lane & 15), s2 * 32 + (lane >> 4) * 8));
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         KdS[jt] = zero4();
@@ -1091,6 +1114,11 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       }
       aMR = swz_cols_frags_sync<XT>(mat(kMatMR, buf), 16 * ww);
     } else {
+      if (c + 1 < nch) {   // dY (its slot takes dUR in phase 2), dYR, checkpoints
+        store_block(c + 1, 1);
+        store_block(c + 1, 2);
+        store_ckpt(c + 1);
+      }
       if (c > 0) {
         issue_gates(c - 1);
         dma_mat64<XT>(mat_src(c - 1, kMatMR), mat(kMatMR, (c - 1) & 1), mdo, ww);
@@ -1100,7 +1128,6 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
 
     // ======== phase 2: dUR = diag(e^{h_C-h}) K dR_end + MR^T dc ========
     if constexpr (CH) {
-      if (c > 0) issue_regs(c - 1);
 #pragma unroll
       for (int jt = 0; jt < JT; ++jt) {
         floatx4 a = zero4();
@@ -1110,6 +1137,8 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         if constexpr (RDN) store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * ww, dUR[jt]);
       }
       if constexpr (RDN) aTR = swz_cols_frags_sync<XT>(mat(kMatTR, 0), 16 * ww);
+    } else {
+      if (c + 1 < nch) store_dv(c + 1);
     }
     barrier_lds();
 
@@ -1137,6 +1166,8 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       aMP = swz_cols_frags_sync<XT>(mat(kMatMP, 0), 16 * ww);
       aMG = swz_cols_frags_sync<XT>(mat(kMatMG, 0), 16 * ww);
     } else {
+      commit_rows(QT, Qn);   // then the next chunk's rows may replace Kn, Qn, on
+      if (c > 0) issue_regs(c - 1);
       if constexpr (RDN) {   // T^R was read into registers before the previous barrier
         if (c > 0) dma_mat64<XT>(mat_src(c - 1, kMatTR), mat(kMatTR, 0), mdo, ww);
       }
@@ -1198,12 +1229,19 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
           *reinterpret_cast<floatx4*>(dvst + tq * BV + jt * 16 + cq) = quad_transpose(val);
         }
       }
-      {   // gradient w.r.t. this chunk's end states (tile maxima from
-          // publish_state_max: dS, dR are unchanged since)
-        const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
-        const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
-        save_state_f16_max<IT>(dS, tmS, reinterpret_cast<f16*>(p.dS_ws) + ob, 32, p.dS_sc + so, DV / 32, ww * (DK / 4));
-        save_state_f16_max<IT>(dR, tmR, reinterpret_cast<f16*>(p.dR_ws) + ob, 32, p.dR_sc + so, DV / 32, ww * (DK / 4));
+      {   // gradient w.r.t. this chunk's end states, packed as stored (tile
+          // maxima from publish_state_max: dS, dR are unchanged since)
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+#pragma unroll
+          for (int it = 0; it < IT; ++it) {
+            const int e = pow2_scale_exp(st ? tmR[it] : tmS[it]);
+            int row, col;
+            const uint4 v = pack_strip_f16(st ? dR[it][0] : dS[it][0], st ? dR[it][1] : dS[it][1], exp2_int(-e), row, col);
+            *reinterpret_cast<uint4*>(ckst + st * DK * BV + (ww * (DK / 4) + 16 * it + row) * BV + col) = v;
+            ckscl[st * (DK / 16) + ww * IT + it] = exp2_int(e);   // every lane: the wave-uniform value
+          }
+        }
       }
       if constexpr (RDN) {   // dU is dead: its slot keeps dY for the block store
 #pragma unroll
@@ -1268,8 +1306,12 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
             if (p.dR0) p.dR0[state_off + (int64_t)i * DV + j] = dR[it][jt][r] * isig;
           }
     }
-  } else {
-    if (nch > 0) store_outputs(0);
+  } else if (nch > 0) {   // the first chunk's outputs
+    store_block(0, 0);
+    store_block(0, 1);
+    store_block(0, 2);
+    store_ckpt(0);
+    store_dv(0);
   }
   };
   if (chain) run(std::true_type{});
