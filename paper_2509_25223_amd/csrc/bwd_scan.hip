@@ -781,7 +781,8 @@ struct BwdWsLayout {
   // tile scales [2][DK / 16]
   static constexpr int kCk = kDv + kChunk * BV * 4;
   static constexpr int kCkSc = kCk + 2 * DK * BV * 2;
-  static constexpr int kBytes = kCkSc + 2 * (DK / 16) * 4;
+  static constexpr int kGraw = kCkSc + 2 * (DK / 16) * 4;   // the gate block (one side wave's DMA)
+  static constexpr int kBytes = kGraw + kGateBlock * 4;
   static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
   __device__ static constexpr int slot(int mat, int buf) { return B::slot(mat, buf); }
@@ -811,6 +812,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
   float* dvst = reinterpret_cast<float*>(smem + L::kDv);
   f16* ckst = reinterpret_cast<f16*>(smem + L::kCk);
   float* ckscl = reinterpret_cast<float*>(smem + L::kCkSc);
+  float* graw = reinterpret_cast<float*>(smem + L::kGraw);   // prep's gate block
   auto mat = [&](int m, int buf) {
     return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
   };
@@ -876,7 +878,6 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
   IN on[kOPerThread];                              // side: its dO vector
   float scS = 1.f, scR = 1.f;
   uint32_t tmS[IT], tmR[IT];
-  float graw0 = 0.f, graw1 = 0.f;      // side: the next chunk's gate-block values
   auto publish_state_max = [&]() {   // chain
     state_tile_absmax<IT>(dS, tmS);
     state_tile_absmax<IT>(dR, tmR);
@@ -918,32 +919,25 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
 #pragma unroll
     for (int u = 0; u < kOPerThread; ++u) on[u] = v[u];
   };
-  // side wave ww loads the two gate-block values its gate vectors need:
-  // 0: g_t, g_{t-1}; 1: h_t, h_C; 2: g_t, g_C; 3: beta_t, gamma_t
+  // side wave 0 moves chunk c's gate block (g, h, beta, gamma) into LDS with
+  // one DMA instruction and, after its wait, forms every gate vector
   auto issue_gates = [&](int c) {
-    const float* gb = p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock;
-    const int t = lane;
-    const int o0 = ww == 1 ? 64 + t : ww == 3 ? 128 + t : t;
-    const int o1 = ww == 0 ? max(t - 1, 0) : ww == 1 ? 64 + kChunk - 1 : ww == 2 ? kChunk - 1 : 192 + t;
-    graw0 = gb[o0];
-    graw1 = gb[o1];
+    if (ww == 0) dma_linear_wave(p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock, graw, kGateBlock * 4);
   };
   auto write_gates = [&](int c) {
+    if (ww != 0) return;
     const int t = lane;
-    if (ww == 0) {
-      gvec(c, 2)[t] = __expf(graw0);
-      gvec(c, 3)[t] = t > 0 ? __expf(graw1) : 1.f;
-    } else if (ww == 1) {
-      gvec(c, 4)[t] = __expf(graw0);
-      gvec(c, 6)[t] = __expf(graw1 - graw0);
-      gvec(c, 7)[1] = __expf(graw1);
-    } else if (ww == 2) {
-      gvec(c, 5)[t] = __expf(graw1 - graw0);
-      gvec(c, 7)[0] = __expf(graw1);
-    } else {
-      gvec(c, 0)[t] = graw0;
-      gvec(c, 1)[t] = graw1;
-    }
+    const float g = graw[t], gp = graw[max(t - 1, 0)], gl = graw[kChunk - 1];
+    const float hr = graw[64 + t], hl = graw[64 + kChunk - 1];
+    gvec(c, 0)[t] = graw[128 + t];
+    gvec(c, 1)[t] = graw[192 + t];
+    gvec(c, 2)[t] = __expf(g);
+    gvec(c, 3)[t] = t > 0 ? __expf(gp) : 1.f;
+    gvec(c, 4)[t] = __expf(hr);
+    gvec(c, 5)[t] = __expf(gl - g);
+    gvec(c, 6)[t] = __expf(hl - hr);
+    gvec(c, 7)[0] = __expf(gl);   // every lane stores the same value
+    gvec(c, 7)[1] = __expf(hl);
   };
   const MatDma<XT> mdo(ww);   // side waves: this lane's matrix DMA offsets
   auto issue_mask = [&](int c) {   // side: rows of BV bytes; padding rows read row 0 (masked by 0 gradients)
@@ -1002,8 +996,10 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
 #pragma unroll
       for (int u = 0; u < 2; ++u)
         *reinterpret_cast<uint4*>(dst + (u * 64 + lane) * 8) = lds_read16_sync(src + (u * 64 + lane) * 8);
-      if (lane < IT)   // one lane per tile scale
-        (st ? p.dR_sc : p.dS_sc)[so + (int64_t)(ww * IT + lane) * (DV / 32)] = ckscl[st * (DK / 16) + ww * IT + lane];
+    }
+    if (lane < 2 * IT) {   // one lane per tile scale, both states in one store
+      const int st = lane / IT, it = lane % IT;
+      (st ? p.dR_sc : p.dS_sc)[so + (int64_t)(ww * IT + it) * (DV / 32)] = ckscl[st * (DK / 16) + ww * IT + it];
     }
   };
   // side: rows 16 ww + (lane & 15) of a K^T or Q^T tile (fp16) from the

@@ -673,7 +673,8 @@ struct FwdWsLayout {
   static constexpr int kGates = kVc + 2 * kVBytes;    // two sets (chunk parity)
   static constexpr int kRst = kGates + 2 * kGateVec * 4;
   static constexpr int kMst = kRst + kBufBytes;
-  static constexpr int kBytes = kMst + kChunk * BV;
+  static constexpr int kGraw = kMst + kChunk * BV;      // the gate block (one side wave's DMA)
+  static constexpr int kBytes = kGraw + kGateBlock * 4;
   static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
   static_assert(kVBytes == 4 * 1024, "V block = one DMA instruction per side wave");
   static_assert(kBytes <= 160 * 1024, "forward scan LDS");
@@ -721,6 +722,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
   float* gates = reinterpret_cast<float*>(smem + L::kGates);
   XT* Rst = reinterpret_cast<XT*>(smem + L::kRst);            // r (saving mode)
   uint8_t* Mst = reinterpret_cast<uint8_t*>(smem + L::kMst);  // clip mask (saving mode)
+  float* graw = reinterpret_cast<float*>(smem + L::kGraw);     // prep's gate block
 
   const int H = p.H, DV = p.DV, tid = threadIdx.x, lane = tid & 63;
   const int wu = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -759,7 +761,6 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
   constexpr bool CH = decltype(role)::value;
   floatx4 Sacc[IT][JT], Racc[IT][JT];  // chain: the states
   typename MI::frag Kn[KS_STEPS], Qn[KS_STEPS];   // chain: next chunk's K, Q rows 16 ww + (lane & 15)
-  float graw0 = 0.f, graw1 = 0.f;      // side: next chunk's gate-block values
   if constexpr (CH) {
 #pragma unroll
     for (int it = 0; it < IT; ++it)
@@ -787,32 +788,25 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     const bool ok = t < chunk_len(c);
     load_rowfrags<IN, DK>(dst, ok ? src + ((tok + t) * H + h) * (int64_t)DK : nullptr);
   };
-  // side wave ww loads the two gate-block values its gate vectors need:
-  // 0: g_t, g_{t-1}; 1: h_t, h_C; 2: g_t, g_C; 3: beta_t, gamma_t
+  // side wave 0 moves chunk c's gate block (g, h, beta, gamma) into LDS with
+  // one DMA instruction and, after its wait, forms every gate vector
   auto issue_gates = [&](int c) {
-    const float* gb = p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock;
-    const int t = lane;
-    const int o0 = ww == 1 ? 64 + t : ww == 3 ? 128 + t : t;
-    const int o1 = ww == 0 ? max(t - 1, 0) : ww == 1 ? 64 + kChunk - 1 : ww == 2 ? kChunk - 1 : 192 + t;
-    graw0 = gb[o0];
-    graw1 = gb[o1];
+    if (ww == 0) dma_linear_wave(p.gate_ws + ((int64_t)(si.chunk0 + c) * H + h) * kGateBlock, graw, kGateBlock * 4);
   };
   auto write_gates = [&](int c) {
+    if (ww != 0) return;
     const int t = lane;
-    if (ww == 0) {
-      gvec(c, 2)[t] = __expf(graw0);
-      gvec(c, 3)[t] = t > 0 ? __expf(graw1) : 1.f;
-    } else if (ww == 1) {
-      gvec(c, 4)[t] = __expf(graw0);
-      gvec(c, 6)[t] = __expf(graw1 - graw0);
-      gvec(c, 7)[1] = __expf(graw1);
-    } else if (ww == 2) {
-      gvec(c, 5)[t] = __expf(graw1 - graw0);
-      gvec(c, 7)[0] = __expf(graw1);
-    } else {
-      gvec(c, 0)[t] = graw0;
-      gvec(c, 1)[t] = graw1;
-    }
+    const float g = graw[t], gp = graw[max(t - 1, 0)], gl = graw[kChunk - 1];
+    const float hr = graw[64 + t], hl = graw[64 + kChunk - 1];
+    gvec(c, 0)[t] = graw[128 + t];
+    gvec(c, 1)[t] = graw[192 + t];
+    gvec(c, 2)[t] = __expf(g);
+    gvec(c, 3)[t] = t > 0 ? __expf(gp) : 1.f;
+    gvec(c, 4)[t] = __expf(hr);
+    gvec(c, 5)[t] = __expf(gl - g);
+    gvec(c, 6)[t] = __expf(hl - hr);
+    gvec(c, 7)[0] = __expf(gl);   // every lane stores the same value
+    gvec(c, 7)[1] = __expf(hl);
   };
   const MatDma<XT> mdo(ww);   // side waves: this lane's matrix DMA offsets
   auto issue_early = [&](int c) {   // V, MG, MP, T^R, MR of chunk c (double-buffered)
