@@ -49,12 +49,12 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("58be47277bb005b2", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168042589, 109707264),
-    "grad_absmax": ("58aebcb3891a399f", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196002, 131178),
-    "bwd_scan": ("a715cec40acbb23c", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 346969119, 613419008),
-    "bwd_grad": ("f3b7657e103f78f1", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232663241, 302373232),
-    "fwd_scan": ("f561cad3aa9097b4", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 313238770, 638582918),
-    "decode": ("093edbbe40eefd13", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746642, 539571891),
+    "prep": ("a65f761e8057f476", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168043097, 109707264),
+    "grad_absmax": ("27fac8f619a3f435", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196090, 131130),
+    "bwd_scan": ("b0458713c1d2bac9", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 347068885, 613502826),
+    "bwd_grad": ("5315ddfd228e0690", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232683179, 302484138),
+    "fwd_scan": ("22989059739cdac2", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 313287570, 638592435),
+    "decode": ("1dfdc074703e2d69", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542737987, 539561446),
 }
 
 
