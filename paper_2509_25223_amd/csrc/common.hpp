@@ -609,6 +609,44 @@ __device__ __forceinline__ MatFrags<T> swz_rows_frags(const T* M, int r0) {
   for (int s = 0; s < kChunk / Mfma<T>::kStep; ++s) a.f[s] = swz_load_rows<T>(M, r0, s * Mfma<T>::kStep);
   return a;
 }
+// ---------------------------------------------------------------------------
+// Chunk matrices kept in LDS as stored in global memory: the ten 16 x 16
+// blocks on and below the diagonal (tri_off order, 512 bytes each in fp16),
+// copied by five 1 KiB LDS-DMA instructions.  Inside a block the two 16-byte
+// halves of rows 8 .. 15 trade places, so that the 16 rows an MFMA fragment
+// read touches at one half fall in distinct banks.  Reads of blocks above the
+// diagonal go to a shared 16-byte zero region.
+// ---------------------------------------------------------------------------
+constexpr int kPkBytes = kMatPacked * 2;   // fp16 matrix in LDS (5 KiB)
+
+// LDS-DMA of one packed fp16 matrix (global tri_off layout) into LDS by the
+// wave with index w (0 .. nw - 1) of the nw waves sharing the copy; dma_k is
+// this wave's first instruction index of the five, in steps of nw.
+__device__ __forceinline__ void dma_mat_packed(const f16* gsrc, f16* lds, int w, int nw) {
+  const int lane = threadIdx.x & 63;
+  for (int i = w; i < kPkBytes / 1024; i += nw) {
+    const int P = i * 64 + lane;                    // LDS 16-byte chunk
+    const int b = P >> 5, r = (P & 31) >> 1, h = (P & 1) ^ ((r >> 3) & 1);
+    dma16(reinterpret_cast<const char*>(gsrc) + (b * 32 + r * 2 + h) * 16,
+          reinterpret_cast<char*>(lds) + i * 1024);
+  }
+}
+
+// A-operand fragments (MatFrags) of rows 16 bi .. 16 bi + 15 of a packed
+// fp16 matrix in LDS; `zero` is 16 zero bytes in LDS.
+__device__ __forceinline__ MatFrags<f16> packed_rows_frags(const f16* M, int bi, const f16* zero) {
+  const int lane = threadIdx.x & 63, r = lane & 15, q = lane >> 4;
+  MatFrags<f16> a;
+#pragma unroll
+  for (int s = 0; s < kChunk / 32; ++s) {
+    const int bj = 2 * s + (q >> 1), h = (q & 1) ^ ((r >> 3) & 1);
+    const int off = ((bi * (bi + 1) / 2 + bj) * 32 + r * 2 + h) * 16;
+    const char* src = bj <= bi ? reinterpret_cast<const char*>(M) + off : reinterpret_cast<const char*>(zero);
+    a.f[s] = *reinterpret_cast<const typename Mfma<f16>::frag*>(src);
+  }
+  return a;
+}
+
 template <typename T>
 __device__ __forceinline__ MatFrags<T> swz_cols_frags(const T* M, int t0) {
   MatFrags<T> a;

@@ -665,7 +665,7 @@ struct FwdWsLayout {
   static constexpr int kCopies = kKT + kChunk * TK::kRowB;
   static constexpr int kCopyBytes = BV * TSC::kRowB;
   static constexpr int kMats = kCopies + 4 * kCopyBytes;
-  static constexpr int kBufs = kMats + kNumSlots * Swz<XT>::kBytes;
+  static constexpr int kBufs = kMats + kNumSlots * kPkBytes;   // matrices as their ten lower blocks
   static constexpr int kBufBytes = BV * TT::kRowB;
   static constexpr int kVBytes = kChunk * BV * (int)sizeof(IN);
   static constexpr int kVc = kBufs + 5 * kBufBytes;   // two V blocks (chunk parity)
@@ -674,7 +674,8 @@ struct FwdWsLayout {
   static constexpr int kRst = kGates + 2 * kGateVec * 4;
   static constexpr int kMst = kRst + kBufBytes;
   static constexpr int kGraw = kMst + kChunk * BV;      // the gate block (one side wave's DMA)
-  static constexpr int kBytes = kGraw + kGateBlock * 4;
+  static constexpr int kZero = kGraw + kGateBlock * 4;   // 16 zero bytes (blocks above the diagonal)
+  static constexpr int kBytes = kZero + 16;
   static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
   static_assert(kVBytes == 4 * 1024, "V block = one DMA instruction per side wave");
   static_assert(kBytes <= 160 * 1024, "forward scan LDS");
@@ -711,8 +712,9 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
   IN* Slo = reinterpret_cast<IN*>(smem + L::kCopies + 2 * L::kCopyBytes);
   IN* Rlo = reinterpret_cast<IN*>(smem + L::kCopies + 3 * L::kCopyBytes);
   auto mat = [&](int m, int buf) {
-    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
+    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * kPkBytes);
   };
+  const XT* zero16 = reinterpret_cast<const XT*>(smem + L::kZero);
   XT* Yt = reinterpret_cast<XT*>(smem + L::kBufs);               // Y, later YR
   XT* Ut = reinterpret_cast<XT*>(smem + L::kBufs + 1 * L::kBufBytes);
   XT* URt = reinterpret_cast<XT*>(smem + L::kBufs + 2 * L::kBufBytes);
@@ -808,7 +810,12 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     gvec(c, 7)[0] = __expf(gl);   // every lane stores the same value
     gvec(c, 7)[1] = __expf(hl);
   };
-  const MatDma<XT> mdo(ww);   // side waves: this lane's matrix DMA offsets
+  // side waves: the five DMA instructions of the g-th matrix of a group are
+  // dealt round-robin over the four side waves (the group's instruction k
+  // to wave k mod 4)
+  auto dma_mat = [&](int c, int m, int slot_buf, int g) {
+    dma_mat_packed(mat_src(c, m), mat(m, slot_buf), ((ww - 5 * g) % 4 + 4) % 4, kWaves);
+  };
   auto issue_early = [&](int c) {   // V, MG, MP, T^R, MR of chunk c (double-buffered)
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
@@ -817,13 +824,14 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     const int ts = t < len ? t : len - 1;   // padding rows: any valid row (multiplied by 0)
     dma16(vg + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * (16 / (int)sizeof(IN)),
           reinterpret_cast<char*>(vblk(c)) + ww * 1024);
-    dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, c & 1), mdo, ww);
-    dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, c & 1), mdo, ww);
-    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, c & 1), mdo, ww);
-    dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo, ww);
+    int g = 0;
+    dma_mat(c, kMatMG, c & 1, g++);
+    dma_mat(c, kMatMP, c & 1, g++);
+    if constexpr (RDN) dma_mat(c, kMatTR, c & 1, g++);
+    dma_mat(c, kMatMR, c & 1, g++);
   };
   auto issue_ts = [&](int c) {   // T^S (single-buffered)
-    if constexpr (RDN) dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo, ww);
+    if constexpr (RDN) dma_mat(c, kMatTS, 0, 0);
   };
   // side waves: tokens 16 ww .. 16 ww + 15 of a token-major block, one
   // 64-byte segment per token (lane (g, i): token 16 ww + i, values 8 g ..
@@ -920,6 +928,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
   };
 
   // ---- prologue: chunk 0's staging and the initial state copies ----
+  if (threadIdx.x == 0) *reinterpret_cast<uint4*>(smem + L::kZero) = uint4{0, 0, 0, 0};
   if (nch > 0) {
     if constexpr (CH) {
       issue_rows(Kn, kg, 0);
@@ -987,8 +996,8 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
           store_acc_tile<TT>(DUt, jt * 16, 16 * ww, du);
         }
       }
-      if constexpr (RDN) aTS = swz_rows_frags<XT>(mat(kMatTS, 0), 16 * ww);
-      else aMG = swz_rows_frags<XT>(mat(kMatMG, buf), 16 * ww);
+      if constexpr (RDN) aTS = packed_rows_frags(mat(kMatTS, 0), ww, zero16);
+      else aMG = packed_rows_frags(mat(kMatMG, buf), ww, zero16);
     } else {
       if constexpr (WRITE_O) {
         if (c > 0) store_o(c - 1);   // before the DMA below refills chunk c - 1's V block
@@ -1018,9 +1027,9 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
           store_acc_tile<TT>(Ut, jt * 16, 16 * ww, u);
           store_acc_tile<TT>(DUt, jt * 16, 16 * ww, du);
         }
-        aMG = swz_rows_frags<XT>(mat(kMatMG, buf), 16 * ww);
+        aMG = packed_rows_frags(mat(kMatMG, buf), ww, zero16);
       }
-      if constexpr (WRITE_O) aMP = swz_rows_frags<XT>(mat(kMatMP, buf), 16 * ww);
+      if constexpr (WRITE_O) aMP = packed_rows_frags(mat(kMatMP, buf), ww, zero16);
       if (more) {   // the next K, Q rows, while the side waves issue little
         issue_rows(Kn, kg, c + 1);
         issue_rows(Qn, qg, c + 1);
@@ -1066,7 +1075,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
           for (int r = 0; r < 4; ++r) base[jt][r] = __builtin_fmaf(egs[16 * ww + acc_row(r)], QS[jt][r], mpu[r]);
         }
       }
-      if constexpr (RDN) aTR = swz_rows_frags<XT>(mat(kMatTR, buf), 16 * ww);
+      if constexpr (RDN) aTR = packed_rows_frags(mat(kMatTR, buf), ww, zero16);
     } else {
       if constexpr (CKPT) {   // chunk-start R
         floatx4 xr[IT][JT];
@@ -1091,7 +1100,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
           store_acc_tile<TT>(DURt, jt * 16, 16 * ww, du);
         }
       }
-      if constexpr (WRITE_O) aMR = swz_rows_frags<XT>(mat(kMatMR, buf), 16 * ww);
+      if constexpr (WRITE_O) aMR = packed_rows_frags(mat(kMatMR, buf), ww, zero16);
     } else {
       if constexpr (CKPT) {
         store_block(c, 2, Rst);
