@@ -771,9 +771,12 @@ struct BwdWsLayout {
   typedef typename B::TKQ TKQ;
   typedef typename B::TSC TSC;
   static constexpr int kKT = B::kKT, kQT = B::kQT, kCopies = B::kCopies, kCopyBytes = B::kCopyBytes;
-  static constexpr int kMats = B::kMats, kBufs = B::kBufs, kBufBytes = B::kBufBytes, kMask = B::kMask;
+  static constexpr int kMats = B::kMats, kBufBytes = B::kBufBytes;
+  // matrix slots: the packed lower blocks (kPkBytes each)
+  static constexpr int kBufs = kMats + B::kNumSlots * kPkBytes;
+  static constexpr int kMask = kBufs + B::kNumBufs * kBufBytes;
   static constexpr int kGateVec = 8 * kChunk;   // floats per chunk's gate vectors
-  static constexpr int kGates = B::kMask + B::kMaskBytes;   // two sets (chunk parity)
+  static constexpr int kGates = kMask + B::kMaskBytes;   // two sets (chunk parity)
   static constexpr int kYst = kGates + 2 * kGateVec * 4;    // dYR (token tile)
   static constexpr int kRed = kYst + kBufBytes;             // per-wave maxima [8]
   static constexpr int kDv = kRed + 8 * 4;                  // dv, fp32 [64][BV]
@@ -782,7 +785,8 @@ struct BwdWsLayout {
   static constexpr int kCk = kDv + kChunk * BV * 4;
   static constexpr int kCkSc = kCk + 2 * DK * BV * 2;
   static constexpr int kGraw = kCkSc + 2 * (DK / 16) * 4;   // the gate block (one side wave's DMA)
-  static constexpr int kBytes = kGraw + kGateBlock * 4;
+  static constexpr int kZero = kGraw + kGateBlock * 4;      // 16 zero bytes (blocks above the diagonal)
+  static constexpr int kBytes = kZero + 16;
   static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
   static_assert(kBytes <= 160 * 1024, "backward scan LDS");
   __device__ static constexpr int slot(int mat, int buf) { return B::slot(mat, buf); }
@@ -814,8 +818,9 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
   float* ckscl = reinterpret_cast<float*>(smem + L::kCkSc);
   float* graw = reinterpret_cast<float*>(smem + L::kGraw);   // prep's gate block
   auto mat = [&](int m, int buf) {
-    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * Swz<XT>::kBytes);
+    return reinterpret_cast<XT*>(smem + L::kMats + L::slot(m, buf) * kPkBytes);
   };
+  const XT* zero16 = reinterpret_cast<const XT*>(smem + L::kZero);
   auto blk = [&](int b) { return reinterpret_cast<XT*>(smem + L::kBufs + b * L::kBufBytes); };
   // gate vectors of chunk c: beta, gamma, e^{g_t}, e^{g_{t-1}}, e^{h_t},
   // e^{g_C - g_t}, e^{h_C - h_t}, then [e^{g_C}, e^{h_C}]
@@ -939,7 +944,11 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
     gvec(c, 7)[0] = __expf(gl);   // every lane stores the same value
     gvec(c, 7)[1] = __expf(hl);
   };
-  const MatDma<XT> mdo(ww);   // side waves: this lane's matrix DMA offsets
+  // side: chunk c's matrix m into slot buffer buf; the side wave x issues two
+  // of the five DMA instructions (chosen per matrix to even out the phases)
+  auto dma_mat = [&](int c, int m, int buf, int x) {
+    dma_mat_packed<true>(mat_src(c, m), mat(m, buf), (ww - x) & 3, kWaves);
+  };
   auto issue_mask = [&](int c) {   // side: rows of BV bytes; padding rows read row 0 (masked by 0 gradients)
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
@@ -1042,16 +1051,17 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       issue_gates(c);
       issue_mask(c);
       if constexpr (RDN) {
-        dma_mat64<XT>(mat_src(c, kMatTS), mat(kMatTS, 0), mdo, ww);
-        dma_mat64<XT>(mat_src(c, kMatTR), mat(kMatTR, 0), mdo, ww);
+        dma_mat(c, kMatTS, 0, 1);
+        dma_mat(c, kMatTR, 0, 2);
       }
-      dma_mat64<XT>(mat_src(c, kMatMG), mat(kMatMG, 0), mdo, ww);
-      dma_mat64<XT>(mat_src(c, kMatMP), mat(kMatMP, 0), mdo, ww);
-      dma_mat64<XT>(mat_src(c, kMatMR), mat(kMatMR, c & 1), mdo, ww);
+      dma_mat(c, kMatMG, 0, 2);
+      dma_mat(c, kMatMP, 0, 3);
+      dma_mat(c, kMatMR, c & 1, 3);
       wait_vmem();
       write_gates(c);
     }
   }
+  if (tid == 0) *reinterpret_cast<uint4*>(smem + L::kZero) = uint4{0, 0, 0, 0};
   barrier_lds();
 
   floatx4 KdS[JT], KdR[JT], dUR[JT], dX[JT];
@@ -1108,7 +1118,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         store_acc_tile<TT>(blk(bQDB), jt * 16, 16 * ww, qdb);
         store_acc_tile<TT>(blk(bQDC), jt * 16, 16 * ww, qdc);
       }
-      aMR = swz_cols_frags_sync<XT>(mat(kMatMR, buf), 16 * ww);
+      aMR = packed_cols_frags_sync(mat(kMatMR, buf), ww, zero16);
     } else {
       if (c + 1 < nch) {   // dY (its slot takes dUR in phase 2), dYR, checkpoints
         store_block(c + 1, 1);
@@ -1117,7 +1127,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       }
       if (c > 0) {
         issue_gates(c - 1);
-        dma_mat64<XT>(mat_src(c - 1, kMatMR), mat(kMatMR, (c - 1) & 1), mdo, ww);
+        dma_mat(c - 1, kMatMR, (c - 1) & 1, 3);
       }
     }
     barrier_lds();
@@ -1132,7 +1142,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) dUR[jt][r] = dlr[16 * ww + acc_row(r)] * KdR[jt][r] + a[r];
         if constexpr (RDN) store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * ww, dUR[jt]);
       }
-      if constexpr (RDN) aTR = swz_cols_frags_sync<XT>(mat(kMatTR, 0), 16 * ww);
+      if constexpr (RDN) aTR = packed_cols_frags_sync(mat(kMatTR, 0), ww, zero16);
     } else {
       if (c + 1 < nch) store_dv(c + 1);
     }
@@ -1159,13 +1169,13 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         store_acc_tile<TT>(blk(bDKR), jt * 16, 16 * ww, RDN ? dkr : dks);
         store_acc_tile<TT>(Yst, jt * 16, 16 * ww, dYR);
       }
-      aMP = swz_cols_frags_sync<XT>(mat(kMatMP, 0), 16 * ww);
-      aMG = swz_cols_frags_sync<XT>(mat(kMatMG, 0), 16 * ww);
+      aMP = packed_cols_frags_sync(mat(kMatMP, 0), ww, zero16);
+      aMG = packed_cols_frags_sync(mat(kMatMG, 0), ww, zero16);
     } else {
       commit_rows(QT, Qn);   // then the next chunk's rows may replace Kn, Qn, on
       if (c > 0) issue_regs(c - 1);
       if constexpr (RDN) {   // T^R was read into registers before the previous barrier
-        if (c > 0) dma_mat64<XT>(mat_src(c - 1, kMatTR), mat(kMatTR, 0), mdo, ww);
+        if (c > 0) dma_mat(c - 1, kMatTR, 0, 2);
       }
     }
     barrier_lds();
@@ -1182,12 +1192,12 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         for (int r = 0; r < 4; ++r) dU[jt][r] = dls[16 * ww + acc_row(r)] * KdS[jt][r] + a[r] - b[r];
         store_acc_tile<TT>(blk(bDUR_DU), jt * 16, 16 * ww, dU[jt]);
       }
-      if constexpr (RDN) aTS = swz_cols_frags_sync<XT>(mat(kMatTS, 0), 16 * ww);
+      if constexpr (RDN) aTS = packed_cols_frags_sync(mat(kMatTS, 0), ww, zero16);
     } else {
       if (c > 0) {   // the mask (read in phase 3) and MG, MP (read into registers)
         issue_mask(c - 1);
-        dma_mat64<XT>(mat_src(c - 1, kMatMG), mat(kMatMG, 0), mdo, ww);
-        dma_mat64<XT>(mat_src(c - 1, kMatMP), mat(kMatMP, 0), mdo, ww);
+        dma_mat(c - 1, kMatMG, 0, 2);
+        dma_mat(c - 1, kMatMP, 0, 3);
       }
     }
     barrier_lds();
@@ -1245,7 +1255,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       }
     } else {
       if constexpr (RDN) {   // T^S was read into registers before the previous barrier
-        if (c > 0) dma_mat64<XT>(mat_src(c - 1, kMatTS), mat(kMatTS, 0), mdo, ww);
+        if (c > 0) dma_mat(c - 1, kMatTS, 0, 1);
       }
     }
     barrier_lds();

@@ -612,22 +612,33 @@ __device__ __forceinline__ MatFrags<T> swz_rows_frags(const T* M, int r0) {
 // ---------------------------------------------------------------------------
 // Chunk matrices kept in LDS as stored in global memory: the ten 16 x 16
 // blocks on and below the diagonal (tri_off order, 512 bytes each in fp16),
-// copied by five 1 KiB LDS-DMA instructions.  Inside a block the two 16-byte
-// halves of rows 8 .. 15 trade places, so that the 16 rows an MFMA fragment
-// read touches at one half fall in distinct banks.  Reads of blocks above the
+// copied by five 1 KiB LDS-DMA instructions.  Inside a block, row r's two
+// 16-byte halves sit at 16-byte positions pk_pos<COLS>(r, h), arranged for
+// the one kind of read the matrix gets.  For row fragments (COLS false) rows
+// 8 .. 15 swap their halves, so that the 16 rows a read touches at one half
+// fall in distinct banks; for transposed column fragments (COLS true) rows
+// 8 .. 11 and 12 .. 15 trade places, so that rows 0..3 and 8..11 (4..7 and
+// 12..15), read together, fall in distinct banks.  Reads of blocks above the
 // diagonal go to a shared 16-byte zero region.
 // ---------------------------------------------------------------------------
 constexpr int kPkBytes = kMatPacked * 2;   // fp16 matrix in LDS (5 KiB)
 
-// LDS-DMA of one packed fp16 matrix (global tri_off layout) into LDS by the
-// wave with index w (0 .. nw - 1) of the nw waves sharing the copy; dma_k is
-// this wave's first instruction index of the five, in steps of nw.
+// 16-byte position inside a block of row r's half h (an involution)
+template <bool COLS>
+__device__ __forceinline__ int pk_pos(int r, int h) {
+  return COLS ? (r ^ ((r >> 3) << 2)) * 2 + h : r * 2 + (h ^ (r >> 3));
+}
+
+// LDS-DMA of one packed fp16 matrix (global tri_off layout) into LDS by wave
+// w (0 .. nw - 1) of the nw waves sharing the copy: the wave issues the
+// instructions w, w + nw, .. of the five.
+template <bool COLS>
 __device__ __forceinline__ void dma_mat_packed(const f16* gsrc, f16* lds, int w, int nw) {
   const int lane = threadIdx.x & 63;
   for (int i = w; i < kPkBytes / 1024; i += nw) {
     const int P = i * 64 + lane;                    // LDS 16-byte chunk
-    const int b = P >> 5, r = (P & 31) >> 1, h = (P & 1) ^ ((r >> 3) & 1);
-    dma16(reinterpret_cast<const char*>(gsrc) + (b * 32 + r * 2 + h) * 16,
+    const int b = P >> 5, rh = pk_pos<COLS>((P & 31) >> 1, P & 1);   // the (row, half) stored there
+    dma16(reinterpret_cast<const char*>(gsrc) + (b * 32 + rh) * 16,
           reinterpret_cast<char*>(lds) + i * 1024);
   }
 }
@@ -639,10 +650,44 @@ __device__ __forceinline__ MatFrags<f16> packed_rows_frags(const f16* M, int bi,
   MatFrags<f16> a;
 #pragma unroll
   for (int s = 0; s < kChunk / 32; ++s) {
-    const int bj = 2 * s + (q >> 1), h = (q & 1) ^ ((r >> 3) & 1);
-    const int off = ((bi * (bi + 1) / 2 + bj) * 32 + r * 2 + h) * 16;
+    const int bj = 2 * s + (q >> 1);
+    const int off = ((bi * (bi + 1) / 2 + bj) * 32 + pk_pos<false>(r, q & 1)) * 16;
     const char* src = bj <= bi ? reinterpret_cast<const char*>(M) + off : reinterpret_cast<const char*>(zero);
     a.f[s] = *reinterpret_cast<const typename Mfma<f16>::frag*>(src);
+  }
+  return a;
+}
+
+// A-operand fragments of rows 16 bj .. 16 bj + 15 of the transpose of a
+// packed fp16 matrix in LDS (its columns 16 bj ..), from transpose reads as
+// in swz_cols_frags_sync (inline assembly, waited for inside, so that the
+// compiler does not drain in-flight LDS-DMA first); `zero` is 16 zero bytes
+// in LDS.  Lane (q, j) of the read for k-rows 32 s + 8 q + 4 n .. addresses
+// 4 elements of matrix row 32 s + 8 q + (j >> 2) + 4 n at column
+// 16 bj + 4 (j & 3).
+__device__ __forceinline__ MatFrags<f16> packed_cols_frags_sync(const f16* M, int bj, const f16* zero) {
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  const int lane = threadIdx.x & 63, j = lane & 15, q = lane >> 4;
+  const int h = (j & 3) >> 1, sub = (j & 1) * 8;
+  const char* b = reinterpret_cast<const char*>(M);
+  u16x4 x[2], y[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int bi = 2 * s + (q >> 1), r = 8 * (q & 1) + (j >> 2);
+    const int blk = (bi * (bi + 1) / 2 + bj) * 512;
+    const char* p0 = bj <= bi ? b + blk + pk_pos<true>(r, h) * 16 + sub : reinterpret_cast<const char*>(zero);
+    const char* p1 = bj <= bi ? b + blk + pk_pos<true>(r + 4, h) * 16 + sub : reinterpret_cast<const char*>(zero);
+    const uint32_t a0 = (uint32_t)(uintptr_t)(lds_ptr)(p0);
+    const uint32_t a1 = (uint32_t)(uintptr_t)(lds_ptr)(p1);
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(x[s]) : "v"(a0));
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(y[s]) : "v"(a1));
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x[0]), "+v"(y[0]), "+v"(x[1]), "+v"(y[1]));
+  MatFrags<f16> a;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const u16x8 v = {x[s][0], x[s][1], x[s][2], x[s][3], y[s][0], y[s][1], y[s][2], y[s][3]};
+    a.f[s] = __builtin_bit_cast(typename Mfma<f16>::frag, v);
   }
   return a;
 }

@@ -814,7 +814,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
   // dealt round-robin over the four side waves (the group's instruction k
   // to wave k mod 4)
   auto dma_mat = [&](int c, int m, int slot_buf, int g) {
-    dma_mat_packed(mat_src(c, m), mat(m, slot_buf), ((ww - 5 * g) % 4 + 4) % 4, kWaves);
+    dma_mat_packed<false>(mat_src(c, m), mat(m, slot_buf), ((ww - 5 * g) % 4 + 4) % 4, kWaves);
   };
   auto issue_early = [&](int c) {   // V, MG, MP, T^R, MR of chunk c (double-buffered)
     const int64_t tok = si.start + (int64_t)c * kChunk;
