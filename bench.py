@@ -49,12 +49,12 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("a65f761e8057f476", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168043097, 109707264),
-    "grad_absmax": ("27fac8f619a3f435", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196090, 131130),
-    "bwd_scan": ("b0458713c1d2bac9", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 347068885, 613502826),
-    "bwd_grad": ("5315ddfd228e0690", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232683179, 302484138),
-    "fwd_scan": ("22989059739cdac2", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 313287570, 638592435),
-    "decode": ("1dfdc074703e2d69", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542737987, 539561446),
+    "prep": ("59ede1e495b6c351", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168043918, 109707264),
+    "grad_absmax": ("58e13bd352c77f52", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196034, 131114),
+    "bwd_scan": ("78dd018929f7fbd4", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344455036, 613694282),
+    "bwd_grad": ("d749302e6a4d34fd", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232628510, 302970816),
+    "fwd_scan": ("5b8f8225244c9c16", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310671701, 638592102),
+    "decode": ("5afcfaaf0efc70bb", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746899, 539593088),
 }
 
 
