@@ -780,10 +780,11 @@ struct BwdWsLayout {
   static constexpr int kYst = kGates + 2 * kGateVec * 4;    // dYR (token tile)
   static constexpr int kRed = kYst + kBufBytes;             // per-wave maxima [8]
   static constexpr int kDv = kRed + 8 * 4;                  // dv, fp32 [64][BV]
-  // chunk-end checkpoints of dS, dR as stored: fp16 [DK][BV] each, then the
-  // tile scales [2][DK / 16]
+  // chunk-end checkpoints of dS, dR in fp16, each 16-row tile divided by its
+  // power of two, in the state-copy layout ([BV][DK] padded rows, TSC), then
+  // the tile scales [2][DK / 16]
   static constexpr int kCk = kDv + kChunk * BV * 4;
-  static constexpr int kCkSc = kCk + 2 * DK * BV * 2;
+  static constexpr int kCkSc = kCk + 2 * BV * TSC::kRowB;
   static constexpr int kGraw = kCkSc + 2 * (DK / 16) * 4;   // the gate block (one side wave's DMA)
   static constexpr int kZero = kGraw + kGateBlock * 4;      // 16 zero bytes (blocks above the diagonal)
   static constexpr int kBytes = kZero + 16;
@@ -993,18 +994,21 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
     }
   };
   // side: chunk c's end-state checkpoints from LDS, rows 32 ww .. 32 ww + 31
-  // of each (2 KiB contiguous: two 1 KiB stores), and their tile scales
+  // of each: two transpose reads give a lane 16 bytes of one row, so each
+  // store writes 16 rows (1 KiB contiguous); and their tile scales
   auto store_ckpt = [&](int c) {
     const int64_t gc = si.chunk0 + c;
     const int64_t ob = ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
     const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
-      f16* dst = reinterpret_cast<f16*>(st ? p.dR_ws : p.dS_ws) + ob + ww * (DK / 4) * BV;
-      const f16* src = ckst + st * DK * BV + ww * (DK / 4) * BV;
+      f16* dst = reinterpret_cast<f16*>(st ? p.dR_ws : p.dS_ws) + ob;
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
-        *reinterpret_cast<uint4*>(dst + (u * 64 + lane) * 8) = lds_read16_sync(src + (u * 64 + lane) * 8);
+      for (int u = 0; u < 2; ++u) {
+        const int t0 = ww * (DK / 4) + 16 * u;
+        const uint4 x = tile_token_rows16_sync<TSC>(ckst + st * BV * (TSC::kRowB / 2), t0);
+        *reinterpret_cast<uint4*>(dst + (int64_t)(t0 + (lane & 15)) * BV + 8 * (lane >> 4)) = x;
+      }
     }
     if (lane < 2 * IT) {   // one lane per tile scale, both states in one store
       const int st = lane / IT, it = lane % IT;
@@ -1235,16 +1239,19 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
           *reinterpret_cast<floatx4*>(dvst + tq * BV + jt * 16 + cq) = quad_transpose(val);
         }
       }
-      {   // gradient w.r.t. this chunk's end states, packed as stored (tile
-          // maxima from publish_state_max: dS, dR are unchanged since)
+      {   // gradient w.r.t. this chunk's end states (tile maxima from
+          // publish_state_max: dS, dR are unchanged since), each 16-row tile
+          // divided by its power of two, in the state-copy layout
 #pragma unroll
         for (int st = 0; st < 2; ++st) {
 #pragma unroll
           for (int it = 0; it < IT; ++it) {
             const int e = pow2_scale_exp(st ? tmR[it] : tmS[it]);
-            int row, col;
-            const uint4 v = pack_strip_f16(st ? dR[it][0] : dS[it][0], st ? dR[it][1] : dS[it][1], exp2_int(-e), row, col);
-            *reinterpret_cast<uint4*>(ckst + st * DK * BV + (ww * (DK / 4) + 16 * it + row) * BV + col) = v;
+            const float sc = exp2_int(-e);
+#pragma unroll
+            for (int jt = 0; jt < JT; ++jt)
+              store_state_copy<TSC>(ckst + st * BV * (TSC::kRowB / 2), jt * 16, ww * (DK / 4) + 16 * it,
+                                    (st ? dR[it][jt] : dS[it][jt]) * sc);
             ckscl[st * (DK / 16) + ww * IT + it] = exp2_int(e);   // every lane: the wave-uniform value
           }
         }
