@@ -843,34 +843,36 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     const uint4 x = keep_if(tile_token_rows16_sync<TT>(src, 16 * ww), t < chunk_len(c));
     *reinterpret_cast<uint4*>(fblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
   };
-  // side waves: chunk-start state X from its copies (hi + lo), rows
-  // 32 ww .. 32 ww + 31, fp16 blocked [DV / 32][DK][32] with one power-of-two
-  // scale per 16-row tile; the wave's two tile scales leave in one store
-  // (lane l writes tile l & 1's)
-  auto load_ckpt = [&](int st, floatx4 (&xv)[IT][JT]) {   // st: 0 = S, 1 = R
+  // side waves: chunk-start state X (st: 0 = S, 1 = R) from its copies
+  // (hi + lo), rows 32 ww .. 32 ww + 31, fp16 blocked [DV / 32][DK][32] with
+  // one power-of-two scale per 16-row tile.  Transpose reads of the copies
+  // give lane (g, i) state row t0 + i at columns 8 g .. 8 g + 7, so one
+  // 16-row tile is one 1 KiB store; the wave's two tile scales leave in one
+  // store (lane l writes tile l's)
+  auto store_ckpt = [&](int c, int st) {
+    const int64_t gc = si.chunk0 + c;
     const IN* hi = st ? Rhi : Shi;
     const IN* lo = st ? Rlo : Slo;
-#pragma unroll
-    for (int it = 0; it < IT; ++it)
-#pragma unroll
-      for (int jt = 0; jt < JT; ++jt) {
-        const int c0 = ww * (DK / 4) + it * 16;
-        xv[it][jt] = load_acc_tile<TSC>(hi, jt * 16, c0) + load_acc_tile<TSC>(lo, jt * 16, c0);
-      }
-  };
-  auto store_ckpt = [&](int c, int st, const floatx4 (&xv)[IT][JT]) {
-    const int64_t gc = si.chunk0 + c;
-    uint32_t mt[IT];
-    state_tile_absmax<IT>(xv, mt);
     f16* dst = reinterpret_cast<f16*>(st ? p.ck_R : p.ck_S) + ((int64_t)gc * H + h) * DK * DV + (int64_t)j0 * DK;
     float sc[IT];
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-      const int e = pow2_scale_exp(mt[it]);
-      int row, col;
-      const uint4 v = pack_strip_f16(xv[it][0], xv[it][1], exp2_int(-e), row, col);
-      *reinterpret_cast<uint4*>(dst + (int64_t)(ww * (DK / 4) + 16 * it + row) * 32 + col) = v;
-      sc[it] = exp2_int(e);
+      const int t0 = ww * (DK / 4) + 16 * it;
+      const uint4 xh = tile_token_rows16_sync<TSC>(hi, t0), xl = tile_token_rows16_sync<TSC>(lo, t0);
+      const uint32_t wh[4] = {xh.x, xh.y, xh.z, xh.w}, wl[4] = {xl.x, xl.y, xl.z, xl.w};
+      floatx4 a, b;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float v0 = __uint_as_float(wh[e] << 16) + __uint_as_float(wl[e] << 16);
+        const float v1 = __uint_as_float(wh[e] & 0xFFFF0000u) + __uint_as_float(wl[e] & 0xFFFF0000u);
+        if (e < 2) { a[2 * e] = v0; a[2 * e + 1] = v1; } else { b[2 * e - 4] = v0; b[2 * e - 3] = v1; }
+      }
+      const int ex = pow2_scale_exp(wave_absmax_bits(lane_absmax_bits(a, b)));
+      const float f = exp2_int(-ex);
+      const uint4 v = {cvt_pk_f16(a[0] * f, a[1] * f), cvt_pk_f16(a[2] * f, a[3] * f),
+                       cvt_pk_f16(b[0] * f, b[1] * f), cvt_pk_f16(b[2] * f, b[3] * f)};
+      *reinterpret_cast<uint4*>(dst + (int64_t)(t0 + (lane & 15)) * 32 + 8 * (lane >> 4)) = v;
+      sc[it] = exp2_int(ex);
     }
     static_assert(IT == 2, "two tiles per wave");
     const int64_t so = ((int64_t)gc * H + h) * (DK / 16) * (DV / 32) + j0 / 32;
@@ -1006,11 +1008,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
         issue_early(c + 1);
         issue_gates(c + 1);
       }
-      if constexpr (CKPT) {   // chunk-start S
-        floatx4 xs[IT][JT];
-        load_ckpt(0, xs);
-        store_ckpt(c, 0, xs);
-      }
+      if constexpr (CKPT) store_ckpt(c, 0);   // chunk-start S
     }
     barrier_lds();
 
@@ -1077,11 +1075,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
       }
       if constexpr (RDN) aTR = packed_rows_frags(mat(kMatTR, buf), ww, zero16);
     } else {
-      if constexpr (CKPT) {   // chunk-start R
-        floatx4 xr[IT][JT];
-        load_ckpt(1, xr);
-        store_ckpt(c, 1, xr);
-      }
+      if constexpr (CKPT) store_ckpt(c, 1);   // chunk-start R
       if constexpr (CKPT) store_block(c, 0, Ut);
     }
     barrier_lds();
