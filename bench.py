@@ -49,11 +49,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("59ede1e495b6c351", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168043918, 109707264),
-    "grad_absmax": ("58e13bd352c77f52", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196034, 131114),
-    "bwd_scan": ("78dd018929f7fbd4", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344455036, 613694282),
-    "bwd_grad": ("d749302e6a4d34fd", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232628510, 302970816),
-    "fwd_scan": ("5b8f8225244c9c16", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310671701, 638592102),
+    "prep": ("59ede1e495b6c351", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168044345, 109707264),
+    "grad_absmax": ("58e13bd352c77f52", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67195941, 131088),
+    "bwd_scan": ("51e05b04e92d36d2", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344454509, 613600992),
+    "bwd_grad": ("d749302e6a4d34fd", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232657477, 302453989),
+    "fwd_scan": ("ce900fe68676522c", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310657683, 638599443),
     "decode": ("5afcfaaf0efc70bb", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746899, 539593088),
 }
 
