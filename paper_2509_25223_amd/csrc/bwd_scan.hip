@@ -911,17 +911,31 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
         store_state_copy<TSC>(dRc, jt * 16, ww * (DK / 4) + it * 16, dR[it][jt] * iR);
       }
   };
+  // The side's global addresses are a chunk's uniform base plus a 32-bit
+  // lane offset that does not change from chunk to chunk, so the memory
+  // instructions take a scalar base and the lane part is formed once.
+  // K or Q rows: token row 16 ww + (lane & 15) of the chunk whose rows start at base
+  auto load_rows = [&](typename MI::frag (&afr)[KS_STEPS], const IN* base, bool ok) {
+    const uint32_t o = (uint32_t)((16 * ww + (lane & 15)) * H * DK + (lane >> 4) * 8);
+#pragma unroll
+    for (int s2 = 0; s2 < KS_STEPS; ++s2) {
+      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (ok) v = *reinterpret_cast<const u16x8*>(base + o + s2 * 32);
+      afr[s2] = __builtin_bit_cast(typename MI::frag, v);
+    }
+  };
   auto issue_regs = [&](int c) {   // side: K, Q rows and this thread's dO vector of chunk c
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
-    const int t = 16 * ww + (lane & 15);
-    const int64_t roff = ((tok + t) * H + h) * (int64_t)DK;
-    load_rowfrags<IN, DK>(Kn, t < len ? kg + roff : nullptr);
-    load_rowfrags<IN, DK>(Qn, t < len ? qg + roff : nullptr);
+    const bool ok = 16 * ww + (lane & 15) < len;
+    const int64_t rb = (tok * H + h) * (int64_t)DK;
+    load_rows(Kn, kg + rb, ok);
+    load_rows(Qn, qg + rb, ok);
     typedef IN INV __attribute__((ext_vector_type(kOPerThread)));
     const int tt = lane, j = ww * kOPerThread;
     INV v = {};
-    if (tt < len) v = *reinterpret_cast<const INV*>(dog + ((tok + tt) * H + h) * (int64_t)DV + j0 + j);
+    if (tt < len)
+      v = *reinterpret_cast<const INV*>(dog + (tok * H + h) * (int64_t)DV + j0 + j + (uint32_t)(tt * H * DV));
 #pragma unroll
     for (int u = 0; u < kOPerThread; ++u) on[u] = v[u];
   };
@@ -959,7 +973,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
     if (ww < kInst) {
       const int P = ww * 64 + lane, t = P / kPerRow, cc = P % kPerRow;
       const int ts = t < len ? t : 0;
-      dma16(p.ck_mask + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * 16, mask + ww * 1024);
+      dma16(p.ck_mask + (tok * H + h) * (int64_t)DV + j0 + (uint32_t)(ts * H * DV + cc * 16), mask + ww * 1024);
     }
   };
   // side: block b (0 dX, 1 dY, 2 dYR) of chunk c, tokens 16 ww .. 16 ww + 15,
@@ -970,7 +984,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
     const XT* srcb = b == 0 ? blk(bDC_DX) : b == 1 ? blk(bDUR_DU) : Yst;
     const int t = 16 * ww + (lane & 15);
     const uint4 x = keep_if(tile_token_rows16_sync<TT>(srcb, 16 * ww), t < chunk_len(c));
-    *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
+    *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + j0 + (uint32_t)(t * DV + 8 * (lane >> 4))) = x;
   };
   auto store_dv = [&](int c) {   // side: dv rows 16 ww + 8 u + lane / 8, columns 4 (lane % 8) ..
     const int64_t tok = si.start + (int64_t)c * kChunk;
@@ -980,15 +994,16 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       const int t = 16 * ww + 8 * u + (lane >> 3), col = 4 * (lane & 7);
       const uint4 x = lds_read16_sync(dvst + t * BV + col);
       if (t < len) {
-        const int64_t o = ((tok + t) * H + h) * (int64_t)DV + j0 + col;
+        const int64_t ob = (tok * H + h) * (int64_t)DV + j0;
+        const uint32_t ol = (uint32_t)(t * H * DV + col);
         if (p.out_bf16) {
           const floatx4 f = {__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w)};
           u16x4 b;
 #pragma unroll
           for (int e = 0; e < 4; ++e) b[e] = f2bf(f[e]);
-          *reinterpret_cast<u16x4*>(reinterpret_cast<u16*>(p.dv) + o) = b;
+          *reinterpret_cast<u16x4*>(reinterpret_cast<u16*>(p.dv) + ob + ol) = b;
         } else {
-          *reinterpret_cast<uint4*>(reinterpret_cast<float*>(p.dv) + o) = x;
+          *reinterpret_cast<uint4*>(reinterpret_cast<float*>(p.dv) + ob + ol) = x;
         }
       }
     }
@@ -1007,7 +1022,7 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
       for (int u = 0; u < 2; ++u) {
         const int t0 = ww * (DK / 4) + 16 * u;
         const uint4 x = tile_token_rows16_sync<TSC>(ckst + st * BV * (TSC::kRowB / 2), t0);
-        *reinterpret_cast<uint4*>(dst + (int64_t)(t0 + (lane & 15)) * BV + 8 * (lane >> 4)) = x;
+        *reinterpret_cast<uint4*>(dst + (uint32_t)((t0 + (lane & 15)) * BV + 8 * (lane >> 4))) = x;
       }
     }
     if (lane < 2 * IT) {   // one lane per tile scale, both states in one store

@@ -514,7 +514,7 @@ __device__ __forceinline__ void dma_mat64(const T* gsrc, T* lds, const MatDma<T,
 __device__ __forceinline__ void dma_linear_wave(const void* gsrc, void* lds, int bytes) {
   const int lane = threadIdx.x & 63;
   for (int b = 0; b < bytes; b += 1024)
-    dma16(reinterpret_cast<const char*>(gsrc) + b + lane * 16, reinterpret_cast<char*>(lds) + b);
+    dma16(reinterpret_cast<const char*>(gsrc) + (uint32_t)(b + lane * 16), reinterpret_cast<char*>(lds) + b);
 }
 
 // Waits for this wave's outstanding vector memory operations (loads, stores
@@ -638,7 +638,7 @@ __device__ __forceinline__ void dma_mat_packed(const f16* gsrc, f16* lds, int w,
   for (int i = w; i < kPkBytes / 1024; i += nw) {
     const int P = i * 64 + lane;                    // LDS 16-byte chunk
     const int b = P >> 5, rh = pk_pos<COLS>((P & 31) >> 1, P & 1);   // the (row, half) stored there
-    dma16(reinterpret_cast<const char*>(gsrc) + (b * 32 + rh) * 16,
+    dma16(reinterpret_cast<const char*>(gsrc) + (uint32_t)((b * 32 + rh) * 16),
           reinterpret_cast<char*>(lds) + i * 1024);
   }
 }

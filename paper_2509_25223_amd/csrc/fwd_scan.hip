@@ -784,11 +784,21 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
         store_state_copy<TSC>(Rhi, Rlo, jt * 16, ww * (DK / 4) + it * 16, Racc[it][jt]);
       }
   };
+  // Global addresses are a chunk's uniform base plus a 32-bit lane offset
+  // that does not change from chunk to chunk, so the memory instructions take
+  // a scalar base and the lane part is formed once.
   auto issue_rows = [&](typename MI::frag (&dst)[KS_STEPS], const IN* src, int c) {
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int t = 16 * ww + (lane & 15);
     const bool ok = t < chunk_len(c);
-    load_rowfrags<IN, DK>(dst, ok ? src + ((tok + t) * H + h) * (int64_t)DK : nullptr);
+    const IN* base = src + (tok * H + h) * (int64_t)DK;
+    const uint32_t o = (uint32_t)(t * H * DK + (lane >> 4) * 8);
+#pragma unroll
+    for (int s2 = 0; s2 < KS_STEPS; ++s2) {
+      u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (ok) v = *reinterpret_cast<const u16x8*>(base + o + s2 * 32);
+      dst[s2] = __builtin_bit_cast(typename MI::frag, v);
+    }
   };
   // side wave 0 moves chunk c's gate block (g, h, beta, gamma) into LDS with
   // one DMA instruction and, after its wait, forms every gate vector
@@ -822,7 +832,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     constexpr int kChunksPerRow = BV * (int)sizeof(IN) / 16;
     const int P = ww * 64 + lane, t = P / kChunksPerRow, cc = P % kChunksPerRow;
     const int ts = t < len ? t : len - 1;   // padding rows: any valid row (multiplied by 0)
-    dma16(vg + ((tok + ts) * H + h) * (int64_t)DV + j0 + cc * (16 / (int)sizeof(IN)),
+    dma16(vg + (tok * H + h) * (int64_t)DV + j0 + (uint32_t)(ts * H * DV + cc * (16 / (int)sizeof(IN))),
           reinterpret_cast<char*>(vblk(c)) + ww * 1024);
     int g = 0;
     dma_mat(c, kMatMG, c & 1, g++);
@@ -841,7 +851,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     const int64_t gc = si.chunk0 + c;
     const int t = 16 * ww + (lane & 15);
     const uint4 x = keep_if(tile_token_rows16_sync<TT>(src, 16 * ww), t < chunk_len(c));
-    *reinterpret_cast<uint4*>(fblk + blk_off(gc, h, H, b, DV) + (int64_t)t * DV + j0 + 8 * (lane >> 4)) = x;
+    *reinterpret_cast<uint4*>(fblk + blk_off(gc, h, H, b, DV) + j0 + (uint32_t)(t * DV + 8 * (lane >> 4))) = x;
   };
   // side waves: chunk-start state X (st: 0 = S, 1 = R) from its copies
   // (hi + lo), rows 32 ww .. 32 ww + 31, fp16 blocked [DV / 32][DK][32] with
@@ -871,7 +881,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
       const float f = exp2_int(-ex);
       const uint4 v = {cvt_pk_f16(a[0] * f, a[1] * f), cvt_pk_f16(a[2] * f, a[3] * f),
                        cvt_pk_f16(b[0] * f, b[1] * f), cvt_pk_f16(b[2] * f, b[3] * f)};
-      *reinterpret_cast<uint4*>(dst + (int64_t)(t0 + (lane & 15)) * 32 + 8 * (lane >> 4)) = v;
+      *reinterpret_cast<uint4*>(dst + (uint32_t)((t0 + (lane & 15)) * 32 + 8 * (lane >> 4))) = v;
       sc[it] = exp2_int(ex);
     }
     static_assert(IT == 2, "two tiles per wave");
@@ -925,7 +935,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     for (int jt = 0; jt < JT; ++jt) {
       const uint4 v = lds_read16_sync(ostage(c, jt) + (lane % (16 * 16 / kVE)) * 16);
       if (lane < 16 * 16 / kVE && t < len)
-        *reinterpret_cast<uint4*>(og + (tok + t) * H * (int64_t)DV + h * (int64_t)DV + j0 + jt * 16 + col) = v;
+        *reinterpret_cast<uint4*>(og + (tok * H + h) * (int64_t)DV + j0 + jt * 16 + (uint32_t)(t * H * DV + col)) = v;
     }
   };
 
@@ -1104,7 +1114,7 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
           constexpr int kVPR = BV / 16;
           const int e = (ww & 1) * 64 + lane, t = min(e / kVPR, len - 1), v = e % kVPR;
           if (ww < 2)
-            *reinterpret_cast<uint4*>(p.ck_mask + ((tok + t) * H + h) * (int64_t)DV + j0 + v * 16) =
+            *reinterpret_cast<uint4*>(p.ck_mask + (tok * H + h) * (int64_t)DV + j0 + (uint32_t)(t * H * DV + v * 16)) =
                 lds_read16_sync(Mst + t * BV + v * 16);
         }
       }
