@@ -206,12 +206,14 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     if constexpr (BF) {
       // blocked layout [DV / 32][DK][32]: k-step ks is column block ks
       static_assert(M::kStep == 32, "one 32-column block per k-step");
-      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff + (int64_t)i * 32;
-      const float* scp = scs[st] + sco + (int64_t)(i >> 4) * (DV / 32);
+      // the state's uniform base plus a 32-bit lane offset (scalar-base loads)
+      const f16* rowp = reinterpret_cast<const f16*>(srcs[st]) + soff;
+      const uint32_t ro = (uint32_t)(i * 32 + 8 * (lane >> 4));
+      const float* scp = scs[st] + sco + (i0 >> 4) * (DV / 32);
       float sc[KSV], mx = 0.f;
 #pragma unroll
       for (int ks = 0; ks < KSV; ++ks) {
-        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + (int64_t)ks * DK * 32 + 8 * (lane >> 4));
+        x.fr[ks] = *reinterpret_cast<const Frag*>(rowp + ro + ks * DK * 32);
         sc[ks] = scp[ks];
         mx = fmaxf(mx, sc[ks]);
       }
@@ -249,20 +251,20 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
   for (int u = 0; u < kKV; ++u) {
     const int e = tid + u * NT, t = in_row(e / (DK / kE)), i = (e % (DK / kE)) * kE;
-    const int64_t off = ((tok + t) * H + h) * (int64_t)DK + i;
+    const int64_t off = (tok * H + h) * (int64_t)DK + (uint32_t)(t * H * DK + i);
     kv[u] = *reinterpret_cast<const uint4*>(kg + off);
     qv[u] = *reinterpret_cast<const uint4*>(qg + off);
   }
 #pragma unroll
   for (int u = 0; u < kOV; ++u) {
     const int e = tid + u * NT, t = in_row(e / (DV / kE)), j = (e % (DV / kE)) * kE;
-    ov[u] = *reinterpret_cast<const uint4*>(dog + ((tok + t) * H + h) * (int64_t)DV + j);
+    ov[u] = *reinterpret_cast<const uint4*>(dog + (tok * H + h) * (int64_t)DV + (uint32_t)(t * H * DV + j));
   }
   // this token's decay inputs for the gate gradients of wave 0 (lane = token),
   // loaded now so that their latency is not left to the kernel's end
   float a_s = 0.f, a_r = 0.f;
   if (w == 0) {
-    const int64_t gi = (tok + in_row(lane)) * H + h;
+    const int64_t gi = tok * H + h + (uint32_t)(in_row(lane) * H);
     a_s = p.alpha_s[gi];
     a_r = p.alpha_r[gi];
   }
@@ -283,8 +285,8 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 #pragma unroll
   for (int u = 0; u < kVV; ++u) {
     const int e = tid + u * NT, t = e / (DV / kE), j = (e % (DV / kE)) * kE;
-    vrow[u] = *reinterpret_cast<const uint4*>(vg + ((tok + in_row(t)) * H + h) * (int64_t)DV + j);
-    rrow[u] = *reinterpret_cast<const uint4*>(fb + blk_off(c, h, H, 2, DV) + t * DV + j);
+    vrow[u] = *reinterpret_cast<const uint4*>(vg + (tok * H + h) * (int64_t)DV + (uint32_t)(in_row(t) * H * DV + j));
+    rrow[u] = *reinterpret_cast<const uint4*>(fb + blk_off(c, h, H, 2, DV) + (uint32_t)(t * DV + j));
   }
   // K, Q, dO rows: converted to the operand type (dO multiplied by the
   // upstream-gradient scale), stored swizzled
@@ -689,7 +691,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     // ss, sr: gradients of log aS_t, log aR_t
     float pa = 0.f, pb = 0.f;   // this token's share of d/da_h, d/db_h (pre-activations)
     if (t < len) {
-      const int64_t gi = (tok + t) * H + h;
+      const int64_t gi = tok * H + h + (uint32_t)(t * H);
       const float db = (esum[t] + tot_at(sB, t) + tot_at(sZB, t)) * isig;
       const float dgm = (esum[kChunk + t] + tot_at(sGM, t) + tot_at(sZGM, t)) * isig;
       if (vf & kVarGatePreact) {
@@ -755,7 +757,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * tt + acc_row(r);
         if (t < len) {
-          const int64_t gi = ((tok + t) * H + h) * (int64_t)DK + 16 * (w + NW * m) + acc_col();
+          const int64_t gi = (tok * H + h) * (int64_t)DK + 16 * (w + NW * m) + (uint32_t)(t * H * DK + acc_col());
           dqg[gi] = from_f<OT>(dQ[m][tt][r] * isig);
           dkg[gi] = from_f<OT>(dK[m][tt][r] * isig);
         }

@@ -463,7 +463,7 @@ __device__ __forceinline__ void dma_tile64(const void* gsrc, void* lds) {
     const int blk = w * (kInst / NW) + m;
     const int P = blk * 64 + lane;                  // physical 16-byte chunk
     const int r = P / TL::kCpr, c = (P % TL::kCpr) ^ TL::sw(r);   // logical chunk stored there
-    dma16(reinterpret_cast<const char*>(gsrc) + r * TL::kRowB + c * 16,
+    dma16(reinterpret_cast<const char*>(gsrc) + (uint32_t)(r * TL::kRowB + c * 16),
           reinterpret_cast<char*>(lds) + blk * 1024);
   }
 }
