@@ -49,12 +49,12 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("59ede1e495b6c351", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168044345, 109707264),
-    "grad_absmax": ("58e13bd352c77f52", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67195941, 131088),
-    "bwd_scan": ("51e05b04e92d36d2", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344454509, 613600992),
-    "bwd_grad": ("d749302e6a4d34fd", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232657477, 302453989),
-    "fwd_scan": ("ce900fe68676522c", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310657683, 638599443),
-    "decode": ("5afcfaaf0efc70bb", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746899, 539593088),
+    "prep": ("01c38c66fb9baf49", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168043622, 109707264),
+    "grad_absmax": ("5f906b00aae98bb1", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196253, 131125),
+    "bwd_scan": ("e47492c4c1bfba81", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344445504, 613576778),
+    "bwd_grad": ("015004e4bfe9a319", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232620451, 302532122),
+    "fwd_scan": ("3f1d7a30640ac565", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310655013, 638610662),
+    "decode": ("d33c8ae255924039", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542747027, 539552614),
 }
 
 
