@@ -278,7 +278,15 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
   }
   // the blocks on and below the diagonal, packed (tri_off): wave w holds
   // block row w
-  if constexpr (sizeof(XT) == 2) {   // fp16 rows leave in 16-byte stores (two strips of 32 columns)
+  if constexpr (sizeof(XT) == 2) {
+    // fp16 rows leave in 16-byte stores: each 16 x 32 half strip goes through
+    // this wave's block-product scratch (1 KiB, unused until the inversion),
+    // written column-major (one 8-byte store of 4 rows per tile and lane) and
+    // read back with transpose reads that give lane (g, i) row 16 w + i at
+    // columns 8 g .. 8 g + 7 of the half strip
+    typedef PadRows<XT, 16, 0> TS;   // [32 columns][16 rows]
+    XT* stg = reinterpret_cast<XT*>(W + w * 256);
+    const int g = (tid & 63) >> 4, i = tid & 15;
 #pragma unroll
     for (int m = 0; m < 3; ++m) {
       const floatx4* x = m == 0 ? mg : m == 1 ? mp : mr;
@@ -286,12 +294,21 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(OpParams p) {
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         if (2 * half > w) continue;   // both blocks of the strip pair above the diagonal
-        int row, col;
-        const uint4 v = pack_strip_f16(x[2 * half], x[2 * half + 1], 1.f, row, col);
-        const int s0 = 32 * half + col;
-        if ((s0 >> 4) <= w) *reinterpret_cast<uint4*>(base + tri_off(16 * w + row, s0)) = v;
+        asm volatile("" ::: "memory");   // the previous half strip's reads come first
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          f16x4 v4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v4[r] = (f16)x[2 * half + k][r];
+          *reinterpret_cast<f16x4*>(TS::ptr(stg, 16 * k + acc_col(), acc_row(0))) = v4;
+        }
+        asm volatile("" ::: "memory");   // the stores above come before the reads
+        const uint4 v = tile_token_rows16_sync<TS>(stg, 0);
+        const int s0 = 32 * half + 8 * g;
+        if ((s0 >> 4) <= w) *reinterpret_cast<uint4*>(base + tri_off(16 * w + i, s0)) = v;
       }
     }
+    asm volatile("" ::: "memory");
   } else {
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
