@@ -104,10 +104,21 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 // Per-wave per-token sums in LDS, written branch-free: all lanes that hold
 // the same sum store the same value to the same address.
-// Row sums of a tile quantity (lane: rows 4*(lane>>4)+r) into dst[t0 + row].
+// Row sums of a tile quantity (lane: rows 4*(lane>>4)+r) into dst[t0 + row],
+// by a transpose-reduce: exchanges with lanes c ^ 1 and c ^ 2 leave lane c
+// (c = lane % 16) with the sum over its quad of row 2 (c & 1) + ((c >> 1) & 1);
+// rotations by 8 and then 4 inside the 16-lane row add the four quads (after
+// the first the values repeat with period 8, so the four lanes of a row end
+// with the same bits and store the same value).
 __device__ __forceinline__ void put_rows(float* dst, int t0, const float (&v)[4]) {
-#pragma unroll
-  for (int r = 0; r < 4; ++r) dst[t0 + acc_row(r)] = group_sum<16>(v[r]);
+  const int lane = threadIdx.x & 63;
+  const bool b0 = lane & 1, b1 = lane & 2;
+  const float x0 = (b0 ? v[2] : v[0]) + dpp<0xB1>(b0 ? v[0] : v[2]);   // quad_perm [1,0,3,2]
+  const float x1 = (b0 ? v[3] : v[1]) + dpp<0xB1>(b0 ? v[1] : v[3]);
+  float y = (b1 ? x1 : x0) + dpp<0x4E>(b1 ? x0 : x1);                  // quad_perm [2,3,0,1]
+  y += dpp<0x128>(y);   // row_ror:8
+  y += dpp<0x124>(y);   // row_ror:4
+  dst[t0 + 4 * (lane >> 4) + 2 * (lane & 1) + ((lane >> 1) & 1)] = y;
 }
 
 // Column sums of a tile quantity (lane: column lane & 15) into dst[s0 + column].
@@ -465,14 +476,17 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
     for (int tt = 0; tt < 4; ++tt) { dQ[m][tt] = zero4(); dK[m][tt] = zero4(); }
   float gsC = 0.f, grC = 0.f;
 
-  // sum over this lane's elements of a (.) b
+  // sum over this lane's elements of a (.) b (fp16 pairs by v_dot2_f32_f16:
+  // fp16 products are exact in fp32, accumulated in fp32)
   auto frag_dot = [&](const StateRows& a, const StateRows& b) {
     float s = 0.f;
 #pragma unroll
     for (int ks = 0; ks < KSV; ++ks) {
       if constexpr (BF) {
+        typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-        for (int e = 0; e < 8; ++e) s += (float)a.fr[ks][e] * (float)b.fr[ks][e];
+        for (int e = 0; e < 8; e += 2)
+          s = __builtin_amdgcn_fdot2(h2{a.fr[ks][e], a.fr[ks][e + 1]}, h2{b.fr[ks][e], b.fr[ks][e + 1]}, s, false);
       } else {
         s += a.fr[ks] * b.fr[ks];
       }
