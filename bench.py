@@ -49,11 +49,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("01c38c66fb9baf49", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168043622, 109707264),
-    "grad_absmax": ("5f906b00aae98bb1", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196253, 131125),
-    "bwd_scan": ("e47492c4c1bfba81", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344445504, 613576778),
-    "bwd_grad": ("015004e4bfe9a319", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232620451, 302532122),
-    "fwd_scan": ("3f1d7a30640ac565", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310655013, 638610662),
+    "prep": ("31153e7c49df92f0", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168030722, 109707264),
+    "grad_absmax": ("5f906b00aae98bb1", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67195893, 131141),
+    "bwd_scan": ("e47492c4c1bfba81", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344444791, 613591456),
+    "bwd_grad": ("6cdda306e1c47432", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232620437, 302533984),
+    "fwd_scan": ("3f1d7a30640ac565", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310654005, 638589478),
     "decode": ("d33c8ae255924039", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542747027, 539552614),
 }
 
