@@ -779,11 +779,12 @@ struct BwdWsLayout {
   static constexpr int kGates = kMask + B::kMaskBytes;   // two sets (chunk parity)
   static constexpr int kYst = kGates + 2 * kGateVec * 4;    // dYR (token tile)
   static constexpr int kRed = kYst + kBufBytes;             // per-wave maxima [8]
-  static constexpr int kDv = kRed + 8 * 4;                  // dv, fp32 [64][BV]
+  static constexpr int kDvLd = kChunk + 4;                  // dv row stride (floats)
+  static constexpr int kDv = kRed + 8 * 4;                  // dv, fp32 [BV][kDvLd] (column-major)
   // chunk-end checkpoints of dS, dR in fp16, each 16-row tile divided by its
   // power of two, in the state-copy layout ([BV][DK] padded rows, TSC), then
   // the tile scales [2][DK / 16]
-  static constexpr int kCk = kDv + kChunk * BV * 4;
+  static constexpr int kCk = kDv + BV * kDvLd * 4;
   static constexpr int kCkSc = kCk + 2 * BV * TSC::kRowB;
   static constexpr int kGraw = kCkSc + 2 * (DK / 16) * 4;   // the gate block (one side wave's DMA)
   static constexpr int kZero = kGraw + kGateBlock * 4;      // 16 zero bytes (blocks above the diagonal)
@@ -986,13 +987,15 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
     const uint4 x = keep_if(tile_token_rows16_sync<TT>(srcb, 16 * ww), t < chunk_len(c));
     *reinterpret_cast<uint4*>(bblk + blk_off(gc, h, H, b, DV) + j0 + (uint32_t)(t * DV + 8 * (lane >> 4))) = x;
   };
-  auto store_dv = [&](int c) {   // side: dv rows 16 ww + 8 u + lane / 8, columns 4 (lane % 8) ..
+  // side: dv rows 16 ww + 8 u + lane / 8, columns 4 (lane % 8) .. from the
+  // column-major stage (four reads per 16 bytes)
+  auto store_dv = [&](int c) {
     const int64_t tok = si.start + (int64_t)c * kChunk;
     const int len = chunk_len(c);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       const int t = 16 * ww + 8 * u + (lane >> 3), col = 4 * (lane & 7);
-      const uint4 x = lds_read16_sync(dvst + t * BV + col);
+      const uint4 x = lds_read4x1_sync(dvst + col * L::kDvLd + t, L::kDvLd * 4);
       if (t < len) {
         const int64_t ob = (tok * H + h) * (int64_t)DV + j0;
         const uint32_t ol = (uint32_t)(t * H * DV + col);
@@ -1241,17 +1244,16 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
 #pragma unroll
         for (int jt = 0; jt < JT; ++jt) tail[jt] = dU[jt];
       }
-      {   // dv = dX + diag(b) tail into LDS: a quad transpose gives lane 4g + i
-          // token t0 + i at columns 4 g .. 4 g + 3 of each 16-column tile
+      {   // dv = dX + diag(b) tail into the column-major stage: this lane's 4
+          // tokens t0 .. t0 + 3 of column 16 jt + (lane & 15), one 16-byte store
         const int t0 = 16 * ww + acc_row(0);
         const floatx4 b4 = *reinterpret_cast<const floatx4*>(gbt + t0);
-        const int tq = t0 + (lane & 3), cq = 4 * ((lane & 15) >> 2);
 #pragma unroll
         for (int jt = 0; jt < JT; ++jt) {
           floatx4 val;
 #pragma unroll
           for (int r = 0; r < 4; ++r) val[r] = __builtin_fmaf(b4[r], tail[jt][r], dX[jt][r]) * isig;
-          *reinterpret_cast<floatx4*>(dvst + tq * BV + jt * 16 + cq) = quad_transpose(val);
+          *reinterpret_cast<floatx4*>(dvst + (jt * 16 + acc_col()) * L::kDvLd + t0) = val;
         }
       }
       {   // gradient w.r.t. this chunk's end states (tile maxima from

@@ -348,6 +348,21 @@ __device__ __forceinline__ uint4 tile_token_rows16_sync(const void* base, int t0
                c[0] | ((uint32_t)c[1] << 16), c[2] | ((uint32_t)c[3] << 16)};
 }
 
+// Four 4-byte LDS values at p, p + stride, p + 2 stride, p + 3 stride (bytes)
+// as 16 bytes, issued as inline assembly like lds_read16_sync (no drain of
+// in-flight LDS-DMA) and waited for by the function.
+__device__ __forceinline__ uint4 lds_read4x1_sync(const void* p, int stride) {
+  typedef __attribute__((address_space(3))) const char* lds_ptr;
+  const uint32_t a = (uint32_t)(uintptr_t)(lds_ptr)(reinterpret_cast<const char*>(p));
+  uint32_t x, y, z, w;
+  asm volatile("ds_read_b32 %0, %1" : "=v"(x) : "v"(a));
+  asm volatile("ds_read_b32 %0, %1" : "=v"(y) : "v"(a + stride));
+  asm volatile("ds_read_b32 %0, %1" : "=v"(z) : "v"(a + 2 * stride));
+  asm volatile("ds_read_b32 %0, %1" : "=v"(w) : "v"(a + 3 * stride));
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(x), "+v"(y), "+v"(z), "+v"(w));
+  return uint4{x, y, z, w};
+}
+
 // 16 bytes from LDS, issued as inline assembly so that the compiler does not
 // drain the wave's in-flight LDS-DMA before it (it cannot always prove the
 // addresses disjoint); waits for its own read.
