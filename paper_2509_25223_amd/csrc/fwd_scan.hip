@@ -675,7 +675,11 @@ struct FwdWsLayout {
   static constexpr int kMst = kRst + kBufBytes;
   static constexpr int kGraw = kMst + kChunk * BV;      // the gate block (one side wave's DMA)
   static constexpr int kZero = kGraw + kGateBlock * 4;   // 16 zero bytes (blocks above the diagonal)
-  static constexpr int kBytes = kZero + 16;
+  // fp32 outputs: o of a chunk, column-major [BV][kOstLd] (the pad keeps the
+  // side's 4-byte gathers of one token's 4 columns in distinct banks)
+  static constexpr int kOstLd = kChunk + 4;
+  static constexpr int kOst = kZero + 16;
+  static constexpr int kBytes = kOst + BV * kOstLd * 4;
   static_assert(sizeof(IN) == 2 && DK == 128 && BV == 32, "bf16, d_k 128, 32 columns");
   static_assert(kVBytes == 4 * 1024, "V block = one DMA instruction per side wave");
   static_assert(kBytes <= 160 * 1024, "forward scan LDS");
@@ -926,6 +930,9 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
   auto ostage = [&](int c, int jt) {
     return reinterpret_cast<char*>(jt ? reinterpret_cast<char*>(Rst) : reinterpret_cast<char*>(vblk(c))) + ww * 1024;
   };
+  // fp32 o from the column-major stage: four 4-byte reads give a lane 4
+  // columns of one token
+  float* ost = reinterpret_cast<float*>(smem + L::kOst);
   auto store_o = [&](int c) {   // side waves: chunk c's o rows 16 ww .. 16 ww + 15
     constexpr int kVE = 16 / (int)sizeof(OT);   // elements per 16 bytes
     const int64_t tok = si.start + (int64_t)c * kChunk;
@@ -933,7 +940,8 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
     const int t = 16 * ww + lane / (16 / kVE), col = (lane % (16 / kVE)) * kVE;
 #pragma unroll
     for (int jt = 0; jt < JT; ++jt) {
-      const uint4 v = lds_read16_sync(ostage(c, jt) + (lane % (16 * 16 / kVE)) * 16);
+      const uint4 v = sizeof(OT) == 4 ? lds_read4x1_sync(ost + (jt * 16 + col) * L::kOstLd + t, L::kOstLd * 4)
+                                      : lds_read16_sync(ostage(c, jt) + (lane % (16 * 16 / kVE)) * 16);
       if (lane < 16 * 16 / kVE && t < len)
         *reinterpret_cast<uint4*>(og + (tok * H + h) * (int64_t)DV + j0 + jt * 16 + (uint32_t)(t * H * DV + col)) = v;
     }
@@ -1157,14 +1165,14 @@ __global__ __launch_bounds__(2 * kThreads) void fwd_scan_ws_kernel(OpParams p) {
             const int t = 16 * ww + acc_row(r);
             ov[r] = __builtin_fmaf(ggm[t], __builtin_fmaf(egr[t], QR[jt][r], mru[r]), base[jt][r]);
           }
-          // quad transpose: this lane's row 4 (lane / 16) + lane % 4, columns
-          // 4 ((lane % 16) / 4) .. + 3 of the wave's 16 x 16 tile
-          const floatx4 x = quad_transpose(ov);
-          const int row = 4 * (lane >> 4) + (lane & 3), col = 4 * ((lane & 15) >> 2);
-          char* dst = ostage(c, jt) + (row * 16 + col) * (int)sizeof(OT);
-          if constexpr (sizeof(OT) == 4) {
-            *reinterpret_cast<floatx4*>(dst) = x;
+          if constexpr (sizeof(OT) == 4) {   // this lane's 4 tokens of its column, one store
+            *reinterpret_cast<floatx4*>(ost + (jt * 16 + acc_col()) * L::kOstLd + 16 * ww + acc_row(0)) = ov;
           } else {
+            // quad transpose: this lane's row 4 (lane / 16) + lane % 4, columns
+            // 4 ((lane % 16) / 4) .. + 3 of the wave's 16 x 16 tile
+            const floatx4 x = quad_transpose(ov);
+            const int row = 4 * (lane >> 4) + (lane & 3), col = 4 * ((lane & 15) >> 2);
+            char* dst = ostage(c, jt) + (row * 16 + col) * (int)sizeof(OT);
             u16x4 b;
 #pragma unroll
             for (int k = 0; k < 4; ++k) b[k] = f2bf(x[k]);
