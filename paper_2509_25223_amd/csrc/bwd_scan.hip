@@ -885,17 +885,17 @@ __global__ __launch_bounds__(2 * kThreads) void bwd_scan_ws_kernel(OpParams p) {
   IN on[kOPerThread];                              // side: its dO vector
   float scS = 1.f, scR = 1.f;
   uint32_t tmS[IT], tmR[IT];
-  auto publish_state_max = [&]() {   // chain
-    state_tile_absmax<IT>(dS, tmS);
-    state_tile_absmax<IT>(dR, tmR);
-    uint32_t ms = tmS[0], mr = tmR[0];
-#pragma unroll
-    for (int it = 1; it < IT; ++it) {
-      ms = max(ms, tmS[it]);
-      mr = max(mr, tmR[it]);
-    }
-    smax[ww] = ms;   // every lane stores the wave-uniform value
-    smax[4 + ww] = mr;
+  auto publish_state_max = [&]() {   // chain: the four tile maxima, reduced together
+    static_assert(IT == 2, "two tiles of each state per wave");
+    const uint32_t lm[4] = {lane_absmax_bits(dS[0][0], dS[0][1]), lane_absmax_bits(dS[1][0], dS[1][1]),
+                            lane_absmax_bits(dR[0][0], dR[0][1]), lane_absmax_bits(dR[1][0], dR[1][1])};
+    const uint32_t y = wave_max4_bits(lm);
+    tmS[0] = __builtin_amdgcn_readlane(y, 0);
+    tmS[1] = __builtin_amdgcn_readlane(y, 2);
+    tmR[0] = __builtin_amdgcn_readlane(y, 1);
+    tmR[1] = __builtin_amdgcn_readlane(y, 3);
+    smax[ww] = max(tmS[0], tmS[1]);   // every lane stores the wave-uniform value
+    smax[4 + ww] = max(tmR[0], tmR[1]);
   };
   auto write_copies = [&]() {   // chain, after a barrier that follows publish_state_max
     const uint32_t ms = max(max(smax[0], smax[1]), max(smax[2], smax[3]));

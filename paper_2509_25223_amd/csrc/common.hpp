@@ -873,6 +873,25 @@ __device__ __forceinline__ uint32_t wave_absmax_bits(uint32_t m) {
              max((uint32_t)__builtin_amdgcn_readlane((int)m, 32), (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
 }
 
+// Largest of four values per lane over the wave, the four reduced together
+// (a transpose-reduce): exchanges with lanes c ^ 1 and c ^ 2 inside each quad
+// leave lane c (c = lane % 16) with the quad's largest v[2 (c & 1) + ((c >> 1)
+// & 1)], rotations by 8 and 4 inside the 16-lane row and exchanges across
+// rows then give every lane that value's wave maximum; lanes 0, 2, 1, 3 hold
+// those of v[0], v[1], v[2], v[3].  Unsigned maxima (fp32 magnitude bits):
+// exact, so the order does not matter.
+__device__ __forceinline__ uint32_t wave_max4_bits(const uint32_t (&v)[4]) {
+  const int lane = threadIdx.x & 63;
+  const bool b0 = lane & 1, b1 = lane & 2;
+  const uint32_t x0 = max(b0 ? v[2] : v[0], dpp_u32<0xB1>(b0 ? v[0] : v[2]));   // quad_perm [1,0,3,2]
+  const uint32_t x1 = max(b0 ? v[3] : v[1], dpp_u32<0xB1>(b0 ? v[1] : v[3]));
+  uint32_t y = max(b1 ? x1 : x0, dpp_u32<0x4E>(b1 ? x0 : x1));                  // quad_perm [2,3,0,1]
+  y = max(y, dpp_u32<0x128>(y));   // row_ror:8
+  y = max(y, dpp_u32<0x124>(y));   // row_ror:4
+  y = max(y, (uint32_t)__shfl_xor((int)y, 16, 64));
+  return max(y, (uint32_t)__shfl_xor((int)y, 32, 64));
+}
+
 // 4 x 4 transpose across the lanes of each quad (lanes 4g + i, i = 0..3): lane
 // i enters with x[r] = M[i][r] and leaves with x[r] = M[r][i].  Two exchange
 // rounds, with lane i ^ 1 for the registers whose index differs from i in bit
