@@ -47,6 +47,22 @@ template <> __device__ __forceinline__ f16 from_f<f16>(float x) { return to_f16(
 // with fp32 range.  Used for state operands (split-bf16 products).
 __device__ __forceinline__ u16 bf16_lo(float x, u16 hi) { return f2bf(x - bf2f(hi)); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// The same split for a pair, as two packed words (first element in the low
+// half): hi by one v_cvt_pk_bf16_f32; each residual x - hi, exact in fp32, as
+// the bf16 dot product hi . (-1, -0) + x (v_dot2_f32_bf16: bf16 products are
+// exact), in place of a shift or mask and a subtraction; lo by one more
+// pair conversion.  The zero is -0 so that neither constant matches an
+// inline constant: (-1, +0) is emitted as the inline -1.0, which the
+// two-operand form reads as the fp32 word 0xBF800000, the pair (0, -1).
+__device__ __forceinline__ void bf16_split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+  const bf16x2 h = {(__bf16)a, (__bf16)b};
+  const float ra = __builtin_amdgcn_fdot2_f32_bf16(h, bf16x2{(__bf16)-1.f, (__bf16)-0.f}, a, false);
+  const float rb = __builtin_amdgcn_fdot2_f32_bf16(h, bf16x2{(__bf16)-0.f, (__bf16)-1.f}, b, false);
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)ra, (__bf16)rb});
+}
+
 // ---------------------------------------------------------------------------
 // MFMA 16x16 tiles.  One wave computes D[16 x 16] += A[16 x K] * B[K x 16].
 //   bf16 (T = u16): v_mfma_f32_16x16x32_bf16, 8 k-values per lane per step.

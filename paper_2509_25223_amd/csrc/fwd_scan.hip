@@ -96,14 +96,11 @@ __device__ __forceinline__ void store_state_copy(IN* hi, IN* lo, int r0, int c0,
   // r0, c0 multiples of 16
   const int o = TL::off_split(r0, acc_col(), acc_row(0) * (int)sizeof(IN), c0 * (int)sizeof(IN));
   if constexpr (sizeof(IN) == 2) {   // 8-byte stores of 4 consecutive rows
-    u16x4 h4, l4;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      h4[k] = f2bf(v[k]);
-      l4[k] = bf16_lo(v[k], h4[k]);
-    }
-    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(hi) + o) = h4;
-    *reinterpret_cast<u16x4*>(reinterpret_cast<char*>(lo) + o) = l4;
+    uint2 h2, l2;
+    bf16_split2(v[0], v[1], h2.x, l2.x);
+    bf16_split2(v[2], v[3], h2.y, l2.y);
+    *reinterpret_cast<uint2*>(reinterpret_cast<char*>(hi) + o) = h2;
+    *reinterpret_cast<uint2*>(reinterpret_cast<char*>(lo) + o) = l2;
   } else {
     *reinterpret_cast<floatx4*>(reinterpret_cast<char*>(hi) + o) = v;
   }
