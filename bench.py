@@ -49,12 +49,12 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("31153e7c49df92f0", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168030722, 109707264),
-    "grad_absmax": ("5f906b00aae98bb1", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67195893, 131141),
-    "bwd_scan": ("e47492c4c1bfba81", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344444791, 613591456),
-    "bwd_grad": ("6cdda306e1c47432", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232620437, 302533984),
-    "fwd_scan": ("3f1d7a30640ac565", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310654005, 638589478),
-    "decode": ("d33c8ae255924039", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542747027, 539552614),
+    "prep": ("6d1faa0c02a5a94f", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168030291, 109707264),
+    "grad_absmax": ("cf6a1e89483c351b", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196130, 131120),
+    "bwd_scan": ("89cbf6b2fe761bee", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344435528, 613735018),
+    "bwd_grad": ("b30eec821722c9e7", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232645538, 302653941),
+    "fwd_scan": ("017ad91aed089cd7", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310660695, 638594515),
+    "decode": ("a6d19635132fd623", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746720, 539558630),
 }
 
 
