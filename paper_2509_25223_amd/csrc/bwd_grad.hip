@@ -178,7 +178,7 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
 
   // heads vary fastest over consecutive workgroups, which then read one
   // contiguous stretch of the token rows (every head of the chunk)
-  const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int h = blockIdx.x, c = blockIdx.y, tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   float* wsum = sums + w * kNumSums * kChunk;   // this wave's sums
   auto sum_row = [&](int q) { return wsum + q * kChunk; };
   ChunkInfo ci;
@@ -386,9 +386,20 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
   constexpr int kMyTiles = (10 + NW - 1) / NW;   // share of the 10 lower tiles per wave
   floatx4 tW1[kMyTiles], tW2[kMyTiles], tW3[kMyTiles], tW4[kMyTiles], tW5[kMyTiles];
   floatx4 tG[kMyTiles], tP[kMyTiles];
-  auto tile_of = [](int idx, int& tt, int& st) {   // lower tiles, row by row
-    tt = idx >= 6 ? 3 : idx >= 3 ? 2 : idx >= 1 ? 1 : 0;
-    st = idx - (tt * (tt + 1)) / 2;
+  // Lower tiles (token block rows tt >= st). With eight waves, waves 0 and 1
+  // take two tiles each: those four are strictly below the diagonal (no
+  // masks, the cheaper decay step), the four diagonal tiles go to waves 2-5,
+  // and each wave's tiles differ in both row and column block (every per-wave
+  // sum entry is written once).  Other wave counts: row by row.
+  auto tile_of = [](int idx, int& tt, int& st) {
+    if constexpr (NW == 8) {   // (tt, st) of idx 0..9, two bits each
+      constexpr int kT = 0xfee49, kS = 0x91e40;
+      tt = (kT >> (2 * idx)) & 3;
+      st = (kS >> (2 * idx)) & 3;
+    } else {
+      tt = idx >= 6 ? 3 : idx >= 3 ? 2 : idx >= 1 ? 1 : 0;
+      st = idx - (tt * (tt + 1)) / 2;
+    }
   };
 #pragma unroll
   for (int x = 0; x < kMyTiles; ++x) {
@@ -432,13 +443,17 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
       int tt, st;
       tile_of(idx, tt, st);
       float zs[4], zp[4], zr[4], zb[4], zg[4];
+      // SL: a tile strictly below the diagonal (s < t everywhere: no masks,
+      // and every exponent is already <= 0)
+      auto decay_step = [&](auto strict) {
+      constexpr bool SL = decltype(strict)::value;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = 16 * tt + acc_row(r), s = 16 * st + acc_col();
-        const bool lower = s < t, diag = s <= t;
-        const float es = __expf(fminf(gsv[t] - gsv[s], 0.f));
-        const float ep = __expf(fminf(gspv[t] - gsv[s], 0.f));
-        const float er = __expf(fminf(grv[t] - grv[s], 0.f));
+        const bool lower = SL || s < t, diag = SL || s <= t;
+        const float es = __expf(SL ? gsv[t] - gsv[s] : fminf(gsv[t] - gsv[s], 0.f));
+        const float ep = __expf(SL ? gspv[t] - gsv[s] : fminf(gspv[t] - gsv[s], 0.f));
+        const float er = __expf(SL ? grv[t] - grv[s] : fminf(grv[t] - grv[s], 0.f));
         const float W1 = tW1[x][r], W2 = tW2[x][r], W3 = tW3[x][r];
         const float G = tG[x][r], P = tP[x][r];
         const float dAs = RDN ? -tW4[x][r] : 0.f, dAr = RDN ? -tW5[x][r] : 0.f;
@@ -458,6 +473,9 @@ __global__ __launch_bounds__(64 * (DK / 16)) void bwd_grad_kernel(OpParams p) {
         edp[x][r] = dp;
         edg[x][r] = dg;
       }
+      };
+      if (tt > st) decay_step(std::true_type{});
+      else decay_step(std::false_type{});
       put_rows(sum_row(sZRS), 16 * tt, zs);
       put_rows(sum_row(sZRP), 16 * tt, zp);
       put_rows(sum_row(sZRR), 16 * tt, zr);
