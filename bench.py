@@ -49,11 +49,11 @@ PEAK_HBM_GBS = 8000.0
 # numbers and commands are in profiles/), keyed by a hash of the kernel's
 # sources: a kernel changed since its counters were taken reports null.
 MEASURED_TRAFFIC = {
-    "prep": ("6d1faa0c02a5a94f", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168030291, 109707264),
-    "grad_absmax": ("cf6a1e89483c351b", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196130, 131120),
-    "bwd_scan": ("89cbf6b2fe761bee", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344435528, 613735018),
-    "bwd_grad": ("b30eec821722c9e7", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232645538, 302653941),
-    "fwd_scan": ("017ad91aed089cd7", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310660695, 638594515),
+    "prep": ("6d1faa0c02a5a94f", ('prep.hip', 'common.hpp', 'kernels.hpp'), 168030112, 109707264),
+    "grad_absmax": ("4b44d1d3f6c4cf05", ('grad_scale.hip', 'common.hpp', 'kernels.hpp'), 67196357, 131370),
+    "bwd_scan": ("89cbf6b2fe761bee", ('bwd_scan.hip', 'common.hpp', 'kernels.hpp'), 344435965, 613594794),
+    "bwd_grad": ("08848c41c5e9ad23", ('bwd_grad.hip', 'common.hpp', 'kernels.hpp'), 1232656230, 302521893),
+    "fwd_scan": ("017ad91aed089cd7", ('fwd_scan.hip', 'common.hpp', 'kernels.hpp'), 310649896, 638591833),
     "decode": ("a6d19635132fd623", ('decode.hip', 'common.hpp', 'kernels.hpp'), 542746720, 539558630),
 }
 
